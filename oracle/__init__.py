@@ -1,0 +1,181 @@
+"""Oracle for the gradient sparsifier (Wangni et al., arXiv 1710.09854).
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg
+of ``bench.py`` may import this package. It is a plain, slow, double-precision CPU statement of
+what the sparsifier computes, written from the paper; it shares no code with the GPU library
+(``paper_1710_09854_amd``) and imports nothing from it.
+
+The arithmetic lives in ``oracle.cpp`` (built to ``liboracle.so`` by ``oracle/build.py``); this
+module only marshals numpy arrays. Every function is pinned by a test in ``tests/test_oracle_*.py``.
+
+Functions and the passage each follows:
+
+* ``exact_sum``           -- exactly rounded sum of non-negative doubles (helper for every sum).
+* ``philox4x32_10``/``words`` -- Philox4x32-10 (Salmon et al., SC'11), the random source that
+  replaces the paper's precomputed random array (Section 5.3, engineering tricks).
+* ``solve_exact``         -- Proposition 1 + eq. (5) + Algorithm 2's criterion, density budget.
+* ``solve_variance``      -- Algorithm 2 verbatim (variance budget eps, eqs. 6-7).
+* ``solve_greedy``        -- Algorithm 3 as printed (vector form).
+* ``solve_greedy_scale``  -- Algorithm 3 rewritten through lambda (cross-check).
+* ``sample_compact``      -- Section 3's protocol: Z_i ~ Bernoulli(p_i), Q(g)_i = Z_i g_i / p_i,
+  survivors in ascending index order.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+FLAG_NONFINITE = 1
+FLAG_OVERFLOW = 2
+FLAG_ALLZERO = 4
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _build
+
+        _build.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
+    f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
+    u32p = np.ctypeslib.ndpointer(np.uint32, flags="C_CONTIGUOUS")
+    i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
+    i64 = ctypes.c_int64
+    pd = ctypes.POINTER(ctypes.c_double)
+    pi64 = ctypes.POINTER(ctypes.c_int64)
+    pu32 = ctypes.POINTER(ctypes.c_uint32)
+    pint = ctypes.POINTER(ctypes.c_int)
+    lib.orc_philox4x32_10.argtypes = [u32p, u32p, u32p]
+    lib.orc_philox4x32_10.restype = None
+    lib.orc_words.argtypes = [ctypes.c_uint64, i64, u32p]
+    lib.orc_words.restype = None
+    lib.orc_exact_sum.argtypes = [f64p, i64]
+    lib.orc_exact_sum.restype = ctypes.c_double
+    lib.orc_exact_density.argtypes = [f32p, i64, ctypes.c_double, f64p, pd, pi64, pu32]
+    lib.orc_exact_density.restype = ctypes.c_int
+    lib.orc_exact_variance.argtypes = [f32p, i64, ctypes.c_double, f64p, pd, pi64, pu32]
+    lib.orc_exact_variance.restype = ctypes.c_int
+    for name in ("orc_greedy_alg3", "orc_greedy_scale"):
+        fn = getattr(lib, name)
+        fn.argtypes = [f32p, i64, ctypes.c_double, ctypes.c_int, f64p, pd, pi64, pint, pu32]
+        fn.restype = ctypes.c_int
+    lib.orc_sample.argtypes = [f32p, f64p, i64, ctypes.c_uint64, i32p, f32p, i64, pi64]
+    lib.orc_sample.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+@dataclass
+class Solution:
+    p: np.ndarray        # float64 [d], keep probabilities
+    lam: float           # lambda of Proposition 1 (inf when every nonzero is kept surely)
+    k: int               # size of the capped set {p_i = 1}
+    iters: int           # greedy rescale steps taken (0 for the exact solvers)
+    flags: int           # FLAG_* bits
+
+
+def _f32(g) -> np.ndarray:
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    if g.ndim != 1:
+        raise ValueError("oracle works on one row at a time")
+    return g
+
+
+def exact_sum(x) -> float:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    if np.any(x < 0) or not np.all(np.isfinite(x)):
+        raise ValueError("exact_sum takes finite non-negative values")
+    return float(_load().orc_exact_sum(x, x.size))
+
+
+def philox4x32_10(counter, key):
+    c = np.ascontiguousarray(counter, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, np.uint32)
+    _load().orc_philox4x32_10(c, k, out)
+    return out
+
+
+def words(seed: int, d: int) -> np.ndarray:
+    """x_i for i < d: word (i mod 4) of Philox4x32-10(key=seed, counter=(i//4, 0, 0))."""
+    x = np.zeros(d, np.uint32)
+    _load().orc_words(ctypes.c_uint64(seed), d, x)
+    return x
+
+
+def _solve(fn, g, param, iters=None) -> Solution:
+    g = _f32(g)
+    p = np.zeros(g.size, np.float64)
+    lam = ctypes.c_double()
+    k = ctypes.c_int64()
+    fl = ctypes.c_uint32()
+    if iters is None:
+        rc = fn(g, g.size, float(param), p, ctypes.byref(lam), ctypes.byref(k), ctypes.byref(fl))
+        used = 0
+    else:
+        u = ctypes.c_int()
+        rc = fn(g, g.size, float(param), int(iters), p, ctypes.byref(lam), ctypes.byref(k),
+                ctypes.byref(u), ctypes.byref(fl))
+        used = u.value
+    if rc != 0:
+        raise RuntimeError(f"oracle solver failed ({rc})")
+    return Solution(p, lam.value, k.value, used, fl.value)
+
+
+def solve_exact(g, rho: float) -> Solution:
+    return _solve(_load().orc_exact_density, g, rho)
+
+
+def solve_variance(g, eps: float) -> Solution:
+    return _solve(_load().orc_exact_variance, g, eps)
+
+
+def solve_greedy(g, rho: float, iters: int = 2) -> Solution:
+    return _solve(_load().orc_greedy_alg3, g, rho, iters)
+
+
+def solve_greedy_scale(g, rho: float, iters: int = 2) -> Solution:
+    return _solve(_load().orc_greedy_scale, g, rho, iters)
+
+
+def solve(g, rho: float, solver: str = "greedy", iters: int = 2) -> Solution:
+    if solver == "greedy":
+        return solve_greedy(g, rho, iters)
+    if solver == "exact":
+        return solve_exact(g, rho)
+    raise ValueError(solver)
+
+
+def sample_compact(g, p, seed: int, cap: int | None = None):
+    """Returns (idx int32, val float32, nnz) with survivors in ascending index order."""
+    g = _f32(g)
+    p = np.ascontiguousarray(p, dtype=np.float64)
+    if p.shape != g.shape:
+        raise ValueError("p and g differ in shape")
+    cap = g.size if cap is None else int(cap)
+    idx = np.zeros(max(cap, 1), np.int32)
+    val = np.zeros(max(cap, 1), np.float32)
+    n = ctypes.c_int64()
+    _load().orc_sample(g, p, g.size, ctypes.c_uint64(seed), idx, val, cap, ctypes.byref(n))
+    m = min(n.value, cap)
+    return idx[:m].copy(), val[:m].copy(), n.value
+
+
+def sparsify(g, rho: float, solver: str = "greedy", iters: int = 2, seed: int = 0):
+    """Solve, then sample, amplify and compact one row. Returns (Solution, idx, val, nnz)."""
+    sol = solve(g, rho, solver, iters)
+    if sol.flags & FLAG_NONFINITE:
+        return sol, np.zeros(0, np.int32), np.zeros(0, np.float32), 0
+    idx, val, n = sample_compact(g, sol.p, seed)
+    return sol, idx, val, n
