@@ -1,0 +1,137 @@
+/*
+ * gspar -- gradient sparsification on AMD Instinct MI355X (gfx950).
+ *
+ * Implements the sparsifier of Wangni, Wang, Liu and Zhang, "Gradient Sparsification for
+ * Communication-Efficient Distributed Optimization" (arXiv 1710.09854):
+ *
+ *   1. keep probabilities p_i = min(lambda * |g_i|, 1)                      (Proposition 1)
+ *      with lambda chosen so that sum_i p_i = rho * d, either exactly
+ *      (Algorithm 2's criterion with a density budget, eqs. 5-7) or by the greedy rescaling of
+ *      Algorithm 3 run for a fixed number of steps;
+ *   2. Bernoulli selection Z_i with P(Z_i = 1) = p_i                         (Section 3)
+ *   3. amplification Q(g)_i = Z_i * g_i / p_i, i.e. g_i on the capped set and sign(g_i)/lambda
+ *      elsewhere (Section 3.3; the division-free form of Section 5.3);
+ *   4. compaction of the survivors into ascending (int32 index, fp32 value) pairs, the layout of
+ *      the Q_A / Q_B lists of Section 3.3 (eqs. 8-10).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers are DEVICE pointers unless marked (host). The caller owns every buffer, including
+ *    the workspace; the library never allocates or frees device memory.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream). All work is enqueued
+ *    on it; no call synchronises the host. Results (lambda, k, nnz, flags, p, idx, val) become
+ *    valid when the stream reaches them.
+ *  - A row is one worker's gradient (Algorithm 1, steps 4-5). Batched calls take rows of length d
+ *    with a leading dimension ld >= d (elements); row r is independent of every other row and
+ *    bit-identical to a single-row call on that row with the same rho and seed.
+ *  - Budget: B = rho * d computed in double. rho must lie in [0, 1].
+ *  - Solvers: GSPAR_EXACT (the lambda solving sum_i min(lambda|g_i|, 1) = B exactly, capped set
+ *    never splitting ties) or GSPAR_GREEDY (Algorithm 3 for `greedy_iters` rescale steps; the
+ *    paper's experiments use 2). Special cases: if B >= nnz(g), every nonzero is kept with
+ *    probability one (lambda = +inf, Q(g) = g); if rho = 0 nothing is kept (lambda = 0).
+ *  - Random source: coordinate i of a row with seed s uses word (i mod 4) of Philox4x32-10 with
+ *    key (s low 32, s high 32) and counter (floor(i/4) low 32, floor(i/4) high 32, 0, 0);
+ *    Z_i = 1 iff word < p_i * 2^32 (Salmon et al., SC'11 for the generator).
+ *  - Output is a pure function of (g bytes, d, rho, solver, greedy_iters, seed): identical across
+ *    runs, launch geometries and streams.
+ *  - Errors detectable on the host are returned synchronously before anything is enqueued:
+ *    GSPAR_ERR_ARG (NULL required pointer, d < 1 or d > 2^31 - 1, rows < 1, ld < d, rho outside
+ *    [0, 1] or NaN for scalar rho, greedy_iters outside [0, 64], unknown solver, negative
+ *    capacity), GSPAR_ERR_WORKSPACE (ws NULL or ws_bytes below gspar_workspace_bytes) and
+ *    GSPAR_ERR_HIP (a launch failed). Data-dependent conditions are reported per row in `flags`.
+ *  - Calls that share a workspace must be stream-ordered; concurrent calls need distinct
+ *    workspaces. The library keeps no other state (apart from the optional timing hook below).
+ */
+#ifndef GSPAR_H
+#define GSPAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GSPAR_OK = 0,
+  GSPAR_ERR_ARG = -1,
+  GSPAR_ERR_WORKSPACE = -2,
+  GSPAR_ERR_HIP = -3
+} gspar_status;
+
+typedef enum { GSPAR_GREEDY = 0, GSPAR_EXACT = 1 } gspar_solver;
+
+/* Per-row flag bits written to `flags[r]`. */
+enum {
+  GSPAR_FLAG_NONFINITE = 1, /* g holds Inf or NaN: nothing is sampled, nnz = 0, lambda = NaN  */
+  GSPAR_FLAG_OVERFLOW = 2,  /* more survivors than capacity: the first `capacity` pairs are
+                               written and nnz holds the true count                          */
+  GSPAR_FLAG_ALLZERO = 4,   /* g is identically zero: nnz = 0                                 */
+  GSPAR_FLAG_BADRHO = 8     /* (batched) rho[r] outside [0, 1] or NaN: row skipped, nnz = 0  */
+};
+
+/* Bytes of device workspace needed by a call on `rows` rows of length d with `solver`. The
+ * workspace needs no initialisation; 256-byte alignment is required. */
+size_t gspar_workspace_bytes(int64_t rows, int64_t d, int solver);
+
+/* A capacity that holds every survivor except with negligible probability:
+ * min(d, ceil(rho*d + 8*sqrt(rho*d) + 64)). The expected number of survivors is
+ * sum_i p_i <= rho*d (Section 3.1, expected sparsity). */
+int64_t gspar_capacity_hint(int64_t d, double rho);
+
+/* Keep probabilities of one row (Proposition 1 with lambda from the chosen solver).
+ *   g       [d] fp32 gradient (read only)
+ *   p       [d] fp32 output p_i = min(lambda |g_i|, 1), exactly 1 on the capped set; may be NULL
+ *           to compute lambda only
+ *   lambda  [1] fp64 output; k [1] int64 output (size of the capped set, may be NULL);
+ *   flags   [1] uint32 output (may be NULL). */
+int sparsify_probs(const float* g, int64_t d, double rho, int solver, int greedy_iters, float* p,
+                   double* lambda, int64_t* k, uint32_t* flags, void* ws, size_t ws_bytes,
+                   void* stream);
+
+/* Solve, sample, amplify and compact one row.
+ *   idx [capacity] int32 and val [capacity] fp32 receive the survivors in ascending index order:
+ *   val = g_i on the capped set (p_i = 1) and sign(g_i)/lambda rounded to fp32 elsewhere.
+ *   nnz [1] int64 receives the true survivor count (it may exceed capacity, see FLAG_OVERFLOW).
+ *   lambda, k and flags are optional outputs ([1] each, may be NULL). */
+int sparsify_sample_compact(const float* g, int64_t d, double rho, int solver, int greedy_iters,
+                            uint64_t seed, int32_t* idx, float* val, int64_t capacity,
+                            int64_t* nnz, double* lambda, int64_t* k, uint32_t* flags, void* ws,
+                            size_t ws_bytes, void* stream);
+
+/* Batched keep probabilities: rows x d gradients with leading dimension ld.
+ *   rho [rows] fp64 DEVICE array; p [rows*ld] or NULL; lambda [rows] (required), k [rows] and
+ *   flags [rows] optional. */
+int sparsify_probs_batched(const float* g, int64_t rows, int64_t d, int64_t ld, const double* rho,
+                           int solver, int greedy_iters, float* p, double* lambda, int64_t* k,
+                           uint32_t* flags, void* ws, size_t ws_bytes, void* stream);
+
+/* Batched solve + sample + compact. rho [rows] fp64 and seeds [rows] uint64 are DEVICE arrays.
+ * Row r writes its survivors to idx[r*cap_per_row ...] and val[r*cap_per_row ...] and its count
+ * to nnz[r]; lambda, k and flags ([rows] each) are optional. */
+int sparsify_sample_compact_batched(const float* g, int64_t rows, int64_t d, int64_t ld,
+                                    const double* rho, int solver, int greedy_iters,
+                                    const uint64_t* seeds, int32_t* idx, float* val,
+                                    int64_t cap_per_row, int64_t* nnz, double* lambda, int64_t* k,
+                                    uint32_t* flags, void* ws, size_t ws_bytes, void* stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* gspar_status_string(int status);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int gspar_version(void);
+
+/* Measurement hook for benchmarks (process-global, not thread-safe): while armed, every launch
+ * of kernel `which` (0 = sample/compact, 1 = statistics pass, 2 = probabilities) is bracketed by
+ * a pair of HIP timing events on its stream, for up to `max_launches` launches.
+ * gspar_timing_read synchronises on the last event and returns the summed kernel time in ms and
+ * the number of bracketed launches; gspar_timing_disarm releases the events. */
+int gspar_timing_arm(int which, int max_launches);
+int gspar_timing_read(double* total_ms, int* launches);
+int gspar_timing_disarm(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GSPAR_H */

@@ -60,6 +60,8 @@ def _load():
     lib.orc_philox4x32_10.restype = None
     lib.orc_words.argtypes = [ctypes.c_uint64, i64, u32p]
     lib.orc_words.restype = None
+    lib.orc_words_at.argtypes = [ctypes.c_uint64, i64, np.ctypeslib.ndpointer(np.int64, flags="C_CONTIGUOUS"), u32p]
+    lib.orc_words_at.restype = None
     lib.orc_exact_sum.argtypes = [f64p, i64]
     lib.orc_exact_sum.restype = ctypes.c_double
     lib.orc_exact_density.argtypes = [f32p, i64, ctypes.c_double, f64p, pd, pi64, pu32]
@@ -111,6 +113,14 @@ def words(seed: int, d: int) -> np.ndarray:
     """x_i for i < d: word (i mod 4) of Philox4x32-10(key=seed, counter=(i//4, 0, 0))."""
     x = np.zeros(d, np.uint32)
     _load().orc_words(ctypes.c_uint64(seed), d, x)
+    return x
+
+
+def words_at(seed: int, idx) -> np.ndarray:
+    """x_i for the given coordinates i (same layout as ``words``)."""
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    x = np.zeros(idx.size, np.uint32)
+    _load().orc_words_at(ctypes.c_uint64(seed), idx.size, idx, x)
     return x
 
 

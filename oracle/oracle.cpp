@@ -201,6 +201,10 @@ void orc_words(uint64_t seed, int64_t d, uint32_t* x) {
   for (int64_t i = 0; i < d; ++i) x[i] = word_for(seed, i);
 }
 
+void orc_words_at(uint64_t seed, int64_t n, const int64_t* idx, uint32_t* x) {
+  for (int64_t j = 0; j < n; ++j) x[j] = word_for(seed, idx[j]);
+}
+
 double orc_exact_sum(const double* x, int64_t n) {
   Exact e;
   for (int64_t i = 0; i < n; ++i) e.add(x[i]);

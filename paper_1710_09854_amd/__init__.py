@@ -1,0 +1,325 @@
+"""Python binding of libgspar (gradient sparsification on MI355X).
+
+Argument marshalling only: every step of the sparsifier runs in the HIP kernels of
+``csrc/gspar.hip`` behind the C ABI declared in ``include/gspar.h``; PyTorch provides device
+memory and the current stream. There is no CPU fallback: every entry point raises if the
+library has not been built (``__graft_entry__.build()`` or ``python -m paper_1710_09854_amd.build``).
+
+Entry points mirror the C ABI:
+
+* ``sparsify_probs(g, rho, solver, iters)``                  -> Probs(p, lam, k, flags)
+* ``sparsify_sample_compact(g, rho, seed, solver, iters)``   -> Sparse(idx, val, nnz, lam, k, flags)
+* ``sparsify_probs_batched(g2d, rho, solver, iters)``
+* ``sparsify_sample_compact_batched(g2d, rho, seeds, ...)``
+* ``Plan``: a preallocated batched sample/compact call for timing loops.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgspar.so")
+
+GREEDY = 0
+EXACT = 1
+FLAG_NONFINITE = 1
+FLAG_OVERFLOW = 2
+FLAG_ALLZERO = 4
+FLAG_BADRHO = 8
+FLAG_INTERNAL = 16
+
+OK = 0
+ERR_ARG = -1
+ERR_WORKSPACE = -2
+ERR_HIP = -3
+
+_lib = None
+
+
+def lib():
+    """The loaded C library; raises if it was never built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build the HIP library first "
+                           "(python -m paper_1710_09854_amd.build)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, u64, f64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_int
+    L.gspar_workspace_bytes.argtypes = [i64, i64, i32]
+    L.gspar_workspace_bytes.restype = ctypes.c_size_t
+    L.gspar_capacity_hint.argtypes = [i64, f64]
+    L.gspar_capacity_hint.restype = i64
+    L.sparsify_probs.argtypes = [vp, i64, f64, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_probs.restype = i32
+    L.sparsify_sample_compact.argtypes = [vp, i64, f64, i32, i32, u64, vp, vp, i64, vp, vp, vp, vp, vp,
+                                          ctypes.c_size_t, vp]
+    L.sparsify_sample_compact.restype = i32
+    L.sparsify_probs_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, vp, vp,
+                                         ctypes.c_size_t, vp]
+    L.sparsify_probs_batched.restype = i32
+    L.sparsify_sample_compact_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp, vp,
+                                                  vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_compact_batched.restype = i32
+    L.gspar_status_string.argtypes = [i32]
+    L.gspar_status_string.restype = ctypes.c_char_p
+    L.gspar_version.argtypes = []
+    L.gspar_version.restype = i32
+    L.gspar_timing_arm.argtypes = [i32, i32]
+    L.gspar_timing_arm.restype = i32
+    L.gspar_timing_read.argtypes = [ctypes.POINTER(f64), ctypes.POINTER(i32)]
+    L.gspar_timing_read.restype = i32
+    L.gspar_timing_disarm.argtypes = []
+    L.gspar_timing_disarm.restype = i32
+    _lib = L
+    return L
+
+
+def _solver_id(solver) -> int:
+    if solver in ("greedy", GREEDY):
+        return GREEDY
+    if solver in ("exact", EXACT):
+        return EXACT
+    raise ValueError(f"unknown solver {solver!r}")
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        msg = lib().gspar_status_string(rc).decode()
+        raise RuntimeError(f"{what} failed: {msg} ({rc})")
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def workspace_bytes(rows: int, d: int, solver="greedy") -> int:
+    return int(lib().gspar_workspace_bytes(rows, d, _solver_id(solver)))
+
+
+def capacity_hint(d: int, rho: float) -> int:
+    return int(lib().gspar_capacity_hint(d, rho))
+
+
+class Workspace:
+    """Grow-only device workspace (the library itself never allocates)."""
+
+    def __init__(self, device=None):
+        self.device = torch.device("cuda" if device is None else device)
+        self.buf = None
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+_default_ws: dict = {}
+
+
+def _ws(ws, device, nbytes):
+    if ws is None:
+        key = torch.device(device).index if torch.device(device).index is not None else torch.cuda.current_device()
+        ws = _default_ws.setdefault(key, Workspace(device))
+    buf = ws.get(nbytes)
+    return buf, buf.numel()
+
+
+def _as_row(g):
+    if not (isinstance(g, torch.Tensor) and g.is_cuda and g.dtype == torch.float32):
+        raise TypeError("g must be a float32 CUDA tensor")
+    if g.dim() != 1 or not g.is_contiguous():
+        raise ValueError("g must be a contiguous 1-D tensor")
+    return g
+
+
+def _as_rows(g):
+    if not (isinstance(g, torch.Tensor) and g.is_cuda and g.dtype == torch.float32):
+        raise TypeError("g must be a float32 CUDA tensor")
+    if g.dim() != 2 or g.stride(1) != 1:
+        raise ValueError("g must be 2-D with unit stride along a row")
+    return g
+
+
+@dataclass
+class Probs:
+    p: torch.Tensor | None
+    lam: torch.Tensor
+    k: torch.Tensor
+    flags: torch.Tensor
+
+
+@dataclass
+class Sparse:
+    idx: torch.Tensor
+    val: torch.Tensor
+    nnz: torch.Tensor
+    lam: torch.Tensor
+    k: torch.Tensor
+    flags: torch.Tensor
+
+
+def sparsify_probs(g, rho: float, solver="greedy", iters: int = 2, want_p: bool = True, workspace=None,
+                   stream=None) -> Probs:
+    g = _as_row(g)
+    d = g.numel()
+    dev = g.device
+    p = torch.empty(d, dtype=torch.float32, device=dev) if want_p else None
+    lam = torch.empty(1, dtype=torch.float64, device=dev)
+    k = torch.empty(1, dtype=torch.int64, device=dev)
+    fl = torch.empty(1, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid))
+    rc = lib().sparsify_probs(g.data_ptr(), d, float(rho), sid, int(iters), _ptr(p), lam.data_ptr(),
+                              k.data_ptr(), fl.data_ptr(), buf.data_ptr(), nb, _stream(stream))
+    _check(rc, "sparsify_probs")
+    return Probs(p, lam, k, fl)
+
+
+def sparsify_sample_compact(g, rho: float, seed: int = 0, solver="greedy", iters: int = 2,
+                            capacity: int | None = None, workspace=None, stream=None) -> Sparse:
+    g = _as_row(g)
+    d = g.numel()
+    dev = g.device
+    cap = capacity_hint(d, rho) if capacity is None else int(capacity)
+    idx = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    val = torch.empty(max(cap, 1), dtype=torch.float32, device=dev)
+    nnz = torch.empty(1, dtype=torch.int64, device=dev)
+    lam = torch.empty(1, dtype=torch.float64, device=dev)
+    k = torch.empty(1, dtype=torch.int64, device=dev)
+    fl = torch.empty(1, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid))
+    rc = lib().sparsify_sample_compact(g.data_ptr(), d, float(rho), sid, int(iters),
+                                       int(seed) & 0xFFFFFFFFFFFFFFFF, idx.data_ptr(), val.data_ptr(), cap,
+                                       nnz.data_ptr(), lam.data_ptr(), k.data_ptr(), fl.data_ptr(),
+                                       buf.data_ptr(), nb, _stream(stream))
+    _check(rc, "sparsify_sample_compact")
+    return Sparse(idx[:cap], val[:cap], nnz, lam, k, fl)
+
+
+def _rho_dev(rho, rows, dev):
+    if isinstance(rho, torch.Tensor):
+        r = rho.to(device=dev, dtype=torch.float64).contiguous()
+    else:
+        if isinstance(rho, (int, float)):
+            rho = [float(rho)] * rows
+        r = torch.tensor(list(rho), dtype=torch.float64, device=dev)
+    if r.numel() != rows:
+        raise ValueError("rho needs one value per row")
+    return r
+
+
+def _seeds_dev(seeds, rows, dev):
+    if isinstance(seeds, torch.Tensor):
+        s = seeds.to(device=dev, dtype=torch.int64).contiguous()
+    else:
+        vals = [int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds]
+        vals = [v - (1 << 64) if v >= (1 << 63) else v for v in vals]  # same 64 bits, signed view
+        s = torch.tensor(vals, dtype=torch.int64, device=dev)
+    if s.numel() != rows:
+        raise ValueError("seeds need one value per row")
+    return s
+
+
+def sparsify_probs_batched(g, rho, solver="greedy", iters: int = 2, want_p: bool = True, workspace=None,
+                           stream=None) -> Probs:
+    g = _as_rows(g)
+    rows, d = g.shape
+    ld = g.stride(0)
+    dev = g.device
+    r = _rho_dev(rho, rows, dev)
+    p = torch.empty((rows, ld), dtype=torch.float32, device=dev) if want_p else None
+    lam = torch.empty(rows, dtype=torch.float64, device=dev)
+    k = torch.empty(rows, dtype=torch.int64, device=dev)
+    fl = torch.empty(rows, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid))
+    rc = lib().sparsify_probs_batched(g.data_ptr(), rows, d, ld, r.data_ptr(), sid, int(iters), _ptr(p),
+                                      lam.data_ptr(), k.data_ptr(), fl.data_ptr(), buf.data_ptr(), nb,
+                                      _stream(stream))
+    _check(rc, "sparsify_probs_batched")
+    return Probs(None if p is None else p[:, :d], lam, k, fl)
+
+
+class Plan:
+    """Preallocated batched solve + sample + compact: inputs, outputs and workspace stay resident,
+    so a timing loop measures only the library's kernels."""
+
+    def __init__(self, rows: int, d: int, ld: int | None = None, solver="greedy", iters: int = 2,
+                 cap_per_row: int | None = None, rho_for_cap: float = 1.0, device="cuda"):
+        self.rows, self.d = rows, d
+        self.ld = d if ld is None else ld
+        self.sid = _solver_id(solver)
+        self.iters = int(iters)
+        self.cap = capacity_hint(d, rho_for_cap) if cap_per_row is None else int(cap_per_row)
+        dev = torch.device(device)
+        self.idx = torch.empty((rows, max(self.cap, 1)), dtype=torch.int32, device=dev)
+        self.val = torch.empty((rows, max(self.cap, 1)), dtype=torch.float32, device=dev)
+        self.nnz = torch.empty(rows, dtype=torch.int64, device=dev)
+        self.lam = torch.empty(rows, dtype=torch.float64, device=dev)
+        self.k = torch.empty(rows, dtype=torch.int64, device=dev)
+        self.flags = torch.empty(rows, dtype=torch.int32, device=dev)
+        self.ws = torch.empty(workspace_bytes(rows, d, self.sid), dtype=torch.uint8, device=dev)
+
+    def run(self, g, rho_dev, seeds_dev, stream=None):
+        rc = lib().sparsify_sample_compact_batched(
+            g.data_ptr(), self.rows, self.d, self.ld, rho_dev.data_ptr(), self.sid, self.iters,
+            seeds_dev.data_ptr(), self.idx.data_ptr(), self.val.data_ptr(), self.cap, self.nnz.data_ptr(),
+            self.lam.data_ptr(), self.k.data_ptr(), self.flags.data_ptr(), self.ws.data_ptr(),
+            self.ws.numel(), _stream(stream))
+        _check(rc, "sparsify_sample_compact_batched")
+
+
+def sparsify_sample_compact_batched(g, rho, seeds, solver="greedy", iters: int = 2,
+                                    cap_per_row: int | None = None, workspace=None, stream=None) -> Sparse:
+    g = _as_rows(g)
+    rows, d = g.shape
+    ld = g.stride(0)
+    dev = g.device
+    r = _rho_dev(rho, rows, dev)
+    s = _seeds_dev(seeds, rows, dev)
+    if cap_per_row is None:
+        rmax = float(r.max().item()) if rows else 0.0
+        cap_per_row = capacity_hint(d, min(max(rmax, 0.0), 1.0))
+    cap = int(cap_per_row)
+    idx = torch.empty((rows, max(cap, 1)), dtype=torch.int32, device=dev)
+    val = torch.empty((rows, max(cap, 1)), dtype=torch.float32, device=dev)
+    nnz = torch.empty(rows, dtype=torch.int64, device=dev)
+    lam = torch.empty(rows, dtype=torch.float64, device=dev)
+    k = torch.empty(rows, dtype=torch.int64, device=dev)
+    fl = torch.empty(rows, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid))
+    rc = lib().sparsify_sample_compact_batched(g.data_ptr(), rows, d, ld, r.data_ptr(), sid, int(iters),
+                                               s.data_ptr(), idx.data_ptr(), val.data_ptr(), cap, nnz.data_ptr(),
+                                               lam.data_ptr(), k.data_ptr(), fl.data_ptr(), buf.data_ptr(), nb,
+                                               _stream(stream))
+    _check(rc, "sparsify_sample_compact_batched")
+    return Sparse(idx[:, :cap], val[:, :cap], nnz, lam, k, fl)
+
+
+class KernelTimer:
+    """Brackets every launch of one kernel (0 sample/compact, 1 statistics, 2 probabilities) with
+    HIP events on its stream; ``read()`` returns (total ms, launches)."""
+
+    def __init__(self, which: int, max_launches: int):
+        _check(lib().gspar_timing_arm(which, max_launches), "gspar_timing_arm")
+
+    def read(self):
+        ms = ctypes.c_double()
+        n = ctypes.c_int()
+        _check(lib().gspar_timing_read(ctypes.byref(ms), ctypes.byref(n)), "gspar_timing_read")
+        return ms.value, n.value
+
+    def close(self):
+        lib().gspar_timing_disarm()

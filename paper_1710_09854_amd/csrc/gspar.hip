@@ -1,0 +1,1409 @@
+// gspar: gradient sparsification (Wangni, Wang, Liu, Zhang; arXiv 1710.09854) for MI355X / gfx950.
+//
+// Pipeline per call (all launches on the caller's stream, no host synchronisation):
+//   k_init     clears the per-call workspace and writes each row's budget B = rho*d.
+//   k_stats    one streaming pass over g: a 4096-bin LDS histogram of the magnitude bit pattern
+//              (count, exact significand sum, max) per workgroup, flushed as per-binade totals;
+//              the last workgroup of each row runs the solver (Proposition 1; Algorithm 2's
+//              criterion with a density budget, or Algorithm 3).
+//   k_refine   (launched a fixed number of times, exits at once unless the solver asked for it)
+//              histograms only the magnitudes inside one binade (4096 sub-bins) or inside one
+//              sub-bin (2048 single bit patterns), so every threshold the solvers need is resolved
+//              exactly, then resumes the solver.
+//   k_sample   one streaming pass: Philox4x32-10 per group of four coordinates, Bernoulli selection,
+//              amplification to g_i or sign(g_i)/lambda, order-preserving compaction with a
+//              decoupled look-back across ticketed tiles.
+//   k_probs    (probabilities entry points) writes p_i = min(lambda |g_i|, 1).
+//
+// Sums of magnitudes are exact: a magnitude's bit pattern (its "key") fixes its binade, bins never
+// straddle a binade, so per-bin sums of 24-bit significands are exact integers and are combined
+// in a 320-bit fixed-point accumulator (unit 2^-149) that is rounded once to double. Hence lambda,
+// the capped set and every decision are independent of the launch geometry and of atomic order.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "gspar.h"
+
+#define GS_HD __host__ __device__ __forceinline__
+
+namespace gspar {
+
+constexpr uint32_t kKeyInf = 0x7F800000u;   // bit pattern of +inf: keys >= this are non-finite
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+constexpr int kNT = 512;                    // threads of the histogram / solver workgroups
+constexpr int kFine = 4096;                 // LDS bins of the statistics pass (key >> 19)
+constexpr int kB1 = 256;                    // level 1: one bin per binade (key >> 23)
+constexpr int kB2 = 4096;                   // level 2: one binade, 2^11 keys per bin
+constexpr int kB3 = 2048;                   // level 3: one level-2 bin, one key per bin
+constexpr int kTileThreads = 256;
+constexpr int kTileGroups = 4;              // float4 groups per thread per tile
+constexpr int kTileElems = kTileThreads * kTileGroups * 4;
+constexpr int kMaxIters = 64;
+constexpr int64_t kMaxChunk = (1 << 20) - 4;  // LDS packing holds < 2^20 elements per workgroup
+constexpr uint32_t kSpinLimit = 1u << 22;
+
+enum : uint32_t { kFlagInternal = 16 };
+
+// ------------------------------------------------------------------------------------------
+// 320-bit fixed point, value = x * 2^-149 (the smallest subnormal float).
+// ------------------------------------------------------------------------------------------
+struct Fx {
+  uint64_t w[5];
+};
+
+GS_HD Fx fx_zero() {
+  Fx r;
+  for (int i = 0; i < 5; ++i) r.w[i] = 0;
+  return r;
+}
+GS_HD void fx_add(Fx& a, const Fx& b) {
+  uint64_t c = 0;
+  for (int i = 0; i < 5; ++i) {
+    uint64_t s = a.w[i] + b.w[i];
+    uint64_t c1 = s < a.w[i];
+    uint64_t s2 = s + c;
+    uint64_t c2 = s2 < s;
+    a.w[i] = s2;
+    c = c1 | c2;
+  }
+}
+GS_HD Fx fx_sub(const Fx& a, const Fx& b) {  // requires a >= b
+  Fx r;
+  uint64_t br = 0;
+  for (int i = 0; i < 5; ++i) {
+    uint64_t d1 = a.w[i] - b.w[i];
+    uint64_t b1 = a.w[i] < b.w[i];
+    uint64_t d2 = d1 - br;
+    uint64_t b2 = d1 < br;
+    r.w[i] = d2;
+    br = b1 | b2;
+  }
+  return r;
+}
+GS_HD Fx fx_shifted(uint64_t v, int s) {  // v * 2^s, s in [0, 253]
+  Fx r = fx_zero();
+  int li = s >> 6, off = s & 63;
+  r.w[li] = v << off;
+  if (off && li + 1 < 5) r.w[li + 1] = v >> (64 - off);
+  return r;
+}
+GS_HD bool fx_bit(const Fx& a, int k) { return (a.w[k >> 6] >> (k & 63)) & 1; }
+GS_HD bool fx_any_below(const Fx& a, int k) {  // any set bit at positions [0, k)
+  if (k <= 0) return false;
+  int li = k >> 6, off = k & 63;
+  for (int i = 0; i < li && i < 5; ++i)
+    if (a.w[i]) return true;
+  if (li < 5 && off && (a.w[li] & ((1ull << off) - 1))) return true;
+  return false;
+}
+// Round to the nearest double, ties to even.
+GS_HD double fx_to_double(const Fx& a) {
+  int top = -1;
+  for (int i = 4; i >= 0; --i)
+    if (a.w[i]) {
+      top = i * 64 + 63 - __builtin_clzll(a.w[i]);
+      break;
+    }
+  if (top < 0) return 0.0;
+  if (top < 53) return ldexp((double)a.w[0], -149);
+  int lo = top - 52;
+  int li = lo >> 6, off = lo & 63;
+  uint64_t m = a.w[li] >> off;
+  if (off && li + 1 < 5) m |= a.w[li + 1] << (64 - off);
+  m &= (1ull << 53) - 1;
+  bool rnd = fx_bit(a, lo - 1);
+  bool sticky = fx_any_below(a, lo - 1);
+  if (rnd && (sticky || (m & 1))) m += 1;
+  return ldexp((double)m, lo - 149);
+}
+
+// ------------------------------------------------------------------------------------------
+// Magnitude keys.
+// ------------------------------------------------------------------------------------------
+GS_HD uint32_t key_of(float x) {
+  uint32_t u;
+  memcpy(&u, &x, 4);
+  return u & 0x7FFFFFFFu;
+}
+GS_HD double key_value(uint32_t k) {
+  float f;
+  memcpy(&f, &k, 4);
+  return (double)f;
+}
+GS_HD uint64_t key_sig(uint32_t key) {  // integer significand: value = sig * 2^(max(e,1) - 150)
+  uint32_t e = key >> 23, m = key & 0x7FFFFFu;
+  return e ? (uint64_t)(m | 0x800000u) : (uint64_t)m;
+}
+GS_HD int binade_shift(int e) { return (e > 0 ? e : 1) - 1; }  // in units of 2^-149
+
+// Smallest key t with fl(lambda * value(t)) >= 1, i.e. capped <=> key >= t for p = min(lambda a, 1).
+// kKeyInf when no finite magnitude is capped.
+GS_HD uint32_t cap_key(double lam) {
+  if (!(lam > 0.0)) return kKeyInf;
+  if (lam == INFINITY) return 1;
+  double x = 1.0 / lam;
+  uint32_t k;
+  if (x >= 3.4028234663852886e38) {
+    k = kKeyInf;
+  } else {
+    k = key_of((float)x);
+    if (k == 0) k = 1;
+  }
+  for (int it = 0; it < 4 && k > 1 && lam * key_value(k - 1) >= 1.0; ++it) --k;
+  for (int it = 0; it < 4 && k < kKeyInf && !(lam * key_value(k) >= 1.0); ++it) ++k;
+  return k;
+}
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32->64 products on
+// counter words 0 and 2, high halves crossed with words 1, 3 and the round key; the key advances
+// by the golden-ratio and sqrt(3)-1 Weyl increments after each round.
+GS_HD void philox10(uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    uint64_t m0 = (uint64_t)c0 * 0xD2511F53u;
+    uint64_t m1 = (uint64_t)c2 * 0xCD9E8D57u;
+    uint32_t x0 = (uint32_t)(m1 >> 32) ^ c1 ^ k0;
+    uint32_t x2 = (uint32_t)(m0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)m1;
+    c3 = (uint32_t)m0;
+    c0 = x0;
+    c2 = x2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Workspace.
+// ------------------------------------------------------------------------------------------
+struct alignas(256) RowCtl {
+  double B;          // rho * d
+  double lam;        // greedy: current lambda; final: lambda of Proposition 1
+  Fx S;              // exact sum of |g|
+  Fx fbW;            // exact solver: capped sum of the best candidate found so far
+  uint64_t fbK;      // exact solver: capped count of that candidate
+  uint64_t zeros;    // zero entries of the row (statistics pass)
+  uint64_t kcount;   // capped coordinates counted by the probabilities pass
+  float inv_lam;     // fl32(1/lambda): the amplified value off the capped set
+  uint32_t fbTcap;   // exact solver: candidate's capped threshold key
+  uint32_t fbValid;
+  uint32_t tcap;     // final: coordinate capped (p = 1) iff key >= tcap
+  uint32_t flags;
+  uint32_t need;     // 0: none; 2 / 3: a level-2 / level-3 pass is requested
+  uint32_t done;     // 1 once lambda and tcap are final
+  uint32_t arrive;   // workgroups of the current histogram pass that have flushed
+  uint32_t parrive;  // workgroups of the probabilities pass that have finished
+  uint32_t l2exp;    // binade of the level-2 window (kNone: none)
+  uint32_t l3base;   // first key of the level-3 window (kNone: none)
+  int32_t iter;      // greedy rescale steps taken
+  int32_t stage;     // 0 before the first solve; exact solver: next level to examine
+  int32_t solver;
+  int32_t T;
+};
+static_assert(sizeof(RowCtl) == 256, "RowCtl layout");
+
+struct Hist1 {
+  uint64_t cnt[kB1];
+  uint64_t sig[kB1];
+  uint32_t mx[kB1];
+};
+struct Hist2 {
+  uint64_t cnt[kB2];
+  uint64_t sig[kB2];
+  uint32_t mx[kB2];
+};
+struct Hist3 {
+  uint64_t cnt[kB3];
+  uint64_t sig[kB3];
+  uint32_t mx[kB3];
+};
+
+GS_HD size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t ctl, h1, h2, h3, status, total;
+  int64_t tiles;  // tiles per row of the sample pass
+};
+
+GS_HD Layout layout_of(int64_t rows, int64_t d) {
+  Layout L;
+  L.tiles = (d + kTileElems - 1) / kTileElems;
+  size_t off = 256;  // header: ticket counter
+  L.ctl = off;
+  off += align256((size_t)rows * sizeof(RowCtl));
+  L.h1 = off;
+  off += align256((size_t)rows * sizeof(Hist1));
+  L.h2 = off;
+  off += align256((size_t)rows * sizeof(Hist2));
+  L.h3 = off;
+  off += align256((size_t)rows * sizeof(Hist3));
+  L.status = off;
+  off += align256((size_t)rows * (size_t)L.tiles * sizeof(uint64_t));
+  L.total = off;
+  return L;
+}
+
+struct Args {
+  const float* g;
+  int64_t rows, d, ld;
+  const double* rho_dev;  // per-row densities, or nullptr to use `rho`
+  double rho;
+  const uint64_t* seed_dev;
+  uint64_t seed;
+  int solver, T;
+  char* ws;
+  Layout lay;
+  int nb;          // workgroups per row of the histogram passes
+  int64_t chunk;   // elements per histogram workgroup (multiple of 4)
+  int32_t* idx;
+  float* val;
+  int64_t cap;
+  int64_t* nnz;
+  double* lam_out;
+  int64_t* k_out;
+  uint32_t* flags_out;
+  float* p;
+};
+
+__device__ __forceinline__ RowCtl* ctl_of(const Args& a, int64_t r) {
+  return reinterpret_cast<RowCtl*>(a.ws + a.lay.ctl) + r;
+}
+__device__ __forceinline__ Hist1* h1_of(const Args& a, int64_t r) {
+  return reinterpret_cast<Hist1*>(a.ws + a.lay.h1) + r;
+}
+__device__ __forceinline__ Hist2* h2_of(const Args& a, int64_t r) {
+  return reinterpret_cast<Hist2*>(a.ws + a.lay.h2) + r;
+}
+__device__ __forceinline__ Hist3* h3_of(const Args& a, int64_t r) {
+  return reinterpret_cast<Hist3*>(a.ws + a.lay.h3) + r;
+}
+__device__ __forceinline__ uint64_t* status_of(const Args& a) {
+  return reinterpret_cast<uint64_t*>(a.ws + a.lay.status);
+}
+
+__device__ __forceinline__ uint64_t ald64(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ald32(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Four consecutive coordinates 4q..4q+3 of a row; entries at or beyond `end` read as 0 and are
+// flagged invalid in the returned mask (bit c set = coordinate 4q+c exists).
+template <bool VEC>
+__device__ __forceinline__ uint32_t load4(const float* __restrict__ row, int64_t q, int64_t end, float v[4]) {
+  int64_t i = 4 * q;
+  if (VEC && i + 3 < end) {
+    float4 x = *reinterpret_cast<const float4*>(row + i);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    return 0xF;
+  }
+  uint32_t m = 0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    bool ok = i + c < end;
+    v[c] = ok ? row[i + c] : 0.0f;
+    m |= (uint32_t)ok << c;
+  }
+  return m;
+}
+
+// ------------------------------------------------------------------------------------------
+// Block-wide helpers for the solver workgroup (kNT threads, uniform control flow).
+// ------------------------------------------------------------------------------------------
+struct HistLds {
+  unsigned long long pk[kFine];  // (count << 44) | significand sum
+  uint32_t mx[kFine];
+};
+struct BinInfo {
+  uint64_t Kab;  // count of keys strictly above the bin (including above the window)
+  Fx Wab;        // their exact sum
+  uint64_t cnt;
+  Fx Wb;
+  uint32_t mx;
+};
+struct SolveLds {
+  uint64_t sk[2][kNT];
+  Fx sw[2][kNT];
+  int ired[kNT / 64];
+  BinInfo bi;
+  RowCtl c;  // working copy of the row's control block
+  int flag;
+};
+union SharedU {
+  HistLds h;
+  SolveLds s;
+};
+
+__device__ int block_max(SolveLds& s, int v) {
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+  if ((threadIdx.x & 63) == 0) s.ired[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int r = s.ired[0];
+  for (int i = 1; i < kNT / 64; ++i) r = max(r, s.ired[i]);
+  __syncthreads();
+  return r;
+}
+__device__ int block_min(SolveLds& s, int v) {
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
+  if ((threadIdx.x & 63) == 0) s.ired[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int r = s.ired[0];
+  for (int i = 1; i < kNT / 64; ++i) r = min(r, s.ired[i]);
+  __syncthreads();
+  return r;
+}
+
+// Exclusive suffix scan over thread index: (exK, exW) = sum over threads t' > t.
+__device__ void suffix_scan(SolveLds& s, uint64_t k, const Fx& w, uint64_t& exK, Fx& exW) {
+  const int r = kNT - 1 - (int)threadIdx.x;
+  s.sk[0][r] = k;
+  s.sw[0][r] = w;
+  __syncthreads();
+  int cur = 0;
+  for (int off = 1; off < kNT; off <<= 1) {
+    uint64_t kk = s.sk[cur][r];
+    Fx ww = s.sw[cur][r];
+    if (r >= off) {
+      kk += s.sk[cur][r - off];
+      fx_add(ww, s.sw[cur][r - off]);
+    }
+    s.sk[cur ^ 1][r] = kk;
+    s.sw[cur ^ 1][r] = ww;
+    __syncthreads();
+    cur ^= 1;
+  }
+  exK = s.sk[cur][r] - k;
+  exW = fx_sub(s.sw[cur][r], w);
+  __syncthreads();
+}
+
+// One histogram level: bins b = 0..nbins-1, thread t owns bins [t*per, t*per + per).
+struct Lvl {
+  const uint64_t* cnt;
+  const uint64_t* sig;
+  const uint32_t* mx;
+  int nbins, per;
+  int E;  // binade of every bin, or -1 when the bin index is the binade (level 1)
+  uint64_t Kaw;
+  Fx Waw;  // aggregates of keys above the window
+};
+struct Walk {
+  uint64_t exK;
+  Fx exW;
+};
+
+__device__ __forceinline__ Fx lvl_binW(const Lvl& L, int b, uint64_t sg) {
+  return fx_shifted(sg, binade_shift(L.E < 0 ? b : L.E));
+}
+
+__device__ void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
+  uint64_t k = 0;
+  Fx W = fx_zero();
+  const int b0 = threadIdx.x * L.per;
+  for (int j = 0; j < L.per; ++j) {
+    int b = b0 + j;
+    if (b < L.nbins) {
+      uint64_t c = ald64(&L.cnt[b]);
+      if (c) {
+        k += c;
+        fx_add(W, lvl_binW(L, b, ald64(&L.sig[b])));
+      }
+    }
+  }
+  suffix_scan(s, k, W, w.exK, w.exW);
+  w.exK += L.Kaw;
+  fx_add(w.exW, L.Waw);
+}
+
+// Aggregates above bin b and the bin's own totals, broadcast to every thread (b uniform).
+__device__ void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo& out) {
+  if ((int)threadIdx.x == b / L.per) {
+    uint64_t K = w.exK;
+    Fx W = w.exW;
+    for (int j = L.per - 1; j >= 0; --j) {
+      int bb = threadIdx.x * L.per + j;
+      if (bb >= L.nbins) continue;
+      uint64_t c = ald64(&L.cnt[bb]);
+      Fx wb = c ? lvl_binW(L, bb, ald64(&L.sig[bb])) : fx_zero();
+      if (bb == b) {
+        s.bi.Kab = K;
+        s.bi.Wab = W;
+        s.bi.cnt = c;
+        s.bi.Wb = wb;
+        s.bi.mx = ald32(&L.mx[bb]);
+        break;
+      }
+      K += c;
+      fx_add(W, wb);
+    }
+  }
+  __syncthreads();
+  out = s.bi;
+  __syncthreads();
+}
+
+// Exact solver step on one level: b1 = highest non-empty bin whose maximum v satisfies
+// (B - #{a > v}) * v <= fl(S - sum{a > v}) (the density-budget form of Algorithm 2's criterion,
+// evaluated at a data value), b2 = lowest non-empty bin above b1 (INT_MAX if none).
+__device__ void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLds& s, int& b1,
+                          int& b2) {
+  int best = -1;
+  uint64_t K = w.exK;
+  Fx W = w.exW;
+  for (int j = L.per - 1; j >= 0 && best < 0; --j) {
+    int b = threadIdx.x * L.per + j;
+    if (b >= L.nbins) continue;
+    uint64_t c = ald64(&L.cnt[b]);
+    if (!c) continue;
+    double v = key_value(ald32(&L.mx[b]));
+    double T1 = fx_to_double(fx_sub(S, W));
+    if ((B - (double)K) * v <= T1) best = b;
+    K += c;
+    fx_add(W, lvl_binW(L, b, ald64(&L.sig[b])));
+  }
+  b1 = block_max(s, best);
+  int lowest = INT_MAX;
+  for (int j = 0; j < L.per; ++j) {
+    int b = threadIdx.x * L.per + j;
+    if (b < L.nbins && b > b1 && ald64(&L.cnt[b])) {
+      lowest = b;
+      break;
+    }
+  }
+  b2 = block_min(s, lowest);
+}
+
+// ------------------------------------------------------------------------------------------
+// The per-row solver. Runs in the last workgroup of a histogram pass, all kNT threads.
+// ------------------------------------------------------------------------------------------
+struct Solver {
+  const Args& a;
+  int64_t row;
+  RowCtl* gc;
+  SolveLds& s;
+  Hist1* h1;
+  Hist2* h2;
+  Hist3* h3;
+
+  __device__ Lvl lvl1() const {
+    Lvl L;
+    L.cnt = h1->cnt; L.sig = h1->sig; L.mx = h1->mx;
+    L.nbins = kB1; L.per = 1; L.E = -1; L.Kaw = 0; L.Waw = fx_zero();
+    return L;
+  }
+  __device__ Lvl lvl2(uint32_t E, uint64_t Kaw, const Fx& Waw) const {
+    Lvl L;
+    L.cnt = h2->cnt; L.sig = h2->sig; L.mx = h2->mx;
+    L.nbins = kB2; L.per = kB2 / kNT; L.E = (int)E; L.Kaw = Kaw; L.Waw = Waw;
+    return L;
+  }
+  __device__ Lvl lvl3(uint32_t E, uint64_t Kaw, const Fx& Waw) const {
+    Lvl L;
+    L.cnt = h3->cnt; L.sig = h3->sig; L.mx = h3->mx;
+    L.nbins = kB3; L.per = kB3 / kNT; L.E = (int)E; L.Kaw = Kaw; L.Waw = Waw;
+    return L;
+  }
+
+  __device__ void finalize(double lam, uint32_t tcap) {
+    if (threadIdx.x == 0) {
+      s.c.lam = lam;
+      s.c.tcap = tcap;
+      s.c.inv_lam = (lam > 0.0 && lam < INFINITY) ? (float)(1.0 / lam) : 0.0f;
+      s.c.done = 1;
+      s.c.need = 0;
+    }
+    __syncthreads();
+  }
+
+  // Ask for a histogram of binade E (level 2) or of keys [base, base + 2048) (level 3).
+  __device__ void request(int level, uint32_t E, uint32_t base) {
+    if (level == 2) {
+      for (int b = threadIdx.x; b < kB2; b += kNT) { h2->cnt[b] = 0; h2->sig[b] = 0; h2->mx[b] = 0; }
+    } else {
+      for (int b = threadIdx.x; b < kB3; b += kNT) { h3->cnt[b] = 0; h3->sig[b] = 0; h3->mx[b] = 0; }
+    }
+    if (threadIdx.x == 0) {
+      s.c.need = level;
+      if (level == 2) {
+        s.c.l2exp = E;
+        s.c.l3base = kNone;
+      } else {
+        s.c.l3base = base;
+      }
+    }
+    __syncthreads();
+  }
+
+  // Count and exact sum of keys >= t. Returns 0 when resolved, else the level to request (and
+  // leaves the request made).
+  __device__ int query(uint32_t t, uint64_t& K, Fx& W) {
+    Lvl L1 = lvl1();
+    Walk w1;
+    lvl_scan(L1, s, w1);
+    const int e = (int)(t >> 23);
+    BinInfo i1;
+    lvl_bin_info(L1, w1, e, s, i1);
+    if ((t & 0x7FFFFFu) == 0) {
+      K = i1.Kab + i1.cnt; W = i1.Wab; fx_add(W, i1.Wb);
+      return 0;
+    }
+    if (i1.cnt == 0 || i1.mx < t) {
+      K = i1.Kab; W = i1.Wab;
+      return 0;
+    }
+    if (s.c.l2exp != (uint32_t)e) {
+      request(2, (uint32_t)e, 0);
+      return 2;
+    }
+    Lvl L2 = lvl2((uint32_t)e, i1.Kab, i1.Wab);
+    Walk w2;
+    lvl_scan(L2, s, w2);
+    const int sb = (int)((t >> 11) & (kB2 - 1));
+    BinInfo i2;
+    lvl_bin_info(L2, w2, sb, s, i2);
+    if ((t & 2047u) == 0) {
+      K = i2.Kab + i2.cnt; W = i2.Wab; fx_add(W, i2.Wb);
+      return 0;
+    }
+    if (i2.cnt == 0 || i2.mx < t) {
+      K = i2.Kab; W = i2.Wab;
+      return 0;
+    }
+    const uint32_t base = t & ~2047u;
+    if (s.c.l3base != base) {
+      request(3, 0, base);
+      return 3;
+    }
+    Lvl L3 = lvl3((uint32_t)e, i2.Kab, i2.Wab);
+    Walk w3;
+    lvl_scan(L3, s, w3);
+    BinInfo i3;
+    lvl_bin_info(L3, w3, (int)(t - base), s, i3);
+    K = i3.Kab + i3.cnt; W = i3.Wab; fx_add(W, i3.Wb);
+    return 0;
+  }
+
+  // Algorithm 3 in scale form: lambda_{j+1} = (B - k_j) / U_j, stop when it does not grow.
+  __device__ void greedy() {
+    while (s.c.iter < s.c.T) {
+      const double lam = s.c.lam;
+      uint64_t K;
+      Fx W;
+      if (query(cap_key(lam), K, W)) return;
+      const double U = fx_to_double(fx_sub(s.c.S, W));
+      if (U == 0.0) break;
+      const double ln = (s.c.B - (double)K) / U;
+      if (!(ln > lam)) break;
+      if (threadIdx.x == 0) {
+        s.c.lam = ln;
+        s.c.iter += 1;
+      }
+      __syncthreads();
+    }
+    finalize(s.c.lam, cap_key(s.c.lam));
+  }
+
+  __device__ void exact_finish(uint64_t K, const Fx& W, uint32_t tcap) {
+    const double T1 = fx_to_double(fx_sub(s.c.S, W));
+    finalize((s.c.B - (double)K) / T1, tcap);
+  }
+
+  // The exact solver descends levels: at each one it finds the highest bin whose maximum passes
+  // the criterion (b1) and the lowest occupied bin above it (b2); the answer is b1's maximum
+  // unless b2 holds two or more values that could still pass, in which case b2 is refined.
+  __device__ void exact() {
+    const int level = s.c.stage;
+    Lvl L1 = lvl1();
+    Walk w1;
+    lvl_scan(L1, s, w1);
+    Lvl L = L1;
+    Walk w = w1;
+    uint32_t E = 0;
+    if (level >= 2) {
+      E = s.c.l2exp;
+      BinInfo i1;
+      lvl_bin_info(L1, w1, (int)E, s, i1);
+      Lvl L2 = lvl2(E, i1.Kab, i1.Wab);
+      Walk w2;
+      lvl_scan(L2, s, w2);
+      L = L2;
+      w = w2;
+      if (level == 3) {
+        BinInfo i2;
+        lvl_bin_info(L2, w2, (int)((s.c.l3base >> 11) & (kB2 - 1)), s, i2);
+        Lvl L3 = lvl3(E, i2.Kab, i2.Wab);
+        Walk w3;
+        lvl_scan(L3, s, w3);
+        L = L3;
+        w = w3;
+      }
+    }
+    int b1, b2;
+    lvl_exact(L, w, s.c.B, s.c.S, s, b1, b2);
+    if (b1 < 0) {
+      // no value in this window passes: the answer is the candidate found one level up
+      if (s.c.fbValid) {
+        exact_finish(s.c.fbK, s.c.fbW, s.c.fbTcap);
+      } else {
+        if (threadIdx.x == 0) s.c.flags |= kFlagInternal;
+        finalize(NAN, kKeyInf);
+      }
+      return;
+    }
+    BinInfo i1;
+    lvl_bin_info(L, w, b1, s, i1);
+    const uint32_t cand_tcap = i1.mx + 1;
+    if (b2 != INT_MAX && level < 3) {
+      BinInfo i2;
+      lvl_bin_info(L, w, b2, s, i2);
+      if (i2.cnt >= 2) {
+        if (threadIdx.x == 0) {
+          s.c.fbValid = 1;
+          s.c.fbK = i1.Kab;
+          s.c.fbW = i1.Wab;
+          s.c.fbTcap = cand_tcap;
+          s.c.stage = level + 1;
+        }
+        __syncthreads();
+        if (level == 1) request(2, (uint32_t)b2, 0);
+        else request(3, 0, (E << 23) | ((uint32_t)b2 << 11));
+        return;
+      }
+    }
+    exact_finish(i1.Kab, i1.Wab, cand_tcap);
+  }
+
+  // First solve after the statistics pass: totals and the special cases.
+  __device__ void start() {
+    Lvl L1 = lvl1();
+    Walk w1;
+    lvl_scan(L1, s, w1);
+    // total of all finite keys = everything above bin 0 plus bin 0, minus bin 255 (non-finite)
+    BinInfo i0, inf;
+    lvl_bin_info(L1, w1, 0, s, i0);
+    lvl_bin_info(L1, w1, 255, s, inf);
+    if (threadIdx.x == 0) {
+      Fx tot = i0.Wab;
+      fx_add(tot, i0.Wb);
+      s.c.S = tot;  // bin 255 holds only non-finite keys; its significand sum is never used
+      if (inf.cnt) {
+        Fx t2 = fx_sub(tot, inf.Wb);
+        s.c.S = t2;
+        s.c.flags |= GSPAR_FLAG_NONFINITE;
+      }
+      s.c.stage = 1;
+    }
+    __syncthreads();
+    const uint64_t nnz = (uint64_t)a.d - s.c.zeros;
+    if (s.c.flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO)) {
+      finalize(NAN, kKeyInf);
+      return;
+    }
+    if (nnz == 0) {
+      if (threadIdx.x == 0) s.c.flags |= GSPAR_FLAG_ALLZERO;
+      __syncthreads();
+      finalize(INFINITY, 1);
+      return;
+    }
+    if (s.c.B >= (double)nnz) {
+      finalize(INFINITY, 1);
+      return;
+    }
+    if (s.c.B == 0.0) {
+      finalize(0.0, kKeyInf);
+      return;
+    }
+    if (s.c.solver == GSPAR_GREEDY) {
+      if (threadIdx.x == 0) {
+        s.c.lam = s.c.B / fx_to_double(s.c.S);
+        s.c.iter = 0;
+      }
+      __syncthreads();
+      greedy();
+    } else {
+      exact();
+    }
+  }
+
+  __device__ void run() {
+    if (threadIdx.x == 0) {
+      s.c = *gc;
+      s.c.zeros = ald64(&gc->zeros);
+      s.c.need = 0;
+      s.c.arrive = 0;
+    }
+    __syncthreads();
+    if (s.c.done) return;
+    if (s.c.stage == 0) start();
+    else if (s.c.solver == GSPAR_GREEDY) greedy();
+    else exact();
+    __syncthreads();
+    if (threadIdx.x == 0) *gc = s.c;
+    __threadfence();
+  }
+};
+
+// ------------------------------------------------------------------------------------------
+// Kernels.
+// ------------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) k_init(Args a) {
+  const int64_t tid = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  if (tid == 0) *reinterpret_cast<uint32_t*>(a.ws) = 0;  // tile ticket
+  // level-1 histograms
+  uint64_t* h1 = reinterpret_cast<uint64_t*>(a.ws + a.lay.h1);
+  const int64_t n1 = a.rows * (int64_t)(sizeof(Hist1) / 8);
+  for (int64_t i = tid; i < n1; i += stride) h1[i] = 0;
+  uint64_t* st = status_of(a);
+  const int64_t ns = a.rows * a.lay.tiles;
+  for (int64_t i = tid; i < ns; i += stride) st[i] = 0;
+  for (int64_t r = tid; r < a.rows; r += stride) {
+    RowCtl c;
+    memset(&c, 0, sizeof(c));
+    const double rho = a.rho_dev ? a.rho_dev[r] : a.rho;
+    c.B = rho * (double)a.d;
+    if (!(rho >= 0.0 && rho <= 1.0)) c.flags = GSPAR_FLAG_BADRHO;
+    c.l2exp = kNone;
+    c.l3base = kNone;
+    c.solver = a.solver;
+    c.T = a.T;
+    *ctl_of(a, r) = c;
+  }
+}
+
+// Streaming statistics pass. Grid: rows * nb workgroups of kNT threads.
+template <bool VEC>
+__global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))) k_stats(Args a) {
+  __shared__ SharedU sm;
+  __shared__ uint32_t s_last;
+  const int64_t row = blockIdx.x / a.nb;
+  const int64_t blk = blockIdx.x % a.nb;
+  for (int b = threadIdx.x; b < kFine; b += kNT) {
+    sm.h.pk[b] = 0;
+    sm.h.mx[b] = 0;
+  }
+  __syncthreads();
+  const float* __restrict__ gr = a.g + row * a.ld;
+  const int64_t beg = blk * a.chunk;
+  const int64_t end = min(a.d, beg + a.chunk);
+  uint32_t zeros = 0;
+  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += kNT) {
+    float v[4];
+    const uint32_t m = load4<VEC>(gr, q, end, v);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[c]);
+      if (key == 0) {
+        zeros += (m >> c) & 1;
+      } else {
+        const uint32_t f = key >> 19;
+        atomicAdd(&sm.h.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
+        atomicMax(&sm.h.mx[f], key);
+      }
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) zeros += __shfl_xor(zeros, o);
+  __syncthreads();
+  RowCtl* ctl = ctl_of(a, row);
+  if ((threadIdx.x & 63) == 0 && zeros) atomicAdd((unsigned long long*)&ctl->zeros, (unsigned long long)zeros);
+  // flush one binade per thread
+  if (threadIdx.x < kB1) {
+    const int e = threadIdx.x;
+    uint64_t cnt = 0, sg = 0;
+    uint32_t mx = 0;
+    for (int j = 0; j < 16; ++j) {
+      const uint64_t p = sm.h.pk[e * 16 + j];
+      cnt += p >> 44;
+      sg += p & ((1ull << 44) - 1);
+      mx = max(mx, sm.h.mx[e * 16 + j]);
+    }
+    if (cnt) {
+      Hist1* h = h1_of(a, row);
+      atomicAdd((unsigned long long*)&h->cnt[e], (unsigned long long)cnt);
+      atomicAdd((unsigned long long*)&h->sig[e], (unsigned long long)sg);
+      atomicMax(&h->mx[e], mx);
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(&ctl->arrive, 1u) == (uint32_t)(a.nb - 1);
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  Solver sv{a, row, ctl, sm.s, h1_of(a, row), h2_of(a, row), h3_of(a, row)};
+  sv.run();
+}
+
+// Refinement pass over one window of keys, when the row's solver asked for one.
+template <bool VEC>
+__global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))) k_refine(Args a) {
+  __shared__ SharedU sm;
+  __shared__ uint32_t s_last;
+  const int64_t row = blockIdx.x / a.nb;
+  const int64_t blk = blockIdx.x % a.nb;
+  RowCtl* ctl = ctl_of(a, row);
+  const uint32_t need = ctl->need;
+  if (need != 2 && need != 3) return;
+  uint32_t lo, shift;
+  int nbins;
+  uint64_t *gcnt, *gsig;
+  uint32_t* gmx;
+  if (need == 2) {
+    lo = ctl->l2exp << 23;
+    shift = 11;
+    nbins = kB2;
+    Hist2* h = h2_of(a, row);
+    gcnt = h->cnt; gsig = h->sig; gmx = h->mx;
+  } else {
+    lo = ctl->l3base;
+    shift = 0;
+    nbins = kB3;
+    Hist3* h = h3_of(a, row);
+    gcnt = h->cnt; gsig = h->sig; gmx = h->mx;
+  }
+  const uint32_t span = (uint32_t)nbins << shift;
+  for (int b = threadIdx.x; b < nbins; b += kNT) {
+    sm.h.pk[b] = 0;
+    sm.h.mx[b] = 0;
+  }
+  __syncthreads();
+  const float* __restrict__ gr = a.g + row * a.ld;
+  const int64_t beg = blk * a.chunk;
+  const int64_t end = min(a.d, beg + a.chunk);
+  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += kNT) {
+    float v[4];
+    load4<VEC>(gr, q, end, v);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[c]);
+      const uint32_t rel = key - lo;
+      if (key != 0 && rel < span) {
+        const uint32_t b = rel >> shift;
+        atomicAdd(&sm.h.pk[b], (unsigned long long)((1ull << 44) + key_sig(key)));
+        atomicMax(&sm.h.mx[b], key);
+      }
+    }
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < nbins; b += kNT) {
+    const uint64_t p = sm.h.pk[b];
+    if (p) {
+      atomicAdd((unsigned long long*)&gcnt[b], (unsigned long long)(p >> 44));
+      atomicAdd((unsigned long long*)&gsig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
+      atomicMax(&gmx[b], sm.h.mx[b]);
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(&ctl->arrive, 1u) == (uint32_t)(a.nb - 1);
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  Solver sv{a, row, ctl, sm.s, h1_of(a, row), h2_of(a, row), h3_of(a, row)};
+  sv.run();
+}
+
+// Sampling, amplification and order-preserving compaction. One ticketed tile of kTileElems
+// coordinates per workgroup; tile prefixes chain through a decoupled look-back whose status word
+// packs (flag:2 | capped survivors:31 | survivors:31).
+constexpr uint64_t kStAgg = 1ull << 62, kStInc = 2ull << 62, kStVal = (1ull << 62) - 1;
+
+template <bool VEC>
+__global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
+  __shared__ uint32_t s_tile;
+  __shared__ uint64_t s_wave[kTileThreads / 64];
+  __shared__ uint32_t s_capw[kTileThreads / 64];
+  __shared__ uint64_t s_excl;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (tid == 0) s_tile = atomicAdd(reinterpret_cast<uint32_t*>(a.ws), 1u);
+  __syncthreads();
+  const int64_t t = s_tile;
+  const int64_t row = t / a.lay.tiles;
+  const int64_t part = t % a.lay.tiles;
+  const RowCtl* ctl = ctl_of(a, row);
+  const double lam = ctl->lam;
+  const uint32_t tcap = ctl->tcap;
+  const float inv = ctl->inv_lam;
+  const bool live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO));
+  const uint64_t seed = a.seed_dev ? a.seed_dev[row] : a.seed;
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  const float* __restrict__ gr = a.g + row * a.ld;
+
+  float v[kTileGroups][4];
+  uint32_t zb[kTileGroups], cb[kTileGroups];
+  uint64_t packed = 0;
+  uint32_t ncap = 0;
+#pragma unroll
+  for (int j = 0; j < kTileGroups; ++j) {
+    const int64_t q = part * (kTileElems / 4) + j * kTileThreads + tid;
+    const uint32_t m = load4<VEC>(gr, q, a.d, v[j]);
+    uint32_t x0 = (uint32_t)q, x1 = (uint32_t)((uint64_t)q >> 32), x2 = 0, x3 = 0;
+    philox10(x0, x1, x2, x3, k0, k1);
+    const uint32_t xr[4] = {x0, x1, x2, x3};
+    uint32_t z = 0, cz = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[j][c]);
+      const bool capped = key >= tcap;
+      const bool pick = capped || ((double)xr[c] * 0x1p-32 < lam * (double)fabsf(v[j][c]));
+      const bool sel = live && ((m >> c) & 1) && key != 0 && pick;
+      z |= (uint32_t)sel << c;
+      cz |= (uint32_t)(sel && capped) << c;
+    }
+    zb[j] = z;
+    cb[j] = cz;
+    packed |= (uint64_t)__popc(z) << (16 * j);
+    ncap += __popc(cz);
+  }
+  // block exclusive scan of the packed per-group counts (four 16-bit fields)
+  unsigned long long inc = packed;
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long y = __shfl_up(inc, (unsigned)o);
+    if (lane >= o) inc += y;
+  }
+  uint32_t capw = ncap;
+  for (int o = 32; o > 0; o >>= 1) capw += __shfl_xor(capw, o);
+  if (lane == 63) s_wave[wv] = inc;
+  if (lane == 0) s_capw[wv] = capw;
+  __syncthreads();
+  uint64_t wpre = 0, tot = 0;
+  uint32_t tcapn = 0;
+  for (int i = 0; i < kTileThreads / 64; ++i) {
+    if (i < wv) wpre += s_wave[i];
+    tot += s_wave[i];
+    tcapn += s_capw[i];
+  }
+  const uint64_t excl = wpre + inc - packed;
+  uint32_t fsum[kTileGroups];
+  uint64_t nsel = 0;
+#pragma unroll
+  for (int j = 0; j < kTileGroups; ++j) {
+    fsum[j] = (uint32_t)((tot >> (16 * j)) & 0xFFFF);
+    nsel += fsum[j];
+  }
+  const uint64_t agg = ((uint64_t)tcapn << 31) | nsel;
+
+  // decoupled look-back for the tile's exclusive prefix within its row
+  uint64_t* st = status_of(a);
+  if (part == 0) {
+    if (tid == 0) {
+      __hip_atomic_store(&st[t], kStInc | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_excl = 0;
+    }
+  } else {
+    if (tid == 0) __hip_atomic_store(&st[t], kStAgg | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (wv == 0) {
+      const int64_t first = t - part;
+      int64_t look = t - 1;
+      uint64_t ex = 0;
+      bool bad = false;
+      while (true) {
+        const int64_t i = look - lane;
+        uint64_t s = kStInc;
+        if (i >= first) {
+          uint32_t spins = 0;
+          do {
+            s = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          } while ((s >> 62) == 0 && ++spins < kSpinLimit);
+          if ((s >> 62) == 0) {
+            bad = true;
+            s = kStInc;
+          }
+        }
+        const uint64_t incl_mask = __ballot((s >> 62) == 2);
+        const int stop = incl_mask ? (__ffsll((unsigned long long)incl_mask) - 1) : 64;
+        uint64_t contrib = lane <= stop ? (s & kStVal) : 0;
+        for (int o = 32; o > 0; o >>= 1) contrib += __shfl_xor(contrib, o);
+        ex += contrib;
+        if (incl_mask) break;
+        look -= 64;
+      }
+      const bool anybad = __ballot(bad) != 0;
+      if (lane == 0) {
+        __hip_atomic_store(&st[t], kStInc | (ex + agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_excl = ex;
+        if (anybad) atomicOr(&ctl_of(a, row)->flags, (uint32_t)kFlagInternal);
+      }
+    }
+  }
+  __syncthreads();
+  const uint64_t base = s_excl & 0x7FFFFFFFull;  // survivors before this tile
+  int32_t* __restrict__ oi = a.idx + row * a.cap;
+  float* __restrict__ ov = a.val + row * a.cap;
+  uint64_t gpre = 0;
+#pragma unroll
+  for (int j = 0; j < kTileGroups; ++j) {
+    uint32_t z = zb[j];
+    if (z) {
+      const int64_t q = part * (kTileElems / 4) + j * kTileThreads + tid;
+      uint64_t pos = base + gpre + ((excl >> (16 * j)) & 0xFFFF);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        if ((z >> c) & 1) {
+          if ((int64_t)pos < a.cap) {
+            oi[pos] = (int32_t)(4 * q + c);
+            ov[pos] = ((cb[j] >> c) & 1) ? v[j][c] : copysignf(inv, v[j][c]);
+          }
+          ++pos;
+        }
+      }
+    }
+    gpre += fsum[j];
+  }
+  if (part == a.lay.tiles - 1 && tid == 0) {
+    const uint64_t incl = s_excl + agg;
+    const int64_t n = (int64_t)(incl & 0x7FFFFFFFull);
+    const int64_t kc = (int64_t)((incl >> 31) & 0x7FFFFFFFull);
+    if (a.nnz) a.nnz[row] = n;
+    if (a.k_out) a.k_out[row] = kc;
+    if (a.lam_out) a.lam_out[row] = ctl->lam;
+    uint32_t fl = __hip_atomic_load(&ctl_of(a, row)->flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!ctl->done) fl |= kFlagInternal;
+    if (n > a.cap) fl |= GSPAR_FLAG_OVERFLOW;
+    if (a.flags_out) a.flags_out[row] = fl;
+  }
+}
+
+// p_i = min(lambda |g_i|, 1), exactly 1 on the capped set. Grid: rows * nb workgroups.
+template <bool VEC>
+__global__ void __launch_bounds__(256) k_probs(Args a) {
+  __shared__ uint32_t s_last;
+  __shared__ uint32_t s_cnt[4];
+  const int64_t row = blockIdx.x / a.nb;
+  const int64_t blk = blockIdx.x % a.nb;
+  RowCtl* ctl = ctl_of(a, row);
+  const double lam = ctl->lam;
+  const uint32_t tcap = ctl->tcap;
+  const bool live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO));
+  const float* __restrict__ gr = a.g + row * a.ld;
+  float* __restrict__ pr = a.p ? a.p + row * a.ld : nullptr;
+  const int64_t beg = blk * a.chunk;
+  const int64_t end = min(a.d, beg + a.chunk);
+  uint32_t kc = 0;
+  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += blockDim.x) {
+    float v[4], o[4];
+    const uint32_t m = load4<VEC>(gr, q, end, v);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[c]);
+      const bool capped = live && key != 0 && key >= tcap;
+      double pv = capped ? 1.0 : (live ? fmin(lam * (double)fabsf(v[c]), 1.0) : 0.0);
+      if (key == 0) pv = 0.0;
+      o[c] = (float)pv;
+      kc += capped && ((m >> c) & 1);
+    }
+    if (pr) {
+      if (VEC && m == 0xF) {
+        *reinterpret_cast<float4*>(pr + 4 * q) = make_float4(o[0], o[1], o[2], o[3]);
+      } else {
+        for (int c = 0; c < 4; ++c)
+          if ((m >> c) & 1) pr[4 * q + c] = o[c];
+      }
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) kc += __shfl_xor(kc, o);
+  if ((threadIdx.x & 63) == 0) s_cnt[threadIdx.x >> 6] = kc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t tot = 0;
+    for (int i = 0; i < (int)(blockDim.x / 64); ++i) tot += s_cnt[i];
+    if (tot) atomicAdd((unsigned long long*)&ctl->kcount, (unsigned long long)tot);
+    __threadfence();
+    s_last = atomicAdd(&ctl->parrive, 1u) == (uint32_t)(a.nb - 1);
+  }
+  __syncthreads();
+  if (!s_last || threadIdx.x != 0) return;
+  __threadfence();
+  if (a.lam_out) a.lam_out[row] = lam;
+  if (a.k_out) a.k_out[row] = (int64_t)ald64(&ctl->kcount);
+  uint32_t fl = ctl->flags;
+  if (!ctl->done) fl |= kFlagInternal;
+  if (a.flags_out) a.flags_out[row] = fl;
+}
+
+// ------------------------------------------------------------------------------------------
+// Host side.
+// ------------------------------------------------------------------------------------------
+struct Timing {
+  int which = -1;
+  int max = 0;
+  int n = 0;
+  hipEvent_t* ev = nullptr;
+};
+static Timing g_timing;
+
+static void time_before(int which, hipStream_t s) {
+  if (g_timing.which == which && g_timing.n < g_timing.max) (void)hipEventRecord(g_timing.ev[2 * g_timing.n], s);
+}
+static void time_after(int which, hipStream_t s) {
+  if (g_timing.which == which && g_timing.n < g_timing.max) {
+    (void)hipEventRecord(g_timing.ev[2 * g_timing.n + 1], s);
+    g_timing.n += 1;
+  }
+}
+
+static bool rho_ok(double rho) { return rho >= 0.0 && rho <= 1.0; }
+
+static int check_common(const float* g, int64_t rows, int64_t d, int64_t ld, int solver, int iters,
+                        void* ws, size_t ws_bytes) {
+  if (!g || rows < 1 || d < 1 || d > INT32_MAX || ld < d) return GSPAR_ERR_ARG;
+  if (solver != GSPAR_GREEDY && solver != GSPAR_EXACT) return GSPAR_ERR_ARG;
+  if (iters < 0 || iters > kMaxIters) return GSPAR_ERR_ARG;
+  if (rows > (int64_t)1 << 24) return GSPAR_ERR_ARG;
+  const Layout L = layout_of(rows, d);
+  if ((double)rows * (double)L.tiles >= 2147483647.0) return GSPAR_ERR_ARG;  // sample grid, tickets
+  const int64_t min_chunk = d < kMaxChunk ? d : kMaxChunk;
+  if ((double)rows * (double)((d + min_chunk - 1) / min_chunk) >= 2147483647.0) return GSPAR_ERR_ARG;
+  if (!ws || ((uintptr_t)ws & 255) || ws_bytes < L.total) return GSPAR_ERR_WORKSPACE;
+  return GSPAR_OK;
+}
+
+static void plan(Args& a) {
+  a.lay = layout_of(a.rows, a.d);
+  const int64_t target = 512;
+  int64_t nbt = (target + a.rows - 1) / a.rows;
+  if (nbt < 1) nbt = 1;
+  int64_t chunk = (a.d + nbt - 1) / nbt;
+  chunk = (chunk + 3) & ~(int64_t)3;
+  if (chunk < 8192) chunk = 8192;
+  if (chunk > kMaxChunk) chunk = kMaxChunk;
+  a.chunk = chunk;
+  a.nb = (int)((a.d + chunk - 1) / chunk);
+}
+
+static bool vec_ok(const Args& a) { return ((uintptr_t)a.g % 16 == 0) && (a.ld % 4 == 0); }
+
+static int launch_solve(Args& a, hipStream_t s) {
+  const bool vec = vec_ok(a);
+  const int64_t zero_items = a.rows * (int64_t)(sizeof(Hist1) / 8) + a.rows * a.lay.tiles;
+  int ib = (int)((zero_items + 255) / 256);
+  if (ib > 1024) ib = 1024;
+  if (ib < 1) ib = 1;
+  hipLaunchKernelGGL(k_init, dim3(ib), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)(a.rows * a.nb));
+  time_before(1, s);
+  if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
+  else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
+  time_after(1, s);
+  const int R = a.solver == GSPAR_GREEDY ? 2 * a.T : 2;
+  for (int r = 0; r < R; ++r) {
+    if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
+    else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
+  }
+  return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
+}
+
+static int run_sample(Args& a, hipStream_t s) {
+  plan(a);
+  int rc = launch_solve(a, s);
+  if (rc) return rc;
+  const bool vec = vec_ok(a);
+  const dim3 grid((unsigned)(a.rows * a.lay.tiles));
+  time_before(0, s);
+  if (vec) hipLaunchKernelGGL(k_sample<true>, grid, dim3(kTileThreads), 0, s, a);
+  else hipLaunchKernelGGL(k_sample<false>, grid, dim3(kTileThreads), 0, s, a);
+  time_after(0, s);
+  return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
+}
+
+static int run_probs(Args& a, hipStream_t s) {
+  plan(a);
+  int rc = launch_solve(a, s);
+  if (rc) return rc;
+  const bool vec = vec_ok(a) && (!a.p || (uintptr_t)a.p % 16 == 0);
+  const dim3 grid((unsigned)(a.rows * a.nb));
+  time_before(2, s);
+  if (vec) hipLaunchKernelGGL(k_probs<true>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_probs<false>, grid, dim3(256), 0, s, a);
+  time_after(2, s);
+  return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
+}
+
+static Args base_args(const float* g, int64_t rows, int64_t d, int64_t ld, int solver, int iters, void* ws) {
+  Args a;
+  memset(&a, 0, sizeof(a));
+  a.g = g;
+  a.rows = rows;
+  a.d = d;
+  a.ld = ld;
+  a.solver = solver;
+  a.T = iters;
+  a.ws = static_cast<char*>(ws);
+  return a;
+}
+
+}  // namespace gspar
+
+using namespace gspar;
+
+extern "C" {
+
+size_t gspar_workspace_bytes(int64_t rows, int64_t d, int solver) {
+  (void)solver;
+  if (rows < 1 || d < 1) return 0;
+  return layout_of(rows, d).total;
+}
+
+int64_t gspar_capacity_hint(int64_t d, double rho) {
+  if (d < 1 || !rho_ok(rho)) return 0;
+  const double B = rho * (double)d;
+  double c = std::ceil(B + 8.0 * std::sqrt(B) + 64.0);
+  if (c > (double)d) c = (double)d;
+  return (int64_t)c;
+}
+
+int sparsify_probs(const float* g, int64_t d, double rho, int solver, int greedy_iters, float* p,
+                   double* lambda, int64_t* k, uint32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!lambda || !rho_ok(rho)) return GSPAR_ERR_ARG;
+  int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws);
+  a.rho = rho;
+  a.p = p;
+  a.lam_out = lambda;
+  a.k_out = k;
+  a.flags_out = flags;
+  return run_probs(a, (hipStream_t)stream);
+}
+
+int sparsify_sample_compact(const float* g, int64_t d, double rho, int solver, int greedy_iters, uint64_t seed,
+                            int32_t* idx, float* val, int64_t capacity, int64_t* nnz, double* lambda, int64_t* k,
+                            uint32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!nnz || capacity < 0 || (capacity > 0 && (!idx || !val)) || !rho_ok(rho)) return GSPAR_ERR_ARG;
+  int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws);
+  a.rho = rho;
+  a.seed = seed;
+  a.idx = idx;
+  a.val = val;
+  a.cap = capacity;
+  a.nnz = nnz;
+  a.lam_out = lambda;
+  a.k_out = k;
+  a.flags_out = flags;
+  return run_sample(a, (hipStream_t)stream);
+}
+
+int sparsify_probs_batched(const float* g, int64_t rows, int64_t d, int64_t ld, const double* rho, int solver,
+                           int greedy_iters, float* p, double* lambda, int64_t* k, uint32_t* flags, void* ws,
+                           size_t ws_bytes, void* stream) {
+  if (!rho || !lambda) return GSPAR_ERR_ARG;
+  int rc = check_common(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws);
+  a.rho_dev = rho;
+  a.p = p;
+  a.lam_out = lambda;
+  a.k_out = k;
+  a.flags_out = flags;
+  return run_probs(a, (hipStream_t)stream);
+}
+
+int sparsify_sample_compact_batched(const float* g, int64_t rows, int64_t d, int64_t ld, const double* rho,
+                                    int solver, int greedy_iters, const uint64_t* seeds, int32_t* idx, float* val,
+                                    int64_t cap_per_row, int64_t* nnz, double* lambda, int64_t* k, uint32_t* flags,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  if (!rho || !seeds || !nnz || cap_per_row < 0 || (cap_per_row > 0 && (!idx || !val))) return GSPAR_ERR_ARG;
+  int rc = check_common(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws);
+  a.rho_dev = rho;
+  a.seed_dev = seeds;
+  a.idx = idx;
+  a.val = val;
+  a.cap = cap_per_row;
+  a.nnz = nnz;
+  a.lam_out = lambda;
+  a.k_out = k;
+  a.flags_out = flags;
+  return run_sample(a, (hipStream_t)stream);
+}
+
+const char* gspar_status_string(int status) {
+  switch (status) {
+    case GSPAR_OK: return "ok";
+    case GSPAR_ERR_ARG: return "invalid argument";
+    case GSPAR_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case GSPAR_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+int gspar_version(void) { return 100; }
+
+int gspar_timing_arm(int which, int max_launches) {
+  if (which < 0 || which > 2 || max_launches < 1) return GSPAR_ERR_ARG;
+  gspar_timing_disarm();
+  g_timing.ev = new hipEvent_t[2 * (size_t)max_launches];
+  for (int i = 0; i < 2 * max_launches; ++i) {
+    if (hipEventCreate(&g_timing.ev[i]) != hipSuccess) {
+      for (int j = 0; j < i; ++j) (void)hipEventDestroy(g_timing.ev[j]);
+      delete[] g_timing.ev;
+      g_timing.ev = nullptr;
+      return GSPAR_ERR_HIP;
+    }
+  }
+  g_timing.which = which;
+  g_timing.max = max_launches;
+  g_timing.n = 0;
+  return GSPAR_OK;
+}
+
+int gspar_timing_read(double* total_ms, int* launches) {
+  if (!total_ms || !launches) return GSPAR_ERR_ARG;
+  *total_ms = 0.0;
+  *launches = g_timing.n;
+  if (!g_timing.ev || g_timing.n == 0) return GSPAR_OK;
+  if (hipEventSynchronize(g_timing.ev[2 * g_timing.n - 1]) != hipSuccess) return GSPAR_ERR_HIP;
+  double tot = 0.0;
+  for (int i = 0; i < g_timing.n; ++i) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]) != hipSuccess) return GSPAR_ERR_HIP;
+    tot += ms;
+  }
+  *total_ms = tot;
+  return GSPAR_OK;
+}
+
+int gspar_timing_disarm(void) {
+  if (g_timing.ev) {
+    for (int i = 0; i < 2 * g_timing.max; ++i) (void)hipEventDestroy(g_timing.ev[i]);
+    delete[] g_timing.ev;
+  }
+  g_timing = Timing();
+  return GSPAR_OK;
+}
+
+// Host-side checks of the device arithmetic (same source, compiled for the host): rounding of the
+// exact accumulator, the capped-threshold search and the random generator.
+double gspar_check_fx_round(const uint64_t* limbs5) {
+  Fx f;
+  for (int i = 0; i < 5; ++i) f.w[i] = limbs5[i];
+  return fx_to_double(f);
+}
+
+double gspar_check_exact_sum(const float* x, int64_t n) {
+  Fx acc = fx_zero();
+  for (int64_t i = 0; i < n; ++i) {
+    const uint32_t key = key_of(x[i]);
+    if (key == 0 || key >= kKeyInf) continue;
+    fx_add(acc, fx_shifted(key_sig(key), binade_shift((int)(key >> 23))));
+  }
+  return fx_to_double(acc);
+}
+
+uint32_t gspar_check_cap_key(double lam) { return cap_key(lam); }
+
+void gspar_check_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
+  uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+  philox10(c0, c1, c2, c3, key[0], key[1]);
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+}  // extern "C"

@@ -1,0 +1,177 @@
+"""CPU checks of the C-ABI library: it loads, exports every declared symbol, rejects bad
+arguments before enqueuing anything, and its host-compiled arithmetic building blocks (exact
+accumulator rounding, capped-threshold search, Philox) are right. No GPU is touched: every
+sparsify_* call here carries an argument error, which the library reports before any HIP call."""
+import fractions
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import ctypes
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gspar.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_1710_09854_amd as gs
+
+    if not os.path.exists(gs.LIB_PATH):
+        from paper_1710_09854_amd import build
+
+        build.build()
+    return gs.lib()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", src)) - {"defined"})
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert "sparsify_probs" in names and "sparsify_sample_compact_batched" in names
+    for n in names:
+        assert hasattr(L, n), f"symbol {n} declared in gspar.h is not exported"
+
+
+def test_workspace_and_capacity(L):
+    assert L.gspar_workspace_bytes(0, 10, 0) == 0
+    a = L.gspar_workspace_bytes(1, 65536, 0)
+    b = L.gspar_workspace_bytes(16, 1 << 20, 0)
+    assert a > 0 and b > a and b % 256 == 0
+    assert L.gspar_capacity_hint(1000, 0.1) == min(1000, math.ceil(100 + 8 * 10 + 64))
+    assert L.gspar_capacity_hint(100, 0.9) == 100
+    assert L.gspar_capacity_hint(100, 1.5) == 0
+    assert L.gspar_version() >= 100
+
+
+FAKE = 0x10000  # a non-null, 256-aligned address that is never dereferenced
+
+
+def _sc(L, g=FAKE, d=1000, rho=0.1, solver=0, iters=2, idx=FAKE, val=FAKE, cap=10, nnz=FAKE, ws=FAKE, wsb=None):
+    if wsb is None:
+        wsb = L.gspar_workspace_bytes(1, max(d, 1), 0)
+    return L.sparsify_sample_compact(g, d, rho, solver, iters, 0, idx, val, cap, nnz, None, None, None, ws, wsb, None)
+
+
+def test_argument_errors(L):
+    import paper_1710_09854_amd as gs
+
+    assert _sc(L, g=None) == gs.ERR_ARG
+    assert _sc(L, d=0) == gs.ERR_ARG
+    assert _sc(L, d=(1 << 31)) == gs.ERR_ARG
+    assert _sc(L, rho=-0.1) == gs.ERR_ARG
+    assert _sc(L, rho=1.5) == gs.ERR_ARG
+    assert _sc(L, rho=float("nan")) == gs.ERR_ARG
+    assert _sc(L, solver=2) == gs.ERR_ARG
+    assert _sc(L, iters=-1) == gs.ERR_ARG
+    assert _sc(L, iters=65) == gs.ERR_ARG
+    assert _sc(L, cap=-1) == gs.ERR_ARG
+    assert _sc(L, idx=None) == gs.ERR_ARG
+    assert _sc(L, nnz=None) == gs.ERR_ARG
+    assert _sc(L, ws=None) == gs.ERR_WORKSPACE
+    assert _sc(L, ws=FAKE + 8) == gs.ERR_WORKSPACE
+    assert _sc(L, wsb=100) == gs.ERR_WORKSPACE
+    # probabilities
+    wsb = L.gspar_workspace_bytes(1, 1000, 1)
+    assert L.sparsify_probs(FAKE, 1000, 0.1, 1, 2, None, None, None, None, FAKE, wsb, None) == gs.ERR_ARG
+    assert L.sparsify_probs(FAKE, 1000, 2.0, 1, 2, None, FAKE, None, None, FAKE, wsb, None) == gs.ERR_ARG
+    # batched
+    wsb = L.gspar_workspace_bytes(4, 1000, 0)
+    assert L.sparsify_sample_compact_batched(FAKE, 4, 1000, 999, FAKE, 0, 2, FAKE, FAKE, FAKE, 10, FAKE,
+                                             None, None, None, FAKE, wsb, None) == gs.ERR_ARG  # ld < d
+    assert L.sparsify_sample_compact_batched(FAKE, 0, 1000, 1000, FAKE, 0, 2, FAKE, FAKE, FAKE, 10, FAKE,
+                                             None, None, None, FAKE, wsb, None) == gs.ERR_ARG
+    assert L.sparsify_sample_compact_batched(FAKE, 4, 1000, 1000, None, 0, 2, FAKE, FAKE, FAKE, 10, FAKE,
+                                             None, None, None, FAKE, wsb, None) == gs.ERR_ARG
+    assert L.sparsify_sample_compact_batched(FAKE, 4, 1000, 1000, FAKE, 0, 2, None, FAKE, FAKE, 10, FAKE,
+                                             None, None, None, FAKE, wsb, None) == gs.ERR_ARG
+    assert L.sparsify_probs_batched(FAKE, 4, 1000, 1000, FAKE, 0, 2, None, FAKE, None, None, FAKE, 10, None) \
+        == gs.ERR_WORKSPACE
+    assert L.gspar_status_string(gs.ERR_ARG) == b"invalid argument"
+
+
+def _fx_limbs(v: int):
+    return (ctypes.c_uint64 * 5)(*[(v >> (64 * i)) & 0xFFFFFFFFFFFFFFFF for i in range(5)])
+
+
+def test_fixed_point_rounding_is_correct(L):
+    L.gspar_check_fx_round.argtypes = [ctypes.c_uint64 * 5]
+    L.gspar_check_fx_round.restype = ctypes.c_double
+    rng = np.random.default_rng(3)
+    cases = [0, 1, (1 << 53) - 1, 1 << 53, (1 << 53) + 1, (1 << 54) + 2, (1 << 54) + 6, (1 << 300) - 1]
+    for _ in range(3000):
+        bits = int(rng.integers(1, 310))
+        v = int(rng.integers(0, 1 << 62)) << max(0, bits - 62)
+        v |= int(rng.integers(0, 1 << 20))
+        cases.append(v & ((1 << 310) - 1))
+    # ties: exactly half an ulp above a representable value
+    for sh in (0, 7, 100):
+        m = (1 << 52) + int(rng.integers(0, 1 << 52))
+        cases.append(((2 * m + 1) << sh))
+    for v in cases:
+        want = float(fractions.Fraction(v, 1 << 149))
+        assert L.gspar_check_fx_round(_fx_limbs(v)) == want, hex(v)
+
+
+def test_exact_sum_matches_fsum(L):
+    L.gspar_check_exact_sum.argtypes = [np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS"), ctypes.c_int64]
+    L.gspar_check_exact_sum.restype = ctypes.c_double
+    rng = np.random.default_rng(4)
+    for t in range(20):
+        x = (rng.standard_normal(5000) * np.exp2(rng.uniform(-150, 120, 5000))).astype(np.float32)
+        x[:10] = 0
+        assert L.gspar_check_exact_sum(x, x.size) == math.fsum(np.abs(x.astype(np.float64)))
+
+
+def test_cap_key_is_smallest_capped_pattern(L):
+    L.gspar_check_cap_key.argtypes = [ctypes.c_double]
+    L.gspar_check_cap_key.restype = ctypes.c_uint32
+    rng = np.random.default_rng(5)
+    lams = list(np.exp(rng.uniform(-90, 100, 3000))) + [1.0, 0.5, 3.0, 1e-45, 1e40, 2.0 ** -126]
+
+    def val(k):
+        return float(np.array([k], np.uint32).view(np.float32)[0])
+
+    for lam in lams:
+        lam = float(lam)
+        k = L.gspar_check_cap_key(lam)
+        assert 1 <= k <= 0x7F800000
+        if k < 0x7F800000:
+            assert lam * val(k) >= 1.0
+        if k > 1:
+            assert lam * val(k - 1) < 1.0
+    assert L.gspar_check_cap_key(0.0) == 0x7F800000
+    assert L.gspar_check_cap_key(float("inf")) == 1
+    assert L.gspar_check_cap_key(float("nan")) == 0x7F800000
+
+
+def test_device_philox_known_answers(L):
+    u32p = np.ctypeslib.ndpointer(np.uint32, flags="C_CONTIGUOUS")
+    L.gspar_check_philox.argtypes = [u32p, u32p, u32p]
+    L.gspar_check_philox.restype = None
+    path = os.path.join(ROOT, "tests", "golden", "philox4x32_10_kat.txt")
+    n = 0
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        v = [int(t, 16) for t in line.split()]
+        out = np.zeros(4, np.uint32)
+        L.gspar_check_philox(np.array(v[0:4], np.uint32), np.array(v[4:6], np.uint32), out)
+        assert out.tolist() == v[6:10]
+        n += 1
+    assert n == 3
+
+
+def test_no_cpu_fallback_in_binding():
+    """The binding must not compute anything itself: its only numeric dependency is torch for
+    allocation; it never imports the oracle or numpy."""
+    src = open(os.path.join(ROOT, "paper_1710_09854_amd", "__init__.py")).read()
+    assert "import oracle" not in src and "from oracle" not in src
+    assert "import numpy" not in src

@@ -1,0 +1,243 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle, element by element, at sizes
+the oracle finishes in seconds that still span many tiles and ragged tails, plus edge cases,
+batching, determinism, capacity overflow, the unaligned (scalar-load) path and sampling
+statistics. Rule: index sets equal except where |u_i - p_i| <= 1e-6, values to rel 1e-5, lambda
+to rel 1e-9, probabilities to 1e-6 absolute."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from oracle.compare import compare_probs, compare_sample, lam_close
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def gs():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1710_09854_amd as m
+
+    m.lib()
+    return m
+
+
+def _run_row(gs, g, rho, solver, seed, iters=2, cap=None):
+    gd = torch.from_numpy(g).cuda()
+    out = gs.sparsify_sample_compact(gd, rho, seed=seed, solver=solver, iters=iters, capacity=cap)
+    torch.cuda.synchronize()
+    n = int(out.nnz.item())
+    m = min(n, out.idx.numel())
+    return (out.idx[:m].cpu().numpy(), out.val[:m].cpu().numpy(), n, float(out.lam.item()),
+            int(out.k.item()), int(out.flags.item()) & 0xFFFFFFFF)
+
+
+VECTORS = {
+    "normal_65536": lambda: W.normal(65536, 0),
+    "normal_ragged_100003": lambda: W.normal(100003, 1),
+    "tmix_200001": lambda: W.t_mixture(200001, 2),
+    "ties_50001": lambda: W.integer_ties(50001, 3),
+    "wide_range_120000": lambda: W.wide_range(120000, 4),
+    "two_level_70001": lambda: W.two_level(70001, 300, 50.0, 1.0, 5),
+    "approx_sparse_40000": lambda: W.approx_sparse(40000, 200, 0.05, 6),
+    "tiny_7": lambda: W.normal(7, 7),
+    "one_1": lambda: np.array([-2.5], np.float32),
+    "laplace_row": lambda: W.c2(rows=1, d=1 << 18).g[0].copy(),
+}
+
+
+@pytest.mark.parametrize("name", list(VECTORS))
+@pytest.mark.parametrize("solver", ["greedy", "exact"])
+@pytest.mark.parametrize("rho", [0.001, 0.01, 0.1, 0.5])
+def test_row_parity(gs, name, solver, rho):
+    g = VECTORS[name]()
+    seed = 1234 + len(name)
+    _say(f"[parity] {name} d={g.size} solver={solver} rho={rho} seed={seed}")
+    sol = oracle.solve(g, rho, solver, 2)
+    idx, val, n, lam, k, fl = _run_row(gs, g, rho, solver, seed, cap=g.size)
+    assert fl == 0, fl
+    rep = compare_sample(g, sol.p, seed, idx, val, n, lam, sol.lam)
+    assert k == sol.k or solver == "greedy", (k, sol.k)
+    if solver == "greedy":
+        # the capped count reported is that of the returned lambda
+        assert k == int(np.count_nonzero(lam * np.abs(g.astype(np.float64)) >= 1.0)) or np.isinf(lam)
+    _say(f"   ok nnz={n} oracle={rep['nnz_oracle']} excused={rep['excused']} lam={lam:.12g}")
+
+
+@pytest.mark.parametrize("iters", [0, 1, 3, 8])
+def test_greedy_iterations(gs, iters):
+    g = W.t_mixture(150000, 11)
+    _say(f"[greedy-iters] T={iters}")
+    for rho in (0.01, 0.1, 0.3):
+        sol = oracle.solve_greedy(g, rho, iters)
+        idx, val, n, lam, k, fl = _run_row(gs, g, rho, "greedy", 5, iters=iters, cap=g.size)
+        compare_sample(g, sol.p, 5, idx, val, n, lam, sol.lam)
+
+
+def test_exact_is_bit_identical_lambda(gs):
+    """Exact sums on both sides: the exact solver's lambda must match the oracle's to the bit."""
+    for maker, rho in [(lambda: W.t_mixture(300000, 21), 0.05), (lambda: W.normal(100000, 22), 0.2),
+                       (lambda: W.integer_ties(80000, 23), 0.3), (lambda: W.wide_range(90000, 24), 0.02)]:
+        g = maker()
+        sol = oracle.solve_exact(g, rho)
+        _, _, _, lam, k, fl = _run_row(gs, g, rho, "exact", 1, cap=1)
+        _say(f"[bit-lambda] d={g.size} rho={rho} gpu={lam!r} oracle={sol.lam!r} k={k}/{sol.k}")
+        assert lam == sol.lam and k == sol.k
+
+
+@pytest.mark.parametrize("solver", ["greedy", "exact"])
+def test_probs_parity(gs, solver):
+    for maker, rho in [(lambda: W.t_mixture(100001, 31), 0.1), (lambda: W.normal(65536, 32), 0.01),
+                       (lambda: W.integer_ties(30000, 33), 0.4)]:
+        g = maker()
+        _say(f"[probs] {solver} d={g.size} rho={rho}")
+        sol = oracle.solve(g, rho, solver, 2)
+        out = gs.sparsify_probs(torch.from_numpy(g).cuda(), rho, solver=solver, iters=2)
+        torch.cuda.synchronize()
+        compare_probs(out.p.cpu().numpy(), sol.p)
+        assert lam_close(float(out.lam.item()), sol.lam)
+        assert int(out.k.item()) == int(np.count_nonzero(out.p.cpu().numpy() == 1.0))
+        assert int(out.flags.item()) == 0
+
+
+def test_special_cases(gs):
+    d = 50000
+    z = np.zeros(d, np.float32)
+    _say("[special] all-zero")
+    idx, val, n, lam, k, fl = _run_row(gs, z, 0.1, "exact", 0, cap=10)
+    assert n == 0 and fl & gs.FLAG_ALLZERO
+    g = W.normal(d, 41)
+    g[::3] = 0
+    for solver in ("greedy", "exact"):
+        _say(f"[special] rho=0 and rho=1 {solver}")
+        idx, val, n, lam, k, fl = _run_row(gs, g, 0.0, solver, 0, cap=10)
+        assert n == 0 and lam == 0.0 and fl == 0
+        idx, val, n, lam, k, fl = _run_row(gs, g, 1.0, solver, 0, cap=d)
+        nzi = np.flatnonzero(g)
+        assert n == nzi.size and np.array_equal(idx, nzi) and np.array_equal(val, g[nzi])
+        assert np.isinf(lam) and k == nzi.size
+        idx, val, n, lam, k, fl = _run_row(gs, g, 0.6, solver, 0, cap=d)  # B >= nnz
+        assert n == nzi.size and np.array_equal(val, g[nzi])
+    for bad in (np.inf, -np.inf, np.nan):
+        h = W.normal(d, 42)
+        h[12345] = bad
+        _say(f"[special] non-finite {bad}")
+        idx, val, n, lam, k, fl = _run_row(gs, h, 0.1, "greedy", 0, cap=100)
+        assert n == 0 and fl & gs.FLAG_NONFINITE and np.isnan(lam)
+
+
+def test_capacity_overflow(gs):
+    g = W.t_mixture(200000, 51)
+    sol = oracle.solve_exact(g, 0.1)
+    cap = 777
+    _say("[overflow]")
+    idx, val, n, lam, k, fl = _run_row(gs, g, 0.1, "exact", 9, cap=cap)
+    assert fl & gs.FLAG_OVERFLOW and n > cap and idx.size == cap
+    compare_sample(g, sol.p, 9, idx, val, n, lam, sol.lam, cap=cap)
+
+
+def test_unaligned_scalar_path(gs):
+    g = W.t_mixture(100001, 61)
+    big = torch.from_numpy(np.concatenate([np.zeros(1, np.float32), g])).cuda()
+    view = big[1:]
+    assert view.data_ptr() % 16 != 0
+    _say("[unaligned]")
+    for solver in ("greedy", "exact"):
+        a = gs.sparsify_sample_compact(view, 0.05, seed=3, solver=solver, capacity=g.size)
+        b = gs.sparsify_sample_compact(torch.from_numpy(g).cuda(), 0.05, seed=3, solver=solver, capacity=g.size)
+        torch.cuda.synchronize()
+        na, nb = int(a.nnz.item()), int(b.nnz.item())
+        assert na == nb and float(a.lam.item()) == float(b.lam.item())
+        assert torch.equal(a.idx[:na], b.idx[:nb]) and torch.equal(a.val[:na], b.val[:nb])
+
+
+def test_batched_equals_rows_and_oracle(gs):
+    rows, d = 12, 50003
+    rng = np.random.default_rng(71)
+    g = np.stack([W.t_mixture(d, 100 + r) * np.float32(10.0 ** rng.uniform(-3, 0)) for r in range(rows)])
+    rhos = [0.01, 0.1, 0.3, 0.001] * 3
+    seeds = [1000 + r for r in range(rows)] + []
+    seeds[5] = 0xFFFFFFFFFFFFFFF1  # a seed using the high key word
+    ld = d + 13  # padded rows: leading dimension > d
+    buf = np.zeros((rows, ld), np.float32)
+    buf[:, :d] = g
+    gd = torch.from_numpy(buf).cuda()[:, :d]
+    for solver in ("greedy", "exact"):
+        _say(f"[batched] {solver} rows={rows} d={d} ld={ld}")
+        out = gs.sparsify_sample_compact_batched(gd, rhos, seeds, solver=solver, iters=2, cap_per_row=d)
+        torch.cuda.synchronize()
+        for r in range(rows):
+            n = int(out.nnz[r].item())
+            sol = oracle.solve(g[r], rhos[r], solver, 2)
+            compare_sample(g[r], sol.p, seeds[r], out.idx[r, :n].cpu().numpy(), out.val[r, :n].cpu().numpy(), n,
+                           float(out.lam[r].item()), sol.lam)
+            one = gs.sparsify_sample_compact(torch.from_numpy(g[r].copy()).cuda(), rhos[r], seed=seeds[r],
+                                             solver=solver, capacity=d)
+            torch.cuda.synchronize()
+            assert int(one.nnz.item()) == n
+            assert torch.equal(one.idx[:n], out.idx[r, :n]) and torch.equal(one.val[:n], out.val[r, :n])
+            assert float(one.lam.item()) == float(out.lam[r].item())
+
+
+def test_deterministic_reruns(gs):
+    g = torch.from_numpy(W.t_mixture(500000, 81)).cuda()
+    _say("[determinism]")
+    ref = gs.sparsify_sample_compact(g, 0.05, seed=4, solver="exact", capacity=500000)
+    torch.cuda.synchronize()
+    n = int(ref.nnz.item())
+    for _ in range(5):
+        o = gs.sparsify_sample_compact(g, 0.05, seed=4, solver="exact", capacity=500000)
+        torch.cuda.synchronize()
+        assert int(o.nnz.item()) == n and torch.equal(o.idx[:n], ref.idx[:n]) and torch.equal(o.val[:n], ref.val[:n])
+
+
+def test_bad_rho_row_flagged(gs):
+    g = torch.from_numpy(np.stack([W.normal(10000, 91), W.normal(10000, 92)])).cuda()
+    _say("[bad-rho]")
+    out = gs.sparsify_sample_compact_batched(g, [0.1, 1.5], [1, 2], cap_per_row=10000)
+    torch.cuda.synchronize()
+    assert int(out.flags[1].item()) & gs.FLAG_BADRHO and int(out.nnz[1].item()) == 0
+    assert int(out.flags[0].item()) == 0 and int(out.nnz[0].item()) > 0
+
+
+def test_unbiased_over_seeds(gs):
+    """E[Q(g)_i] = g_i: one batched call with the same row under S different seeds."""
+    d, S = 256, 8192
+    rng = np.random.default_rng(7)
+    g = (rng.standard_t(2, d) * 2).astype(np.float32)
+    g[:8] = 0
+    sol = oracle.solve_exact(g, 0.2)
+    p = sol.p
+    gd = torch.from_numpy(np.tile(g, (S, 1))).cuda()
+    _say("[unbiased]")
+    out = gs.sparsify_sample_compact_batched(gd, [0.2] * S, list(range(50_000, 50_000 + S)), solver="exact",
+                                             cap_per_row=d)
+    torch.cuda.synchronize()
+    nnz = out.nnz.cpu().numpy()
+    idx = out.idx.cpu().numpy()
+    val = out.val.cpu().numpy().astype(np.float64)
+    counts = np.zeros(d)
+    qsum = np.zeros(d)
+    for s in range(S):
+        n = nnz[s]
+        counts[idx[s, :n]] += 1
+        qsum[idx[s, :n]] += val[s, :n]
+    live = (p > 0) & (p < 1)
+    z = (counts[live] - S * p[live]) / np.sqrt(S * p[live] * (1 - p[live]))
+    m = z.size
+    assert np.count_nonzero(np.abs(z) > 3) <= m * 0.0027 + 4 * np.sqrt(m * 0.0027) + 1
+    assert abs((z ** 2).mean() - 1) < 4 * np.sqrt(2 / m) + 0.1
+    assert np.all(counts[p == 1] == S) and np.all(counts[p == 0] == 0)
+    sd = np.sqrt(np.where(p > 0, g.astype(np.float64) ** 2 * (1 - p) / np.where(p > 0, p, 1), 0) / S)
+    assert np.all(np.abs(qsum / S - g) <= 4 * sd + 1e-6 * np.abs(g))
+    assert abs(nnz.mean() - p.sum()) < 4 * np.sqrt((p * (1 - p)).sum() / S)
