@@ -84,39 +84,51 @@ GS_HD Fx fx_sub(const Fx& a, const Fx& b) {  // requires a >= b
   }
   return r;
 }
-GS_HD Fx fx_shifted(uint64_t v, int s) {  // v * 2^s, s in [0, 253]
-  Fx r = fx_zero();
-  int li = s >> 6, off = s & 63;
-  r.w[li] = v << off;
-  if (off && li + 1 < 5) r.w[li + 1] = v >> (64 - off);
+// Limb i of a, with i in [0, 5) known only at run time; written as selects so the accumulator
+// stays in registers (no dynamically indexed private array).
+GS_HD uint64_t fx_limb(const Fx& a, int i) {
+  uint64_t r = 0;
+#pragma unroll
+  for (int j = 0; j < 5; ++j) r = (j == i) ? a.w[j] : r;
   return r;
 }
-GS_HD bool fx_bit(const Fx& a, int k) { return (a.w[k >> 6] >> (k & 63)) & 1; }
+GS_HD Fx fx_shifted(uint64_t v, int s) {  // v * 2^s, s in [0, 253]
+  s = s < 0 ? 0 : (s > 255 ? 255 : s);
+  const int li = s >> 6, off = s & 63;
+  const uint64_t lo = v << off;
+  const uint64_t hi = off ? (v >> (64 - off)) : 0;
+  Fx r;
+#pragma unroll
+  for (int j = 0; j < 5; ++j) r.w[j] = (j == li) ? lo : ((j == li + 1) ? hi : 0);
+  return r;
+}
+GS_HD bool fx_bit(const Fx& a, int k) { return (fx_limb(a, k >> 6) >> (k & 63)) & 1; }
 GS_HD bool fx_any_below(const Fx& a, int k) {  // any set bit at positions [0, k)
   if (k <= 0) return false;
-  int li = k >> 6, off = k & 63;
-  for (int i = 0; i < li && i < 5; ++i)
-    if (a.w[i]) return true;
-  if (li < 5 && off && (a.w[li] & ((1ull << off) - 1))) return true;
-  return false;
+  const int li = k >> 6, off = k & 63;
+  bool any = false;
+#pragma unroll
+  for (int j = 0; j < 5; ++j) {
+    const uint64_t m = j < li ? ~0ull : ((j == li && off) ? ((1ull << off) - 1) : 0ull);
+    any = any || (a.w[j] & m) != 0;
+  }
+  return any;
 }
 // Round to the nearest double, ties to even.
 GS_HD double fx_to_double(const Fx& a) {
   int top = -1;
-  for (int i = 4; i >= 0; --i)
-    if (a.w[i]) {
-      top = i * 64 + 63 - __builtin_clzll(a.w[i]);
-      break;
-    }
+#pragma unroll
+  for (int i = 0; i < 5; ++i)
+    if (a.w[i]) top = i * 64 + 63 - __builtin_clzll(a.w[i]);
   if (top < 0) return 0.0;
   if (top < 53) return ldexp((double)a.w[0], -149);
-  int lo = top - 52;
-  int li = lo >> 6, off = lo & 63;
-  uint64_t m = a.w[li] >> off;
-  if (off && li + 1 < 5) m |= a.w[li + 1] << (64 - off);
+  const int lo = top - 52;
+  const int li = lo >> 6, off = lo & 63;
+  uint64_t m = fx_limb(a, li) >> off;
+  if (off) m |= fx_limb(a, li + 1) << (64 - off);
   m &= (1ull << 53) - 1;
-  bool rnd = fx_bit(a, lo - 1);
-  bool sticky = fx_any_below(a, lo - 1);
+  const bool rnd = fx_bit(a, lo - 1);
+  const bool sticky = fx_any_below(a, lo - 1);
   if (rnd && (sticky || (m & 1))) m += 1;
   return ldexp((double)m, lo - 149);
 }
@@ -313,8 +325,12 @@ __device__ __forceinline__ uint32_t load4(const float* __restrict__ row, int64_t
 }
 
 // ------------------------------------------------------------------------------------------
-// Block-wide helpers for the solver workgroup (kNT threads, uniform control flow).
+// The per-row solver: kernel k_solve, one workgroup of kNT threads per row. Every helper is
+// force-inlined into that kernel so its LDS and global pointers keep their address spaces and
+// no call frames or scratch are needed.
 // ------------------------------------------------------------------------------------------
+#define GS_DI __device__ __attribute__((always_inline)) inline
+
 struct HistLds {
   unsigned long long pk[kFine];  // (count << 44) | significand sum
   uint32_t mx[kFine];
@@ -332,14 +348,14 @@ struct SolveLds {
   int ired[kNT / 64];
   BinInfo bi;
   RowCtl c;  // working copy of the row's control block
-  int flag;
 };
-union SharedU {
-  HistLds h;
-  SolveLds s;
+struct Hists {
+  const Hist1* h1;
+  Hist2* h2;
+  Hist3* h3;
 };
 
-__device__ int block_max(SolveLds& s, int v) {
+GS_DI int block_max(SolveLds& s, int v) {
   for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
   if ((threadIdx.x & 63) == 0) s.ired[threadIdx.x >> 6] = v;
   __syncthreads();
@@ -348,7 +364,7 @@ __device__ int block_max(SolveLds& s, int v) {
   __syncthreads();
   return r;
 }
-__device__ int block_min(SolveLds& s, int v) {
+GS_DI int block_min(SolveLds& s, int v) {
   for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
   if ((threadIdx.x & 63) == 0) s.ired[threadIdx.x >> 6] = v;
   __syncthreads();
@@ -359,7 +375,7 @@ __device__ int block_min(SolveLds& s, int v) {
 }
 
 // Exclusive suffix scan over thread index: (exK, exW) = sum over threads t' > t.
-__device__ void suffix_scan(SolveLds& s, uint64_t k, const Fx& w, uint64_t& exK, Fx& exW) {
+GS_DI void suffix_scan(SolveLds& s, uint64_t k, const Fx& w, uint64_t& exK, Fx& exW) {
   const int r = kNT - 1 - (int)threadIdx.x;
   s.sk[0][r] = k;
   s.sw[0][r] = w;
@@ -397,21 +413,38 @@ struct Walk {
   Fx exW;
 };
 
-__device__ __forceinline__ Fx lvl_binW(const Lvl& L, int b, uint64_t sg) {
-  return fx_shifted(sg, binade_shift(L.E < 0 ? b : L.E));
+GS_DI Fx lvl_binW(const Lvl& L, int b, uint64_t sg) { return fx_shifted(sg, binade_shift(L.E < 0 ? b : L.E)); }
+
+GS_DI Lvl lvl1(const Hists& H) {
+  Lvl L;
+  L.cnt = H.h1->cnt; L.sig = H.h1->sig; L.mx = H.h1->mx;
+  L.nbins = kB1; L.per = 1; L.E = -1; L.Kaw = 0; L.Waw = fx_zero();
+  return L;
+}
+GS_DI Lvl lvl2(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
+  Lvl L;
+  L.cnt = H.h2->cnt; L.sig = H.h2->sig; L.mx = H.h2->mx;
+  L.nbins = kB2; L.per = kB2 / kNT; L.E = (int)E; L.Kaw = Kaw; L.Waw = Waw;
+  return L;
+}
+GS_DI Lvl lvl3(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
+  Lvl L;
+  L.cnt = H.h3->cnt; L.sig = H.h3->sig; L.mx = H.h3->mx;
+  L.nbins = kB3; L.per = kB3 / kNT; L.E = (int)E; L.Kaw = Kaw; L.Waw = Waw;
+  return L;
 }
 
-__device__ void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
+GS_DI void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
   uint64_t k = 0;
   Fx W = fx_zero();
   const int b0 = threadIdx.x * L.per;
   for (int j = 0; j < L.per; ++j) {
-    int b = b0 + j;
+    const int b = b0 + j;
     if (b < L.nbins) {
-      uint64_t c = ald64(&L.cnt[b]);
+      const uint64_t c = L.cnt[b];
       if (c) {
         k += c;
-        fx_add(W, lvl_binW(L, b, ald64(&L.sig[b])));
+        fx_add(W, lvl_binW(L, b, L.sig[b]));
       }
     }
   }
@@ -421,21 +454,21 @@ __device__ void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
 }
 
 // Aggregates above bin b and the bin's own totals, broadcast to every thread (b uniform).
-__device__ void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo& out) {
+GS_DI void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo& out) {
   if ((int)threadIdx.x == b / L.per) {
     uint64_t K = w.exK;
     Fx W = w.exW;
     for (int j = L.per - 1; j >= 0; --j) {
-      int bb = threadIdx.x * L.per + j;
+      const int bb = threadIdx.x * L.per + j;
       if (bb >= L.nbins) continue;
-      uint64_t c = ald64(&L.cnt[bb]);
-      Fx wb = c ? lvl_binW(L, bb, ald64(&L.sig[bb])) : fx_zero();
+      const uint64_t c = L.cnt[bb];
+      const Fx wb = c ? lvl_binW(L, bb, L.sig[bb]) : fx_zero();
       if (bb == b) {
         s.bi.Kab = K;
         s.bi.Wab = W;
         s.bi.cnt = c;
         s.bi.Wb = wb;
-        s.bi.mx = ald32(&L.mx[bb]);
+        s.bi.mx = L.mx[bb];
         break;
       }
       K += c;
@@ -450,27 +483,26 @@ __device__ void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, Bi
 // Exact solver step on one level: b1 = highest non-empty bin whose maximum v satisfies
 // (B - #{a > v}) * v <= fl(S - sum{a > v}) (the density-budget form of Algorithm 2's criterion,
 // evaluated at a data value), b2 = lowest non-empty bin above b1 (INT_MAX if none).
-__device__ void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLds& s, int& b1,
-                          int& b2) {
+GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
   int best = -1;
   uint64_t K = w.exK;
   Fx W = w.exW;
   for (int j = L.per - 1; j >= 0 && best < 0; --j) {
-    int b = threadIdx.x * L.per + j;
+    const int b = threadIdx.x * L.per + j;
     if (b >= L.nbins) continue;
-    uint64_t c = ald64(&L.cnt[b]);
+    const uint64_t c = L.cnt[b];
     if (!c) continue;
-    double v = key_value(ald32(&L.mx[b]));
-    double T1 = fx_to_double(fx_sub(S, W));
+    const double v = key_value(L.mx[b]);
+    const double T1 = fx_to_double(fx_sub(S, W));
     if ((B - (double)K) * v <= T1) best = b;
     K += c;
-    fx_add(W, lvl_binW(L, b, ald64(&L.sig[b])));
+    fx_add(W, lvl_binW(L, b, L.sig[b]));
   }
   b1 = block_max(s, best);
   int lowest = INT_MAX;
   for (int j = 0; j < L.per; ++j) {
-    int b = threadIdx.x * L.per + j;
-    if (b < L.nbins && b > b1 && ald64(&L.cnt[b])) {
+    const int b = threadIdx.x * L.per + j;
+    if (b < L.nbins && b > b1 && L.cnt[b]) {
       lowest = b;
       break;
     }
@@ -478,275 +510,239 @@ __device__ void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, So
   b2 = block_min(s, lowest);
 }
 
-// ------------------------------------------------------------------------------------------
-// The per-row solver. Runs in the last workgroup of a histogram pass, all kNT threads.
-// ------------------------------------------------------------------------------------------
-struct Solver {
-  const Args& a;
-  int64_t row;
-  RowCtl* gc;
-  SolveLds& s;
-  Hist1* h1;
-  Hist2* h2;
-  Hist3* h3;
+// Thread 0 alone writes the shared control block. Every write is preceded by a barrier, so no
+// thread can still be reading a field that decides its control flow (which must stay uniform
+// across the workgroup) while it changes.
+GS_DI void sv_finalize(SolveLds& s, double lam, uint32_t tcap) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    s.c.lam = lam;
+    s.c.tcap = tcap;
+    s.c.inv_lam = (lam > 0.0 && lam < INFINITY) ? (float)(1.0 / lam) : 0.0f;
+    s.c.done = 1;
+    s.c.need = 0;
+  }
+  __syncthreads();
+}
 
-  __device__ Lvl lvl1() const {
-    Lvl L;
-    L.cnt = h1->cnt; L.sig = h1->sig; L.mx = h1->mx;
-    L.nbins = kB1; L.per = 1; L.E = -1; L.Kaw = 0; L.Waw = fx_zero();
-    return L;
+// Ask for a histogram of binade E (level 2) or of keys [base, base + 2048) (level 3).
+GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32_t base) {
+  __syncthreads();
+  if (level == 2) {
+    for (int b = threadIdx.x; b < kB2; b += kNT) { H.h2->cnt[b] = 0; H.h2->sig[b] = 0; H.h2->mx[b] = 0; }
+  } else {
+    for (int b = threadIdx.x; b < kB3; b += kNT) { H.h3->cnt[b] = 0; H.h3->sig[b] = 0; H.h3->mx[b] = 0; }
   }
-  __device__ Lvl lvl2(uint32_t E, uint64_t Kaw, const Fx& Waw) const {
-    Lvl L;
-    L.cnt = h2->cnt; L.sig = h2->sig; L.mx = h2->mx;
-    L.nbins = kB2; L.per = kB2 / kNT; L.E = (int)E; L.Kaw = Kaw; L.Waw = Waw;
-    return L;
-  }
-  __device__ Lvl lvl3(uint32_t E, uint64_t Kaw, const Fx& Waw) const {
-    Lvl L;
-    L.cnt = h3->cnt; L.sig = h3->sig; L.mx = h3->mx;
-    L.nbins = kB3; L.per = kB3 / kNT; L.E = (int)E; L.Kaw = Kaw; L.Waw = Waw;
-    return L;
-  }
-
-  __device__ void finalize(double lam, uint32_t tcap) {
-    if (threadIdx.x == 0) {
-      s.c.lam = lam;
-      s.c.tcap = tcap;
-      s.c.inv_lam = (lam > 0.0 && lam < INFINITY) ? (float)(1.0 / lam) : 0.0f;
-      s.c.done = 1;
-      s.c.need = 0;
-    }
-    __syncthreads();
-  }
-
-  // Ask for a histogram of binade E (level 2) or of keys [base, base + 2048) (level 3).
-  __device__ void request(int level, uint32_t E, uint32_t base) {
+  if (threadIdx.x == 0) {
+    s.c.need = level;
     if (level == 2) {
-      for (int b = threadIdx.x; b < kB2; b += kNT) { h2->cnt[b] = 0; h2->sig[b] = 0; h2->mx[b] = 0; }
+      s.c.l2exp = E;
+      s.c.l3base = kNone;
     } else {
-      for (int b = threadIdx.x; b < kB3; b += kNT) { h3->cnt[b] = 0; h3->sig[b] = 0; h3->mx[b] = 0; }
+      s.c.l3base = base;
     }
-    if (threadIdx.x == 0) {
-      s.c.need = level;
-      if (level == 2) {
-        s.c.l2exp = E;
-        s.c.l3base = kNone;
-      } else {
-        s.c.l3base = base;
-      }
-    }
-    __syncthreads();
   }
+  __syncthreads();
+}
 
-  // Count and exact sum of keys >= t. Returns 0 when resolved, else the level to request (and
-  // leaves the request made).
-  __device__ int query(uint32_t t, uint64_t& K, Fx& W) {
-    Lvl L1 = lvl1();
-    Walk w1;
-    lvl_scan(L1, s, w1);
-    const int e = (int)(t >> 23);
-    BinInfo i1;
-    lvl_bin_info(L1, w1, e, s, i1);
-    if ((t & 0x7FFFFFu) == 0) {
-      K = i1.Kab + i1.cnt; W = i1.Wab; fx_add(W, i1.Wb);
-      return 0;
-    }
-    if (i1.cnt == 0 || i1.mx < t) {
-      K = i1.Kab; W = i1.Wab;
-      return 0;
-    }
-    if (s.c.l2exp != (uint32_t)e) {
-      request(2, (uint32_t)e, 0);
-      return 2;
-    }
-    Lvl L2 = lvl2((uint32_t)e, i1.Kab, i1.Wab);
-    Walk w2;
-    lvl_scan(L2, s, w2);
-    const int sb = (int)((t >> 11) & (kB2 - 1));
-    BinInfo i2;
-    lvl_bin_info(L2, w2, sb, s, i2);
-    if ((t & 2047u) == 0) {
-      K = i2.Kab + i2.cnt; W = i2.Wab; fx_add(W, i2.Wb);
-      return 0;
-    }
-    if (i2.cnt == 0 || i2.mx < t) {
-      K = i2.Kab; W = i2.Wab;
-      return 0;
-    }
-    const uint32_t base = t & ~2047u;
-    if (s.c.l3base != base) {
-      request(3, 0, base);
-      return 3;
-    }
-    Lvl L3 = lvl3((uint32_t)e, i2.Kab, i2.Wab);
-    Walk w3;
-    lvl_scan(L3, s, w3);
-    BinInfo i3;
-    lvl_bin_info(L3, w3, (int)(t - base), s, i3);
-    K = i3.Kab + i3.cnt; W = i3.Wab; fx_add(W, i3.Wb);
+// Count and exact sum of keys >= t. Returns 0 when resolved, else the level it requested.
+GS_DI int sv_query(SolveLds& s, const Hists& H, uint32_t t, uint64_t& K, Fx& W) {
+  const Lvl L1 = lvl1(H);
+  Walk w1;
+  lvl_scan(L1, s, w1);
+  const int e = (int)(t >> 23);
+  BinInfo i1;
+  lvl_bin_info(L1, w1, e, s, i1);
+  if ((t & 0x7FFFFFu) == 0) {
+    K = i1.Kab + i1.cnt; W = i1.Wab; fx_add(W, i1.Wb);
     return 0;
   }
-
-  // Algorithm 3 in scale form: lambda_{j+1} = (B - k_j) / U_j, stop when it does not grow.
-  __device__ void greedy() {
-    while (s.c.iter < s.c.T) {
-      const double lam = s.c.lam;
-      uint64_t K;
-      Fx W;
-      if (query(cap_key(lam), K, W)) return;
-      const double U = fx_to_double(fx_sub(s.c.S, W));
-      if (U == 0.0) break;
-      const double ln = (s.c.B - (double)K) / U;
-      if (!(ln > lam)) break;
-      if (threadIdx.x == 0) {
-        s.c.lam = ln;
-        s.c.iter += 1;
-      }
-      __syncthreads();
-    }
-    finalize(s.c.lam, cap_key(s.c.lam));
+  if (i1.cnt == 0 || i1.mx < t) {
+    K = i1.Kab; W = i1.Wab;
+    return 0;
   }
-
-  __device__ void exact_finish(uint64_t K, const Fx& W, uint32_t tcap) {
-    const double T1 = fx_to_double(fx_sub(s.c.S, W));
-    finalize((s.c.B - (double)K) / T1, tcap);
+  if (s.c.l2exp != (uint32_t)e) {
+    sv_request(s, H, 2, (uint32_t)e, 0);
+    return 2;
   }
+  const Lvl L2 = lvl2(H, (uint32_t)e, i1.Kab, i1.Wab);
+  Walk w2;
+  lvl_scan(L2, s, w2);
+  const int sb = (int)((t >> 11) & (kB2 - 1));
+  BinInfo i2;
+  lvl_bin_info(L2, w2, sb, s, i2);
+  if ((t & 2047u) == 0) {
+    K = i2.Kab + i2.cnt; W = i2.Wab; fx_add(W, i2.Wb);
+    return 0;
+  }
+  if (i2.cnt == 0 || i2.mx < t) {
+    K = i2.Kab; W = i2.Wab;
+    return 0;
+  }
+  const uint32_t base = t & ~2047u;
+  if (s.c.l3base != base) {
+    sv_request(s, H, 3, 0, base);
+    return 3;
+  }
+  const Lvl L3 = lvl3(H, (uint32_t)e, i2.Kab, i2.Wab);
+  Walk w3;
+  lvl_scan(L3, s, w3);
+  BinInfo i3;
+  lvl_bin_info(L3, w3, (int)(t - base), s, i3);
+  K = i3.Kab + i3.cnt; W = i3.Wab; fx_add(W, i3.Wb);
+  return 0;
+}
 
-  // The exact solver descends levels: at each one it finds the highest bin whose maximum passes
-  // the criterion (b1) and the lowest occupied bin above it (b2); the answer is b1's maximum
-  // unless b2 holds two or more values that could still pass, in which case b2 is refined.
-  __device__ void exact() {
-    const int level = s.c.stage;
-    Lvl L1 = lvl1();
-    Walk w1;
-    lvl_scan(L1, s, w1);
-    Lvl L = L1;
-    Walk w = w1;
-    uint32_t E = 0;
-    if (level >= 2) {
-      E = s.c.l2exp;
-      BinInfo i1;
-      lvl_bin_info(L1, w1, (int)E, s, i1);
-      Lvl L2 = lvl2(E, i1.Kab, i1.Wab);
-      Walk w2;
-      lvl_scan(L2, s, w2);
-      L = L2;
-      w = w2;
-      if (level == 3) {
-        BinInfo i2;
-        lvl_bin_info(L2, w2, (int)((s.c.l3base >> 11) & (kB2 - 1)), s, i2);
-        Lvl L3 = lvl3(E, i2.Kab, i2.Wab);
-        Walk w3;
-        lvl_scan(L3, s, w3);
-        L = L3;
-        w = w3;
-      }
+// Algorithm 3 in scale form: lambda_{j+1} = (B - k_j) / U_j, stop when it does not grow.
+GS_DI void sv_greedy(SolveLds& s, const Hists& H) {
+  while (s.c.iter < s.c.T) {
+    const double lam = s.c.lam;
+    uint64_t K;
+    Fx W;
+    if (sv_query(s, H, cap_key(lam), K, W)) return;
+    const double U = fx_to_double(fx_sub(s.c.S, W));
+    if (U == 0.0) break;
+    const double ln = (s.c.B - (double)K) / U;
+    if (!(ln > lam)) break;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      s.c.lam = ln;
+      s.c.iter += 1;
     }
-    int b1, b2;
-    lvl_exact(L, w, s.c.B, s.c.S, s, b1, b2);
-    if (b1 < 0) {
-      // no value in this window passes: the answer is the candidate found one level up
-      if (s.c.fbValid) {
-        exact_finish(s.c.fbK, s.c.fbW, s.c.fbTcap);
-      } else {
-        if (threadIdx.x == 0) s.c.flags |= kFlagInternal;
-        finalize(NAN, kKeyInf);
-      }
-      return;
-    }
+    __syncthreads();
+  }
+  const double lam = s.c.lam;
+  sv_finalize(s, lam, cap_key(lam));
+}
+
+GS_DI void sv_exact_finish(SolveLds& s, uint64_t K, const Fx& W, uint32_t tcap) {
+  const double T1 = fx_to_double(fx_sub(s.c.S, W));
+  const double lam = (s.c.B - (double)K) / T1;
+  sv_finalize(s, lam, tcap);
+}
+
+// The exact solver descends levels: at each one it finds the highest bin whose maximum passes
+// the criterion (b1) and the lowest occupied bin above it (b2); the answer is b1's maximum
+// unless b2 holds two or more values that could still pass, in which case b2 is refined.
+GS_DI void sv_exact(SolveLds& s, const Hists& H) {
+  const int level = s.c.stage;
+  const Lvl L1 = lvl1(H);
+  Walk w1;
+  lvl_scan(L1, s, w1);
+  Lvl L = L1;
+  Walk w = w1;
+  uint32_t E = 0;
+  if (level >= 2) {
+    E = s.c.l2exp;
     BinInfo i1;
-    lvl_bin_info(L, w, b1, s, i1);
-    const uint32_t cand_tcap = i1.mx + 1;
-    if (b2 != INT_MAX && level < 3) {
+    lvl_bin_info(L1, w1, (int)E, s, i1);
+    const Lvl L2 = lvl2(H, E, i1.Kab, i1.Wab);
+    Walk w2;
+    lvl_scan(L2, s, w2);
+    L = L2;
+    w = w2;
+    if (level == 3) {
       BinInfo i2;
-      lvl_bin_info(L, w, b2, s, i2);
-      if (i2.cnt >= 2) {
-        if (threadIdx.x == 0) {
-          s.c.fbValid = 1;
-          s.c.fbK = i1.Kab;
-          s.c.fbW = i1.Wab;
-          s.c.fbTcap = cand_tcap;
-          s.c.stage = level + 1;
-        }
-        __syncthreads();
-        if (level == 1) request(2, (uint32_t)b2, 0);
-        else request(3, 0, (E << 23) | ((uint32_t)b2 << 11));
-        return;
-      }
+      lvl_bin_info(L2, w2, (int)((s.c.l3base >> 11) & (kB2 - 1)), s, i2);
+      const Lvl L3 = lvl3(H, E, i2.Kab, i2.Wab);
+      Walk w3;
+      lvl_scan(L3, s, w3);
+      L = L3;
+      w = w3;
     }
-    exact_finish(i1.Kab, i1.Wab, cand_tcap);
   }
-
-  // First solve after the statistics pass: totals and the special cases.
-  __device__ void start() {
-    Lvl L1 = lvl1();
-    Walk w1;
-    lvl_scan(L1, s, w1);
-    // total of all finite keys = everything above bin 0 plus bin 0, minus bin 255 (non-finite)
-    BinInfo i0, inf;
-    lvl_bin_info(L1, w1, 0, s, i0);
-    lvl_bin_info(L1, w1, 255, s, inf);
-    if (threadIdx.x == 0) {
-      Fx tot = i0.Wab;
-      fx_add(tot, i0.Wb);
-      s.c.S = tot;  // bin 255 holds only non-finite keys; its significand sum is never used
-      if (inf.cnt) {
-        Fx t2 = fx_sub(tot, inf.Wb);
-        s.c.S = t2;
-        s.c.flags |= GSPAR_FLAG_NONFINITE;
-      }
-      s.c.stage = 1;
-    }
-    __syncthreads();
-    const uint64_t nnz = (uint64_t)a.d - s.c.zeros;
-    if (s.c.flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO)) {
-      finalize(NAN, kKeyInf);
-      return;
-    }
-    if (nnz == 0) {
-      if (threadIdx.x == 0) s.c.flags |= GSPAR_FLAG_ALLZERO;
-      __syncthreads();
-      finalize(INFINITY, 1);
-      return;
-    }
-    if (s.c.B >= (double)nnz) {
-      finalize(INFINITY, 1);
-      return;
-    }
-    if (s.c.B == 0.0) {
-      finalize(0.0, kKeyInf);
-      return;
-    }
-    if (s.c.solver == GSPAR_GREEDY) {
-      if (threadIdx.x == 0) {
-        s.c.lam = s.c.B / fx_to_double(s.c.S);
-        s.c.iter = 0;
-      }
-      __syncthreads();
-      greedy();
+  int b1, b2;
+  lvl_exact(L, w, s.c.B, s.c.S, s, b1, b2);
+  if (b1 < 0) {
+    // no value in this window passes: the answer is the candidate found one level up
+    if (s.c.fbValid) {
+      const uint64_t K = s.c.fbK;
+      const Fx W = s.c.fbW;
+      const uint32_t tc = s.c.fbTcap;
+      sv_exact_finish(s, K, W, tc);
     } else {
-      exact();
+      __syncthreads();
+      if (threadIdx.x == 0) s.c.flags |= kFlagInternal;
+      sv_finalize(s, NAN, kKeyInf);
+    }
+    return;
+  }
+  BinInfo i1;
+  lvl_bin_info(L, w, b1, s, i1);
+  const uint32_t cand_tcap = i1.mx + 1;
+  if (b2 != INT_MAX && level < 3) {
+    BinInfo i2;
+    lvl_bin_info(L, w, b2, s, i2);
+    if (i2.cnt >= 2) {
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        s.c.fbValid = 1;
+        s.c.fbK = i1.Kab;
+        s.c.fbW = i1.Wab;
+        s.c.fbTcap = cand_tcap;
+        s.c.stage = level + 1;
+      }
+      __syncthreads();
+      if (level == 1) sv_request(s, H, 2, (uint32_t)b2, 0);
+      else sv_request(s, H, 3, 0, (E << 23) | ((uint32_t)b2 << 11));
+      return;
     }
   }
+  sv_exact_finish(s, i1.Kab, i1.Wab, cand_tcap);
+}
 
-  __device__ void run() {
+// First solve after the statistics pass: totals and the special cases.
+GS_DI void sv_start(SolveLds& s, const Hists& H, int64_t d) {
+  const Lvl L1 = lvl1(H);
+  Walk w1;
+  lvl_scan(L1, s, w1);
+  BinInfo i0, inf;
+  lvl_bin_info(L1, w1, 0, s, i0);
+  lvl_bin_info(L1, w1, 255, s, inf);
+  if (threadIdx.x == 0) {
+    // every finite key lies in bins 0..254; bin 255 counts only Inf/NaN
+    Fx tot = i0.Wab;
+    fx_add(tot, i0.Wb);
+    if (inf.cnt) {
+      tot = fx_sub(tot, inf.Wb);
+      s.c.flags |= GSPAR_FLAG_NONFINITE;
+    }
+    s.c.S = tot;
+    s.c.stage = 1;
+  }
+  __syncthreads();
+  const uint64_t nnz = (uint64_t)d - s.c.zeros;
+  if (s.c.flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO)) {
+    sv_finalize(s, NAN, kKeyInf);
+    return;
+  }
+  if (nnz == 0) {
+    __syncthreads();
+    if (threadIdx.x == 0) s.c.flags |= GSPAR_FLAG_ALLZERO;
+    __syncthreads();
+    sv_finalize(s, INFINITY, 1);
+    return;
+  }
+  if (s.c.B >= (double)nnz) {
+    sv_finalize(s, INFINITY, 1);
+    return;
+  }
+  if (s.c.B == 0.0) {
+    sv_finalize(s, 0.0, kKeyInf);
+    return;
+  }
+  if (s.c.solver == GSPAR_GREEDY) {
+    __syncthreads();
     if (threadIdx.x == 0) {
-      s.c = *gc;
-      s.c.zeros = ald64(&gc->zeros);
-      s.c.need = 0;
-      s.c.arrive = 0;
+      s.c.lam = s.c.B / fx_to_double(s.c.S);
+      s.c.iter = 0;
     }
     __syncthreads();
-    if (s.c.done) return;
-    if (s.c.stage == 0) start();
-    else if (s.c.solver == GSPAR_GREEDY) greedy();
-    else exact();
-    __syncthreads();
-    if (threadIdx.x == 0) *gc = s.c;
-    __threadfence();
+    sv_greedy(s, H);
+  } else {
+    sv_exact(s, H);
   }
-};
+}
 
 // ------------------------------------------------------------------------------------------
 // Kernels.
@@ -776,16 +772,16 @@ __global__ void __launch_bounds__(256) k_init(Args a) {
   }
 }
 
-// Streaming statistics pass. Grid: rows * nb workgroups of kNT threads.
+// Streaming statistics pass. Grid: rows * nb workgroups of kNT threads; each flushes its
+// histogram as per-binade totals (count, exact significand sum, maximum key).
 template <bool VEC>
-__global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))) k_stats(Args a) {
-  __shared__ SharedU sm;
-  __shared__ uint32_t s_last;
+__global__ void __launch_bounds__(kNT) k_stats(Args a) {
+  __shared__ HistLds sm;
   const int64_t row = blockIdx.x / a.nb;
   const int64_t blk = blockIdx.x % a.nb;
   for (int b = threadIdx.x; b < kFine; b += kNT) {
-    sm.h.pk[b] = 0;
-    sm.h.mx[b] = 0;
+    sm.pk[b] = 0;
+    sm.mx[b] = 0;
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + row * a.ld;
@@ -802,8 +798,8 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))
         zeros += (m >> c) & 1;
       } else {
         const uint32_t f = key >> 19;
-        atomicAdd(&sm.h.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
-        atomicMax(&sm.h.mx[f], key);
+        atomicAdd(&sm.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
+        atomicMax(&sm.mx[f], key);
       }
     }
   }
@@ -817,10 +813,10 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))
     uint64_t cnt = 0, sg = 0;
     uint32_t mx = 0;
     for (int j = 0; j < 16; ++j) {
-      const uint64_t p = sm.h.pk[e * 16 + j];
+      const uint64_t p = sm.pk[e * 16 + j];
       cnt += p >> 44;
       sg += p & ((1ull << 44) - 1);
-      mx = max(mx, sm.h.mx[e * 16 + j]);
+      mx = max(mx, sm.mx[e * 16 + j]);
     }
     if (cnt) {
       Hist1* h = h1_of(a, row);
@@ -829,21 +825,12 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))
       atomicMax(&h->mx[e], mx);
     }
   }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&ctl->arrive, 1u) == (uint32_t)(a.nb - 1);
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  Solver sv{a, row, ctl, sm.s, h1_of(a, row), h2_of(a, row), h3_of(a, row)};
-  sv.run();
 }
 
-// Refinement pass over one window of keys, when the row's solver asked for one.
+// Refinement pass over one window of keys, for the rows whose solver asked for one.
 template <bool VEC>
-__global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))) k_refine(Args a) {
-  __shared__ SharedU sm;
-  __shared__ uint32_t s_last;
+__global__ void __launch_bounds__(kNT) k_refine(Args a) {
+  __shared__ HistLds sm;
   const int64_t row = blockIdx.x / a.nb;
   const int64_t blk = blockIdx.x % a.nb;
   RowCtl* ctl = ctl_of(a, row);
@@ -868,8 +855,8 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))
   }
   const uint32_t span = (uint32_t)nbins << shift;
   for (int b = threadIdx.x; b < nbins; b += kNT) {
-    sm.h.pk[b] = 0;
-    sm.h.mx[b] = 0;
+    sm.pk[b] = 0;
+    sm.mx[b] = 0;
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + row * a.ld;
@@ -884,28 +871,40 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4, 8))
       const uint32_t rel = key - lo;
       if (key != 0 && rel < span) {
         const uint32_t b = rel >> shift;
-        atomicAdd(&sm.h.pk[b], (unsigned long long)((1ull << 44) + key_sig(key)));
-        atomicMax(&sm.h.mx[b], key);
+        atomicAdd(&sm.pk[b], (unsigned long long)((1ull << 44) + key_sig(key)));
+        atomicMax(&sm.mx[b], key);
       }
     }
   }
   __syncthreads();
   for (int b = threadIdx.x; b < nbins; b += kNT) {
-    const uint64_t p = sm.h.pk[b];
+    const uint64_t p = sm.pk[b];
     if (p) {
       atomicAdd((unsigned long long*)&gcnt[b], (unsigned long long)(p >> 44));
       atomicAdd((unsigned long long*)&gsig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
-      atomicMax(&gmx[b], sm.h.mx[b]);
+      atomicMax(&gmx[b], sm.mx[b]);
     }
   }
-  __threadfence();
+}
+
+// Solver for one row per workgroup: runs after every histogram pass and either finishes the row
+// (lambda and the capped threshold become final) or requests the next refinement window.
+__global__ void __launch_bounds__(kNT) k_solve(Args a) {
+  __shared__ SolveLds s;
+  const int64_t row = blockIdx.x;
+  RowCtl* gc = ctl_of(a, row);
+  if (threadIdx.x == 0) {
+    s.c = *gc;
+    s.c.need = 0;
+  }
   __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&ctl->arrive, 1u) == (uint32_t)(a.nb - 1);
+  if (s.c.done) return;
+  const Hists H{h1_of(a, row), h2_of(a, row), h3_of(a, row)};
+  if (s.c.stage == 0) sv_start(s, H, a.d);
+  else if (s.c.solver == GSPAR_GREEDY) sv_greedy(s, H);
+  else sv_exact(s, H);
   __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  Solver sv{a, row, ctl, sm.s, h1_of(a, row), h2_of(a, row), h3_of(a, row)};
-  sv.run();
+  if (threadIdx.x == 0) *gc = s.c;
 }
 
 // Sampling, amplification and order-preserving compaction. One ticketed tile of kTileElems
@@ -1190,10 +1189,14 @@ static int launch_solve(Args& a, hipStream_t s) {
   if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
   else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
   time_after(1, s);
+  const dim3 rgrid((unsigned)a.rows);
+  hipLaunchKernelGGL(k_solve, rgrid, dim3(kNT), 0, s, a);
+  // each greedy step may need a level-2 and a level-3 window, the exact solver at most both once
   const int R = a.solver == GSPAR_GREEDY ? 2 * a.T : 2;
   for (int r = 0; r < R; ++r) {
     if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
     else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
+    hipLaunchKernelGGL(k_solve, rgrid, dim3(kNT), 0, s, a);
   }
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }

@@ -1,0 +1,34 @@
+"""Builds the CPU emulation of libgspar (test infrastructure): the unchanged HIP source compiled
+with g++ against tests/emu/hip/hip_runtime.h, optionally with AddressSanitizer."""
+import os
+import subprocess
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+SRC = os.path.join(ROOT, "paper_1710_09854_amd", "csrc", "gspar.hip")
+OUT_DIR = os.path.join(HERE, "_build")
+
+
+def build(asan: bool = False) -> str:
+    os.makedirs(OUT_DIR, exist_ok=True)
+    out = os.path.join(OUT_DIR, "libgspar_emu_asan.so" if asan else "libgspar_emu.so")
+    if os.path.exists(out) and os.path.getmtime(out) > max(os.path.getmtime(SRC),
+                                                         os.path.getmtime(os.path.join(HERE, "hip", "hip_runtime.h"))):
+        return out
+    cmd = ["g++", "-std=c++20", "-O1", "-g", "-fPIC", "-shared", "-pthread", "-Wno-attributes",
+           "-Wno-unknown-pragmas", "-I", HERE, "-I", os.path.join(ROOT, "include"), "-x", "c++", SRC,
+           "-o", out + ".tmp"]
+    if asan:
+        cmd[1:1] = ["-fsanitize=address", "-fno-omit-frame-pointer"]
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+def asan_runtime() -> str:
+    return subprocess.run(["g++", "-print-file-name=libasan.so"], capture_output=True, text=True,
+                          check=True).stdout.strip()
+
+
+if __name__ == "__main__":
+    print(build(False), build(True))

@@ -1,0 +1,204 @@
+"""Runs the emulated library on host buffers and checks it against the oracle (test
+infrastructure). Usable in-process or as a script (so it can run under AddressSanitizer)."""
+import ctypes
+import os
+import sys
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import oracle  # noqa: E402
+import workloads as W  # noqa: E402
+from oracle.compare import compare_probs, compare_sample  # noqa: E402
+
+
+def load(path):
+    L = ctypes.CDLL(path)
+    vp, i64, u64, f64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_int
+    L.gspar_workspace_bytes.argtypes = [i64, i64, i32]
+    L.gspar_workspace_bytes.restype = ctypes.c_size_t
+    L.sparsify_sample_compact.argtypes = [vp, i64, f64, i32, i32, u64, vp, vp, i64, vp, vp, vp, vp, vp,
+                                          ctypes.c_size_t, vp]
+    L.sparsify_probs.argtypes = [vp, i64, f64, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_compact_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp, vp,
+                                                  vp, vp, vp, ctypes.c_size_t, vp]
+    return L
+
+
+def _aligned(nbytes):
+    raw = np.zeros(nbytes + 512, np.uint8)
+    off = (-raw.ctypes.data) % 256
+    return raw, raw[off:off + nbytes]
+
+
+def sample_row(L, g, rho, solver, seed, iters=2, cap=None):
+    d = g.size
+    cap = d if cap is None else cap
+    idx = np.zeros(max(cap, 1), np.int32)
+    val = np.zeros(max(cap, 1), np.float32)
+    nnz = np.zeros(1, np.int64)
+    lam = np.zeros(1)
+    k = np.zeros(1, np.int64)
+    fl = np.zeros(1, np.uint32)
+    sid = 0 if solver == "greedy" else 1
+    wsb = L.gspar_workspace_bytes(1, d, sid)
+    keep, ws = _aligned(wsb)
+    rc = L.sparsify_sample_compact(g.ctypes.data, d, rho, sid, iters, seed, idx.ctypes.data, val.ctypes.data, cap,
+                                   nnz.ctypes.data, lam.ctypes.data, k.ctypes.data, fl.ctypes.data, ws.ctypes.data,
+                                   wsb, None)
+    assert rc == 0, rc
+    n = int(nnz[0])
+    m = min(n, cap)
+    return idx[:m], val[:m], n, float(lam[0]), int(k[0]), int(fl[0])
+
+
+def probs_row(L, g, rho, solver, iters=2):
+    d = g.size
+    p = np.zeros(d, np.float32)
+    lam = np.zeros(1)
+    k = np.zeros(1, np.int64)
+    fl = np.zeros(1, np.uint32)
+    sid = 0 if solver == "greedy" else 1
+    wsb = L.gspar_workspace_bytes(1, d, sid)
+    keep, ws = _aligned(wsb)
+    rc = L.sparsify_probs(g.ctypes.data, d, rho, sid, iters, p.ctypes.data, lam.ctypes.data, k.ctypes.data,
+                          fl.ctypes.data, ws.ctypes.data, wsb, None)
+    assert rc == 0, rc
+    return p, float(lam[0]), int(k[0]), int(fl[0])
+
+
+CASES = [
+    ("normal_65536", lambda: W.normal(65536, 0)),
+    ("normal_spiked_65536", lambda: np.concatenate([W.normal(37, 9) * np.float32(40), W.normal(65536 - 37, 0)])),
+    ("tmix_50001", lambda: W.t_mixture(50001, 2)),
+    ("ties_20001", lambda: W.integer_ties(20001, 3)),
+    ("wide_range_30000", lambda: W.wide_range(30000, 4)),
+    ("two_level_20001", lambda: W.two_level(20001, 100, 50.0, 1.0, 5)),
+    ("approx_sparse_20000", lambda: W.approx_sparse(20000, 100, 0.05, 6)),
+    ("tiny_7", lambda: W.normal(7, 7)),
+]
+
+
+def run_all(path, rhos=(0.001, 0.01, 0.1, 0.5), verbose=True):
+    L = load(path)
+    n_checked = 0
+    for name, mk in CASES:
+        g = np.ascontiguousarray(mk(), np.float32)
+        for solver in ("greedy", "exact"):
+            for rho in rhos:
+                seed = 99 + len(name)
+                sol = oracle.solve(g, rho, solver, 2)
+                idx, val, n, lam, k, fl = sample_row(L, g, rho, solver, seed)
+                assert fl == 0, (name, solver, rho, fl)
+                rep = compare_sample(g, sol.p, seed, idx, val, n, lam, sol.lam)
+                if solver == "exact":
+                    assert lam == sol.lam and k == sol.k, (name, rho, lam, sol.lam, k, sol.k)
+                n_checked += 1
+                if verbose:
+                    print(f"{name} {solver} rho={rho}: nnz={n} excused={rep['excused']} lam={lam:.12g}", flush=True)
+        p, lam, k, fl = probs_row(L, g, 0.1, "exact")
+        compare_probs(p, oracle.solve_exact(g, 0.1).p)
+    return n_checked
+
+
+
+
+def batched(L, g2, rhos, seeds, solver, iters=2, cap=None, ld=None):
+    rows, d = g2.shape
+    ld = d if ld is None else ld
+    buf = np.zeros((rows, ld), np.float32)
+    buf[:, :d] = g2
+    cap = d if cap is None else cap
+    idx = np.zeros((rows, max(cap, 1)), np.int32)
+    val = np.zeros((rows, max(cap, 1)), np.float32)
+    nnz = np.zeros(rows, np.int64)
+    lam = np.zeros(rows)
+    k = np.zeros(rows, np.int64)
+    fl = np.zeros(rows, np.uint32)
+    r = np.ascontiguousarray(rhos, np.float64)
+    s = np.array([int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds], np.uint64)
+    sid = 0 if solver == "greedy" else 1
+    wsb = L.gspar_workspace_bytes(rows, d, sid)
+    keep, ws = _aligned(wsb)
+    rc = L.sparsify_sample_compact_batched(buf.ctypes.data, rows, d, ld, r.ctypes.data, sid, iters, s.ctypes.data,
+                                           idx.ctypes.data, val.ctypes.data, cap, nnz.ctypes.data, lam.ctypes.data,
+                                           k.ctypes.data, fl.ctypes.data, ws.ctypes.data, wsb, None)
+    assert rc == 0, rc
+    return idx, val, nnz, lam, k, fl
+
+
+def run_extra(path, verbose=True):
+    L = load(path)
+    # greedy step counts
+    g = W.t_mixture(30001, 11)
+    for T in (0, 1, 3, 8):
+        for rho in (0.01, 0.3):
+            sol = oracle.solve_greedy(g, rho, T)
+            idx, val, n, lam, k, fl = sample_row(L, g, rho, "greedy", 5, iters=T)
+            compare_sample(g, sol.p, 5, idx, val, n, lam, sol.lam)
+    # special cases
+    d = 10000
+    idx, val, n, lam, k, fl = sample_row(L, np.zeros(d, np.float32), 0.1, "exact", 0, cap=10)
+    assert n == 0 and fl & 4
+    h = W.normal(d, 41)
+    h[::3] = 0
+    nzi = np.flatnonzero(h)
+    for solver in ("greedy", "exact"):
+        idx, val, n, lam, k, fl = sample_row(L, h, 0.0, solver, 0, cap=10)
+        assert n == 0 and lam == 0.0 and fl == 0
+        for rho in (1.0, 0.7):
+            idx, val, n, lam, k, fl = sample_row(L, h, rho, solver, 0, cap=d)
+            assert n == nzi.size and np.array_equal(idx, nzi) and np.array_equal(val, h[nzi]) and np.isinf(lam)
+    for bad in (np.inf, np.nan):
+        q = W.normal(d, 42)
+        q[1234] = bad
+        idx, val, n, lam, k, fl = sample_row(L, q, 0.1, "greedy", 0, cap=100)
+        assert n == 0 and fl & 1 and np.isnan(lam)
+    # capacity overflow
+    g = W.t_mixture(40000, 51)
+    sol = oracle.solve_exact(g, 0.1)
+    idx, val, n, lam, k, fl = sample_row(L, g, 0.1, "exact", 9, cap=333)
+    assert fl & 2 and n > 333
+    compare_sample(g, sol.p, 9, idx, val, n, lam, sol.lam, cap=333)
+    # batched rows with a padded leading dimension, per-row rho and seeds, and a bad rho
+    rows, d = 6, 12003
+    rng = np.random.default_rng(71)
+    g2 = np.stack([W.t_mixture(d, 100 + r) * np.float32(10.0 ** rng.uniform(-3, 0)) for r in range(rows)])
+    rhos = [0.01, 0.1, 0.3, 0.001, 0.5, 0.05]
+    seeds = [1000, 1001, 0xFFFFFFFFFFFFFFF1, 3, 4, 5]
+    for solver in ("greedy", "exact"):
+        idx, val, nnz, lam, k, fl = batched(L, g2, rhos, seeds, solver, ld=d + 13)
+        for r in range(rows):
+            sol = oracle.solve(g2[r], rhos[r], solver, 2)
+            n = int(nnz[r])
+            compare_sample(g2[r], sol.p, seeds[r], idx[r, :n], val[r, :n], n, lam[r], sol.lam)
+            one = sample_row(L, np.ascontiguousarray(g2[r]), rhos[r], solver, seeds[r])
+            assert one[2] == n and np.array_equal(one[0], idx[r, :n]) and np.array_equal(one[1], val[r, :n])
+            assert one[3] == lam[r]
+    idx, val, nnz, lam, k, fl = batched(L, g2[:2], [0.1, 1.5], [1, 2], "greedy")
+    assert fl[1] & 8 and nnz[1] == 0 and fl[0] == 0 and nnz[0] > 0
+    # unaligned row start (scalar-load path)
+    g = W.t_mixture(20001, 61)
+    buf = np.zeros(20002 + 16, np.float32)
+    base = (-buf.ctypes.data // 4) % 4 + 1  # a start that is not 16-byte aligned
+    view = buf[base:base + 20001]
+    view[:] = g
+    assert view.ctypes.data % 16 != 0
+    a = sample_row(L, view, 0.05, "exact", 3)
+    b = sample_row(L, g, 0.05, "exact", 3)
+    assert a[2] == b[2] and np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    if verbose:
+        print("extra cases ok", flush=True)
+    return True
+
+
+if __name__ == "__main__":
+    which = sys.argv[2] if len(sys.argv) > 2 else "all"
+    if which in ("all", "extra"):
+        run_extra(sys.argv[1])
+    if which in ("all", "main"):
+        print("checked", run_all(sys.argv[1]))

@@ -1,0 +1,61 @@
+"""CPU runs of the HIP kernels through the host emulation in tests/emu (no GPU needed).
+
+The unchanged library source is compiled with g++ against a small HIP-runtime emulation in which
+workgroup threads are host threads. These tests check kernel indexing, the solver's control flow
+(every thread of a workgroup must pass the same barriers) and the whole pipeline against the
+oracle, on small inputs. GSPAR_EMU_FULL=1 runs the full sweep, GSPAR_EMU_ASAN=1 reruns it under
+AddressSanitizer in a subprocess."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, os.path.join(HERE, "emu"))
+
+import build as emu_build  # noqa: E402
+import runner  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def emu_lib():
+    return emu_build.build(asan=False)
+
+
+def test_emulated_special_batched_overflow_unaligned(emu_lib):
+    assert runner.run_extra(emu_lib, verbose=False)
+
+
+def test_emulated_parity_subset(emu_lib):
+    L = runner.load(emu_lib)
+    import oracle
+    import workloads as W
+    from oracle.compare import compare_sample
+
+    for name, mk in [("spiked", lambda: np.concatenate([W.normal(37, 9) * np.float32(40), W.normal(20000, 0)])),
+                     ("tmix", lambda: W.t_mixture(30001, 2)), ("ties", lambda: W.integer_ties(12001, 3))]:
+        g = np.ascontiguousarray(mk(), np.float32)
+        for solver in ("greedy", "exact"):
+            for rho in (0.01, 0.5):
+                sol = oracle.solve(g, rho, solver, 2)
+                idx, val, n, lam, k, fl = runner.sample_row(L, g, rho, solver, 77)
+                assert fl == 0
+                compare_sample(g, sol.p, 77, idx, val, n, lam, sol.lam)
+                if solver == "exact":
+                    assert lam == sol.lam and k == sol.k
+
+
+@pytest.mark.skipif(os.environ.get("GSPAR_EMU_FULL") != "1", reason="full emulated sweep: set GSPAR_EMU_FULL=1")
+def test_emulated_full_sweep(emu_lib):
+    assert runner.run_all(emu_lib, verbose=False) == 64
+
+
+@pytest.mark.skipif(os.environ.get("GSPAR_EMU_ASAN") != "1", reason="ASan sweep: set GSPAR_EMU_ASAN=1")
+def test_emulated_under_asan():
+    lib = emu_build.build(asan=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0", LD_PRELOAD=emu_build.asan_runtime())
+    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "all"], env=env,
+                       capture_output=True, text=True, timeout=3600)
+    assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-2000:]

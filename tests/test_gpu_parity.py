@@ -126,7 +126,7 @@ def test_special_cases(gs):
         nzi = np.flatnonzero(g)
         assert n == nzi.size and np.array_equal(idx, nzi) and np.array_equal(val, g[nzi])
         assert np.isinf(lam) and k == nzi.size
-        idx, val, n, lam, k, fl = _run_row(gs, g, 0.6, solver, 0, cap=d)  # B >= nnz
+        idx, val, n, lam, k, fl = _run_row(gs, g, 0.7, solver, 0, cap=d)  # B >= nnz
         assert n == nzi.size and np.array_equal(val, g[nzi])
     for bad in (np.inf, -np.inf, np.nan):
         h = W.normal(d, 42)
