@@ -233,18 +233,23 @@ struct Hist3 {
   uint64_t sig[kB3];
   uint32_t mx[kB3];
 };
+// Per binade b: count and exact sum of all keys in binades above b (filled by the first solve).
+struct L1Above {
+  uint64_t K[kB1];
+  Fx W[kB1];
+};
 
 GS_HD size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctl, h1, h2, h3, status, total;
+  size_t ctl, h1, h2, h3, a1, status, total;
   int64_t tiles;  // tiles per row of the sample pass
 };
 
 GS_HD Layout layout_of(int64_t rows, int64_t d) {
   Layout L;
   L.tiles = (d + kTileElems - 1) / kTileElems;
-  size_t off = 256;  // header: ticket counter
+  size_t off = 256;  // header (reserved)
   L.ctl = off;
   off += align256((size_t)rows * sizeof(RowCtl));
   L.h1 = off;
@@ -253,6 +258,8 @@ GS_HD Layout layout_of(int64_t rows, int64_t d) {
   off += align256((size_t)rows * sizeof(Hist2));
   L.h3 = off;
   off += align256((size_t)rows * sizeof(Hist3));
+  L.a1 = off;
+  off += align256((size_t)rows * sizeof(L1Above));
   L.status = off;
   off += align256((size_t)rows * (size_t)L.tiles * sizeof(uint64_t));
   L.total = off;
@@ -292,6 +299,9 @@ __device__ __forceinline__ Hist2* h2_of(const Args& a, int64_t r) {
 }
 __device__ __forceinline__ Hist3* h3_of(const Args& a, int64_t r) {
   return reinterpret_cast<Hist3*>(a.ws + a.lay.h3) + r;
+}
+__device__ __forceinline__ L1Above* a1_of(const Args& a, int64_t r) {
+  return reinterpret_cast<L1Above*>(a.ws + a.lay.a1) + r;
 }
 __device__ __forceinline__ uint64_t* status_of(const Args& a) {
   return reinterpret_cast<uint64_t*>(a.ws + a.lay.status);
@@ -344,7 +354,8 @@ struct BinInfo {
 };
 struct SolveLds {
   uint64_t sk[2][kNT];
-  Fx sw[2][kNT];
+  uint64_t ss[2][kNT];
+  Fx sw[2][kB1];
   int ired[kNT / 64];
   BinInfo bi;
   RowCtl c;  // working copy of the row's control block
@@ -353,6 +364,7 @@ struct Hists {
   const Hist1* h1;
   Hist2* h2;
   Hist3* h3;
+  L1Above* a1;
 };
 
 GS_DI int block_max(SolveLds& s, int v) {
@@ -374,105 +386,145 @@ GS_DI int block_min(SolveLds& s, int v) {
   return r;
 }
 
-// Exclusive suffix scan over thread index: (exK, exW) = sum over threads t' > t.
-GS_DI void suffix_scan(SolveLds& s, uint64_t k, const Fx& w, uint64_t& exK, Fx& exW) {
-  const int r = kNT - 1 - (int)threadIdx.x;
-  s.sk[0][r] = k;
-  s.sw[0][r] = w;
+// Level 1 (one bin per binade): exclusive suffix sums over the 256 binades, exact, written once
+// per row to the level-1 cache. Threads 0..255 own one binade each.
+GS_DI void l1_build(SolveLds& s, const Hists& H) {
+  const int t = threadIdx.x;
+  uint64_t k = 0;
+  Fx w = fx_zero();
+  if (t < kB1) {
+    k = H.h1->cnt[t];
+    if (k) w = fx_shifted(H.h1->sig[t], binade_shift(t));
+  }
+  const int r = kB1 - 1 - t;  // reversed index: a prefix over r is a suffix over binades
+  if (t < kB1) {
+    s.sk[0][r] = k;
+    s.sw[0][r] = w;
+  }
   __syncthreads();
   int cur = 0;
-  for (int off = 1; off < kNT; off <<= 1) {
-    uint64_t kk = s.sk[cur][r];
-    Fx ww = s.sw[cur][r];
-    if (r >= off) {
-      kk += s.sk[cur][r - off];
-      fx_add(ww, s.sw[cur][r - off]);
+  for (int off = 1; off < kB1; off <<= 1) {
+    uint64_t kk = 0;
+    Fx ww = fx_zero();
+    if (t < kB1) {
+      kk = s.sk[cur][r];
+      ww = s.sw[cur][r];
+      if (r >= off) {
+        kk += s.sk[cur][r - off];
+        fx_add(ww, s.sw[cur][r - off]);
+      }
     }
-    s.sk[cur ^ 1][r] = kk;
-    s.sw[cur ^ 1][r] = ww;
+    __syncthreads();
+    if (t < kB1) {
+      s.sk[cur ^ 1][r] = kk;
+      s.sw[cur ^ 1][r] = ww;
+    }
     __syncthreads();
     cur ^= 1;
   }
-  exK = s.sk[cur][r] - k;
-  exW = fx_sub(s.sw[cur][r], w);
+  if (t < kB1) {
+    H.a1->K[t] = s.sk[cur][r] - k;
+    H.a1->W[t] = fx_sub(s.sw[cur][r], w);
+  }
   __syncthreads();
 }
 
-// One histogram level: bins b = 0..nbins-1, thread t owns bins [t*per, t*per + per).
+GS_DI BinInfo l1_info(const Hists& H, int e) {
+  BinInfo i;
+  i.Kab = H.a1->K[e];
+  i.Wab = H.a1->W[e];
+  i.cnt = H.h1->cnt[e];
+  i.Wb = i.cnt ? fx_shifted(H.h1->sig[e], binade_shift(e)) : fx_zero();
+  i.mx = H.h1->mx[e];
+  return i;
+}
+
+// A refinement level inside one binade E: bins b = 0..nbins-1, thread t owns bins
+// [t*per, t*per + per). Within one binade, sums of significands are plain integers.
 struct Lvl {
   const uint64_t* cnt;
   const uint64_t* sig;
   const uint32_t* mx;
   int nbins, per;
-  int E;  // binade of every bin, or -1 when the bin index is the binade (level 1)
-  uint64_t Kaw;
-  Fx Waw;  // aggregates of keys above the window
+  int shift;     // binade_shift(E): value = significand * 2^shift (units of 2^-149)
+  uint64_t Kaw;  // count of keys above the window
+  Fx Waw;        // their exact sum
 };
 struct Walk {
-  uint64_t exK;
-  Fx exW;
+  uint64_t exK;  // count above this thread's bins, inside the window
+  uint64_t exS;  // significand sum above this thread's bins, inside the window
 };
 
-GS_DI Fx lvl_binW(const Lvl& L, int b, uint64_t sg) { return fx_shifted(sg, binade_shift(L.E < 0 ? b : L.E)); }
-
-GS_DI Lvl lvl1(const Hists& H) {
-  Lvl L;
-  L.cnt = H.h1->cnt; L.sig = H.h1->sig; L.mx = H.h1->mx;
-  L.nbins = kB1; L.per = 1; L.E = -1; L.Kaw = 0; L.Waw = fx_zero();
-  return L;
-}
 GS_DI Lvl lvl2(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
   Lvl L;
   L.cnt = H.h2->cnt; L.sig = H.h2->sig; L.mx = H.h2->mx;
-  L.nbins = kB2; L.per = kB2 / kNT; L.E = (int)E; L.Kaw = Kaw; L.Waw = Waw;
+  L.nbins = kB2; L.per = kB2 / kNT; L.shift = binade_shift((int)E); L.Kaw = Kaw; L.Waw = Waw;
   return L;
 }
 GS_DI Lvl lvl3(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
   Lvl L;
   L.cnt = H.h3->cnt; L.sig = H.h3->sig; L.mx = H.h3->mx;
-  L.nbins = kB3; L.per = kB3 / kNT; L.E = (int)E; L.Kaw = Kaw; L.Waw = Waw;
+  L.nbins = kB3; L.per = kB3 / kNT; L.shift = binade_shift((int)E); L.Kaw = Kaw; L.Waw = Waw;
   return L;
 }
 
+// Exclusive suffix scan over thread index of (count, significand sum).
 GS_DI void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
-  uint64_t k = 0;
-  Fx W = fx_zero();
+  uint64_t k = 0, sg = 0;
   const int b0 = threadIdx.x * L.per;
   for (int j = 0; j < L.per; ++j) {
     const int b = b0 + j;
     if (b < L.nbins) {
-      const uint64_t c = L.cnt[b];
-      if (c) {
-        k += c;
-        fx_add(W, lvl_binW(L, b, L.sig[b]));
-      }
+      k += L.cnt[b];
+      sg += L.sig[b];
     }
   }
-  suffix_scan(s, k, W, w.exK, w.exW);
-  w.exK += L.Kaw;
-  fx_add(w.exW, L.Waw);
+  const int r = kNT - 1 - (int)threadIdx.x;
+  s.sk[0][r] = k;
+  s.ss[0][r] = sg;
+  __syncthreads();
+  int cur = 0;
+  for (int off = 1; off < kNT; off <<= 1) {
+    uint64_t kk = s.sk[cur][r], ss = s.ss[cur][r];
+    if (r >= off) {
+      kk += s.sk[cur][r - off];
+      ss += s.ss[cur][r - off];
+    }
+    s.sk[cur ^ 1][r] = kk;
+    s.ss[cur ^ 1][r] = ss;
+    __syncthreads();
+    cur ^= 1;
+  }
+  w.exK = s.sk[cur][r] - k;
+  w.exS = s.ss[cur][r] - sg;
+  __syncthreads();
+}
+
+GS_DI Fx lvl_total(const Lvl& L, uint64_t K, uint64_t S, uint64_t& Kout) {
+  Kout = L.Kaw + K;
+  Fx W = L.Waw;
+  if (S) fx_add(W, fx_shifted(S, L.shift));
+  return W;
 }
 
 // Aggregates above bin b and the bin's own totals, broadcast to every thread (b uniform).
 GS_DI void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo& out) {
   if ((int)threadIdx.x == b / L.per) {
-    uint64_t K = w.exK;
-    Fx W = w.exW;
+    uint64_t K = w.exK, S = w.exS;
     for (int j = L.per - 1; j >= 0; --j) {
       const int bb = threadIdx.x * L.per + j;
       if (bb >= L.nbins) continue;
       const uint64_t c = L.cnt[bb];
-      const Fx wb = c ? lvl_binW(L, bb, L.sig[bb]) : fx_zero();
+      const uint64_t sg = L.sig[bb];
       if (bb == b) {
-        s.bi.Kab = K;
-        s.bi.Wab = W;
+        s.bi.Wab = lvl_total(L, K, S, s.bi.Kab);
         s.bi.cnt = c;
-        s.bi.Wb = wb;
+        s.bi.Wb = c ? fx_shifted(sg, L.shift) : fx_zero();
         s.bi.mx = L.mx[bb];
         break;
       }
       K += c;
-      fx_add(W, wb);
+      S += sg;
     }
   }
   __syncthreads();
@@ -480,23 +532,37 @@ GS_DI void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo
   __syncthreads();
 }
 
-// Exact solver step on one level: b1 = highest non-empty bin whose maximum v satisfies
-// (B - #{a > v}) * v <= fl(S - sum{a > v}) (the density-budget form of Algorithm 2's criterion,
-// evaluated at a data value), b2 = lowest non-empty bin above b1 (INT_MAX if none).
+// The density-budget form of Algorithm 2's criterion at a data value v, with k = #{a > v} and
+// W = exact sum{a > v}: (B - k) * v <= fl(S - W).
+GS_DI bool criterion(double B, const Fx& S, uint64_t k, const Fx& W, uint32_t vkey) {
+  return (B - (double)k) * key_value(vkey) <= fx_to_double(fx_sub(S, W));
+}
+
+// Exact solver step: b1 = highest non-empty bin whose maximum satisfies the criterion, b2 =
+// lowest non-empty bin above b1 (INT_MAX if none).
+GS_DI void l1_exact(const Hists& H, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
+  const int t = threadIdx.x;
+  int best = -1, occupied = INT_MAX;
+  if (t < kB1 && H.h1->cnt[t]) {
+    if (criterion(B, S, H.a1->K[t], H.a1->W[t], H.h1->mx[t])) best = t;
+  }
+  b1 = block_max(s, best);
+  if (t < kB1 && t > b1 && H.h1->cnt[t]) occupied = t;
+  b2 = block_min(s, occupied);
+}
 GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
   int best = -1;
-  uint64_t K = w.exK;
-  Fx W = w.exW;
+  uint64_t K = w.exK, Sg = w.exS;
   for (int j = L.per - 1; j >= 0 && best < 0; --j) {
     const int b = threadIdx.x * L.per + j;
     if (b >= L.nbins) continue;
     const uint64_t c = L.cnt[b];
     if (!c) continue;
-    const double v = key_value(L.mx[b]);
-    const double T1 = fx_to_double(fx_sub(S, W));
-    if ((B - (double)K) * v <= T1) best = b;
+    uint64_t Kt;
+    const Fx W = lvl_total(L, K, Sg, Kt);
+    if (criterion(B, S, Kt, W, L.mx[b])) best = b;
     K += c;
-    fx_add(W, lvl_binW(L, b, L.sig[b]));
+    Sg += L.sig[b];
   }
   b1 = block_max(s, best);
   int lowest = INT_MAX;
@@ -510,9 +576,6 @@ GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLd
   b2 = block_min(s, lowest);
 }
 
-// Thread 0 alone writes the shared control block. Every write is preceded by a barrier, so no
-// thread can still be reading a field that decides its control flow (which must stay uniform
-// across the workgroup) while it changes.
 GS_DI void sv_finalize(SolveLds& s, double lam, uint32_t tcap) {
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -547,12 +610,8 @@ GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32
 
 // Count and exact sum of keys >= t. Returns 0 when resolved, else the level it requested.
 GS_DI int sv_query(SolveLds& s, const Hists& H, uint32_t t, uint64_t& K, Fx& W) {
-  const Lvl L1 = lvl1(H);
-  Walk w1;
-  lvl_scan(L1, s, w1);
   const int e = (int)(t >> 23);
-  BinInfo i1;
-  lvl_bin_info(L1, w1, e, s, i1);
+  const BinInfo i1 = l1_info(H, e);
   if ((t & 0x7FFFFFu) == 0) {
     K = i1.Kab + i1.cnt; W = i1.Wab; fx_add(W, i1.Wb);
     return 0;
@@ -626,21 +685,21 @@ GS_DI void sv_exact_finish(SolveLds& s, uint64_t K, const Fx& W, uint32_t tcap) 
 // unless b2 holds two or more values that could still pass, in which case b2 is refined.
 GS_DI void sv_exact(SolveLds& s, const Hists& H) {
   const int level = s.c.stage;
-  const Lvl L1 = lvl1(H);
-  Walk w1;
-  lvl_scan(L1, s, w1);
-  Lvl L = L1;
-  Walk w = w1;
+  int b1, b2;
+  BinInfo c1, c2;  // the bins b1 and b2 at this level
   uint32_t E = 0;
-  if (level >= 2) {
+  if (level == 1) {
+    l1_exact(H, s.c.B, s.c.S, s, b1, b2);
+    if (b1 >= 0) c1 = l1_info(H, b1);
+    if (b2 != INT_MAX) c2 = l1_info(H, b2);
+  } else {
     E = s.c.l2exp;
-    BinInfo i1;
-    lvl_bin_info(L1, w1, (int)E, s, i1);
-    const Lvl L2 = lvl2(H, E, i1.Kab, i1.Wab);
+    const BinInfo iE = l1_info(H, (int)E);
+    const Lvl L2 = lvl2(H, E, iE.Kab, iE.Wab);
     Walk w2;
     lvl_scan(L2, s, w2);
-    L = L2;
-    w = w2;
+    Lvl L = L2;
+    Walk w = w2;
     if (level == 3) {
       BinInfo i2;
       lvl_bin_info(L2, w2, (int)((s.c.l3base >> 11) & (kB2 - 1)), s, i2);
@@ -650,9 +709,10 @@ GS_DI void sv_exact(SolveLds& s, const Hists& H) {
       L = L3;
       w = w3;
     }
+    lvl_exact(L, w, s.c.B, s.c.S, s, b1, b2);
+    if (b1 >= 0) lvl_bin_info(L, w, b1, s, c1);
+    if (b2 != INT_MAX) lvl_bin_info(L, w, b2, s, c2);
   }
-  int b1, b2;
-  lvl_exact(L, w, s.c.B, s.c.S, s, b1, b2);
   if (b1 < 0) {
     // no value in this window passes: the answer is the candidate found one level up
     if (s.c.fbValid) {
@@ -667,40 +727,32 @@ GS_DI void sv_exact(SolveLds& s, const Hists& H) {
     }
     return;
   }
-  BinInfo i1;
-  lvl_bin_info(L, w, b1, s, i1);
-  const uint32_t cand_tcap = i1.mx + 1;
-  if (b2 != INT_MAX && level < 3) {
-    BinInfo i2;
-    lvl_bin_info(L, w, b2, s, i2);
-    if (i2.cnt >= 2) {
-      __syncthreads();
-      if (threadIdx.x == 0) {
-        s.c.fbValid = 1;
-        s.c.fbK = i1.Kab;
-        s.c.fbW = i1.Wab;
-        s.c.fbTcap = cand_tcap;
-        s.c.stage = level + 1;
-      }
-      __syncthreads();
-      if (level == 1) sv_request(s, H, 2, (uint32_t)b2, 0);
-      else sv_request(s, H, 3, 0, (E << 23) | ((uint32_t)b2 << 11));
-      return;
+  const uint32_t cand_tcap = c1.mx + 1;
+  if (b2 != INT_MAX && level < 3 && c2.cnt >= 2) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      s.c.fbValid = 1;
+      s.c.fbK = c1.Kab;
+      s.c.fbW = c1.Wab;
+      s.c.fbTcap = cand_tcap;
+      s.c.stage = level + 1;
     }
+    __syncthreads();
+    if (level == 1) sv_request(s, H, 2, (uint32_t)b2, 0);
+    else sv_request(s, H, 3, 0, (E << 23) | ((uint32_t)b2 << 11));
+    return;
   }
-  sv_exact_finish(s, i1.Kab, i1.Wab, cand_tcap);
+  sv_exact_finish(s, c1.Kab, c1.Wab, cand_tcap);
 }
 
-// First solve after the statistics pass: totals and the special cases.
+// First solve after the statistics pass: the level-1 cache, totals and the special cases.
 GS_DI void sv_start(SolveLds& s, const Hists& H, int64_t d) {
-  const Lvl L1 = lvl1(H);
-  Walk w1;
-  lvl_scan(L1, s, w1);
-  BinInfo i0, inf;
-  lvl_bin_info(L1, w1, 0, s, i0);
-  lvl_bin_info(L1, w1, 255, s, inf);
+  l1_build(s, H);
+  const BinInfo i0 = l1_info(H, 0);
+  const BinInfo inf = l1_info(H, 255);
+  __syncthreads();
   if (threadIdx.x == 0) {
-    // every finite key lies in bins 0..254; bin 255 counts only Inf/NaN
+    // every finite key lies in binades 0..254; binade 255 counts only Inf/NaN
     Fx tot = i0.Wab;
     fx_add(tot, i0.Wb);
     if (inf.cnt) {
@@ -899,7 +951,7 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
   }
   __syncthreads();
   if (s.c.done) return;
-  const Hists H{h1_of(a, row), h2_of(a, row), h3_of(a, row)};
+  const Hists H{h1_of(a, row), h2_of(a, row), h3_of(a, row), a1_of(a, row)};
   if (s.c.stage == 0) sv_start(s, H, a.d);
   else if (s.c.solver == GSPAR_GREEDY) sv_greedy(s, H);
   else sv_exact(s, H);
@@ -907,31 +959,82 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
   if (threadIdx.x == 0) *gc = s.c;
 }
 
-// Sampling, amplification and order-preserving compaction. One ticketed tile of kTileElems
-// coordinates per workgroup; tile prefixes chain through a decoupled look-back whose status word
-// packs (flag:2 | capped survivors:31 | survivors:31).
+// Sampling, amplification and order-preserving compaction. Workgroup t handles tile t (kTileElems
+// coordinates of one row, in row order). Tile prefixes chain through a decoupled look-back whose
+// status word packs (flag:2 | capped survivors:31 | survivors:31). A predecessor that has not yet
+// published after a few polls is counted by the waiting wave itself (decoupled fallback), so no
+// ordering of workgroup dispatch is assumed and no global ticket counter serialises the tiles.
 constexpr uint64_t kStAgg = 1ull << 62, kStInc = 2ull << 62, kStVal = (1ull << 62) - 1;
+constexpr int kPolls = 16;
+
+struct TileCtx {
+  const float* row;
+  int64_t d;
+  double lam;
+  uint32_t tcap;
+  uint32_t k0, k1;
+  bool live;
+};
+
+// Selection bits (bit c: coordinate 4q+c survives) and capped-survivor bits of group q.
+template <bool VEC>
+__device__ __forceinline__ void decide_group(const TileCtx& c, int64_t q, float v[4], uint32_t& z, uint32_t& cz) {
+  const uint32_t m = load4<VEC>(c.row, q, c.d, v);
+  uint32_t x0 = (uint32_t)q, x1 = (uint32_t)((uint64_t)q >> 32), x2 = 0, x3 = 0;
+  philox10(x0, x1, x2, x3, c.k0, c.k1);
+  const uint32_t xr[4] = {x0, x1, x2, x3};
+  z = 0;
+  cz = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t key = key_of(v[k]);
+    const bool capped = key >= c.tcap;
+    const bool pick = capped || ((double)xr[k] * 0x1p-32 < c.lam * (double)fabsf(v[k]));
+    const bool sel = c.live && ((m >> k) & 1) && key != 0 && pick;
+    z |= (uint32_t)sel << k;
+    cz |= (uint32_t)(sel && capped) << k;
+  }
+}
+
+// Aggregate (capped << 31 | survivors) of tile `part` computed by one wave (fallback path).
+template <bool VEC>
+__device__ uint64_t wave_tile_aggregate(const TileCtx& c, int64_t part, int lane) {
+  uint64_t n = 0, nc = 0;
+  for (int j = 0; j < kTileElems / 4 / 64; ++j) {
+    const int64_t q = part * (kTileElems / 4) + j * 64 + lane;
+    float v[4];
+    uint32_t z, cz;
+    decide_group<VEC>(c, q, v, z, cz);
+    n += __popc(z);
+    nc += __popc(cz);
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    n += __shfl_xor(n, o);
+    nc += __shfl_xor(nc, o);
+  }
+  return (nc << 31) | n;
+}
 
 template <bool VEC>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
-  __shared__ uint32_t s_tile;
   __shared__ uint64_t s_wave[kTileThreads / 64];
   __shared__ uint32_t s_capw[kTileThreads / 64];
   __shared__ uint64_t s_excl;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  if (tid == 0) s_tile = atomicAdd(reinterpret_cast<uint32_t*>(a.ws), 1u);
-  __syncthreads();
-  const int64_t t = s_tile;
+  const int64_t t = blockIdx.x;
   const int64_t row = t / a.lay.tiles;
   const int64_t part = t % a.lay.tiles;
   const RowCtl* ctl = ctl_of(a, row);
-  const double lam = ctl->lam;
-  const uint32_t tcap = ctl->tcap;
-  const float inv = ctl->inv_lam;
-  const bool live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO));
+  TileCtx c;
+  c.row = a.g + row * a.ld;
+  c.d = a.d;
+  c.lam = ctl->lam;
+  c.tcap = ctl->tcap;
+  c.live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO));
   const uint64_t seed = a.seed_dev ? a.seed_dev[row] : a.seed;
-  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-  const float* __restrict__ gr = a.g + row * a.ld;
+  c.k0 = (uint32_t)seed;
+  c.k1 = (uint32_t)(seed >> 32);
+  const float inv = ctl->inv_lam;
 
   float v[kTileGroups][4];
   uint32_t zb[kTileGroups], cb[kTileGroups];
@@ -940,24 +1043,9 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
 #pragma unroll
   for (int j = 0; j < kTileGroups; ++j) {
     const int64_t q = part * (kTileElems / 4) + j * kTileThreads + tid;
-    const uint32_t m = load4<VEC>(gr, q, a.d, v[j]);
-    uint32_t x0 = (uint32_t)q, x1 = (uint32_t)((uint64_t)q >> 32), x2 = 0, x3 = 0;
-    philox10(x0, x1, x2, x3, k0, k1);
-    const uint32_t xr[4] = {x0, x1, x2, x3};
-    uint32_t z = 0, cz = 0;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const uint32_t key = key_of(v[j][c]);
-      const bool capped = key >= tcap;
-      const bool pick = capped || ((double)xr[c] * 0x1p-32 < lam * (double)fabsf(v[j][c]));
-      const bool sel = live && ((m >> c) & 1) && key != 0 && pick;
-      z |= (uint32_t)sel << c;
-      cz |= (uint32_t)(sel && capped) << c;
-    }
-    zb[j] = z;
-    cb[j] = cz;
-    packed |= (uint64_t)__popc(z) << (16 * j);
-    ncap += __popc(cz);
+    decide_group<VEC>(c, q, v[j], zb[j], cb[j]);
+    packed |= (uint64_t)__popc(zb[j]) << (16 * j);
+    ncap += __popc(cb[j]);
   }
   // block exclusive scan of the packed per-group counts (four 16-bit fields)
   unsigned long long inc = packed;
@@ -1000,33 +1088,34 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
       const int64_t first = t - part;
       int64_t look = t - 1;
       uint64_t ex = 0;
-      bool bad = false;
       while (true) {
         const int64_t i = look - lane;
-        uint64_t s = kStInc;
+        uint64_t sw = kStInc;
         if (i >= first) {
-          uint32_t spins = 0;
+          int polls = 0;
           do {
-            s = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          } while ((s >> 62) == 0 && ++spins < kSpinLimit);
-          if ((s >> 62) == 0) {
-            bad = true;
-            s = kStInc;
-          }
+            sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          } while ((sw >> 62) == 0 && ++polls < kPolls);
         }
-        const uint64_t incl_mask = __ballot((s >> 62) == 2);
-        const int stop = incl_mask ? (__ffsll((unsigned long long)incl_mask) - 1) : 64;
-        uint64_t contrib = lane <= stop ? (s & kStVal) : 0;
+        const uint64_t incl_mask = __ballot((sw >> 62) == 2);
+        const int stop = incl_mask ? (__ffsll((unsigned long long)incl_mask) - 1) : 63;
+        // predecessors up to `stop` that have not published: count them here
+        uint64_t missing = __ballot((sw >> 62) == 0 && lane <= stop);
+        while (missing) {
+          const int m = __ffsll((unsigned long long)missing) - 1;
+          const uint64_t val = wave_tile_aggregate<VEC>(c, (look - m) - first, lane);
+          if (lane == m) sw = kStAgg | val;
+          missing &= missing - 1;
+        }
+        uint64_t contrib = lane <= stop ? (sw & kStVal) : 0;
         for (int o = 32; o > 0; o >>= 1) contrib += __shfl_xor(contrib, o);
         ex += contrib;
         if (incl_mask) break;
         look -= 64;
       }
-      const bool anybad = __ballot(bad) != 0;
       if (lane == 0) {
         __hip_atomic_store(&st[t], kStInc | (ex + agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_excl = ex;
-        if (anybad) atomicOr(&ctl_of(a, row)->flags, (uint32_t)kFlagInternal);
       }
     }
   }
@@ -1037,16 +1126,16 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   uint64_t gpre = 0;
 #pragma unroll
   for (int j = 0; j < kTileGroups; ++j) {
-    uint32_t z = zb[j];
+    const uint32_t z = zb[j];
     if (z) {
       const int64_t q = part * (kTileElems / 4) + j * kTileThreads + tid;
       uint64_t pos = base + gpre + ((excl >> (16 * j)) & 0xFFFF);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        if ((z >> c) & 1) {
+      for (int k = 0; k < 4; ++k) {
+        if ((z >> k) & 1) {
           if ((int64_t)pos < a.cap) {
-            oi[pos] = (int32_t)(4 * q + c);
-            ov[pos] = ((cb[j] >> c) & 1) ? v[j][c] : copysignf(inv, v[j][c]);
+            oi[pos] = (int32_t)(4 * q + k);
+            ov[pos] = ((cb[j] >> k) & 1) ? v[j][k] : copysignf(inv, v[j][k]);
           }
           ++pos;
         }
@@ -1061,7 +1150,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     if (a.nnz) a.nnz[row] = n;
     if (a.k_out) a.k_out[row] = kc;
     if (a.lam_out) a.lam_out[row] = ctl->lam;
-    uint32_t fl = __hip_atomic_load(&ctl_of(a, row)->flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t fl = ctl->flags;
     if (!ctl->done) fl |= kFlagInternal;
     if (n > a.cap) fl |= GSPAR_FLAG_OVERFLOW;
     if (a.flags_out) a.flags_out[row] = fl;

@@ -151,7 +151,20 @@ inline T atomicMax(T* p, U v) {
   return old;
 }
 #define __HIP_MEMORY_SCOPE_AGENT 0
-#define __hip_atomic_load(p, order, scope) __atomic_load_n((p), __ATOMIC_SEQ_CST)
+namespace emu {
+// EMU_HIDE_STATUS=1: loads of look-back status words (values with either of the top two bits
+// set) read as "not yet published", which drives the look-back into its fallback path.
+inline bool g_hide_status = getenv("EMU_HIDE_STATUS") && atoi(getenv("EMU_HIDE_STATUS")) != 0;
+template <class T>
+inline T atomic_load_emu(T* p) {
+  T v = __atomic_load_n(p, __ATOMIC_SEQ_CST);
+  if constexpr (sizeof(T) == 8) {
+    if (g_hide_status && ((uint64_t)v >> 62) != 0) return (T)0;
+  }
+  return v;
+}
+}  // namespace emu
+#define __hip_atomic_load(p, order, scope) emu::atomic_load_emu(p)
 #define __hip_atomic_store(p, v, order, scope) __atomic_store_n((p), (v), __ATOMIC_SEQ_CST)
 
 namespace emu {

@@ -59,3 +59,12 @@ def test_emulated_under_asan():
     r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "all"], env=env,
                        capture_output=True, text=True, timeout=3600)
     assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-2000:]
+
+
+def test_emulated_lookback_fallback():
+    """Hide every published tile status so each look-back counts its predecessors itself."""
+    lib = emu_build.build(asan=False)
+    env = dict(os.environ, EMU_HIDE_STATUS="1", EMU_STALL_SECONDS="300")
+    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "extra"], env=env,
+                       capture_output=True, text=True, timeout=1200)
+    assert r.returncode == 0 and "extra cases ok" in r.stdout, (r.stdout[-2000:], r.stderr[-2000:])
