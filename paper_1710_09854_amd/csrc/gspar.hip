@@ -40,8 +40,8 @@ constexpr int kB1 = 256;                    // level 1: one bin per binade (key 
 constexpr int kB2 = 4096;                   // level 2: one binade, 2^11 keys per bin
 constexpr int kB3 = 2048;                   // level 3: one level-2 bin, one key per bin
 constexpr int kTileThreads = 256;
-constexpr int kTileGroups = 4;              // float4 groups per thread per tile
-constexpr int kTileElems = kTileThreads * kTileGroups * 4;
+constexpr int kTileGroups = 16;             // float4 groups per thread per tile
+constexpr int kTileElems = kTileThreads * kTileGroups * 4;  // 16384 coordinates per tile
 constexpr int kMaxIters = 64;
 constexpr int64_t kMaxChunk = (1 << 20) - 4;  // LDS packing holds < 2^20 elements per workgroup
 constexpr uint32_t kSpinLimit = 1u << 22;
@@ -335,9 +335,10 @@ __device__ __forceinline__ uint32_t load4(const float* __restrict__ row, int64_t
 }
 
 // ------------------------------------------------------------------------------------------
-// The per-row solver: kernel k_solve, one workgroup of kNT threads per row. Every helper is
-// force-inlined into that kernel so its LDS and global pointers keep their address spaces and
-// no call frames or scratch are needed.
+// The per-row solver, run by one workgroup of kNT threads (the last one of a histogram pass to
+// finish on that row). Every helper is force-inlined so LDS and global pointers keep their address
+// spaces and no call frames or scratch are needed. Histogram words flushed by other workgroups are
+// read with agent-scope atomic loads.
 // ------------------------------------------------------------------------------------------
 #define GS_DI __device__ __attribute__((always_inline)) inline
 
@@ -366,6 +367,10 @@ struct Hists {
   Hist3* h3;
   L1Above* a1;
 };
+union PassLds {
+  HistLds h;
+  SolveLds s;
+};
 
 GS_DI int block_max(SolveLds& s, int v) {
   for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
@@ -393,8 +398,8 @@ GS_DI void l1_build(SolveLds& s, const Hists& H) {
   uint64_t k = 0;
   Fx w = fx_zero();
   if (t < kB1) {
-    k = H.h1->cnt[t];
-    if (k) w = fx_shifted(H.h1->sig[t], binade_shift(t));
+    k = ald64(&H.h1->cnt[t]);
+    if (k) w = fx_shifted(ald64(&H.h1->sig[t]), binade_shift(t));
   }
   const int r = kB1 - 1 - t;  // reversed index: a prefix over r is a suffix over binades
   if (t < kB1) {
@@ -433,9 +438,9 @@ GS_DI BinInfo l1_info(const Hists& H, int e) {
   BinInfo i;
   i.Kab = H.a1->K[e];
   i.Wab = H.a1->W[e];
-  i.cnt = H.h1->cnt[e];
-  i.Wb = i.cnt ? fx_shifted(H.h1->sig[e], binade_shift(e)) : fx_zero();
-  i.mx = H.h1->mx[e];
+  i.cnt = ald64(&H.h1->cnt[e]);
+  i.Wb = i.cnt ? fx_shifted(ald64(&H.h1->sig[e]), binade_shift(e)) : fx_zero();
+  i.mx = ald32(&H.h1->mx[e]);
   return i;
 }
 
@@ -475,8 +480,8 @@ GS_DI void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
   for (int j = 0; j < L.per; ++j) {
     const int b = b0 + j;
     if (b < L.nbins) {
-      k += L.cnt[b];
-      sg += L.sig[b];
+      k += ald64(&L.cnt[b]);
+      sg += ald64(&L.sig[b]);
     }
   }
   const int r = kNT - 1 - (int)threadIdx.x;
@@ -514,13 +519,13 @@ GS_DI void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo
     for (int j = L.per - 1; j >= 0; --j) {
       const int bb = threadIdx.x * L.per + j;
       if (bb >= L.nbins) continue;
-      const uint64_t c = L.cnt[bb];
-      const uint64_t sg = L.sig[bb];
+      const uint64_t c = ald64(&L.cnt[bb]);
+      const uint64_t sg = ald64(&L.sig[bb]);
       if (bb == b) {
         s.bi.Wab = lvl_total(L, K, S, s.bi.Kab);
         s.bi.cnt = c;
         s.bi.Wb = c ? fx_shifted(sg, L.shift) : fx_zero();
-        s.bi.mx = L.mx[bb];
+        s.bi.mx = ald32(&L.mx[bb]);
         break;
       }
       K += c;
@@ -543,11 +548,11 @@ GS_DI bool criterion(double B, const Fx& S, uint64_t k, const Fx& W, uint32_t vk
 GS_DI void l1_exact(const Hists& H, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
   const int t = threadIdx.x;
   int best = -1, occupied = INT_MAX;
-  if (t < kB1 && H.h1->cnt[t]) {
-    if (criterion(B, S, H.a1->K[t], H.a1->W[t], H.h1->mx[t])) best = t;
+  if (t < kB1 && ald64(&H.h1->cnt[t])) {
+    if (criterion(B, S, H.a1->K[t], H.a1->W[t], ald32(&H.h1->mx[t]))) best = t;
   }
   b1 = block_max(s, best);
-  if (t < kB1 && t > b1 && H.h1->cnt[t]) occupied = t;
+  if (t < kB1 && t > b1 && ald64(&H.h1->cnt[t])) occupied = t;
   b2 = block_min(s, occupied);
 }
 GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
@@ -556,19 +561,19 @@ GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLd
   for (int j = L.per - 1; j >= 0 && best < 0; --j) {
     const int b = threadIdx.x * L.per + j;
     if (b >= L.nbins) continue;
-    const uint64_t c = L.cnt[b];
+    const uint64_t c = ald64(&L.cnt[b]);
     if (!c) continue;
     uint64_t Kt;
     const Fx W = lvl_total(L, K, Sg, Kt);
-    if (criterion(B, S, Kt, W, L.mx[b])) best = b;
+    if (criterion(B, S, Kt, W, ald32(&L.mx[b]))) best = b;
     K += c;
-    Sg += L.sig[b];
+    Sg += ald64(&L.sig[b]);
   }
   b1 = block_max(s, best);
   int lowest = INT_MAX;
   for (int j = 0; j < L.per; ++j) {
     const int b = threadIdx.x * L.per + j;
-    if (b < L.nbins && b > b1 && L.cnt[b]) {
+    if (b < L.nbins && b > b1 && ald64(&L.cnt[b])) {
       lowest = b;
       break;
     }
@@ -796,6 +801,25 @@ GS_DI void sv_start(SolveLds& s, const Hists& H, int64_t d) {
   }
 }
 
+// The row's solver, run by the last workgroup of each histogram pass once every workgroup of the
+// row has flushed: it either finishes the row (lambda and the capped threshold become final) or
+// requests the next refinement window for the following pass.
+GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
+  if (threadIdx.x == 0) {
+    s.c = *gc;
+    s.c.zeros = ald64(&gc->zeros);
+    s.c.need = 0;
+    s.c.arrive = 0;
+  }
+  __syncthreads();
+  if (s.c.done) return;
+  if (s.c.stage == 0) sv_start(s, H, d);
+  else if (s.c.solver == GSPAR_GREEDY) sv_greedy(s, H);
+  else sv_exact(s, H);
+  __syncthreads();
+  if (threadIdx.x == 0) *gc = s.c;
+}
+
 // ------------------------------------------------------------------------------------------
 // Kernels.
 // ------------------------------------------------------------------------------------------
@@ -827,31 +851,38 @@ __global__ void __launch_bounds__(256) k_init(Args a) {
 // Streaming statistics pass. Grid: rows * nb workgroups of kNT threads; each flushes its
 // histogram as per-binade totals (count, exact significand sum, maximum key).
 template <bool VEC>
-__global__ void __launch_bounds__(kNT) k_stats(Args a) {
-  __shared__ HistLds sm;
+__global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_stats(Args a) {
+  __shared__ PassLds sm;
+  __shared__ uint32_t s_last;
   const int64_t row = blockIdx.x / a.nb;
   const int64_t blk = blockIdx.x % a.nb;
   for (int b = threadIdx.x; b < kFine; b += kNT) {
-    sm.pk[b] = 0;
-    sm.mx[b] = 0;
+    sm.h.pk[b] = 0;
+    sm.h.mx[b] = 0;
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + row * a.ld;
   const int64_t beg = blk * a.chunk;
   const int64_t end = min(a.d, beg + a.chunk);
   uint32_t zeros = 0;
-  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += kNT) {
-    float v[4];
-    const uint32_t m = load4<VEC>(gr, q, end, v);
+  // four float4 loads in flight per thread before any LDS work
+  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += 4 * kNT) {
+    float v[4][4];
+    uint32_t m[4];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const uint32_t key = key_of(v[c]);
-      if (key == 0) {
-        zeros += (m >> c) & 1;
-      } else {
-        const uint32_t f = key >> 19;
-        atomicAdd(&sm.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
-        atomicMax(&sm.mx[f], key);
+    for (int u = 0; u < 4; ++u) m[u] = load4<VEC>(gr, q + u * kNT, end, v[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t key = key_of(v[u][c]);
+        if (key == 0) {
+          zeros += (m[u] >> c) & 1;
+        } else {
+          const uint32_t f = key >> 19;
+          atomicAdd(&sm.h.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
+          atomicMax(&sm.h.mx[f], key);
+        }
       }
     }
   }
@@ -865,10 +896,10 @@ __global__ void __launch_bounds__(kNT) k_stats(Args a) {
     uint64_t cnt = 0, sg = 0;
     uint32_t mx = 0;
     for (int j = 0; j < 16; ++j) {
-      const uint64_t p = sm.pk[e * 16 + j];
+      const uint64_t p = sm.h.pk[e * 16 + j];
       cnt += p >> 44;
       sg += p & ((1ull << 44) - 1);
-      mx = max(mx, sm.mx[e * 16 + j]);
+      mx = max(mx, sm.h.mx[e * 16 + j]);
     }
     if (cnt) {
       Hist1* h = h1_of(a, row);
@@ -877,12 +908,22 @@ __global__ void __launch_bounds__(kNT) k_stats(Args a) {
       atomicMax(&h->mx[e], mx);
     }
   }
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(&ctl->arrive, 1u) == (uint32_t)(a.nb - 1);
+  __syncthreads();
+  if (!s_last) return;
+  // the last workgroup of the row: every flush above is visible after this acquire fence
+  __threadfence();
+  const Hists H{h1_of(a, row), h2_of(a, row), h3_of(a, row), a1_of(a, row)};
+  solve_row(sm.s, ctl, H, a.d);
 }
 
 // Refinement pass over one window of keys, for the rows whose solver asked for one.
 template <bool VEC>
-__global__ void __launch_bounds__(kNT) k_refine(Args a) {
-  __shared__ HistLds sm;
+__global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_refine(Args a) {
+  __shared__ PassLds sm;
+  __shared__ uint32_t s_last;
   const int64_t row = blockIdx.x / a.nb;
   const int64_t blk = blockIdx.x % a.nb;
   RowCtl* ctl = ctl_of(a, row);
@@ -907,56 +948,49 @@ __global__ void __launch_bounds__(kNT) k_refine(Args a) {
   }
   const uint32_t span = (uint32_t)nbins << shift;
   for (int b = threadIdx.x; b < nbins; b += kNT) {
-    sm.pk[b] = 0;
-    sm.mx[b] = 0;
+    sm.h.pk[b] = 0;
+    sm.h.mx[b] = 0;
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + row * a.ld;
   const int64_t beg = blk * a.chunk;
   const int64_t end = min(a.d, beg + a.chunk);
-  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += kNT) {
-    float v[4];
-    load4<VEC>(gr, q, end, v);
+  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += 4 * kNT) {
+    float v[4][4];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const uint32_t key = key_of(v[c]);
-      const uint32_t rel = key - lo;
-      if (key != 0 && rel < span) {
-        const uint32_t b = rel >> shift;
-        atomicAdd(&sm.pk[b], (unsigned long long)((1ull << 44) + key_sig(key)));
-        atomicMax(&sm.mx[b], key);
+    for (int u = 0; u < 4; ++u) load4<VEC>(gr, q + u * kNT, end, v[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t key = key_of(v[u][c]);
+        const uint32_t rel = key - lo;
+        if (key != 0 && rel < span) {
+          const uint32_t b = rel >> shift;
+          atomicAdd(&sm.h.pk[b], (unsigned long long)((1ull << 44) + key_sig(key)));
+          atomicMax(&sm.h.mx[b], key);
+        }
       }
     }
   }
   __syncthreads();
   for (int b = threadIdx.x; b < nbins; b += kNT) {
-    const uint64_t p = sm.pk[b];
+    const uint64_t p = sm.h.pk[b];
     if (p) {
       atomicAdd((unsigned long long*)&gcnt[b], (unsigned long long)(p >> 44));
       atomicAdd((unsigned long long*)&gsig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
-      atomicMax(&gmx[b], sm.mx[b]);
+      atomicMax(&gmx[b], sm.h.mx[b]);
     }
   }
-}
-
-// Solver for one row per workgroup: runs after every histogram pass and either finishes the row
-// (lambda and the capped threshold become final) or requests the next refinement window.
-__global__ void __launch_bounds__(kNT) k_solve(Args a) {
-  __shared__ SolveLds s;
-  const int64_t row = blockIdx.x;
-  RowCtl* gc = ctl_of(a, row);
-  if (threadIdx.x == 0) {
-    s.c = *gc;
-    s.c.need = 0;
-  }
+  __threadfence();
   __syncthreads();
-  if (s.c.done) return;
+  if (threadIdx.x == 0) s_last = atomicAdd(&ctl->arrive, 1u) == (uint32_t)(a.nb - 1);
+  __syncthreads();
+  if (!s_last) return;
+  // the last workgroup of the row: every flush above is visible after this acquire fence
+  __threadfence();
   const Hists H{h1_of(a, row), h2_of(a, row), h3_of(a, row), a1_of(a, row)};
-  if (s.c.stage == 0) sv_start(s, H, a.d);
-  else if (s.c.solver == GSPAR_GREEDY) sv_greedy(s, H);
-  else sv_exact(s, H);
-  __syncthreads();
-  if (threadIdx.x == 0) *gc = s.c;
+  solve_row(sm.s, ctl, H, a.d);
 }
 
 // Sampling, amplification and order-preserving compaction. Workgroup t handles tile t (kTileElems
@@ -1015,10 +1049,37 @@ __device__ uint64_t wave_tile_aggregate(const TileCtx& c, int64_t part, int lane
   return (nc << 31) | n;
 }
 
+// Block-wide exclusive scan of a 32-bit value (kTileThreads threads); also returns the total.
+__device__ __forceinline__ uint32_t tile_scan(uint32_t x, uint32_t* s_w, uint32_t& total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint32_t inc = x;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(inc, (unsigned)o);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) s_w[wv] = inc;
+  __syncthreads();
+  uint32_t pre = 0;
+  total = 0;
+  for (int i = 0; i < kTileThreads / 64; ++i) {
+    if (i < wv) pre += s_w[i];
+    total += s_w[i];
+  }
+  __syncthreads();
+  return pre + inc - x;
+}
+
+// Phase 1 decides every coordinate of the tile (coalesced float4 loads, one Philox block per
+// group) and records per-group nibbles in LDS: selected, capped-and-selected, negative. After the
+// look-back, phase 2 gives each thread 64 consecutive coordinates, so survivors are emitted in
+// index order from a contiguous range per thread.
 template <bool VEC>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
-  __shared__ uint64_t s_wave[kTileThreads / 64];
-  __shared__ uint32_t s_capw[kTileThreads / 64];
+  __shared__ alignas(16) uint8_t s_z[kTileElems / 4];
+  __shared__ alignas(16) uint8_t s_c[kTileElems / 4];
+  __shared__ alignas(16) uint8_t s_n[kTileElems / 4];
+  __shared__ uint32_t s_w[kTileThreads / 64];
+  __shared__ uint32_t s_w2[kTileThreads / 64];
   __shared__ uint64_t s_excl;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t t = blockIdx.x;
@@ -1036,44 +1097,26 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   c.k1 = (uint32_t)(seed >> 32);
   const float inv = ctl->inv_lam;
 
-  float v[kTileGroups][4];
-  uint32_t zb[kTileGroups], cb[kTileGroups];
-  uint64_t packed = 0;
-  uint32_t ncap = 0;
-#pragma unroll
+  uint32_t nsel = 0, ncap = 0;
+#pragma unroll 4
   for (int j = 0; j < kTileGroups; ++j) {
-    const int64_t q = part * (kTileElems / 4) + j * kTileThreads + tid;
-    decide_group<VEC>(c, q, v[j], zb[j], cb[j]);
-    packed |= (uint64_t)__popc(zb[j]) << (16 * j);
-    ncap += __popc(cb[j]);
-  }
-  // block exclusive scan of the packed per-group counts (four 16-bit fields)
-  unsigned long long inc = packed;
-  for (int o = 1; o < 64; o <<= 1) {
-    const unsigned long long y = __shfl_up(inc, (unsigned)o);
-    if (lane >= o) inc += y;
-  }
-  uint32_t capw = ncap;
-  for (int o = 32; o > 0; o >>= 1) capw += __shfl_xor(capw, o);
-  if (lane == 63) s_wave[wv] = inc;
-  if (lane == 0) s_capw[wv] = capw;
-  __syncthreads();
-  uint64_t wpre = 0, tot = 0;
-  uint32_t tcapn = 0;
-  for (int i = 0; i < kTileThreads / 64; ++i) {
-    if (i < wv) wpre += s_wave[i];
-    tot += s_wave[i];
-    tcapn += s_capw[i];
-  }
-  const uint64_t excl = wpre + inc - packed;
-  uint32_t fsum[kTileGroups];
-  uint64_t nsel = 0;
+    const int gi = j * kTileThreads + tid;  // group inside the tile
+    float v[4];
+    uint32_t z, cz;
+    decide_group<VEC>(c, part * (kTileElems / 4) + gi, v, z, cz);
+    uint32_t neg = 0;
 #pragma unroll
-  for (int j = 0; j < kTileGroups; ++j) {
-    fsum[j] = (uint32_t)((tot >> (16 * j)) & 0xFFFF);
-    nsel += fsum[j];
+    for (int k = 0; k < 4; ++k) neg |= (uint32_t)(__float_as_uint(v[k]) >> 31) << k;
+    s_z[gi] = (uint8_t)z;
+    s_c[gi] = (uint8_t)cz;
+    s_n[gi] = (uint8_t)neg;
+    nsel += __popc(z);
+    ncap += __popc(cz);
   }
-  const uint64_t agg = ((uint64_t)tcapn << 31) | nsel;
+  uint32_t tsel, tcap;
+  tile_scan(nsel, s_w, tsel);
+  tile_scan(ncap, s_w2, tcap);
+  const uint64_t agg = ((uint64_t)tcap << 31) | tsel;
 
   // decoupled look-back for the tile's exclusive prefix within its row
   uint64_t* st = status_of(a);
@@ -1120,28 +1163,38 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     }
   }
   __syncthreads();
-  const uint64_t base = s_excl & 0x7FFFFFFFull;  // survivors before this tile
-  int32_t* __restrict__ oi = a.idx + row * a.cap;
-  float* __restrict__ ov = a.val + row * a.cap;
-  uint64_t gpre = 0;
+  const uint64_t base = s_excl & 0x7FFFFFFFull;  // survivors of the row before this tile
+
+  // phase 2: thread t owns groups [16t, 16t + 16) of the tile, i.e. 64 consecutive coordinates
+  const int g0 = tid * kTileGroups;
+  uint32_t zw[kTileGroups / 4];
 #pragma unroll
-  for (int j = 0; j < kTileGroups; ++j) {
-    const uint32_t z = zb[j];
-    if (z) {
-      const int64_t q = part * (kTileElems / 4) + j * kTileThreads + tid;
-      uint64_t pos = base + gpre + ((excl >> (16 * j)) & 0xFFFF);
+  for (int w = 0; w < kTileGroups / 4; ++w) zw[w] = *reinterpret_cast<const uint32_t*>(&s_z[g0 + 4 * w]);
+  uint32_t mine = 0;
+#pragma unroll
+  for (int w = 0; w < kTileGroups / 4; ++w) mine += __popc(zw[w]);
+  uint32_t dummy;
+  uint64_t pos = base + tile_scan(mine, s_w, dummy);
+  if (mine) {
+    int32_t* __restrict__ oi = a.idx + row * a.cap;
+    float* __restrict__ ov = a.val + row * a.cap;
+    const int64_t e0 = part * (int64_t)kTileElems + 4 * (int64_t)g0;
+    for (int gq = 0; gq < kTileGroups; ++gq) {
+      const uint32_t z = (zw[gq >> 2] >> (8 * (gq & 3))) & 0xF;
+      if (!z) continue;
+      const uint32_t cz = s_c[g0 + gq], ng = s_n[g0 + gq];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         if ((z >> k) & 1) {
           if ((int64_t)pos < a.cap) {
-            oi[pos] = (int32_t)(4 * q + k);
-            ov[pos] = ((cb[j] >> k) & 1) ? v[j][k] : copysignf(inv, v[j][k]);
+            const int64_t i = e0 + 4 * gq + k;
+            oi[pos] = (int32_t)i;
+            ov[pos] = ((cz >> k) & 1) ? c.row[i] : (((ng >> k) & 1) ? -inv : inv);
           }
           ++pos;
         }
       }
     }
-    gpre += fsum[j];
   }
   if (part == a.lay.tiles - 1 && tid == 0) {
     const uint64_t incl = s_excl + agg;
@@ -1278,14 +1331,11 @@ static int launch_solve(Args& a, hipStream_t s) {
   if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
   else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
   time_after(1, s);
-  const dim3 rgrid((unsigned)a.rows);
-  hipLaunchKernelGGL(k_solve, rgrid, dim3(kNT), 0, s, a);
   // each greedy step may need a level-2 and a level-3 window, the exact solver at most both once
   const int R = a.solver == GSPAR_GREEDY ? 2 * a.T : 2;
   for (int r = 0; r < R; ++r) {
     if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
     else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
-    hipLaunchKernelGGL(k_solve, rgrid, dim3(kNT), 0, s, a);
   }
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }

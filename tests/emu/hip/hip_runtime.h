@@ -137,6 +137,11 @@ inline unsigned long long __ballot(int pred) {
   return m;
 }
 inline int __popc(unsigned v) { return __builtin_popcount(v); }
+inline unsigned __float_as_uint(float f) {
+  unsigned u;
+  std::memcpy(&u, &f, 4);
+  return u;
+}
 inline int __ffsll(unsigned long long v) { return __builtin_ffsll((long long)v); }
 
 template <class T, class U>
