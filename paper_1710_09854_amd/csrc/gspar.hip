@@ -1,19 +1,23 @@
 // gspar: gradient sparsification (Wangni, Wang, Liu, Zhang; arXiv 1710.09854) for MI355X / gfx950.
 //
-// Pipeline per call (all launches on the caller's stream, no host synchronisation):
+// Pipeline per call (all launches on the caller's stream, no host synchronisation). Workgroups
+// never wait on one another inside a histogram pass: every cross-workgroup hand-off is a kernel
+// boundary, because device-scope fences are expensive on a multi-XCD part.
 //   k_init     clears the per-call workspace and writes each row's budget B = rho*d.
-//   k_stats    one streaming pass over g: a 4096-bin LDS histogram of the magnitude bit pattern
-//              (count, exact significand sum, max) per workgroup, flushed as per-binade totals;
-//              the last workgroup of each row runs the solver (Proposition 1; Algorithm 2's
-//              criterion with a density budget, or Algorithm 3).
-//   k_refine   (launched a fixed number of times, exits at once unless the solver asked for it)
-//              histograms only the magnitudes inside one binade (4096 sub-bins) or inside one
-//              sub-bin (2048 single bit patterns), so every threshold the solvers need is resolved
-//              exactly, then resumes the solver.
+//   k_stats    one streaming pass over g: an LDS histogram over binades of the magnitude bit pattern
+//              (count, exact significand sum, max), added into per-row global copies.
+//   k_solve    one workgroup per row: sums the copies and runs the solver (Proposition 1;
+//              Algorithm 2's criterion with a density budget, or Algorithm 3), which either
+//              finishes the row or asks for a refinement window.
+//   k_refine   (launched a fixed number of times, each followed by k_solve; exits at once unless
+//              the solver asked for it) histograms only the magnitudes inside one binade (4096
+//              sub-bins) or inside one sub-bin (2048 single bit patterns), so every threshold the
+//              solvers need is resolved exactly.
 //   k_sample   one streaming pass: Philox4x32-10 per group of four coordinates, Bernoulli selection,
 //              amplification to g_i or sign(g_i)/lambda, order-preserving compaction with a
-//              decoupled look-back across ticketed tiles.
-//   k_probs    (probabilities entry points) writes p_i = min(lambda |g_i|, 1).
+//              decoupled look-back across tiles.
+//   k_probs    (probabilities entry points) writes p_i = min(lambda |g_i|, 1); k_probs_out writes
+//              the per-row results.
 //
 // Sums of magnitudes are exact: a magnitude's bit pattern (its "key") fixes its binade, bins never
 // straddle a binade, so per-bin sums of 24-bit significands are exact integers and are combined
@@ -35,7 +39,9 @@ namespace gspar {
 constexpr uint32_t kKeyInf = 0x7F800000u;   // bit pattern of +inf: keys >= this are non-finite
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 constexpr int kNT = 512;                    // threads of the histogram / solver workgroups
-constexpr int kFine = 4096;                 // LDS bins of the statistics pass (key >> 19)
+constexpr int kLaneCopies = 8;              // LDS copies of the statistics histogram (by lane)
+constexpr int kC1 = 8;                      // global copies of the level-1 histogram per row
+constexpr int kC23 = 2;                     // global copies of the level-2 / level-3 histograms
 constexpr int kB1 = 256;                    // level 1: one bin per binade (key >> 23)
 constexpr int kB2 = 4096;                   // level 2: one binade, 2^11 keys per bin
 constexpr int kB3 = 2048;                   // level 3: one level-2 bin, one key per bin
@@ -198,8 +204,8 @@ struct alignas(256) RowCtl {
   Fx S;              // exact sum of |g|
   Fx fbW;            // exact solver: capped sum of the best candidate found so far
   uint64_t fbK;      // exact solver: capped count of that candidate
-  uint64_t zeros;    // zero entries of the row (statistics pass)
-  uint64_t kcount;   // capped coordinates counted by the probabilities pass
+  uint64_t zeros;    // zero entries of the row (d minus the histogram's population)
+  uint64_t spare0;
   float inv_lam;     // fl32(1/lambda): the amplified value off the capped set
   uint32_t fbTcap;   // exact solver: candidate's capped threshold key
   uint32_t fbValid;
@@ -207,8 +213,8 @@ struct alignas(256) RowCtl {
   uint32_t flags;
   uint32_t need;     // 0: none; 2 / 3: a level-2 / level-3 pass is requested
   uint32_t done;     // 1 once lambda and tcap are final
-  uint32_t arrive;   // workgroups of the current histogram pass that have flushed
-  uint32_t parrive;  // workgroups of the probabilities pass that have finished
+  uint32_t spare1;
+  uint32_t spare2;
   uint32_t l2exp;    // binade of the level-2 window (kNone: none)
   uint32_t l3base;   // first key of the level-3 window (kNone: none)
   int32_t iter;      // greedy rescale steps taken
@@ -238,14 +244,21 @@ struct L1Above {
   uint64_t K[kB1];
   Fx W[kB1];
 };
+// Per-row partial count of capped coordinates written by the probabilities pass, one per class.
+struct alignas(128) CountLine {
+  unsigned long long v;
+  unsigned long long pad[15];
+};
 
 GS_HD size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctl, h1, h2, h3, a1, status, total;
+  size_t ctl, h1, h2, h3, a1, kc, status, total;
   int64_t tiles;  // tiles per row of the sample pass
 };
 
+// Histogram copies: row r's copy c of level 1 is h1 + (r * kC1 + c); copy 0 also holds the row's
+// reduced histogram once the first solve has summed the copies into it (likewise for levels 2, 3).
 GS_HD Layout layout_of(int64_t rows, int64_t d) {
   Layout L;
   L.tiles = (d + kTileElems - 1) / kTileElems;
@@ -253,13 +266,15 @@ GS_HD Layout layout_of(int64_t rows, int64_t d) {
   L.ctl = off;
   off += align256((size_t)rows * sizeof(RowCtl));
   L.h1 = off;
-  off += align256((size_t)rows * sizeof(Hist1));
+  off += align256((size_t)rows * kC1 * sizeof(Hist1));
   L.h2 = off;
-  off += align256((size_t)rows * sizeof(Hist2));
+  off += align256((size_t)rows * kC23 * sizeof(Hist2));
   L.h3 = off;
-  off += align256((size_t)rows * sizeof(Hist3));
+  off += align256((size_t)rows * kC23 * sizeof(Hist3));
   L.a1 = off;
   off += align256((size_t)rows * sizeof(L1Above));
+  L.kc = off;
+  off += align256((size_t)rows * 8 * sizeof(CountLine));
   L.status = off;
   off += align256((size_t)rows * (size_t)L.tiles * sizeof(uint64_t));
   L.total = off;
@@ -291,14 +306,17 @@ struct Args {
 __device__ __forceinline__ RowCtl* ctl_of(const Args& a, int64_t r) {
   return reinterpret_cast<RowCtl*>(a.ws + a.lay.ctl) + r;
 }
-__device__ __forceinline__ Hist1* h1_of(const Args& a, int64_t r) {
-  return reinterpret_cast<Hist1*>(a.ws + a.lay.h1) + r;
+__device__ __forceinline__ Hist1* h1_of(const Args& a, int64_t r, int c = 0) {
+  return reinterpret_cast<Hist1*>(a.ws + a.lay.h1) + r * kC1 + c;
 }
-__device__ __forceinline__ Hist2* h2_of(const Args& a, int64_t r) {
-  return reinterpret_cast<Hist2*>(a.ws + a.lay.h2) + r;
+__device__ __forceinline__ Hist2* h2_of(const Args& a, int64_t r, int c = 0) {
+  return reinterpret_cast<Hist2*>(a.ws + a.lay.h2) + r * kC23 + c;
 }
-__device__ __forceinline__ Hist3* h3_of(const Args& a, int64_t r) {
-  return reinterpret_cast<Hist3*>(a.ws + a.lay.h3) + r;
+__device__ __forceinline__ Hist3* h3_of(const Args& a, int64_t r, int c = 0) {
+  return reinterpret_cast<Hist3*>(a.ws + a.lay.h3) + r * kC23 + c;
+}
+__device__ __forceinline__ CountLine* kc_of(const Args& a, int64_t r) {
+  return reinterpret_cast<CountLine*>(a.ws + a.lay.kc) + r * 8;
 }
 __device__ __forceinline__ L1Above* a1_of(const Args& a, int64_t r) {
   return reinterpret_cast<L1Above*>(a.ws + a.lay.a1) + r;
@@ -307,12 +325,11 @@ __device__ __forceinline__ uint64_t* status_of(const Args& a) {
   return reinterpret_cast<uint64_t*>(a.ws + a.lay.status);
 }
 
-__device__ __forceinline__ uint64_t ald64(const uint64_t* p) {
-  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint32_t ald32(const uint32_t* p) {
-  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+
+
+// Histogram words read by the solver (written by an earlier kernel on the same stream).
+__device__ __forceinline__ uint64_t rd64(const uint64_t* p) { return *p; }
+__device__ __forceinline__ uint32_t rd32(const uint32_t* p) { return *p; }
 
 // Four consecutive coordinates 4q..4q+3 of a row; entries at or beyond `end` read as 0 and are
 // flagged invalid in the returned mask (bit c set = coordinate 4q+c exists).
@@ -334,17 +351,76 @@ __device__ __forceinline__ uint32_t load4(const float* __restrict__ row, int64_t
   return m;
 }
 
+// Visits the coordinates [beg, end) of one row (beg a multiple of 4) with the NT threads of a
+// workgroup, calling f(q, v, m) for each float4 group q (m: bit c set when coordinate 4q+c exists).
+// With vector loads, blocks of U groups per thread are loaded unconditionally, all issued before
+// any group is processed, so U loads per thread stay in flight; the last block clamps its addresses
+// to the last whole group and masks the values, and a trailing partial group is loaded by one
+// thread with scalar loads. No memory access sits under a divergent branch, which would make the
+// compiler wait for every outstanding load.
+template <bool VEC, int U, int NT, typename F>
+__device__ __forceinline__ void stream_groups(const float* __restrict__ row, int64_t beg, int64_t end, F&& f) {
+  if (!VEC) {
+    for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += NT) {
+      float v[4];
+      const uint32_t m = load4<false>(row, q, end, v);
+      f(q, v, m);
+    }
+    return;
+  }
+  const int64_t qfull = end / 4;  // groups [beg/4, qfull) lie entirely inside [beg, end)
+  int64_t qb = beg / 4;
+  for (; qb + (int64_t)U * NT <= qfull; qb += (int64_t)U * NT) {
+    float4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = *reinterpret_cast<const float4*>(row + 4 * (qb + threadIdx.x + u * NT));
+    __builtin_amdgcn_sched_barrier(0);  // keep every load of the block ahead of the first use
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float v[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+      f(qb + threadIdx.x + u * NT, v, 0xFu);
+    }
+  }
+  if (qb < qfull) {
+    float4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t q = qb + threadIdx.x + u * NT;
+      x[u] = *reinterpret_cast<const float4*>(row + 4 * (q < qfull ? q : qfull - 1));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t q = qb + threadIdx.x + u * NT;
+      const bool ok = q < qfull;
+      float v[4] = {ok ? x[u].x : 0.0f, ok ? x[u].y : 0.0f, ok ? x[u].z : 0.0f, ok ? x[u].w : 0.0f};
+      f(q, v, ok ? 0xFu : 0u);
+    }
+  }
+  if (4 * qfull < end && threadIdx.x == 0) {
+    float v[4];
+    const uint32_t m = load4<false>(row, qfull, end, v);
+    f(qfull, v, m);
+  }
+}
+
 // ------------------------------------------------------------------------------------------
-// The per-row solver, run by one workgroup of kNT threads (the last one of a histogram pass to
-// finish on that row). Every helper is force-inlined so LDS and global pointers keep their address
-// spaces and no call frames or scratch are needed. Histogram words flushed by other workgroups are
-// read with agent-scope atomic loads.
+// The per-row solver, run by one workgroup of kNT threads per row (k_solve). Every helper is
+// force-inlined so LDS and global pointers keep their address spaces and no call frames or scratch
+// are needed.
 // ------------------------------------------------------------------------------------------
 #define GS_DI __device__ __attribute__((always_inline)) inline
 
-struct HistLds {
-  unsigned long long pk[kFine];  // (count << 44) | significand sum
-  uint32_t mx[kFine];
+// LDS of the statistics pass: per binade and lane class, (count << 44) | significand sum and the
+// maximum key. Counts stay below 2^20 per workgroup, so significand sums stay below 2^44.
+struct StatsLds {
+  unsigned long long pk[kB1 * kLaneCopies];
+  uint32_t mx[kB1 * kLaneCopies];
+};
+// LDS of a refinement pass: one window of at most kB2 bins, same packing.
+struct WinLds {
+  unsigned long long pk[kB2];
+  uint32_t mx[kB2];
 };
 struct BinInfo {
   uint64_t Kab;  // count of keys strictly above the bin (including above the window)
@@ -366,10 +442,6 @@ struct Hists {
   Hist2* h2;
   Hist3* h3;
   L1Above* a1;
-};
-union PassLds {
-  HistLds h;
-  SolveLds s;
 };
 
 GS_DI int block_max(SolveLds& s, int v) {
@@ -398,8 +470,8 @@ GS_DI void l1_build(SolveLds& s, const Hists& H) {
   uint64_t k = 0;
   Fx w = fx_zero();
   if (t < kB1) {
-    k = ald64(&H.h1->cnt[t]);
-    if (k) w = fx_shifted(ald64(&H.h1->sig[t]), binade_shift(t));
+    k = rd64(&H.h1->cnt[t]);
+    if (k) w = fx_shifted(rd64(&H.h1->sig[t]), binade_shift(t));
   }
   const int r = kB1 - 1 - t;  // reversed index: a prefix over r is a suffix over binades
   if (t < kB1) {
@@ -438,9 +510,9 @@ GS_DI BinInfo l1_info(const Hists& H, int e) {
   BinInfo i;
   i.Kab = H.a1->K[e];
   i.Wab = H.a1->W[e];
-  i.cnt = ald64(&H.h1->cnt[e]);
-  i.Wb = i.cnt ? fx_shifted(ald64(&H.h1->sig[e]), binade_shift(e)) : fx_zero();
-  i.mx = ald32(&H.h1->mx[e]);
+  i.cnt = rd64(&H.h1->cnt[e]);
+  i.Wb = i.cnt ? fx_shifted(rd64(&H.h1->sig[e]), binade_shift(e)) : fx_zero();
+  i.mx = rd32(&H.h1->mx[e]);
   return i;
 }
 
@@ -480,8 +552,8 @@ GS_DI void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
   for (int j = 0; j < L.per; ++j) {
     const int b = b0 + j;
     if (b < L.nbins) {
-      k += ald64(&L.cnt[b]);
-      sg += ald64(&L.sig[b]);
+      k += rd64(&L.cnt[b]);
+      sg += rd64(&L.sig[b]);
     }
   }
   const int r = kNT - 1 - (int)threadIdx.x;
@@ -519,13 +591,13 @@ GS_DI void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo
     for (int j = L.per - 1; j >= 0; --j) {
       const int bb = threadIdx.x * L.per + j;
       if (bb >= L.nbins) continue;
-      const uint64_t c = ald64(&L.cnt[bb]);
-      const uint64_t sg = ald64(&L.sig[bb]);
+      const uint64_t c = rd64(&L.cnt[bb]);
+      const uint64_t sg = rd64(&L.sig[bb]);
       if (bb == b) {
         s.bi.Wab = lvl_total(L, K, S, s.bi.Kab);
         s.bi.cnt = c;
         s.bi.Wb = c ? fx_shifted(sg, L.shift) : fx_zero();
-        s.bi.mx = ald32(&L.mx[bb]);
+        s.bi.mx = rd32(&L.mx[bb]);
         break;
       }
       K += c;
@@ -548,11 +620,11 @@ GS_DI bool criterion(double B, const Fx& S, uint64_t k, const Fx& W, uint32_t vk
 GS_DI void l1_exact(const Hists& H, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
   const int t = threadIdx.x;
   int best = -1, occupied = INT_MAX;
-  if (t < kB1 && ald64(&H.h1->cnt[t])) {
-    if (criterion(B, S, H.a1->K[t], H.a1->W[t], ald32(&H.h1->mx[t]))) best = t;
+  if (t < kB1 && rd64(&H.h1->cnt[t])) {
+    if (criterion(B, S, H.a1->K[t], H.a1->W[t], rd32(&H.h1->mx[t]))) best = t;
   }
   b1 = block_max(s, best);
-  if (t < kB1 && t > b1 && ald64(&H.h1->cnt[t])) occupied = t;
+  if (t < kB1 && t > b1 && rd64(&H.h1->cnt[t])) occupied = t;
   b2 = block_min(s, occupied);
 }
 GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
@@ -561,19 +633,19 @@ GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLd
   for (int j = L.per - 1; j >= 0 && best < 0; --j) {
     const int b = threadIdx.x * L.per + j;
     if (b >= L.nbins) continue;
-    const uint64_t c = ald64(&L.cnt[b]);
+    const uint64_t c = rd64(&L.cnt[b]);
     if (!c) continue;
     uint64_t Kt;
     const Fx W = lvl_total(L, K, Sg, Kt);
-    if (criterion(B, S, Kt, W, ald32(&L.mx[b]))) best = b;
+    if (criterion(B, S, Kt, W, rd32(&L.mx[b]))) best = b;
     K += c;
-    Sg += ald64(&L.sig[b]);
+    Sg += rd64(&L.sig[b]);
   }
   b1 = block_max(s, best);
   int lowest = INT_MAX;
   for (int j = 0; j < L.per; ++j) {
     const int b = threadIdx.x * L.per + j;
-    if (b < L.nbins && b > b1 && ald64(&L.cnt[b])) {
+    if (b < L.nbins && b > b1 && rd64(&L.cnt[b])) {
       lowest = b;
       break;
     }
@@ -596,10 +668,15 @@ GS_DI void sv_finalize(SolveLds& s, double lam, uint32_t tcap) {
 // Ask for a histogram of binade E (level 2) or of keys [base, base + 2048) (level 3).
 GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32_t base) {
   __syncthreads();
-  if (level == 2) {
-    for (int b = threadIdx.x; b < kB2; b += kNT) { H.h2->cnt[b] = 0; H.h2->sig[b] = 0; H.h2->mx[b] = 0; }
-  } else {
-    for (int b = threadIdx.x; b < kB3; b += kNT) { H.h3->cnt[b] = 0; H.h3->sig[b] = 0; H.h3->mx[b] = 0; }
+  // clear every copy of the requested level before the pass that fills it
+  for (int c = 0; c < kC23; ++c) {
+    if (level == 2) {
+      Hist2* h = H.h2 + c;
+      for (int b = threadIdx.x; b < kB2; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; }
+    } else {
+      Hist3* h = H.h3 + c;
+      for (int b = threadIdx.x; b < kB3; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; }
+    }
   }
   if (threadIdx.x == 0) {
     s.c.need = level;
@@ -801,18 +878,52 @@ GS_DI void sv_start(SolveLds& s, const Hists& H, int64_t d) {
   }
 }
 
-// The row's solver, run by the last workgroup of each histogram pass once every workgroup of the
-// row has flushed: it either finishes the row (lambda and the capped threshold become final) or
-// requests the next refinement window for the following pass.
-GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
-  if (threadIdx.x == 0) {
-    s.c = *gc;
-    s.c.zeros = ald64(&gc->zeros);
-    s.c.need = 0;
-    s.c.arrive = 0;
+// Sums the copies of a histogram into copy 0 (nbins bins, `copies` consecutive copies). The
+// copies were filled with atomics by an earlier kernel on the same stream.
+template <typename HistT>
+GS_DI void reduce_copies(HistT* h, int copies, int nbins) {
+  for (int b = threadIdx.x; b < nbins; b += kNT) {
+    uint64_t c = h[0].cnt[b], sg = h[0].sig[b];
+    uint32_t mx = h[0].mx[b];
+    for (int k = 1; k < copies; ++k) {
+      c += h[k].cnt[b];
+      sg += h[k].sig[b];
+      mx = max(mx, h[k].mx[b]);
+    }
+    h[0].cnt[b] = c;
+    h[0].sig[b] = sg;
+    h[0].mx[b] = mx;
   }
   __syncthreads();
+}
+
+// The row's solver, run by one workgroup per row after each histogram pass: it either finishes the
+// row (lambda and the capped threshold become final) or requests the next refinement window.
+GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
+  if (threadIdx.x == 0) s.c = *gc;
+  __syncthreads();
   if (s.c.done) return;
+  if (s.c.stage == 0) {
+    reduce_copies(const_cast<Hist1*>(H.h1), kC1, kB1);
+    // zeros = d minus the histogram's population (every nonzero key, finite or not, is binned)
+    uint64_t n = 0;
+    if (threadIdx.x < kB1) n = H.h1->cnt[threadIdx.x];
+    for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o);
+    if ((threadIdx.x & 63) == 0) s.sk[0][threadIdx.x >> 6] = n;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint64_t tot = 0;
+      for (int i = 0; i < kNT / 64; ++i) tot += s.sk[0][i];
+      s.c.zeros = (uint64_t)d - tot;
+    }
+    __syncthreads();
+  } else if (s.c.need == 2) {
+    reduce_copies(H.h2, kC23, kB2);
+  } else if (s.c.need == 3) {
+    reduce_copies(H.h3, kC23, kB3);
+  }
+  if (threadIdx.x == 0) s.c.need = 0;
+  __syncthreads();
   if (s.c.stage == 0) sv_start(s, H, d);
   else if (s.c.solver == GSPAR_GREEDY) sv_greedy(s, H);
   else sv_exact(s, H);
@@ -826,11 +937,13 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
 __global__ void __launch_bounds__(256) k_init(Args a) {
   const int64_t tid = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  if (tid == 0) *reinterpret_cast<uint32_t*>(a.ws) = 0;  // tile ticket
-  // level-1 histograms
+  // level-1 histogram copies, capped-count lines, look-back status words
   uint64_t* h1 = reinterpret_cast<uint64_t*>(a.ws + a.lay.h1);
-  const int64_t n1 = a.rows * (int64_t)(sizeof(Hist1) / 8);
+  const int64_t n1 = a.rows * kC1 * (int64_t)(sizeof(Hist1) / 8);
   for (int64_t i = tid; i < n1; i += stride) h1[i] = 0;
+  uint64_t* kc = reinterpret_cast<uint64_t*>(a.ws + a.lay.kc);
+  const int64_t nkc = (int64_t)((a.lay.status - a.lay.kc) / 8);
+  for (int64_t i = tid; i < nkc; i += stride) kc[i] = 0;
   uint64_t* st = status_of(a);
   const int64_t ns = a.rows * a.lay.tiles;
   for (int64_t i = tid; i < ns; i += stride) st[i] = 0;
@@ -848,158 +961,136 @@ __global__ void __launch_bounds__(256) k_init(Args a) {
   }
 }
 
-// Streaming statistics pass. Grid: rows * nb workgroups of kNT threads; each flushes its
-// histogram as per-binade totals (count, exact significand sum, maximum key).
+// Streaming statistics pass. Grid: rows * nb workgroups of kNT threads. Each builds an LDS
+// histogram over binades (count, exact significand sum, maximum key), kept in kLaneCopies copies
+// by lane to spread same-address LDS atomics, and adds its nonempty bins into one of the row's kC1
+// global copies (chosen by workgroup index) with atomics. k_solve runs next.
 template <bool VEC>
 __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_stats(Args a) {
-  __shared__ PassLds sm;
-  __shared__ uint32_t s_last;
+  __shared__ StatsLds sm_st;
+  StatsLds& sm = sm_st;
   const int64_t row = blockIdx.x / a.nb;
   const int64_t blk = blockIdx.x % a.nb;
-  for (int b = threadIdx.x; b < kFine; b += kNT) {
-    sm.h.pk[b] = 0;
-    sm.h.mx[b] = 0;
+  for (int b = threadIdx.x; b < kB1 * kLaneCopies; b += kNT) {
+    sm.pk[b] = 0;
+    sm.mx[b] = 0;
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + row * a.ld;
   const int64_t beg = blk * a.chunk;
   const int64_t end = min(a.d, beg + a.chunk);
-  uint32_t zeros = 0;
-  // four float4 loads in flight per thread before any LDS work
-  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += 4 * kNT) {
-    float v[4][4];
-    uint32_t m[4];
+  const uint32_t lc = threadIdx.x & (kLaneCopies - 1);
+  stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) m[u] = load4<VEC>(gr, q + u * kNT, end, v[u]);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const uint32_t key = key_of(v[u][c]);
-        if (key == 0) {
-          zeros += (m[u] >> c) & 1;
-        } else {
-          const uint32_t f = key >> 19;
-          atomicAdd(&sm.h.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
-          atomicMax(&sm.h.mx[f], key);
-        }
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[c]);  // coordinates outside [beg, end) read as 0 and are skipped
+      if (key != 0) {
+        const uint32_t f = (key >> 23) * kLaneCopies + lc;
+        atomicAdd(&sm.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
+        // the bin maximum only grows, so a plain read that already covers key skips the atomic
+        if (key > sm.mx[f]) atomicMax(&sm.mx[f], key);
       }
     }
-  }
-  for (int o = 32; o > 0; o >>= 1) zeros += __shfl_xor(zeros, o);
+  });
   __syncthreads();
-  RowCtl* ctl = ctl_of(a, row);
-  if ((threadIdx.x & 63) == 0 && zeros) atomicAdd((unsigned long long*)&ctl->zeros, (unsigned long long)zeros);
-  // flush one binade per thread
+  // flush one binade per thread into copy (blk mod kC1)
   if (threadIdx.x < kB1) {
     const int e = threadIdx.x;
     uint64_t cnt = 0, sg = 0;
     uint32_t mx = 0;
-    for (int j = 0; j < 16; ++j) {
-      const uint64_t p = sm.h.pk[e * 16 + j];
+#pragma unroll
+    for (int j = 0; j < kLaneCopies; ++j) {
+      const uint64_t p = sm.pk[e * kLaneCopies + j];
       cnt += p >> 44;
       sg += p & ((1ull << 44) - 1);
-      mx = max(mx, sm.h.mx[e * 16 + j]);
+      mx = max(mx, sm.mx[e * kLaneCopies + j]);
     }
     if (cnt) {
-      Hist1* h = h1_of(a, row);
+      Hist1* h = h1_of(a, row, (int)(blk % kC1));
       atomicAdd((unsigned long long*)&h->cnt[e], (unsigned long long)cnt);
       atomicAdd((unsigned long long*)&h->sig[e], (unsigned long long)sg);
       atomicMax(&h->mx[e], mx);
     }
   }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&ctl->arrive, 1u) == (uint32_t)(a.nb - 1);
-  __syncthreads();
-  if (!s_last) return;
-  // the last workgroup of the row: every flush above is visible after this acquire fence
-  __threadfence();
-  const Hists H{h1_of(a, row), h2_of(a, row), h3_of(a, row), a1_of(a, row)};
-  solve_row(sm.s, ctl, H, a.d);
 }
 
 // Refinement pass over one window of keys, for the rows whose solver asked for one.
 template <bool VEC>
 __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_refine(Args a) {
-  __shared__ PassLds sm;
-  __shared__ uint32_t s_last;
+  __shared__ WinLds sm_w;
+  WinLds& sm = sm_w;
   const int64_t row = blockIdx.x / a.nb;
   const int64_t blk = blockIdx.x % a.nb;
-  RowCtl* ctl = ctl_of(a, row);
+  const RowCtl* ctl = ctl_of(a, row);
   const uint32_t need = ctl->need;
   if (need != 2 && need != 3) return;
   uint32_t lo, shift;
   int nbins;
   uint64_t *gcnt, *gsig;
   uint32_t* gmx;
+  const int cp = (int)(blk % kC23);
   if (need == 2) {
     lo = ctl->l2exp << 23;
     shift = 11;
     nbins = kB2;
-    Hist2* h = h2_of(a, row);
+    Hist2* h = h2_of(a, row, cp);
     gcnt = h->cnt; gsig = h->sig; gmx = h->mx;
   } else {
     lo = ctl->l3base;
     shift = 0;
     nbins = kB3;
-    Hist3* h = h3_of(a, row);
+    Hist3* h = h3_of(a, row, cp);
     gcnt = h->cnt; gsig = h->sig; gmx = h->mx;
   }
   const uint32_t span = (uint32_t)nbins << shift;
   for (int b = threadIdx.x; b < nbins; b += kNT) {
-    sm.h.pk[b] = 0;
-    sm.h.mx[b] = 0;
+    sm.pk[b] = 0;
+    sm.mx[b] = 0;
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + row * a.ld;
   const int64_t beg = blk * a.chunk;
   const int64_t end = min(a.d, beg + a.chunk);
-  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += 4 * kNT) {
-    float v[4][4];
+  stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) load4<VEC>(gr, q + u * kNT, end, v[u]);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const uint32_t key = key_of(v[u][c]);
-        const uint32_t rel = key - lo;
-        if (key != 0 && rel < span) {
-          const uint32_t b = rel >> shift;
-          atomicAdd(&sm.h.pk[b], (unsigned long long)((1ull << 44) + key_sig(key)));
-          atomicMax(&sm.h.mx[b], key);
-        }
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[c]);
+      const uint32_t rel = key - lo;
+      if (key != 0 && rel < span) {
+        const uint32_t b = rel >> shift;
+        atomicAdd(&sm.pk[b], (unsigned long long)((1ull << 44) + key_sig(key)));
+        if (key > sm.mx[b]) atomicMax(&sm.mx[b], key);
       }
     }
-  }
+  });
   __syncthreads();
   for (int b = threadIdx.x; b < nbins; b += kNT) {
-    const uint64_t p = sm.h.pk[b];
+    const uint64_t p = sm.pk[b];
     if (p) {
       atomicAdd((unsigned long long*)&gcnt[b], (unsigned long long)(p >> 44));
       atomicAdd((unsigned long long*)&gsig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
-      atomicMax(&gmx[b], sm.h.mx[b]);
+      atomicMax(&gmx[b], sm.mx[b]);
     }
   }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&ctl->arrive, 1u) == (uint32_t)(a.nb - 1);
-  __syncthreads();
-  if (!s_last) return;
-  // the last workgroup of the row: every flush above is visible after this acquire fence
-  __threadfence();
+}
+
+// The solver: one workgroup per row, after the statistics pass and after every refinement pass.
+__global__ void __launch_bounds__(kNT) k_solve(Args a) {
+  __shared__ SolveLds sm;
+  const int64_t row = blockIdx.x;
   const Hists H{h1_of(a, row), h2_of(a, row), h3_of(a, row), a1_of(a, row)};
-  solve_row(sm.s, ctl, H, a.d);
+  solve_row(sm, ctl_of(a, row), H, a.d);
 }
 
 // Sampling, amplification and order-preserving compaction. Workgroup t handles tile t (kTileElems
-// coordinates of one row, in row order). Tile prefixes chain through a decoupled look-back whose
-// status word packs (flag:2 | capped survivors:31 | survivors:31). A predecessor that has not yet
-// published after a few polls is counted by the waiting wave itself (decoupled fallback), so no
-// ordering of workgroup dispatch is assumed and no global ticket counter serialises the tiles.
+// coordinates of one row, in row order); wave w of the workgroup owns the tile's w-th quarter and
+// reads it as kTileGroups coalesced float4 loads per lane. Tile prefixes chain through a decoupled
+// look-back whose status word packs (flag:2 | capped survivors:31 | survivors:31). A predecessor
+// that has not published after a long back-off is counted by the waiting wave itself, so no
+// ordering of workgroup dispatch is assumed and every wait ends.
 constexpr uint64_t kStAgg = 1ull << 62, kStInc = 2ull << 62, kStVal = (1ull << 62) - 1;
-constexpr int kPolls = 16;
+constexpr int kPolls = 4096;
+constexpr int kWaveElems = kTileElems / (kTileThreads / 64);  // coordinates per wave per tile
 
 struct TileCtx {
   const float* row;
@@ -1010,10 +1101,10 @@ struct TileCtx {
   bool live;
 };
 
-// Selection bits (bit c: coordinate 4q+c survives) and capped-survivor bits of group q.
-template <bool VEC>
-__device__ __forceinline__ void decide_group(const TileCtx& c, int64_t q, float v[4], uint32_t& z, uint32_t& cz) {
-  const uint32_t m = load4<VEC>(c.row, q, c.d, v);
+// Selection bits (bit c: coordinate 4q+c survives) and capped-survivor bits of group q, whose
+// values v are given (m: bit c set when coordinate 4q+c exists).
+__device__ __forceinline__ void decide_values(const TileCtx& c, int64_t q, const float v[4], uint32_t m, uint32_t& z,
+                                              uint32_t& cz) {
   uint32_t x0 = (uint32_t)q, x1 = (uint32_t)((uint64_t)q >> 32), x2 = 0, x3 = 0;
   philox10(x0, x1, x2, x3, c.k0, c.k1);
   const uint32_t xr[4] = {x0, x1, x2, x3};
@@ -1028,6 +1119,13 @@ __device__ __forceinline__ void decide_group(const TileCtx& c, int64_t q, float 
     z |= (uint32_t)sel << k;
     cz |= (uint32_t)(sel && capped) << k;
   }
+}
+
+// The same for group q loaded here (entries past the row's end read as 0).
+template <bool VEC>
+__device__ __forceinline__ void decide_group(const TileCtx& c, int64_t q, float v[4], uint32_t& z, uint32_t& cz) {
+  const uint32_t m = load4<VEC>(c.row, q, c.d, v);
+  decide_values(c, q, v, m, z, cz);
 }
 
 // Aggregate (capped << 31 | survivors) of tile `part` computed by one wave (fallback path).
@@ -1049,37 +1147,56 @@ __device__ uint64_t wave_tile_aggregate(const TileCtx& c, int64_t part, int lane
   return (nc << 31) | n;
 }
 
-// Block-wide exclusive scan of a 32-bit value (kTileThreads threads); also returns the total.
-__device__ __forceinline__ uint32_t tile_scan(uint32_t x, uint32_t* s_w, uint32_t& total) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  uint32_t inc = x;
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = __shfl_up(inc, (unsigned)o);
-    if (lane >= o) inc += y;
-  }
-  if (lane == 63) s_w[wv] = inc;
-  __syncthreads();
-  uint32_t pre = 0;
-  total = 0;
-  for (int i = 0; i < kTileThreads / 64; ++i) {
-    if (i < wv) pre += s_w[i];
-    total += s_w[i];
-  }
-  __syncthreads();
-  return pre + inc - x;
+// Exclusive prefix over the lanes of a wave of n in [0, 7], from three ballots; `total` receives
+// the wave's sum.
+__device__ __forceinline__ uint32_t wave_prefix_small(uint32_t n, int lane, uint32_t& total) {
+  const unsigned long long b0 = __ballot(n & 1), b1 = __ballot(n & 2), b2 = __ballot(n & 4);
+  const unsigned long long lt = (1ull << lane) - 1;
+  total = (uint32_t)(__popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2));
+  return (uint32_t)(__popcll(b0 & lt) + 2 * __popcll(b1 & lt) + 4 * __popcll(b2 & lt));
 }
 
-// Phase 1 decides every coordinate of the tile (coalesced float4 loads, one Philox block per
-// group) and records per-group nibbles in LDS: selected, capped-and-selected, negative. After the
-// look-back, phase 2 gives each thread 64 consecutive coordinates, so survivors are emitted in
-// index order from a contiguous range per thread.
+// Phase 1: each lane decides kTileGroups groups of its wave's quarter and keeps the selection,
+// capped and sign bits in registers; the values of capped survivors (which are emitted unscaled)
+// are appended, in index order, to a small per-wave LDS list. The wave totals give the tile
+// aggregate, published at once; wave 0 then looks back for the tile's prefix. Phase 2: each wave
+// walks its groups again in index order, places its survivors in a per-wave LDS ring at offsets
+// from a ballot prefix over lanes, and writes the ring out in blocks of 64 consecutive pairs, one
+// coalesced store per array per block. Phase 2 reads no global memory (a load would wait for every
+// store issued before it), except for capped survivors beyond the LDS list's capacity.
+constexpr int kCapList = 256;    // capped survivor values kept per wave
+constexpr int kSampleBatch = 8;  // float4 loads in flight per lane in the sampling pass
+constexpr int kRing = 512;       // per-wave staging ring of (index, value) pairs (power of two)
+static_assert(kTileGroups == 2 * kSampleBatch, "the whole-tile path runs two batches");
+// Below this lambda, lambda * 2^32 * |g| could round differently from (lambda * |g|) * 2^32.
+constexpr double kLamScaledMin = 0x1p-900;
+
+// Whole-tile decisions with the scaled threshold: coordinate i survives iff
+// x_i < fl(lambda * 2^32 * |g_i|), which equals the comparison x_i < fl(lambda * |g_i|) * 2^32
+// (exact scaling by a power of two) for lambda = 0 or lambda >= kLamScaledMin; a capped coordinate
+// has a threshold of at least 2^32, so it always survives and the capped test is that comparison.
+__device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double lam32, uint32_t k0, uint32_t k1,
+                                            uint32_t& z, uint32_t& cz) {
+  uint32_t x0 = (uint32_t)q, x1 = (uint32_t)((uint64_t)q >> 32), x2 = 0, x3 = 0;
+  philox10(x0, x1, x2, x3, k0, k1);
+  const uint32_t xr[4] = {x0, x1, x2, x3};
+  z = 0;
+  cz = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const double t = lam32 * (double)fabsf(v[k]);
+    z |= (uint32_t)((double)xr[k] < t) << k;
+    cz |= (uint32_t)(t >= 0x1p32) << k;
+  }
+}
+
 template <bool VEC>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
-  __shared__ alignas(16) uint8_t s_z[kTileElems / 4];
-  __shared__ alignas(16) uint8_t s_c[kTileElems / 4];
-  __shared__ alignas(16) uint8_t s_n[kTileElems / 4];
-  __shared__ uint32_t s_w[kTileThreads / 64];
-  __shared__ uint32_t s_w2[kTileThreads / 64];
+  __shared__ float s_capv[kTileThreads / 64][kCapList];
+  __shared__ int32_t s_ri[kTileThreads / 64][kRing];
+  __shared__ float s_rv[kTileThreads / 64][kRing];
+  __shared__ uint32_t s_wsel[kTileThreads / 64];
+  __shared__ uint32_t s_wcap[kTileThreads / 64];
   __shared__ uint64_t s_excl;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t t = blockIdx.x;
@@ -1096,27 +1213,78 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   c.k0 = (uint32_t)seed;
   c.k1 = (uint32_t)(seed >> 32);
   const float inv = ctl->inv_lam;
+  // first group of this lane: tile base + wave quarter + lane; iteration j adds 64 groups
+  const int64_t q0 = part * (kTileElems / 4) + (int64_t)wv * (kWaveElems / 4) + lane;
 
-  uint32_t nsel = 0, ncap = 0;
-#pragma unroll 4
-  for (int j = 0; j < kTileGroups; ++j) {
-    const int gi = j * kTileThreads + tid;  // group inside the tile
-    float v[4];
-    uint32_t z, cz;
-    decide_group<VEC>(c, part * (kTileElems / 4) + gi, v, z, cz);
-    uint32_t neg = 0;
+  uint64_t selm = 0, capm = 0, negm = 0;
+  uint32_t ncl = 0;  // capped survivors of this wave so far (the LDS list keeps the first kCapList)
+  auto record = [&](int j, const float v[4], uint32_t z, uint32_t cz) {
+    cz &= z;
+    selm |= (uint64_t)z << (4 * j);
+    if (__ballot(z != 0)) {
+      uint32_t neg = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) neg |= (uint32_t)(__float_as_uint(v[k]) >> 31) << k;
-    s_z[gi] = (uint8_t)z;
-    s_c[gi] = (uint8_t)cz;
-    s_n[gi] = (uint8_t)neg;
-    nsel += __popc(z);
-    ncap += __popc(cz);
+      for (int k = 0; k < 4; ++k) neg |= (__float_as_uint(v[k]) >> 31) << k;
+      negm |= (uint64_t)neg << (4 * j);
+    }
+    if (__ballot(cz != 0)) {
+      capm |= (uint64_t)cz << (4 * j);
+      uint32_t tot;
+      uint32_t p = ncl + wave_prefix_small((uint32_t)__popc(cz), lane, tot);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if ((cz >> k) & 1) {
+          if (p < (uint32_t)kCapList) s_capv[wv][p] = v[k];
+          ++p;
+        }
+      }
+      ncl += tot;
+    }
+  };
+  const bool fast = c.live && (c.lam == 0.0 || c.lam >= kLamScaledMin);
+  if (VEC && fast && (part + 1) * (int64_t)kTileElems <= a.d) {
+    // whole tile inside the row: kSampleBatch unconditional loads in flight per lane
+    const double lam32 = c.lam * 0x1p32;
+#pragma unroll
+    for (int jb = 0; jb < kTileGroups; jb += kSampleBatch) {
+      float4 x[kSampleBatch];
+#pragma unroll
+      for (int u = 0; u < kSampleBatch; ++u)
+        x[u] = *reinterpret_cast<const float4*>(c.row + 4 * (q0 + 64 * (jb + u)));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < kSampleBatch; ++u) {
+        const float v[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+        uint32_t z, cz;
+        decide_fast(q0 + 64 * (jb + u), v, lam32, c.k0, c.k1, z, cz);
+        record(jb + u, v, z, cz);
+      }
+    }
+  } else if (c.live) {
+    for (int j = 0; j < kTileGroups; ++j) {
+      float v[4];
+      uint32_t z, cz;
+      decide_group<VEC>(c, q0 + 64 * j, v, z, cz);
+      record(j, v, z, cz);
+    }
   }
-  uint32_t tsel, tcap;
-  tile_scan(nsel, s_w, tsel);
-  tile_scan(ncap, s_w2, tcap);
-  const uint64_t agg = ((uint64_t)tcap << 31) | tsel;
+  uint32_t nsel = (uint32_t)__popcll(selm), ncap = (uint32_t)__popcll(capm);
+  for (int o = 32; o > 0; o >>= 1) {
+    nsel += __shfl_xor(nsel, o);
+    ncap += __shfl_xor(ncap, o);
+  }
+  if (lane == 0) {
+    s_wsel[wv] = nsel;
+    s_wcap[wv] = ncap;
+  }
+  __syncthreads();
+  uint32_t tsel = 0, tcp = 0, wbase = 0;
+  for (int i = 0; i < kTileThreads / 64; ++i) {
+    if (i < wv) wbase += s_wsel[i];
+    tsel += s_wsel[i];
+    tcp += s_wcap[i];
+  }
+  const uint64_t agg = ((uint64_t)tcp << 31) | tsel;
 
   // decoupled look-back for the tile's exclusive prefix within its row
   uint64_t* st = status_of(a);
@@ -1136,13 +1304,15 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         uint64_t sw = kStInc;
         if (i >= first) {
           int polls = 0;
-          do {
+          sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          while ((sw >> 62) == 0 && ++polls < kPolls) {
+            __builtin_amdgcn_s_sleep(4);
             sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          } while ((sw >> 62) == 0 && ++polls < kPolls);
+          }
         }
         const uint64_t incl_mask = __ballot((sw >> 62) == 2);
         const int stop = incl_mask ? (__ffsll((unsigned long long)incl_mask) - 1) : 63;
-        // predecessors up to `stop` that have not published: count them here
+        // predecessors up to `stop` that never published: count them here
         uint64_t missing = __ballot((sw >> 62) == 0 && lane <= stop);
         while (missing) {
           const int m = __ffsll((unsigned long long)missing) - 1;
@@ -1163,41 +1333,63 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     }
   }
   __syncthreads();
-  const uint64_t base = s_excl & 0x7FFFFFFFull;  // survivors of the row before this tile
+  const uint64_t excl = s_excl;
 
-  // phase 2: thread t owns groups [16t, 16t + 16) of the tile, i.e. 64 consecutive coordinates
-  const int g0 = tid * kTileGroups;
-  uint32_t zw[kTileGroups / 4];
-#pragma unroll
-  for (int w = 0; w < kTileGroups / 4; ++w) zw[w] = *reinterpret_cast<const uint32_t*>(&s_z[g0 + 4 * w]);
-  uint32_t mine = 0;
-#pragma unroll
-  for (int w = 0; w < kTileGroups / 4; ++w) mine += __popc(zw[w]);
-  uint32_t dummy;
-  uint64_t pos = base + tile_scan(mine, s_w, dummy);
-  if (mine) {
+  // phase 2: survivors of this wave, in index order, through the staging ring
+  if (nsel) {
     int32_t* __restrict__ oi = a.idx + row * a.cap;
     float* __restrict__ ov = a.val + row * a.cap;
-    const int64_t e0 = part * (int64_t)kTileElems + 4 * (int64_t)g0;
-    for (int gq = 0; gq < kTileGroups; ++gq) {
-      const uint32_t z = (zw[gq >> 2] >> (8 * (gq & 3))) & 0xF;
-      if (!z) continue;
-      const uint32_t cz = s_c[g0 + gq], ng = s_n[g0 + gq];
+    uint64_t out = (excl & 0x7FFFFFFFull) + wbase;  // output position of the ring's oldest entry
+    uint32_t head = 0, fill = 0;                     // ring window [head, head + fill)
+    uint32_t cl = 0;                                 // capped survivors of this wave emitted so far
+    for (int j = 0; j < kTileGroups; ++j) {
+      const uint32_t z = (uint32_t)(selm >> (4 * j)) & 0xF;
+      if (__ballot(z != 0) == 0) continue;
+      uint32_t tot, ctot = 0;
+      uint32_t slot = head + fill + wave_prefix_small((uint32_t)__popc(z), lane, tot);
+      const int64_t i0 = 4 * (q0 + 64 * j);
+      const uint32_t cz = (uint32_t)(capm >> (4 * j)) & 0xF, ng = (uint32_t)(negm >> (4 * j)) & 0xF;
+      uint32_t cp = 0;
+      if (__ballot(cz != 0)) cp = cl + wave_prefix_small((uint32_t)__popc(cz), lane, ctot);
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         if ((z >> k) & 1) {
-          if ((int64_t)pos < a.cap) {
-            const int64_t i = e0 + 4 * gq + k;
-            oi[pos] = (int32_t)i;
-            ov[pos] = ((cz >> k) & 1) ? c.row[i] : (((ng >> k) & 1) ? -inv : inv);
+          float val = ((ng >> k) & 1) ? -inv : inv;
+          if ((cz >> k) & 1) {
+            val = cp < (uint32_t)kCapList ? s_capv[wv][cp] : c.row[i0 + k];
+            ++cp;
           }
-          ++pos;
+          const uint32_t r = slot & (kRing - 1);
+          s_ri[wv][r] = (int32_t)(i0 + k);
+          s_rv[wv][r] = val;
+          ++slot;
         }
+      }
+      fill += tot;
+      cl += ctot;
+      __builtin_amdgcn_wave_barrier();
+      while (fill >= 64) {
+        const uint32_t r = (head + lane) & (kRing - 1);
+        if ((int64_t)(out + lane) < a.cap) {
+          oi[out + lane] = s_ri[wv][r];
+          ov[out + lane] = s_rv[wv][r];
+        }
+        head = (head + 64) & (kRing - 1);
+        fill -= 64;
+        out += 64;
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    if ((uint32_t)lane < fill) {
+      const uint32_t r = (head + lane) & (kRing - 1);
+      if ((int64_t)(out + lane) < a.cap) {
+        oi[out + lane] = s_ri[wv][r];
+        ov[out + lane] = s_rv[wv][r];
       }
     }
   }
   if (part == a.lay.tiles - 1 && tid == 0) {
-    const uint64_t incl = s_excl + agg;
+    const uint64_t incl = excl + agg;
     const int64_t n = (int64_t)(incl & 0x7FFFFFFFull);
     const int64_t kc = (int64_t)((incl >> 31) & 0x7FFFFFFFull);
     if (a.nnz) a.nnz[row] = n;
@@ -1210,14 +1402,14 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   }
 }
 
-// p_i = min(lambda |g_i|, 1), exactly 1 on the capped set. Grid: rows * nb workgroups.
+// p_i = min(lambda |g_i|, 1), exactly 1 on the capped set. Grid: rows * nb workgroups. Capped
+// coordinates are counted per workgroup and added into one of eight per-row lines.
 template <bool VEC>
 __global__ void __launch_bounds__(256) k_probs(Args a) {
-  __shared__ uint32_t s_last;
   __shared__ uint32_t s_cnt[4];
   const int64_t row = blockIdx.x / a.nb;
   const int64_t blk = blockIdx.x % a.nb;
-  RowCtl* ctl = ctl_of(a, row);
+  const RowCtl* ctl = ctl_of(a, row);
   const double lam = ctl->lam;
   const uint32_t tcap = ctl->tcap;
   const bool live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO));
@@ -1226,9 +1418,8 @@ __global__ void __launch_bounds__(256) k_probs(Args a) {
   const int64_t beg = blk * a.chunk;
   const int64_t end = min(a.d, beg + a.chunk);
   uint32_t kc = 0;
-  for (int64_t q = beg / 4 + threadIdx.x; 4 * q < end; q += blockDim.x) {
-    float v[4], o[4];
-    const uint32_t m = load4<VEC>(gr, q, end, v);
+  stream_groups<VEC, 4, 256>(gr, beg, end, [&](int64_t q, const float v[4], uint32_t m) {
+    float o[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const uint32_t key = key_of(v[c]);
@@ -1246,22 +1437,27 @@ __global__ void __launch_bounds__(256) k_probs(Args a) {
           if ((m >> c) & 1) pr[4 * q + c] = o[c];
       }
     }
-  }
+  });
   for (int o = 32; o > 0; o >>= 1) kc += __shfl_xor(kc, o);
   if ((threadIdx.x & 63) == 0) s_cnt[threadIdx.x >> 6] = kc;
   __syncthreads();
   if (threadIdx.x == 0) {
     uint32_t tot = 0;
     for (int i = 0; i < (int)(blockDim.x / 64); ++i) tot += s_cnt[i];
-    if (tot) atomicAdd((unsigned long long*)&ctl->kcount, (unsigned long long)tot);
-    __threadfence();
-    s_last = atomicAdd(&ctl->parrive, 1u) == (uint32_t)(a.nb - 1);
+    if (tot) atomicAdd(&kc_of(a, row)[blk & 7].v, (unsigned long long)tot);
   }
-  __syncthreads();
-  if (!s_last || threadIdx.x != 0) return;
-  __threadfence();
-  if (a.lam_out) a.lam_out[row] = lam;
-  if (a.k_out) a.k_out[row] = (int64_t)ald64(&ctl->kcount);
+}
+
+// Per-row outputs of the probabilities entry points (one thread per row).
+__global__ void __launch_bounds__(64) k_probs_out(Args a) {
+  const int64_t row = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (row >= a.rows) return;
+  const RowCtl* ctl = ctl_of(a, row);
+  const CountLine* kl = kc_of(a, row);
+  uint64_t ktot = 0;
+  for (int i = 0; i < 8; ++i) ktot += kl[i].v;
+  if (a.lam_out) a.lam_out[row] = ctl->lam;
+  if (a.k_out) a.k_out[row] = (int64_t)ktot;
   uint32_t fl = ctl->flags;
   if (!ctl->done) fl |= kFlagInternal;
   if (a.flags_out) a.flags_out[row] = fl;
@@ -1321,7 +1517,7 @@ static bool vec_ok(const Args& a) { return ((uintptr_t)a.g % 16 == 0) && (a.ld %
 
 static int launch_solve(Args& a, hipStream_t s) {
   const bool vec = vec_ok(a);
-  const int64_t zero_items = a.rows * (int64_t)(sizeof(Hist1) / 8) + a.rows * a.lay.tiles;
+  const int64_t zero_items = a.rows * kC1 * (int64_t)(sizeof(Hist1) / 8) + a.rows * a.lay.tiles;
   int ib = (int)((zero_items + 255) / 256);
   if (ib > 1024) ib = 1024;
   if (ib < 1) ib = 1;
@@ -1331,11 +1527,13 @@ static int launch_solve(Args& a, hipStream_t s) {
   if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
   else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
   time_after(1, s);
+  hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
   // each greedy step may need a level-2 and a level-3 window, the exact solver at most both once
   const int R = a.solver == GSPAR_GREEDY ? 2 * a.T : 2;
   for (int r = 0; r < R; ++r) {
     if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
     else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
+    hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
   }
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
@@ -1363,6 +1561,7 @@ static int run_probs(Args& a, hipStream_t s) {
   if (vec) hipLaunchKernelGGL(k_probs<true>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(k_probs<false>, grid, dim3(256), 0, s, a);
   time_after(2, s);
+  hipLaunchKernelGGL(k_probs_out, dim3((unsigned)((a.rows + 63) / 64)), dim3(64), 0, s, a);
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
 

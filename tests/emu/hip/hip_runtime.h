@@ -136,7 +136,11 @@ inline unsigned long long __ballot(int pred) {
   w.bar->arrive_and_wait();
   return m;
 }
+inline void __builtin_amdgcn_wave_barrier() { emu::wave().bar->arrive_and_wait(); }
 inline int __popc(unsigned v) { return __builtin_popcount(v); }
+inline int __popcll(unsigned long long v) { return __builtin_popcountll(v); }
+inline void __builtin_amdgcn_s_sleep(int) { std::this_thread::yield(); }
+inline void __builtin_amdgcn_sched_barrier(int) {}
 inline unsigned __float_as_uint(float f) {
   unsigned u;
   std::memcpy(&u, &f, 4);
