@@ -29,6 +29,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <type_traits>
 
 #include "gspar.h"
 
@@ -239,11 +240,6 @@ struct Hist3 {
   uint64_t sig[kB3];
   uint32_t mx[kB3];
 };
-// Per binade b: count and exact sum of all keys in binades above b (filled by the first solve).
-struct L1Above {
-  uint64_t K[kB1];
-  Fx W[kB1];
-};
 // Per-row partial count of capped coordinates written by the probabilities pass, one per class.
 struct alignas(128) CountLine {
   unsigned long long v;
@@ -253,7 +249,7 @@ struct alignas(128) CountLine {
 GS_HD size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctl, h1, h2, h3, a1, kc, status, total;
+  size_t ctl, h1, h2, h3, kc, status, total;
   int64_t tiles;  // tiles per row of the sample pass
 };
 
@@ -271,8 +267,6 @@ GS_HD Layout layout_of(int64_t rows, int64_t d) {
   off += align256((size_t)rows * kC23 * sizeof(Hist2));
   L.h3 = off;
   off += align256((size_t)rows * kC23 * sizeof(Hist3));
-  L.a1 = off;
-  off += align256((size_t)rows * sizeof(L1Above));
   L.kc = off;
   off += align256((size_t)rows * 8 * sizeof(CountLine));
   L.status = off;
@@ -318,18 +312,11 @@ __device__ __forceinline__ Hist3* h3_of(const Args& a, int64_t r, int c = 0) {
 __device__ __forceinline__ CountLine* kc_of(const Args& a, int64_t r) {
   return reinterpret_cast<CountLine*>(a.ws + a.lay.kc) + r * 8;
 }
-__device__ __forceinline__ L1Above* a1_of(const Args& a, int64_t r) {
-  return reinterpret_cast<L1Above*>(a.ws + a.lay.a1) + r;
-}
 __device__ __forceinline__ uint64_t* status_of(const Args& a) {
   return reinterpret_cast<uint64_t*>(a.ws + a.lay.status);
 }
 
 
-
-// Histogram words read by the solver (written by an earlier kernel on the same stream).
-__device__ __forceinline__ uint64_t rd64(const uint64_t* p) { return *p; }
-__device__ __forceinline__ uint32_t rd32(const uint32_t* p) { return *p; }
 
 // Four consecutive coordinates 4q..4q+3 of a row; entries at or beyond `end` read as 0 and are
 // flagged invalid in the returned mask (bit c set = coordinate 4q+c exists).
@@ -429,6 +416,21 @@ struct BinInfo {
   Fx Wb;
   uint32_t mx;
 };
+// The solver's working copies of the histograms, in LDS: level 1 with, per binade, the count and
+// exact sum of all keys in binades above it; the level-2 and level-3 windows when they exist.
+struct L1Cache {
+  uint64_t cnt[kB1];
+  uint64_t sig[kB1];
+  uint32_t mx[kB1];
+  uint64_t K[kB1];
+  Fx W[kB1];
+};
+template <int N>
+struct WinCache {
+  uint32_t cnt[N];  // window counts never exceed d < 2^31
+  uint64_t sig[N];
+  uint32_t mx[N];
+};
 struct SolveLds {
   uint64_t sk[2][kNT];
   uint64_t ss[2][kNT];
@@ -436,12 +438,17 @@ struct SolveLds {
   int ired[kNT / 64];
   BinInfo bi;
   RowCtl c;  // working copy of the row's control block
+  L1Cache l1;
+  WinCache<kB2> w2;
+  WinCache<kB3> w3;
 };
 struct Hists {
-  const Hist1* h1;
-  Hist2* h2;
-  Hist3* h3;
-  L1Above* a1;
+  L1Cache* l1;         // LDS
+  WinCache<kB2>* w2;   // LDS
+  WinCache<kB3>* w3;   // LDS
+  const Hist1* h1g;    // the row's global copies, filled by the histogram passes
+  Hist2* h2g;
+  Hist3* h3g;
 };
 
 GS_DI int block_max(SolveLds& s, int v) {
@@ -463,15 +470,15 @@ GS_DI int block_min(SolveLds& s, int v) {
   return r;
 }
 
-// Level 1 (one bin per binade): exclusive suffix sums over the 256 binades, exact, written once
-// per row to the level-1 cache. Threads 0..255 own one binade each.
+// Level 1 (one bin per binade): exclusive suffix sums over the 256 binades, exact, into the LDS
+// cache. Threads 0..255 own one binade each.
 GS_DI void l1_build(SolveLds& s, const Hists& H) {
   const int t = threadIdx.x;
   uint64_t k = 0;
   Fx w = fx_zero();
   if (t < kB1) {
-    k = rd64(&H.h1->cnt[t]);
-    if (k) w = fx_shifted(rd64(&H.h1->sig[t]), binade_shift(t));
+    k = H.l1->cnt[t];
+    if (k) w = fx_shifted(H.l1->sig[t], binade_shift(t));
   }
   const int r = kB1 - 1 - t;  // reversed index: a prefix over r is a suffix over binades
   if (t < kB1) {
@@ -500,26 +507,26 @@ GS_DI void l1_build(SolveLds& s, const Hists& H) {
     cur ^= 1;
   }
   if (t < kB1) {
-    H.a1->K[t] = s.sk[cur][r] - k;
-    H.a1->W[t] = fx_sub(s.sw[cur][r], w);
+    H.l1->K[t] = s.sk[cur][r] - k;
+    H.l1->W[t] = fx_sub(s.sw[cur][r], w);
   }
   __syncthreads();
 }
 
 GS_DI BinInfo l1_info(const Hists& H, int e) {
   BinInfo i;
-  i.Kab = H.a1->K[e];
-  i.Wab = H.a1->W[e];
-  i.cnt = rd64(&H.h1->cnt[e]);
-  i.Wb = i.cnt ? fx_shifted(rd64(&H.h1->sig[e]), binade_shift(e)) : fx_zero();
-  i.mx = rd32(&H.h1->mx[e]);
+  i.Kab = H.l1->K[e];
+  i.Wab = H.l1->W[e];
+  i.cnt = H.l1->cnt[e];
+  i.Wb = i.cnt ? fx_shifted(H.l1->sig[e], binade_shift(e)) : fx_zero();
+  i.mx = H.l1->mx[e];
   return i;
 }
 
 // A refinement level inside one binade E: bins b = 0..nbins-1, thread t owns bins
 // [t*per, t*per + per). Within one binade, sums of significands are plain integers.
 struct Lvl {
-  const uint64_t* cnt;
+  const uint32_t* cnt;
   const uint64_t* sig;
   const uint32_t* mx;
   int nbins, per;
@@ -534,13 +541,13 @@ struct Walk {
 
 GS_DI Lvl lvl2(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
   Lvl L;
-  L.cnt = H.h2->cnt; L.sig = H.h2->sig; L.mx = H.h2->mx;
+  L.cnt = H.w2->cnt; L.sig = H.w2->sig; L.mx = H.w2->mx;
   L.nbins = kB2; L.per = kB2 / kNT; L.shift = binade_shift((int)E); L.Kaw = Kaw; L.Waw = Waw;
   return L;
 }
 GS_DI Lvl lvl3(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
   Lvl L;
-  L.cnt = H.h3->cnt; L.sig = H.h3->sig; L.mx = H.h3->mx;
+  L.cnt = H.w3->cnt; L.sig = H.w3->sig; L.mx = H.w3->mx;
   L.nbins = kB3; L.per = kB3 / kNT; L.shift = binade_shift((int)E); L.Kaw = Kaw; L.Waw = Waw;
   return L;
 }
@@ -552,8 +559,8 @@ GS_DI void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
   for (int j = 0; j < L.per; ++j) {
     const int b = b0 + j;
     if (b < L.nbins) {
-      k += rd64(&L.cnt[b]);
-      sg += rd64(&L.sig[b]);
+      k += (uint64_t)L.cnt[b];
+      sg += (uint64_t)L.sig[b];
     }
   }
   const int r = kNT - 1 - (int)threadIdx.x;
@@ -591,13 +598,13 @@ GS_DI void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo
     for (int j = L.per - 1; j >= 0; --j) {
       const int bb = threadIdx.x * L.per + j;
       if (bb >= L.nbins) continue;
-      const uint64_t c = rd64(&L.cnt[bb]);
-      const uint64_t sg = rd64(&L.sig[bb]);
+      const uint64_t c = (uint64_t)L.cnt[bb];
+      const uint64_t sg = (uint64_t)L.sig[bb];
       if (bb == b) {
         s.bi.Wab = lvl_total(L, K, S, s.bi.Kab);
         s.bi.cnt = c;
         s.bi.Wb = c ? fx_shifted(sg, L.shift) : fx_zero();
-        s.bi.mx = rd32(&L.mx[bb]);
+        s.bi.mx = L.mx[bb];
         break;
       }
       K += c;
@@ -620,11 +627,11 @@ GS_DI bool criterion(double B, const Fx& S, uint64_t k, const Fx& W, uint32_t vk
 GS_DI void l1_exact(const Hists& H, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
   const int t = threadIdx.x;
   int best = -1, occupied = INT_MAX;
-  if (t < kB1 && rd64(&H.h1->cnt[t])) {
-    if (criterion(B, S, H.a1->K[t], H.a1->W[t], rd32(&H.h1->mx[t]))) best = t;
+  if (t < kB1 && H.l1->cnt[t]) {
+    if (criterion(B, S, H.l1->K[t], H.l1->W[t], H.l1->mx[t])) best = t;
   }
   b1 = block_max(s, best);
-  if (t < kB1 && t > b1 && rd64(&H.h1->cnt[t])) occupied = t;
+  if (t < kB1 && t > b1 && H.l1->cnt[t]) occupied = t;
   b2 = block_min(s, occupied);
 }
 GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
@@ -633,19 +640,19 @@ GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLd
   for (int j = L.per - 1; j >= 0 && best < 0; --j) {
     const int b = threadIdx.x * L.per + j;
     if (b >= L.nbins) continue;
-    const uint64_t c = rd64(&L.cnt[b]);
+    const uint64_t c = (uint64_t)L.cnt[b];
     if (!c) continue;
     uint64_t Kt;
     const Fx W = lvl_total(L, K, Sg, Kt);
-    if (criterion(B, S, Kt, W, rd32(&L.mx[b]))) best = b;
+    if (criterion(B, S, Kt, W, L.mx[b])) best = b;
     K += c;
-    Sg += rd64(&L.sig[b]);
+    Sg += (uint64_t)L.sig[b];
   }
   b1 = block_max(s, best);
   int lowest = INT_MAX;
   for (int j = 0; j < L.per; ++j) {
     const int b = threadIdx.x * L.per + j;
-    if (b < L.nbins && b > b1 && rd64(&L.cnt[b])) {
+    if (b < L.nbins && b > b1 && (uint64_t)L.cnt[b]) {
       lowest = b;
       break;
     }
@@ -671,10 +678,10 @@ GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32
   // clear every copy of the requested level before the pass that fills it
   for (int c = 0; c < kC23; ++c) {
     if (level == 2) {
-      Hist2* h = H.h2 + c;
+      Hist2* h = H.h2g + c;
       for (int b = threadIdx.x; b < kB2; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; }
     } else {
-      Hist3* h = H.h3 + c;
+      Hist3* h = H.h3g + c;
       for (int b = threadIdx.x; b < kB3; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; }
     }
   }
@@ -829,7 +836,6 @@ GS_DI void sv_exact(SolveLds& s, const Hists& H) {
 
 // First solve after the statistics pass: the level-1 cache, totals and the special cases.
 GS_DI void sv_start(SolveLds& s, const Hists& H, int64_t d) {
-  l1_build(s, H);
   const BinInfo i0 = l1_info(H, 0);
   const BinInfo inf = l1_info(H, 255);
   __syncthreads();
@@ -878,23 +884,22 @@ GS_DI void sv_start(SolveLds& s, const Hists& H, int64_t d) {
   }
 }
 
-// Sums the copies of a histogram into copy 0 (nbins bins, `copies` consecutive copies). The
-// copies were filled with atomics by an earlier kernel on the same stream.
-template <typename HistT>
-GS_DI void reduce_copies(HistT* h, int copies, int nbins) {
+// Sums the global copies of a histogram (filled with atomics by an earlier kernel on the same
+// stream) into an LDS cache.
+template <typename HistT, typename CntT>
+GS_DI void reduce_into(const HistT* h, int copies, int nbins, CntT* cnt, uint64_t* sig, uint32_t* mx) {
   for (int b = threadIdx.x; b < nbins; b += kNT) {
-    uint64_t c = h[0].cnt[b], sg = h[0].sig[b];
-    uint32_t mx = h[0].mx[b];
-    for (int k = 1; k < copies; ++k) {
+    uint64_t c = 0, sg = 0;
+    uint32_t m = 0;
+    for (int k = 0; k < copies; ++k) {
       c += h[k].cnt[b];
       sg += h[k].sig[b];
-      mx = max(mx, h[k].mx[b]);
+      m = max(m, h[k].mx[b]);
     }
-    h[0].cnt[b] = c;
-    h[0].sig[b] = sg;
-    h[0].mx[b] = mx;
+    cnt[b] = (CntT)c;
+    sig[b] = sg;
+    mx[b] = m;
   }
-  __syncthreads();
 }
 
 // The row's solver, run by one workgroup per row after each histogram pass: it either finishes the
@@ -903,11 +908,14 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
   if (threadIdx.x == 0) s.c = *gc;
   __syncthreads();
   if (s.c.done) return;
+  // the histograms this solve may read: level 1 always, the level-2 / level-3 windows if any
+  reduce_into(H.h1g, kC1, kB1, H.l1->cnt, H.l1->sig, H.l1->mx);
+  if (s.c.l2exp != kNone) reduce_into(H.h2g, kC23, kB2, H.w2->cnt, H.w2->sig, H.w2->mx);
+  if (s.c.l3base != kNone) reduce_into(H.h3g, kC23, kB3, H.w3->cnt, H.w3->sig, H.w3->mx);
+  __syncthreads();
   if (s.c.stage == 0) {
-    reduce_copies(const_cast<Hist1*>(H.h1), kC1, kB1);
     // zeros = d minus the histogram's population (every nonzero key, finite or not, is binned)
-    uint64_t n = 0;
-    if (threadIdx.x < kB1) n = H.h1->cnt[threadIdx.x];
+    uint64_t n = threadIdx.x < kB1 ? H.l1->cnt[threadIdx.x] : 0;
     for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o);
     if ((threadIdx.x & 63) == 0) s.sk[0][threadIdx.x >> 6] = n;
     __syncthreads();
@@ -915,15 +923,13 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
       uint64_t tot = 0;
       for (int i = 0; i < kNT / 64; ++i) tot += s.sk[0][i];
       s.c.zeros = (uint64_t)d - tot;
+      s.c.need = 0;
     }
-    __syncthreads();
-  } else if (s.c.need == 2) {
-    reduce_copies(H.h2, kC23, kB2);
-  } else if (s.c.need == 3) {
-    reduce_copies(H.h3, kC23, kB3);
+  } else if (threadIdx.x == 0) {
+    s.c.need = 0;
   }
-  if (threadIdx.x == 0) s.c.need = 0;
   __syncthreads();
+  l1_build(s, H);
   if (s.c.stage == 0) sv_start(s, H, d);
   else if (s.c.solver == GSPAR_GREEDY) sv_greedy(s, H);
   else sv_exact(s, H);
@@ -1078,7 +1084,7 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
 __global__ void __launch_bounds__(kNT) k_solve(Args a) {
   __shared__ SolveLds sm;
   const int64_t row = blockIdx.x;
-  const Hists H{h1_of(a, row), h2_of(a, row), h3_of(a, row), a1_of(a, row)};
+  const Hists H{&sm.l1, &sm.w2, &sm.w3, h1_of(a, row), h2_of(a, row), h3_of(a, row)};
   solve_row(sm, ctl_of(a, row), H, a.d);
 }
 
@@ -1090,6 +1096,7 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
 // ordering of workgroup dispatch is assumed and every wait ends.
 constexpr uint64_t kStAgg = 1ull << 62, kStInc = 2ull << 62, kStVal = (1ull << 62) - 1;
 constexpr int kPolls = 4096;
+constexpr int kLookDepth = 1;  // status words examined per lane per look-back round trip
 constexpr int kWaveElems = kTileElems / (kTileThreads / 64);  // coordinates per wave per tile
 
 struct TileCtx {
@@ -1167,7 +1174,8 @@ __device__ __forceinline__ uint32_t wave_prefix_small(uint32_t n, int lane, uint
 constexpr int kCapList = 256;    // capped survivor values kept per wave
 constexpr int kSampleBatch = 8;  // float4 loads in flight per lane in the sampling pass
 constexpr int kRing = 512;       // per-wave staging ring of (index, value) pairs (power of two)
-static_assert(kTileGroups == 2 * kSampleBatch, "the whole-tile path runs two batches");
+static_assert(kTileGroups % kSampleBatch == 0 && kTileGroups % 16 == 0, "tile shape");
+constexpr int kMaskWords = kTileGroups / 16;  // 64-bit mask words per lane (4 bits per group)
 // Below this lambda, lambda * 2^32 * |g| could round differently from (lambda * |g|) * 2^32.
 constexpr double kLamScaledMin = 0x1p-900;
 
@@ -1216,19 +1224,23 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   // first group of this lane: tile base + wave quarter + lane; iteration j adds 64 groups
   const int64_t q0 = part * (kTileElems / 4) + (int64_t)wv * (kWaveElems / 4) + lane;
 
-  uint64_t selm = 0, capm = 0, negm = 0;
+  // group j of this lane: bits 4*(j mod 16) .. +3 of mask word j / 16 (word index always a
+  // compile-time constant, so the masks stay in registers)
+  uint64_t selm[kMaskWords], capm[kMaskWords], negm[kMaskWords];
+#pragma unroll
+  for (int w = 0; w < kMaskWords; ++w) selm[w] = capm[w] = negm[w] = 0;
   uint32_t ncl = 0;  // capped survivors of this wave so far (the LDS list keeps the first kCapList)
-  auto record = [&](int j, const float v[4], uint32_t z, uint32_t cz) {
+  auto record = [&](int w, int jj, const float v[4], uint32_t z, uint32_t cz) {
     cz &= z;
-    selm |= (uint64_t)z << (4 * j);
+    selm[w] |= (uint64_t)z << (4 * jj);
     if (__ballot(z != 0)) {
       uint32_t neg = 0;
 #pragma unroll
       for (int k = 0; k < 4; ++k) neg |= (__float_as_uint(v[k]) >> 31) << k;
-      negm |= (uint64_t)neg << (4 * j);
+      negm[w] |= (uint64_t)neg << (4 * jj);
     }
     if (__ballot(cz != 0)) {
-      capm |= (uint64_t)cz << (4 * j);
+      capm[w] |= (uint64_t)cz << (4 * jj);
       uint32_t tot;
       uint32_t p = ncl + wave_prefix_small((uint32_t)__popc(cz), lane, tot);
 #pragma unroll
@@ -1257,18 +1269,26 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         const float v[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
         uint32_t z, cz;
         decide_fast(q0 + 64 * (jb + u), v, lam32, c.k0, c.k1, z, cz);
-        record(jb + u, v, z, cz);
+        record((jb + u) >> 4, (jb + u) & 15, v, z, cz);
       }
     }
   } else if (c.live) {
-    for (int j = 0; j < kTileGroups; ++j) {
-      float v[4];
-      uint32_t z, cz;
-      decide_group<VEC>(c, q0 + 64 * j, v, z, cz);
-      record(j, v, z, cz);
+#pragma unroll
+    for (int w = 0; w < kMaskWords; ++w) {
+      for (int jj = 0; jj < 16; ++jj) {
+        float v[4];
+        uint32_t z, cz;
+        decide_group<VEC>(c, q0 + 64 * (16 * w + jj), v, z, cz);
+        record(w, jj, v, z, cz);
+      }
     }
   }
-  uint32_t nsel = (uint32_t)__popcll(selm), ncap = (uint32_t)__popcll(capm);
+  uint32_t nsel = 0, ncap = 0;
+#pragma unroll
+  for (int w = 0; w < kMaskWords; ++w) {
+    nsel += (uint32_t)__popcll(selm[w]);
+    ncap += (uint32_t)__popcll(capm[w]);
+  }
   for (int o = 32; o > 0; o >>= 1) {
     nsel += __shfl_xor(nsel, o);
     ncap += __shfl_xor(ncap, o);
@@ -1296,35 +1316,54 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   } else {
     if (tid == 0) __hip_atomic_store(&st[t], kStAgg | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (wv == 0) {
+      // lane l examines predecessors t-1-l-64m (m < kLookDepth): kLookDepth*64 tiles per round trip
       const int64_t first = t - part;
       int64_t look = t - 1;
       uint64_t ex = 0;
       while (true) {
-        const int64_t i = look - lane;
-        uint64_t sw = kStInc;
-        if (i >= first) {
+        uint64_t sw[kLookDepth];
+#pragma unroll
+        for (int m = 0; m < kLookDepth; ++m) {
+          const int64_t i = look - lane - 64 * m;
+          sw[m] = i >= first ? __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : kStInc;
+        }
+#pragma unroll
+        for (int m = 0; m < kLookDepth; ++m) {
+          const int64_t i = look - lane - 64 * m;
           int polls = 0;
-          sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          while ((sw >> 62) == 0 && ++polls < kPolls) {
+          while (i >= first && (sw[m] >> 62) == 0 && ++polls < kPolls) {
             __builtin_amdgcn_s_sleep(4);
-            sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            sw[m] = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           }
         }
-        const uint64_t incl_mask = __ballot((sw >> 62) == 2);
-        const int stop = incl_mask ? (__ffsll((unsigned long long)incl_mask) - 1) : 63;
-        // predecessors up to `stop` that never published: count them here
-        uint64_t missing = __ballot((sw >> 62) == 0 && lane <= stop);
-        while (missing) {
-          const int m = __ffsll((unsigned long long)missing) - 1;
-          const uint64_t val = wave_tile_aggregate<VEC>(c, (look - m) - first, lane);
-          if (lane == m) sw = kStAgg | val;
-          missing &= missing - 1;
+        // nearest inclusive predecessor within this window: entry (m, lane) is at distance 64m + lane
+        int mstop = kLookDepth, lstop = 63;
+#pragma unroll
+        for (int m = kLookDepth - 1; m >= 0; --m) {
+          const uint64_t inc = __ballot((sw[m] >> 62) == 2);
+          if (inc) {
+            mstop = m;
+            lstop = __ffsll((unsigned long long)inc) - 1;
+          }
         }
-        uint64_t contrib = lane <= stop ? (sw & kStVal) : 0;
+        uint64_t contrib = 0;
+#pragma unroll
+        for (int m = 0; m < kLookDepth; ++m) {
+          const bool in = m < mstop || (m == mstop && lane <= lstop);
+          // predecessors inside the window that never published: count them here
+          uint64_t missing = __ballot((sw[m] >> 62) == 0 && in);
+          while (missing) {
+            const int ml = __ffsll((unsigned long long)missing) - 1;
+            const uint64_t val = wave_tile_aggregate<VEC>(c, (look - ml - 64 * m) - first, lane);
+            if (lane == ml) sw[m] = kStAgg | val;
+            missing &= missing - 1;
+          }
+          contrib += in ? (sw[m] & kStVal) : 0;
+        }
         for (int o = 32; o > 0; o >>= 1) contrib += __shfl_xor(contrib, o);
         ex += contrib;
-        if (incl_mask) break;
-        look -= 64;
+        if (mstop < kLookDepth) break;
+        look -= 64 * kLookDepth;
       }
       if (lane == 0) {
         __hip_atomic_store(&st[t], kStInc | (ex + agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1335,20 +1374,25 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   __syncthreads();
   const uint64_t excl = s_excl;
 
-  // phase 2: survivors of this wave, in index order, through the staging ring
-  if (nsel) {
+  // phase 2: survivors of this wave, in index order, through the staging ring. Capped survivors
+  // take their value from the LDS list; a wave whose list overflowed reloads them from g instead
+  // (a separate instantiation, so the common path issues no global load at all).
+  auto emit = [&](auto from_lds) {
     int32_t* __restrict__ oi = a.idx + row * a.cap;
     float* __restrict__ ov = a.val + row * a.cap;
     uint64_t out = (excl & 0x7FFFFFFFull) + wbase;  // output position of the ring's oldest entry
     uint32_t head = 0, fill = 0;                     // ring window [head, head + fill)
     uint32_t cl = 0;                                 // capped survivors of this wave emitted so far
-    for (int j = 0; j < kTileGroups; ++j) {
-      const uint32_t z = (uint32_t)(selm >> (4 * j)) & 0xF;
+#pragma unroll
+    for (int w = 0; w < kMaskWords; ++w)
+    for (int jj = 0; jj < 16; ++jj) {
+      const int j = 16 * w + jj;
+      const uint32_t z = (uint32_t)(selm[w] >> (4 * jj)) & 0xF;
       if (__ballot(z != 0) == 0) continue;
       uint32_t tot, ctot = 0;
       uint32_t slot = head + fill + wave_prefix_small((uint32_t)__popc(z), lane, tot);
       const int64_t i0 = 4 * (q0 + 64 * j);
-      const uint32_t cz = (uint32_t)(capm >> (4 * j)) & 0xF, ng = (uint32_t)(negm >> (4 * j)) & 0xF;
+      const uint32_t cz = (uint32_t)(capm[w] >> (4 * jj)) & 0xF, ng = (uint32_t)(negm[w] >> (4 * jj)) & 0xF;
       uint32_t cp = 0;
       if (__ballot(cz != 0)) cp = cl + wave_prefix_small((uint32_t)__popc(cz), lane, ctot);
 #pragma unroll
@@ -1356,7 +1400,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         if ((z >> k) & 1) {
           float val = ((ng >> k) & 1) ? -inv : inv;
           if ((cz >> k) & 1) {
-            val = cp < (uint32_t)kCapList ? s_capv[wv][cp] : c.row[i0 + k];
+            if constexpr (decltype(from_lds)::value) val = s_capv[wv][cp];
+            else val = c.row[i0 + k];
             ++cp;
           }
           const uint32_t r = slot & (kRing - 1);
@@ -1387,6 +1432,10 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         ov[out + lane] = s_rv[wv][r];
       }
     }
+  };
+  if (nsel) {
+    if (ncl <= (uint32_t)kCapList) emit(std::true_type{});
+    else emit(std::false_type{});
   }
   if (part == a.lay.tiles - 1 && tid == 0) {
     const uint64_t incl = excl + agg;
