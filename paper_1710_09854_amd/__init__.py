@@ -145,9 +145,16 @@ def _as_row(g):
 def _as_rows(g):
     if not (isinstance(g, torch.Tensor) and g.is_cuda and g.dtype == torch.float32):
         raise TypeError("g must be a float32 CUDA tensor")
-    if g.dim() != 2 or g.stride(1) != 1:
+    if g.dim() != 2 or (g.stride(1) != 1 and g.shape[1] > 1):
         raise ValueError("g must be 2-D with unit stride along a row")
     return g
+
+
+def _leading_dim(g) -> int:
+    """Row pitch in elements; a single row's stride is irrelevant (size-1 dimensions may report
+    any stride, including 0)."""
+    rows, d = g.shape
+    return d if rows == 1 else g.stride(0)
 
 
 @dataclass
@@ -235,7 +242,7 @@ def sparsify_probs_batched(g, rho, solver="greedy", iters: int = 2, want_p: bool
                            stream=None) -> Probs:
     g = _as_rows(g)
     rows, d = g.shape
-    ld = g.stride(0)
+    ld = _leading_dim(g)
     dev = g.device
     r = _rho_dev(rho, rows, dev)
     p = torch.empty((rows, ld), dtype=torch.float32, device=dev) if want_p else None
@@ -284,7 +291,7 @@ def sparsify_sample_compact_batched(g, rho, seeds, solver="greedy", iters: int =
                                     cap_per_row: int | None = None, workspace=None, stream=None) -> Sparse:
     g = _as_rows(g)
     rows, d = g.shape
-    ld = g.stride(0)
+    ld = _leading_dim(g)
     dev = g.device
     r = _rho_dev(rho, rows, dev)
     s = _seeds_dev(seeds, rows, dev)

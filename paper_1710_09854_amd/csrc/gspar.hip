@@ -432,9 +432,9 @@ struct WinCache {
   uint32_t mx[N];
 };
 struct SolveLds {
-  uint64_t sk[2][kNT];
-  uint64_t ss[2][kNT];
-  Fx sw[2][kB1];
+  uint64_t sk[kNT / 64];  // per-wave partial results of block scans and reductions
+  uint64_t ss[kNT / 64];
+  Fx sw[kB1 / 64];
   int ired[kNT / 64];
   BinInfo bi;
   RowCtl c;  // working copy of the row's control block
@@ -470,45 +470,51 @@ GS_DI int block_min(SolveLds& s, int v) {
   return r;
 }
 
+// Inclusive suffix sums over the lanes of a wave: lane l receives the sum over lanes l..63.
+GS_DI uint64_t wave_suffix(uint64_t x, int lane) {
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t y = __shfl_down(x, (unsigned)o);
+    if (lane + o < 64) x += y;
+  }
+  return x;
+}
+GS_DI Fx wave_suffix(Fx x, int lane) {
+  for (int o = 1; o < 64; o <<= 1) {
+    Fx y;
+#pragma unroll
+    for (int i = 0; i < 5; ++i) y.w[i] = __shfl_down(x.w[i], (unsigned)o);
+    if (lane + o < 64) fx_add(x, y);
+  }
+  return x;
+}
+
 // Level 1 (one bin per binade): exclusive suffix sums over the 256 binades, exact, into the LDS
-// cache. Threads 0..255 own one binade each.
+// cache. Threads 0..255 (waves 0..3) own one binade each: a suffix scan inside each wave, then the
+// totals of the waves above.
 GS_DI void l1_build(SolveLds& s, const Hists& H) {
-  const int t = threadIdx.x;
-  uint64_t k = 0;
-  Fx w = fx_zero();
-  if (t < kB1) {
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  uint64_t k = 0, ik = 0;
+  Fx w = fx_zero(), iw = fx_zero();
+  if (t < kB1) {  // whole waves
     k = H.l1->cnt[t];
     if (k) w = fx_shifted(H.l1->sig[t], binade_shift(t));
-  }
-  const int r = kB1 - 1 - t;  // reversed index: a prefix over r is a suffix over binades
-  if (t < kB1) {
-    s.sk[0][r] = k;
-    s.sw[0][r] = w;
+    ik = wave_suffix(k, lane);
+    iw = wave_suffix(w, lane);
+    if (lane == 0) {
+      s.sk[wv] = ik;
+      s.sw[wv] = iw;
+    }
   }
   __syncthreads();
-  int cur = 0;
-  for (int off = 1; off < kB1; off <<= 1) {
-    uint64_t kk = 0;
-    Fx ww = fx_zero();
-    if (t < kB1) {
-      kk = s.sk[cur][r];
-      ww = s.sw[cur][r];
-      if (r >= off) {
-        kk += s.sk[cur][r - off];
-        fx_add(ww, s.sw[cur][r - off]);
-      }
-    }
-    __syncthreads();
-    if (t < kB1) {
-      s.sk[cur ^ 1][r] = kk;
-      s.sw[cur ^ 1][r] = ww;
-    }
-    __syncthreads();
-    cur ^= 1;
-  }
   if (t < kB1) {
-    H.l1->K[t] = s.sk[cur][r] - k;
-    H.l1->W[t] = fx_sub(s.sw[cur][r], w);
+    uint64_t K = ik - k;
+    Fx W = fx_sub(iw, w);
+    for (int i = wv + 1; i < kB1 / 64; ++i) {
+      K += s.sk[i];
+      fx_add(W, s.sw[i]);
+    }
+    H.l1->K[t] = K;
+    H.l1->W[t] = W;
   }
   __syncthreads();
 }
@@ -552,7 +558,8 @@ GS_DI Lvl lvl3(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
   return L;
 }
 
-// Exclusive suffix scan over thread index of (count, significand sum).
+// Exclusive suffix scan over thread index of (count, significand sum): a suffix scan inside each
+// wave, then the totals of the waves above.
 GS_DI void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
   uint64_t k = 0, sg = 0;
   const int b0 = threadIdx.x * L.per;
@@ -563,24 +570,20 @@ GS_DI void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
       sg += (uint64_t)L.sig[b];
     }
   }
-  const int r = kNT - 1 - (int)threadIdx.x;
-  s.sk[0][r] = k;
-  s.ss[0][r] = sg;
-  __syncthreads();
-  int cur = 0;
-  for (int off = 1; off < kNT; off <<= 1) {
-    uint64_t kk = s.sk[cur][r], ss = s.ss[cur][r];
-    if (r >= off) {
-      kk += s.sk[cur][r - off];
-      ss += s.ss[cur][r - off];
-    }
-    s.sk[cur ^ 1][r] = kk;
-    s.ss[cur ^ 1][r] = ss;
-    __syncthreads();
-    cur ^= 1;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const uint64_t ik = wave_suffix(k, lane), is = wave_suffix(sg, lane);
+  if (lane == 0) {
+    s.sk[wv] = ik;
+    s.ss[wv] = is;
   }
-  w.exK = s.sk[cur][r] - k;
-  w.exS = s.ss[cur][r] - sg;
+  __syncthreads();
+  uint64_t ak = 0, as = 0;
+  for (int i = wv + 1; i < kNT / 64; ++i) {
+    ak += s.sk[i];
+    as += s.ss[i];
+  }
+  w.exK = ik - k + ak;
+  w.exS = is - sg + as;
   __syncthreads();
 }
 
@@ -917,11 +920,11 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
     // zeros = d minus the histogram's population (every nonzero key, finite or not, is binned)
     uint64_t n = threadIdx.x < kB1 ? H.l1->cnt[threadIdx.x] : 0;
     for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o);
-    if ((threadIdx.x & 63) == 0) s.sk[0][threadIdx.x >> 6] = n;
+    if ((threadIdx.x & 63) == 0) s.sk[threadIdx.x >> 6] = n;
     __syncthreads();
     if (threadIdx.x == 0) {
       uint64_t tot = 0;
-      for (int i = 0; i < kNT / 64; ++i) tot += s.sk[0][i];
+      for (int i = 0; i < kNT / 64; ++i) tot += s.sk[i];
       s.c.zeros = (uint64_t)d - tot;
       s.c.need = 0;
     }

@@ -122,6 +122,11 @@ inline T xchg(T v, int src) {
 template <class T>
 inline T __shfl_xor(T v, int mask, int = 64) { return emu::xchg(v, emu::lane() ^ mask); }
 template <class T>
+inline T __shfl_down(T v, unsigned delta, int = 64) {
+  int l = emu::lane();
+  return emu::xchg(v, l + (int)delta < 64 ? l + (int)delta : l);
+}
+template <class T>
 inline T __shfl_up(T v, unsigned delta, int = 64) {
   int l = emu::lane();
   T r = emu::xchg(v, l >= (int)delta ? l - (int)delta : l);

@@ -56,8 +56,8 @@ class Workload:
 
 def c1() -> Workload:
     rng = np.random.default_rng(0)
-    g = rng.standard_normal(65536).astype(np.float32)[None, :]
-    return Workload("c1_normal_d65536", np.ascontiguousarray(g), [0.1], ["greedy", "exact"], [0])
+    g = rng.standard_normal(65536).astype(np.float32).reshape(1, -1)
+    return Workload("c1_normal_d65536", np.ascontiguousarray(g), CONFIG_RHOS["c1"], CONFIG_SOLVERS["c1"], [0])
 
 
 def c2(rows: int = 16, d: int = 1 << 20) -> Workload:
@@ -66,7 +66,7 @@ def c2(rows: int = 16, d: int = 1 << 20) -> Workload:
     g = np.empty((rows, d), np.float32)
     for r in range(rows):
         g[r] = (rng.laplace(0.0, 1.0, d) * scale[r]).astype(np.float32)
-    return Workload(f"c2_laplace_{rows}x{d}", g, [0.01, 0.1], ["greedy"],
+    return Workload(f"c2_laplace_{rows}x{d}", g, CONFIG_RHOS["c2"], CONFIG_SOLVERS["c2"],
                     [1000 + r for r in range(rows)], meta={"row_scale": scale})
 
 
@@ -94,8 +94,8 @@ def c3(n: int = 256, d: int = 1 << 22, density: float = 1e-3, lam_reg: float = 1
         grad += 2.0 * lam_reg * w
     else:
         grad[support] += 2.0 * lam_reg * w[support]
-    g = grad.astype(np.float32)[None, :]
-    return Workload("c3_logreg_256x4194304", np.ascontiguousarray(g), [0.01], ["greedy", "exact"],
+    g = grad.astype(np.float32).reshape(1, -1)
+    return Workload("c3_logreg_256x4194304", np.ascontiguousarray(g), CONFIG_RHOS["c3"], CONFIG_SOLVERS["c3"],
                     [3], meta={"support_fraction": float(support.mean())})
 
 
@@ -108,7 +108,7 @@ def c4() -> Workload:
     for s, sz in zip(sig, RESNET50_SEGMENTS):
         g[off:off + sz] = (rng.standard_normal(sz) * s).astype(np.float32)
         off += sz
-    return Workload("c4_resnet50_d25557032", g[None, :], [0.001, 0.01], ["exact", "greedy"], [4],
+    return Workload("c4_resnet50_d25557032", g.reshape(1, -1), CONFIG_RHOS["c4"], CONFIG_SOLVERS["c4"], [4],
                     meta={"segments": list(RESNET50_SEGMENTS), "sigma": sig})
 
 
@@ -121,11 +121,14 @@ def c5(d: int = 1 << 28, chunk: int = 1 << 24) -> Workload:
         out = rng.random(m) < 0.01
         t[out] *= 100.0
         g[off:off + m] = t.astype(np.float32)
-    return Workload(f"c5_student_t2_outliers_d{d}", g[None, :], [0.001, 0.01, 0.1],
-                    ["exact", "greedy"], [5])
+    return Workload(f"c5_student_t2_outliers_d{d}", g.reshape(1, -1), CONFIG_RHOS["c5"], CONFIG_SOLVERS["c5"], [5])
 
 
 CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5}
+# the solvers and densities each workload is run at (what the generators above attach)
+CONFIG_SOLVERS = {"c1": ["greedy", "exact"], "c2": ["greedy"], "c3": ["greedy", "exact"], "c4": ["exact", "greedy"],
+                  "c5": ["exact", "greedy"]}
+CONFIG_RHOS = {"c1": [0.1], "c2": [0.01, 0.1], "c3": [0.01], "c4": [0.001, 0.01], "c5": [0.001, 0.01, 0.1]}
 
 
 # ------------------------------------------------------------------------------------------
