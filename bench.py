@@ -8,10 +8,15 @@ in HBM; the timed region holds exactly K steps between two device synchronisatio
 Default workload: 16 rows x 2^20 (one per simulated worker), Laplace(0,1) times a per-row scale
 10^U(-3,0), greedy solver with two rescale steps, densities 0.01 and 0.1, Philox seeds 1000 + r.
 
-Prints ONE JSON line with the metric, a roofline object for the dominant kernel (the sampling /
-compaction pass: algorithmic bytes = 4 B per input element + 8 B per survivor, timed with HIP
-events on its stream over the timed region) and the oracle timed on a bounded sample on one host
-core as a CPU baseline.
+Prints ONE JSON line with the metric, a roofline object for the sampling / compaction pass (the
+largest HBM-bound kernel: algorithmic bytes = 4 B per input element + 8 B per survivor, timed with
+HIP events on its stream over the timed region), the time per step of every kernel class, and the
+oracle timed on a bounded sample on one host core as a CPU baseline.
+
+Counter runs: with --copy-probe the run first copies a 512 MiB device buffer three times (a plain
+copy kernel of known size), so that two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) can be
+scaled to bytes; `bench.py --summarize-pmc FETCH_DIR WRITE_DIR` turns those two runs into bytes
+per launch per kernel and records them in profiles/traffic.json for the current kernel source.
 """
 import argparse
 import hashlib
@@ -38,6 +43,9 @@ def parse():
     ap.add_argument("--rho", type=float, default=None, help="restrict to one density")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
+    ap.add_argument("--copy-probe", action="store_true", help="copy a 512 MiB buffer 3 times first (counter scale)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
+                    help="summarise two rocprofv3 --pmc runs of this benchmark into profiles/traffic.json")
     return ap.parse_args()
 
 
@@ -46,20 +54,79 @@ def src_hash() -> str:
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
-def traffic_for(workload: str):
-    """HBM bytes per launch of the sampling kernel from committed rocprofv3 counter summaries,
-    only if they were taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic.json")
+COPY_PROBE_BYTES = 512 << 20
+
+
+def traffic_for(workload: str, kernel: str = "k_sample"):
+    """HBM bytes per launch of one kernel from the committed counter summary, only if it was taken
+    on the current kernel source (otherwise None)."""
+    if not os.path.exists(TRAFFIC_JSON):
         return None
     try:
-        data = json.load(open(path))
-        ent = data.get("k_sample", {}).get(workload)
-        if ent and ent.get("src_sha") == src_hash():
-            return ent.get("bytes_per_launch")
+        data = json.load(open(TRAFFIC_JSON))
+        ent = data.get(workload, {})
+        if ent.get("src_sha") == src_hash():
+            return ent.get("kernels", {}).get(kernel, {}).get("bytes_per_launch")
     except (ValueError, OSError):
         return None
     return None
+
+
+def _pmc_rows(path):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {path}")
+    rows = []
+    for f in files:
+        rows.extend(csv.DictReader(open(f)))
+    return rows
+
+
+def _kernel_class(name: str):
+    for k in ("k_sample", "k_stats", "k_refine", "k_solve", "k_init", "k_probs"):
+        if "gspar::" + k in name:
+            return k
+    if "copyBuffer" in name:  # the runtime's device-to-device copy kernel (the probe)
+        return "copy"
+    return None
+
+
+def summarize_pmc(fetch_dir, write_dir, workload):
+    """Average FETCH_SIZE / WRITE_SIZE (KiB per dispatch) per kernel class; the copy probe's
+    readings divided by its known bytes give the scale from counter units to bytes."""
+    avg = {}
+    for counter, path in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        acc = {}
+        for r in _pmc_rows(path):
+            if r.get("Counter_Name") != counter:
+                continue
+            k = _kernel_class(r.get("Kernel_Name", ""))
+            if k is None:
+                continue
+            v = float(r["Counter_Value"])
+            if k == "copy" and v * 1024.0 < 0.5 * COPY_PROBE_BYTES:
+                continue  # small runtime copies (inputs, scalars), not the probe
+            acc.setdefault(k, []).append(v)
+        avg[counter] = {k: sum(v) / len(v) for k, v in acc.items()}
+    if "copy" not in avg["FETCH_SIZE"] or "copy" not in avg["WRITE_SIZE"]:
+        raise SystemExit("the copy probe is missing from the counter runs (run them with --copy-probe)")
+    fscale = avg["FETCH_SIZE"]["copy"] * 1024.0 / COPY_PROBE_BYTES
+    wscale = avg["WRITE_SIZE"]["copy"] * 1024.0 / COPY_PROBE_BYTES
+    kernels = {}
+    for k in sorted(set(avg["FETCH_SIZE"]) & set(avg["WRITE_SIZE"]) - {"copy"}):
+        fb = avg["FETCH_SIZE"][k] * 1024.0 / fscale
+        wb = avg["WRITE_SIZE"][k] * 1024.0 / wscale
+        kernels[k] = {"fetch_kib_raw": avg["FETCH_SIZE"][k], "write_kib_raw": avg["WRITE_SIZE"][k],
+                      "fetch_bytes": fb, "write_bytes": wb, "bytes_per_launch": fb + wb}
+    data = json.load(open(TRAFFIC_JSON)) if os.path.exists(TRAFFIC_JSON) else {}
+    data[workload] = {"src_sha": src_hash(), "copy_probe_bytes": COPY_PROBE_BYTES,
+                      "fetch_scale": fscale, "write_scale": wscale, "kernels": kernels}
+    with open(TRAFFIC_JSON, "w") as fh:
+        json.dump(data, fh, indent=1, sort_keys=True)
+    print(json.dumps(data[workload], indent=1, sort_keys=True))
 
 
 def cpu_baseline(wl, combos, target_s):
@@ -71,8 +138,9 @@ def cpu_baseline(wl, combos, target_s):
     elems = 0
     done = []
     r = 0
+    prefix = min(wl.d, 1 << 24)  # rows longer than 2^24 are sampled by their leading 2^24 entries
     while True:
-        row = wl.g[r % wl.rows]
+        row = wl.g[r % wl.rows][:prefix]
         for solver, rho in combos:
             sol = oracle.solve(row, rho, solver, wl.iters)
             oracle.sample_compact(row, sol.p, wl.seeds[r % wl.rows])
@@ -83,12 +151,20 @@ def cpu_baseline(wl, combos, target_s):
             break
     dt = time.perf_counter() - t0
     return {"value": elems / dt, "unit": "elements/s", "cores": 1, "kind": "oracle",
-            "sample": f"{r} rows of d={wl.d} x {len(combos)} (solver, rho) combos, {dt:.1f} s, "
-                      "fp64 oracle single thread"}
+            "sample": f"{r} rows of {prefix} of the workload's {wl.d} entries x {len(combos)} (solver, rho) "
+                      f"combos, {dt:.1f} s, fp64 oracle single thread"}
+
+
+KERNEL_CLASSES = {"k_init": 5, "k_stats": 1, "k_solve": 3, "k_refine": 4, "k_sample": 0}
 
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        wl_name = {"c1": "c1_normal_d65536", "c2": "c2_laplace_16x1048576", "c3": "c3_logreg_256x4194304",
+                   "c4": "c4_resnet50_d25557032", "c5": "c5_student_t2_outliers_d268435456"}[args.workload]
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], wl_name)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); multi-GPU runs are not part of "
               "this build", file=sys.stderr)
@@ -118,6 +194,14 @@ def main():
         for plan, rho_dev in plans:
             plan.run(g, rho_dev, seeds)
 
+    if args.copy_probe:
+        src = torch.empty(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -137,6 +221,16 @@ def main():
     timer.close()
     for plan, _ in plans:
         nnz_tot += int(plan.nnz.sum().item())
+    # time per step of every kernel class (separate short loops, one class bracketed at a time)
+    kernels = {}
+    reps = min(args.steps, 10)
+    for name, which in KERNEL_CLASSES.items():
+        t = gs.KernelTimer(which, reps * len(plans) * 16)
+        for _ in range(reps):
+            step()
+        ms, n = t.read()
+        t.close()
+        kernels[name] = {"us_per_step": 1e3 * ms / reps, "launches_per_step": n / reps}
     # survivors are identical in every step (same seeds), so per-step bytes are exact
     elements_per_step = rows * d * len(plans)
     ms_per_step = elapsed * 1e3 / args.steps
@@ -144,7 +238,7 @@ def main():
     alg_bytes_per_step = 4.0 * elements_per_step + 8.0 * nnz_tot
     avg_launch_ms = ksample_ms / max(launches, 1)
     achieved = alg_bytes_per_step / len(plans) / (avg_launch_ms * 1e-3) / 1e9
-    traffic = traffic_for(wl.name)
+    traffic = traffic_for(wl.name) if (args.solver is None and args.rho is None) else None
     line = {
         "metric": METRIC,
         "value": value,
@@ -164,12 +258,14 @@ def main():
                    "parallelism": "single GPU, rows batched in one call"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_sample (Philox sampling, amplification, compaction)",
+                     "kernel": "k_sample (Philox sampling, amplification, compaction; the largest "
+                               "HBM-bound kernel, time per class in 'kernels')",
                      "algorithmic_bytes_per_launch": alg_bytes_per_step / len(plans),
                      "avg_launch_ms": avg_launch_ms, "launches": launches},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, combos, args.cpu_seconds)
+    line["kernels"] = kernels
     line["nnz_per_step"] = nnz_tot
     line["src_sha"] = src_hash()
     print(json.dumps(line), flush=True)

@@ -122,10 +122,12 @@ const char* gspar_status_string(int status);
 int gspar_version(void);
 
 /* Measurement hook for benchmarks (process-global, not thread-safe): while armed, every launch
- * of kernel `which` (0 = sample/compact, 1 = statistics pass, 2 = probabilities) is bracketed by
- * a pair of HIP timing events on its stream, for up to `max_launches` launches.
- * gspar_timing_read synchronises on the last event and returns the summed kernel time in ms and
- * the number of bracketed launches; gspar_timing_disarm releases the events. */
+ * of kernel class `which` (0 = sample/compact, 1 = statistics pass, 2 = probabilities, 3 = solver,
+ * 4 = refinement pass, 5 = workspace initialisation) is bracketed by a pair of HIP timing events
+ * on its stream, for up to `max_launches` launches. gspar_timing_read synchronises on the last
+ * event and returns the summed kernel time in ms and the number of bracketed launches;
+ * gspar_timing_disarm releases the events. Returns GSPAR_ERR_ARG for an unknown class or a
+ * non-positive count, GSPAR_ERR_HIP if the events cannot be created. */
 int gspar_timing_arm(int which, int max_launches);
 int gspar_timing_read(double* total_ms, int* launches);
 int gspar_timing_disarm(void);

@@ -1573,19 +1573,27 @@ static int launch_solve(Args& a, hipStream_t s) {
   int ib = (int)((zero_items + 255) / 256);
   if (ib > 1024) ib = 1024;
   if (ib < 1) ib = 1;
+  time_before(5, s);
   hipLaunchKernelGGL(k_init, dim3(ib), dim3(256), 0, s, a);
+  time_after(5, s);
   const dim3 grid((unsigned)(a.rows * a.nb));
   time_before(1, s);
   if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
   else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
   time_after(1, s);
+  time_before(3, s);
   hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
+  time_after(3, s);
   // each greedy step may need a level-2 and a level-3 window, the exact solver at most both once
   const int R = a.solver == GSPAR_GREEDY ? 2 * a.T : 2;
   for (int r = 0; r < R; ++r) {
+    time_before(4, s);
     if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
     else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
+    time_after(4, s);
+    time_before(3, s);
     hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
+    time_after(3, s);
   }
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
@@ -1731,7 +1739,7 @@ const char* gspar_status_string(int status) {
 int gspar_version(void) { return 100; }
 
 int gspar_timing_arm(int which, int max_launches) {
-  if (which < 0 || which > 2 || max_launches < 1) return GSPAR_ERR_ARG;
+  if (which < 0 || which > 5 || max_launches < 1) return GSPAR_ERR_ARG;
   gspar_timing_disarm();
   g_timing.ev = new hipEvent_t[2 * (size_t)max_launches];
   for (int i = 0; i < 2 * max_launches; ++i) {
