@@ -1166,19 +1166,19 @@ __device__ __forceinline__ uint32_t wave_prefix_small(uint32_t n, int lane, uint
   return (uint32_t)(__popcll(b0 & lt) + 2 * __popcll(b1 & lt) + 4 * __popcll(b2 & lt));
 }
 
-// Phase 1: each lane decides kTileGroups groups of its wave's quarter and keeps the selection,
-// capped and sign bits in registers; the values of capped survivors (which are emitted unscaled)
-// are appended, in index order, to a small per-wave LDS list. The wave totals give the tile
-// aggregate, published at once; wave 0 then looks back for the tile's prefix. Phase 2: each wave
-// walks its groups again in index order, places its survivors in a per-wave LDS ring at offsets
-// from a ballot prefix over lanes, and writes the ring out in blocks of 64 consecutive pairs, one
-// coalesced store per array per block. Phase 2 reads no global memory (a load would wait for every
-// store issued before it), except for capped survivors beyond the LDS list's capacity.
+// Phase 1: each lane decides kTileGroups groups of its wave's quarter (coalesced loads, one
+// Philox block per group) and writes one byte per group to LDS: selection bits (low nibble) and
+// sign bits (high nibble); capped survivors (emitted unscaled) append their value, in index
+// order, to a small per-wave LDS list and set their bit in a second byte array. The wave totals
+// give the tile aggregate, published at once; wave 0 then looks back for the tile's prefix.
+// Phase 2: thread t owns the tile's groups [16t, 16t + 16), i.e. 64 consecutive coordinates
+// inside its own wave's quarter, so its survivors are contiguous in the output: one prefix over
+// the wave's lanes places it, and it writes only its own set bits. Phase 2 reads no global memory
+// (a load would wait for every store issued before it), except for capped survivors beyond the
+// LDS list's capacity (a separate instantiation).
 constexpr int kCapList = 256;    // capped survivor values kept per wave
 constexpr int kSampleBatch = 8;  // float4 loads in flight per lane in the sampling pass
-constexpr int kRing = 512;       // per-wave staging ring of (index, value) pairs (power of two)
-static_assert(kTileGroups % kSampleBatch == 0 && kTileGroups % 16 == 0, "tile shape");
-constexpr int kMaskWords = kTileGroups / 16;  // 64-bit mask words per lane (4 bits per group)
+static_assert(kTileGroups % kSampleBatch == 0 && kTileGroups == 16, "tile shape");
 // Below this lambda, lambda * 2^32 * |g| could round differently from (lambda * |g|) * 2^32.
 constexpr double kLamScaledMin = 0x1p-900;
 
@@ -1201,13 +1201,33 @@ __device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double 
   }
 }
 
+// popcount(m & bits of the lanes below this one)
+__device__ __forceinline__ uint32_t lanes_below(unsigned long long m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+// Exclusive prefix over the lanes of a wave of x in [0, 2^B) from B ballots; `total` receives the
+// wave's sum.
+template <int B>
+__device__ __forceinline__ uint32_t wave_prefix_bits(uint32_t x, uint32_t& total) {
+  uint32_t pre = 0;
+  total = 0;
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    const unsigned long long m = __ballot((x >> b) & 1);
+    pre += lanes_below(m) << b;
+    total += (uint32_t)__popcll(m) << b;
+  }
+  return pre;
+}
+
 template <bool VEC>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   __shared__ float s_capv[kTileThreads / 64][kCapList];
-  __shared__ int32_t s_ri[kTileThreads / 64][kRing];
-  __shared__ float s_rv[kTileThreads / 64][kRing];
+  __shared__ alignas(16) uint8_t s_code[kTileElems / 4];  // per group: selection | sign << 4
+  __shared__ alignas(16) uint8_t s_capb[kTileElems / 4];  // per group: capped-survivor bits
   __shared__ uint32_t s_wsel[kTileThreads / 64];
   __shared__ uint32_t s_wcap[kTileThreads / 64];
+  __shared__ uint32_t s_wcl[kTileThreads / 64];
   __shared__ uint64_t s_excl;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t t = blockIdx.x;
@@ -1224,28 +1244,24 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   c.k0 = (uint32_t)seed;
   c.k1 = (uint32_t)(seed >> 32);
   const float inv = ctl->inv_lam;
-  // first group of this lane: tile base + wave quarter + lane; iteration j adds 64 groups
-  const int64_t q0 = part * (kTileElems / 4) + (int64_t)wv * (kWaveElems / 4) + lane;
+  // phase 1: group j of this lane is tile group wv * (kWaveElems / 4) + 64 j + lane
+  const int tg0 = wv * (kWaveElems / 4) + lane;
+  const int64_t q0 = part * (kTileElems / 4) + tg0;
 
-  // group j of this lane: bits 4*(j mod 16) .. +3 of mask word j / 16 (word index always a
-  // compile-time constant, so the masks stay in registers)
-  uint64_t selm[kMaskWords], capm[kMaskWords], negm[kMaskWords];
-#pragma unroll
-  for (int w = 0; w < kMaskWords; ++w) selm[w] = capm[w] = negm[w] = 0;
+  uint32_t nsel = 0, ncap = 0;
   uint32_t ncl = 0;  // capped survivors of this wave so far (the LDS list keeps the first kCapList)
-  auto record = [&](int w, int jj, const float v[4], uint32_t z, uint32_t cz) {
+  auto record = [&](int j, const float v[4], uint32_t z, uint32_t cz) {
     cz &= z;
-    selm[w] |= (uint64_t)z << (4 * jj);
-    if (__ballot(z != 0)) {
-      uint32_t neg = 0;
+    uint32_t neg = 0;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) neg |= (__float_as_uint(v[k]) >> 31) << k;
-      negm[w] |= (uint64_t)neg << (4 * jj);
-    }
+    for (int k = 0; k < 4; ++k) neg |= (__float_as_uint(v[k]) >> 31) << k;
+    s_code[tg0 + 64 * j] = (uint8_t)(z | (neg << 4));
+    s_capb[tg0 + 64 * j] = (uint8_t)cz;
+    nsel += (uint32_t)__popc(z);
     if (__ballot(cz != 0)) {
-      capm[w] |= (uint64_t)cz << (4 * jj);
+      ncap += (uint32_t)__popc(cz);
       uint32_t tot;
-      uint32_t p = ncl + wave_prefix_small((uint32_t)__popc(cz), lane, tot);
+      uint32_t p = ncl + wave_prefix_bits<3>((uint32_t)__popc(cz), tot);
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         if ((cz >> k) & 1) {
@@ -1272,25 +1288,17 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         const float v[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
         uint32_t z, cz;
         decide_fast(q0 + 64 * (jb + u), v, lam32, c.k0, c.k1, z, cz);
-        record((jb + u) >> 4, (jb + u) & 15, v, z, cz);
+        record(jb + u, v, z, cz);
       }
     }
-  } else if (c.live) {
-#pragma unroll
-    for (int w = 0; w < kMaskWords; ++w) {
-      for (int jj = 0; jj < 16; ++jj) {
-        float v[4];
-        uint32_t z, cz;
-        decide_group<VEC>(c, q0 + 64 * (16 * w + jj), v, z, cz);
-        record(w, jj, v, z, cz);
-      }
+  } else {
+    for (int j = 0; j < kTileGroups; ++j) {
+      float v[4];
+      uint32_t z = 0, cz = 0;
+      if (c.live) decide_group<VEC>(c, q0 + 64 * j, v, z, cz);
+      else v[0] = v[1] = v[2] = v[3] = 0.0f;
+      record(j, v, z, cz);
     }
-  }
-  uint32_t nsel = 0, ncap = 0;
-#pragma unroll
-  for (int w = 0; w < kMaskWords; ++w) {
-    nsel += (uint32_t)__popcll(selm[w]);
-    ncap += (uint32_t)__popcll(capm[w]);
   }
   for (int o = 32; o > 0; o >>= 1) {
     nsel += __shfl_xor(nsel, o);
@@ -1299,6 +1307,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   if (lane == 0) {
     s_wsel[wv] = nsel;
     s_wcap[wv] = ncap;
+    s_wcl[wv] = ncl;
   }
   __syncthreads();
   uint32_t tsel = 0, tcp = 0, wbase = 0;
@@ -1319,54 +1328,35 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   } else {
     if (tid == 0) __hip_atomic_store(&st[t], kStAgg | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (wv == 0) {
-      // lane l examines predecessors t-1-l-64m (m < kLookDepth): kLookDepth*64 tiles per round trip
       const int64_t first = t - part;
       int64_t look = t - 1;
       uint64_t ex = 0;
       while (true) {
-        uint64_t sw[kLookDepth];
-#pragma unroll
-        for (int m = 0; m < kLookDepth; ++m) {
-          const int64_t i = look - lane - 64 * m;
-          sw[m] = i >= first ? __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : kStInc;
-        }
-#pragma unroll
-        for (int m = 0; m < kLookDepth; ++m) {
-          const int64_t i = look - lane - 64 * m;
+        const int64_t i = look - lane;
+        uint64_t sw = kStInc;
+        if (i >= first) {
           int polls = 0;
-          while (i >= first && (sw[m] >> 62) == 0 && ++polls < kPolls) {
+          sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          while ((sw >> 62) == 0 && ++polls < kPolls) {
             __builtin_amdgcn_s_sleep(4);
-            sw[m] = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           }
         }
-        // nearest inclusive predecessor within this window: entry (m, lane) is at distance 64m + lane
-        int mstop = kLookDepth, lstop = 63;
-#pragma unroll
-        for (int m = kLookDepth - 1; m >= 0; --m) {
-          const uint64_t inc = __ballot((sw[m] >> 62) == 2);
-          if (inc) {
-            mstop = m;
-            lstop = __ffsll((unsigned long long)inc) - 1;
-          }
+        const uint64_t incl_mask = __ballot((sw >> 62) == 2);
+        const int stop = incl_mask ? (__ffsll((unsigned long long)incl_mask) - 1) : 63;
+        // predecessors up to `stop` that never published: count them here
+        uint64_t missing = __ballot((sw >> 62) == 0 && lane <= stop);
+        while (missing) {
+          const int m = __ffsll((unsigned long long)missing) - 1;
+          const uint64_t val = wave_tile_aggregate<VEC>(c, (look - m) - first, lane);
+          if (lane == m) sw = kStAgg | val;
+          missing &= missing - 1;
         }
-        uint64_t contrib = 0;
-#pragma unroll
-        for (int m = 0; m < kLookDepth; ++m) {
-          const bool in = m < mstop || (m == mstop && lane <= lstop);
-          // predecessors inside the window that never published: count them here
-          uint64_t missing = __ballot((sw[m] >> 62) == 0 && in);
-          while (missing) {
-            const int ml = __ffsll((unsigned long long)missing) - 1;
-            const uint64_t val = wave_tile_aggregate<VEC>(c, (look - ml - 64 * m) - first, lane);
-            if (lane == ml) sw[m] = kStAgg | val;
-            missing &= missing - 1;
-          }
-          contrib += in ? (sw[m] & kStVal) : 0;
-        }
+        uint64_t contrib = lane <= stop ? (sw & kStVal) : 0;
         for (int o = 32; o > 0; o >>= 1) contrib += __shfl_xor(contrib, o);
         ex += contrib;
-        if (mstop < kLookDepth) break;
-        look -= 64 * kLookDepth;
+        if (incl_mask) break;
+        look -= 64;
       }
       if (lane == 0) {
         __hip_atomic_store(&st[t], kStInc | (ex + agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1377,67 +1367,54 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   __syncthreads();
   const uint64_t excl = s_excl;
 
-  // phase 2: survivors of this wave, in index order, through the staging ring. Capped survivors
-  // take their value from the LDS list; a wave whose list overflowed reloads them from g instead
-  // (a separate instantiation, so the common path issues no global load at all).
-  auto emit = [&](auto from_lds) {
+  // phase 2: thread tid owns tile groups [16 tid, 16 tid + 16) (bit b of its masks is tile
+  // coordinate 64 tid + b)
+  if (s_wsel[wv]) {
+    const uint4 cw = *reinterpret_cast<const uint4*>(&s_code[16 * tid]);
+    const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
+    uint64_t sm = 0, nm = 0;
+#pragma unroll
+    for (int b = 0; b < 16; ++b) {
+      const uint64_t byte = (words[b >> 2] >> (8 * (b & 3))) & 0xFF;
+      sm |= (byte & 0xF) << (4 * b);
+      nm |= (byte >> 4) << (4 * b);
+    }
+    uint32_t wtot;
+    uint64_t pos = (excl & 0x7FFFFFFFull) + wbase + wave_prefix_bits<7>((uint32_t)__popcll(sm), wtot);
     int32_t* __restrict__ oi = a.idx + row * a.cap;
     float* __restrict__ ov = a.val + row * a.cap;
-    uint64_t out = (excl & 0x7FFFFFFFull) + wbase;  // output position of the ring's oldest entry
-    uint32_t head = 0, fill = 0;                     // ring window [head, head + fill)
-    uint32_t cl = 0;                                 // capped survivors of this wave emitted so far
+    const int64_t e0 = part * (int64_t)kTileElems + 64 * tid;
+    auto emit = [&](auto from_lds) {
+      // capped survivors: their bits, and the rank of this thread's first one in the wave's list
+      uint64_t cm = 0;
+      uint32_t cr = 0;
+      if (s_wcap[wv]) {
+        const uint4 bw = *reinterpret_cast<const uint4*>(&s_capb[16 * tid]);
+        const uint32_t cwd[4] = {bw.x, bw.y, bw.z, bw.w};
 #pragma unroll
-    for (int w = 0; w < kMaskWords; ++w)
-    for (int jj = 0; jj < 16; ++jj) {
-      const int j = 16 * w + jj;
-      const uint32_t z = (uint32_t)(selm[w] >> (4 * jj)) & 0xF;
-      if (__ballot(z != 0) == 0) continue;
-      uint32_t tot, ctot = 0;
-      uint32_t slot = head + fill + wave_prefix_small((uint32_t)__popc(z), lane, tot);
-      const int64_t i0 = 4 * (q0 + 64 * j);
-      const uint32_t cz = (uint32_t)(capm[w] >> (4 * jj)) & 0xF, ng = (uint32_t)(negm[w] >> (4 * jj)) & 0xF;
-      uint32_t cp = 0;
-      if (__ballot(cz != 0)) cp = cl + wave_prefix_small((uint32_t)__popc(cz), lane, ctot);
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if ((z >> k) & 1) {
-          float val = ((ng >> k) & 1) ? -inv : inv;
-          if ((cz >> k) & 1) {
-            if constexpr (decltype(from_lds)::value) val = s_capv[wv][cp];
-            else val = c.row[i0 + k];
-            ++cp;
-          }
-          const uint32_t r = slot & (kRing - 1);
-          s_ri[wv][r] = (int32_t)(i0 + k);
-          s_rv[wv][r] = val;
-          ++slot;
+        for (int b = 0; b < 16; ++b) cm |= (uint64_t)((cwd[b >> 2] >> (8 * (b & 3))) & 0xF) << (4 * b);
+        uint32_t ctot;
+        cr = wave_prefix_bits<7>((uint32_t)__popcll(cm), ctot);
+      }
+      uint64_t m = sm;
+      while (m) {
+        const int b = __ffsll((unsigned long long)m) - 1;
+        const uint64_t bit = 1ull << b;
+        float val = (nm & bit) ? -inv : inv;
+        if (cm & bit) {
+          if constexpr (decltype(from_lds)::value) val = s_capv[wv][cr];
+          else val = c.row[e0 + b];
+          ++cr;
         }
-      }
-      fill += tot;
-      cl += ctot;
-      __builtin_amdgcn_wave_barrier();
-      while (fill >= 64) {
-        const uint32_t r = (head + lane) & (kRing - 1);
-        if ((int64_t)(out + lane) < a.cap) {
-          oi[out + lane] = s_ri[wv][r];
-          ov[out + lane] = s_rv[wv][r];
+        if ((int64_t)pos < a.cap) {
+          oi[pos] = (int32_t)(e0 + b);
+          ov[pos] = val;
         }
-        head = (head + 64) & (kRing - 1);
-        fill -= 64;
-        out += 64;
+        ++pos;
+        m &= m - 1;
       }
-      __builtin_amdgcn_wave_barrier();
-    }
-    if ((uint32_t)lane < fill) {
-      const uint32_t r = (head + lane) & (kRing - 1);
-      if ((int64_t)(out + lane) < a.cap) {
-        oi[out + lane] = s_ri[wv][r];
-        ov[out + lane] = s_rv[wv][r];
-      }
-    }
-  };
-  if (nsel) {
-    if (ncl <= (uint32_t)kCapList) emit(std::true_type{});
+    };
+    if (s_wcl[wv] <= (uint32_t)kCapList) emit(std::true_type{});
     else emit(std::false_type{});
   }
   if (part == a.lay.tiles - 1 && tid == 0) {

@@ -142,6 +142,17 @@ inline unsigned long long __ballot(int pred) {
   return m;
 }
 inline void __builtin_amdgcn_wave_barrier() { emu::wave().bar->arrive_and_wait(); }
+inline unsigned __builtin_amdgcn_mbcnt_lo(unsigned m, unsigned acc) {
+  const int l = emu::lane();
+  return acc + (unsigned)__builtin_popcount(l >= 32 ? m : (m & ((1u << l) - 1u)));
+}
+inline unsigned __builtin_amdgcn_mbcnt_hi(unsigned m, unsigned acc) {
+  const int l = emu::lane();
+  return acc + (unsigned)__builtin_popcount(l < 32 ? 0u : (m & (l == 63 ? 0x7fffffffu : ((1u << (l - 32)) - 1u))));
+}
+struct uint4 {
+  unsigned x, y, z, w;
+};
 inline int __popc(unsigned v) { return __builtin_popcount(v); }
 inline int __popcll(unsigned long long v) { return __builtin_popcountll(v); }
 inline void __builtin_amdgcn_s_sleep(int) { std::this_thread::yield(); }
