@@ -51,7 +51,6 @@ constexpr int kTileGroups = 16;             // float4 groups per thread per tile
 constexpr int kTileElems = kTileThreads * kTileGroups * 4;  // 16384 coordinates per tile
 constexpr int kMaxIters = 64;
 constexpr int64_t kMaxChunk = (1 << 20) - 4;  // LDS packing holds < 2^20 elements per workgroup
-constexpr uint32_t kSpinLimit = 1u << 22;
 
 enum : uint32_t { kFlagInternal = 16 };
 
@@ -214,7 +213,7 @@ struct alignas(256) RowCtl {
   uint32_t flags;
   uint32_t need;     // 0: none; 2 / 3: a level-2 / level-3 pass is requested
   uint32_t done;     // 1 once lambda and tcap are final
-  uint32_t spare1;
+  uint32_t qkey;     // greedy: key whose count and sum above the level-2 pass also counts directly
   uint32_t spare2;
   uint32_t l2exp;    // binade of the level-2 window (kNone: none)
   uint32_t l3base;   // first key of the level-3 window (kNone: none)
@@ -234,6 +233,9 @@ struct Hist2 {
   uint64_t cnt[kB2];
   uint64_t sig[kB2];
   uint32_t mx[kB2];
+  uint32_t mnc[kB2];  // bitwise complement of the bin's minimum key (0: empty), so max-combined
+  uint64_t qcnt;      // count of window keys >= the row's qkey
+  uint64_t qsig;      // their significand sum
 };
 struct Hist3 {
   uint64_t cnt[kB3];
@@ -404,10 +406,14 @@ struct StatsLds {
   unsigned long long pk[kB1 * kLaneCopies];
   uint32_t mx[kB1 * kLaneCopies];
 };
-// LDS of a refinement pass: one window of at most kB2 bins, same packing.
+// LDS of a refinement pass: one window of at most kB2 bins, same packing, and for a level-2 window
+// the complemented bin minimum.
 struct WinLds {
   unsigned long long pk[kB2];
   uint32_t mx[kB2];
+  uint32_t mnc[kB2];
+  uint64_t qc[kNT / 64];
+  uint64_t qs[kNT / 64];
 };
 struct BinInfo {
   uint64_t Kab;  // count of keys strictly above the bin (including above the window)
@@ -441,11 +447,15 @@ struct SolveLds {
   L1Cache l1;
   WinCache<kB2> w2;
   WinCache<kB3> w3;
+  uint32_t w2mn[kB2];  // level-2 bin minima (0xFFFFFFFF: empty)
+  uint64_t qcnt, qsig; // direct count and significand sum of keys >= c.qkey in the level-2 window
+  int w2ready;         // the level-2 window has been summed into w2 in this solve
 };
 struct Hists {
   L1Cache* l1;         // LDS
   WinCache<kB2>* w2;   // LDS
   WinCache<kB3>* w3;   // LDS
+  uint32_t* w2mn;      // LDS
   const Hist1* h1g;    // the row's global copies, filled by the histogram passes
   Hist2* h2g;
   Hist3* h3g;
@@ -675,14 +685,16 @@ GS_DI void sv_finalize(SolveLds& s, double lam, uint32_t tcap) {
   __syncthreads();
 }
 
-// Ask for a histogram of binade E (level 2) or of keys [base, base + 2048) (level 3).
-GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32_t base) {
+// Ask for a histogram of binade E (level 2; the pass also counts the keys >= qkey directly, kNone
+// for none) or of keys [base, base + 2048) (level 3).
+GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32_t base, uint32_t qkey = kNone) {
   __syncthreads();
   // clear every copy of the requested level before the pass that fills it
   for (int c = 0; c < kC23; ++c) {
     if (level == 2) {
       Hist2* h = H.h2g + c;
-      for (int b = threadIdx.x; b < kB2; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; }
+      for (int b = threadIdx.x; b < kB2; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; h->mnc[b] = 0; }
+      if (threadIdx.x == 0) { h->qcnt = 0; h->qsig = 0; }
     } else {
       Hist3* h = H.h3g + c;
       for (int b = threadIdx.x; b < kB3; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; }
@@ -693,6 +705,7 @@ GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32
     if (level == 2) {
       s.c.l2exp = E;
       s.c.l3base = kNone;
+      s.c.qkey = qkey;
     } else {
       s.c.l3base = base;
     }
@@ -700,7 +713,33 @@ GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32
   __syncthreads();
 }
 
-// Count and exact sum of keys >= t. Returns 0 when resolved, else the level it requested.
+// Sums the level-2 copies (bins and minima) into the LDS window, once per solve.
+GS_DI void load_w2(SolveLds& s, const Hists& H) {
+  if (s.w2ready) return;
+  for (int b = threadIdx.x; b < kB2; b += kNT) {
+    uint64_t c = 0, sg = 0;
+    uint32_t m = 0, mc = 0;
+    for (int k = 0; k < kC23; ++k) {
+      c += H.h2g[k].cnt[b];
+      sg += H.h2g[k].sig[b];
+      m = max(m, H.h2g[k].mx[b]);
+      mc = max(mc, H.h2g[k].mnc[b]);
+    }
+    H.w2->cnt[b] = (uint32_t)c;
+    H.w2->sig[b] = sg;
+    H.w2->mx[b] = m;
+    H.w2mn[b] = ~mc;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) s.w2ready = 1;
+  __syncthreads();
+}
+
+// Greedy query: count K and exact sum W of the keys >= t. Resolved from level 1 when t's binade
+// is empty, lies below t or starts at t; else from the level-2 pass of that binade, which counted
+// the keys >= its qkey directly, or whose bin holding t has all its keys on one side of t (bin
+// minimum and maximum). Otherwise a level-2 pass of t's binade counting the keys >= t is
+// requested. Returns 0 when resolved, 2 after a request.
 GS_DI int sv_query(SolveLds& s, const Hists& H, uint32_t t, uint64_t& K, Fx& W) {
   const int e = (int)(t >> 23);
   const BinInfo i1 = l1_info(H, e);
@@ -712,36 +751,31 @@ GS_DI int sv_query(SolveLds& s, const Hists& H, uint32_t t, uint64_t& K, Fx& W) 
     K = i1.Kab; W = i1.Wab;
     return 0;
   }
-  if (s.c.l2exp != (uint32_t)e) {
-    sv_request(s, H, 2, (uint32_t)e, 0);
-    return 2;
+  if (s.c.l2exp == (uint32_t)e) {
+    if (s.c.qkey == t) {
+      K = i1.Kab + s.qcnt;
+      W = i1.Wab;
+      if (s.qsig) fx_add(W, fx_shifted(s.qsig, binade_shift(e)));
+      return 0;
+    }
+    load_w2(s, H);
+    const Lvl L2 = lvl2(H, (uint32_t)e, i1.Kab, i1.Wab);
+    Walk w2;
+    lvl_scan(L2, s, w2);
+    const int sb = (int)((t >> 11) & (kB2 - 1));
+    BinInfo i2;
+    lvl_bin_info(L2, w2, sb, s, i2);
+    if (i2.cnt == 0 || i2.mx < t) {
+      K = i2.Kab; W = i2.Wab;
+      return 0;
+    }
+    if (H.w2mn[sb] >= t) {
+      K = i2.Kab + i2.cnt; W = i2.Wab; fx_add(W, i2.Wb);
+      return 0;
+    }
   }
-  const Lvl L2 = lvl2(H, (uint32_t)e, i1.Kab, i1.Wab);
-  Walk w2;
-  lvl_scan(L2, s, w2);
-  const int sb = (int)((t >> 11) & (kB2 - 1));
-  BinInfo i2;
-  lvl_bin_info(L2, w2, sb, s, i2);
-  if ((t & 2047u) == 0) {
-    K = i2.Kab + i2.cnt; W = i2.Wab; fx_add(W, i2.Wb);
-    return 0;
-  }
-  if (i2.cnt == 0 || i2.mx < t) {
-    K = i2.Kab; W = i2.Wab;
-    return 0;
-  }
-  const uint32_t base = t & ~2047u;
-  if (s.c.l3base != base) {
-    sv_request(s, H, 3, 0, base);
-    return 3;
-  }
-  const Lvl L3 = lvl3(H, (uint32_t)e, i2.Kab, i2.Wab);
-  Walk w3;
-  lvl_scan(L3, s, w3);
-  BinInfo i3;
-  lvl_bin_info(L3, w3, (int)(t - base), s, i3);
-  K = i3.Kab + i3.cnt; W = i3.Wab; fx_add(W, i3.Wb);
-  return 0;
+  sv_request(s, H, 2, (uint32_t)e, 0, t);
+  return 2;
 }
 
 // Algorithm 3 in scale form: lambda_{j+1} = (B - k_j) / U_j, stop when it does not grow.
@@ -908,13 +942,28 @@ GS_DI void reduce_into(const HistT* h, int copies, int nbins, CntT* cnt, uint64_
 // The row's solver, run by one workgroup per row after each histogram pass: it either finishes the
 // row (lambda and the capped threshold become final) or requests the next refinement window.
 GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
-  if (threadIdx.x == 0) s.c = *gc;
+  if (threadIdx.x == 0) {
+    s.c = *gc;
+    s.w2ready = 0;
+  }
   __syncthreads();
   if (s.c.done) return;
-  // the histograms this solve may read: level 1 always, the level-2 / level-3 windows if any
+  // the histograms this solve may read: level 1 always; for the exact solver the level-2 /
+  // level-3 windows if any; for the greedy solver the direct count of the last level-2 pass (its
+  // bins are summed only if a query needs them)
   reduce_into(H.h1g, kC1, kB1, H.l1->cnt, H.l1->sig, H.l1->mx);
-  if (s.c.l2exp != kNone) reduce_into(H.h2g, kC23, kB2, H.w2->cnt, H.w2->sig, H.w2->mx);
-  if (s.c.l3base != kNone) reduce_into(H.h3g, kC23, kB3, H.w3->cnt, H.w3->sig, H.w3->mx);
+  if (s.c.solver != GSPAR_GREEDY) {
+    if (s.c.l2exp != kNone) reduce_into(H.h2g, kC23, kB2, H.w2->cnt, H.w2->sig, H.w2->mx);
+    if (s.c.l3base != kNone) reduce_into(H.h3g, kC23, kB3, H.w3->cnt, H.w3->sig, H.w3->mx);
+  } else if (threadIdx.x == 0 && s.c.l2exp != kNone) {
+    uint64_t qc = 0, qs = 0;
+    for (int k = 0; k < kC23; ++k) {
+      qc += H.h2g[k].qcnt;
+      qs += H.h2g[k].qsig;
+    }
+    s.qcnt = qc;
+    s.qsig = qs;
+  }
   __syncthreads();
   if (s.c.stage == 0) {
     // zeros = d minus the histogram's population (every nonzero key, finite or not, is binned)
@@ -964,6 +1013,7 @@ __global__ void __launch_bounds__(256) k_init(Args a) {
     if (!(rho >= 0.0 && rho <= 1.0)) c.flags = GSPAR_FLAG_BADRHO;
     c.l2exp = kNone;
     c.l3base = kNone;
+    c.qkey = kNone;
     c.solver = a.solver;
     c.T = a.T;
     *ctl_of(a, r) = c;
@@ -1052,14 +1102,20 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
     gcnt = h->cnt; gsig = h->sig; gmx = h->mx;
   }
   const uint32_t span = (uint32_t)nbins << shift;
+  // level 2 also keeps bin minima and counts the window's keys >= qkey directly (qkey lies in the
+  // window when set; kNone matches no key)
+  const bool l2 = need == 2;
+  const uint32_t qkey = l2 ? ctl->qkey : kNone;
   for (int b = threadIdx.x; b < nbins; b += kNT) {
     sm.pk[b] = 0;
     sm.mx[b] = 0;
+    sm.mnc[b] = 0;
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + row * a.ld;
   const int64_t beg = blk * a.chunk;
   const int64_t end = min(a.d, beg + a.chunk);
+  uint64_t qc = 0, qs = 0;
   stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -1067,11 +1123,27 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
       const uint32_t rel = key - lo;
       if (key != 0 && rel < span) {
         const uint32_t b = rel >> shift;
-        atomicAdd(&sm.pk[b], (unsigned long long)((1ull << 44) + key_sig(key)));
+        const uint64_t sg = key_sig(key);
+        atomicAdd(&sm.pk[b], (unsigned long long)((1ull << 44) + sg));
         if (key > sm.mx[b]) atomicMax(&sm.mx[b], key);
+        if (l2 && ~key > sm.mnc[b]) atomicMax(&sm.mnc[b], ~key);
+        if (key >= qkey) {
+          ++qc;
+          qs += sg;
+        }
       }
     }
   });
+  if (l2) {
+    for (int o = 32; o > 0; o >>= 1) {
+      qc += __shfl_xor(qc, o);
+      qs += __shfl_xor(qs, o);
+    }
+    if ((threadIdx.x & 63) == 0) {
+      sm.qc[threadIdx.x >> 6] = qc;
+      sm.qs[threadIdx.x >> 6] = qs;
+    }
+  }
   __syncthreads();
   for (int b = threadIdx.x; b < nbins; b += kNT) {
     const uint64_t p = sm.pk[b];
@@ -1079,6 +1151,19 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
       atomicAdd((unsigned long long*)&gcnt[b], (unsigned long long)(p >> 44));
       atomicAdd((unsigned long long*)&gsig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
       atomicMax(&gmx[b], sm.mx[b]);
+      if (l2) atomicMax(&h2_of(a, row, cp)->mnc[b], sm.mnc[b]);
+    }
+  }
+  if (l2 && threadIdx.x == 0) {
+    uint64_t tc = 0, ts = 0;
+    for (int i = 0; i < kNT / 64; ++i) {
+      tc += sm.qc[i];
+      ts += sm.qs[i];
+    }
+    if (tc) {
+      Hist2* h = h2_of(a, row, cp);
+      atomicAdd((unsigned long long*)&h->qcnt, (unsigned long long)tc);
+      atomicAdd((unsigned long long*)&h->qsig, (unsigned long long)ts);
     }
   }
 }
@@ -1087,7 +1172,7 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
 __global__ void __launch_bounds__(kNT) k_solve(Args a) {
   __shared__ SolveLds sm;
   const int64_t row = blockIdx.x;
-  const Hists H{&sm.l1, &sm.w2, &sm.w3, h1_of(a, row), h2_of(a, row), h3_of(a, row)};
+  const Hists H{&sm.l1, &sm.w2, &sm.w3, sm.w2mn, h1_of(a, row), h2_of(a, row), h3_of(a, row)};
   solve_row(sm, ctl_of(a, row), H, a.d);
 }
 
@@ -1099,7 +1184,6 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
 // ordering of workgroup dispatch is assumed and every wait ends.
 constexpr uint64_t kStAgg = 1ull << 62, kStInc = 2ull << 62, kStVal = (1ull << 62) - 1;
 constexpr int kPolls = 4096;
-constexpr int kLookDepth = 1;  // status words examined per lane per look-back round trip
 constexpr int kWaveElems = kTileElems / (kTileThreads / 64);  // coordinates per wave per tile
 
 struct TileCtx {
@@ -1561,8 +1645,9 @@ static int launch_solve(Args& a, hipStream_t s) {
   time_before(3, s);
   hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
   time_after(3, s);
-  // each greedy step may need a level-2 and a level-3 window, the exact solver at most both once
-  const int R = a.solver == GSPAR_GREEDY ? 2 * a.T : 2;
+  // each greedy step needs at most one level-2 pass (which counts its query key directly), the
+  // exact solver at most a level-2 and a level-3 window
+  const int R = a.solver == GSPAR_GREEDY ? a.T : 2;
   for (int r = 0; r < R; ++r) {
     time_before(4, s);
     if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
