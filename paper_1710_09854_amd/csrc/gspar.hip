@@ -205,7 +205,8 @@ struct alignas(256) RowCtl {
   Fx fbW;            // exact solver: capped sum of the best candidate found so far
   uint64_t fbK;      // exact solver: capped count of that candidate
   uint64_t zeros;    // zero entries of the row (d minus the histogram's population)
-  uint64_t spare0;
+  uint64_t wK;       // exact solver, level 3: count of keys above the window
+  Fx wW;             // and their exact sum
   float inv_lam;     // fl32(1/lambda): the amplified value off the capped set
   uint32_t fbTcap;   // exact solver: candidate's capped threshold key
   uint32_t fbValid;
@@ -229,19 +230,27 @@ struct Hist1 {
   uint64_t sig[kB1];
   uint32_t mx[kB1];
 };
-struct Hist2 {
+// Histogram of one refinement window: a level-2 window uses all kB2 bins (one binade, 2^11 keys per
+// bin), a level-3 window the first kB3 (one key per bin).
+struct alignas(256) WinHist {
   uint64_t cnt[kB2];
   uint64_t sig[kB2];
   uint32_t mx[kB2];
-  uint32_t mnc[kB2];  // bitwise complement of the bin's minimum key (0: empty), so max-combined
-  uint64_t qcnt;      // count of window keys >= the row's qkey
+  uint32_t mnc[kB2];  // level 2: bitwise complement of the bin's minimum key (0: empty), so max-combined
+  uint64_t qcnt;      // level 2: count of window keys >= the row's qkey
   uint64_t qsig;      // their significand sum
 };
-struct Hist3 {
-  uint64_t cnt[kB3];
-  uint64_t sig[kB3];
-  uint32_t mx[kB3];
+
+// The level-1 histogram summed over its copies, with per binade the count K and exact sum W of all
+// keys in the binades above it.
+struct alignas(16) L1Cache {
+  uint64_t cnt[kB1];
+  uint64_t sig[kB1];
+  uint32_t mx[kB1];
+  uint64_t K[kB1];
+  Fx W[kB1];
 };
+static_assert(sizeof(L1Cache) % 16 == 0, "L1Cache is copied in 16-byte units");
 // Per-row partial count of capped coordinates written by the probabilities pass, one per class.
 struct alignas(128) CountLine {
   unsigned long long v;
@@ -251,12 +260,12 @@ struct alignas(128) CountLine {
 GS_HD size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctl, h1, h2, h3, kc, status, total;
+  size_t ctl, h1, l1t, win, kc, status, total;
   int64_t tiles;  // tiles per row of the sample pass
 };
 
-// Histogram copies: row r's copy c of level 1 is h1 + (r * kC1 + c); copy 0 also holds the row's
-// reduced histogram once the first solve has summed the copies into it (likewise for levels 2, 3).
+// Histogram copies: row r's copy c of level 1 is h1 + (r * kC1 + c), of a refinement window
+// win + (r * kC23 + c); the solve that requests a refinement pass clears the window's copies.
 GS_HD Layout layout_of(int64_t rows, int64_t d) {
   Layout L;
   L.tiles = (d + kTileElems - 1) / kTileElems;
@@ -265,10 +274,10 @@ GS_HD Layout layout_of(int64_t rows, int64_t d) {
   off += align256((size_t)rows * sizeof(RowCtl));
   L.h1 = off;
   off += align256((size_t)rows * kC1 * sizeof(Hist1));
-  L.h2 = off;
-  off += align256((size_t)rows * kC23 * sizeof(Hist2));
-  L.h3 = off;
-  off += align256((size_t)rows * kC23 * sizeof(Hist3));
+  L.l1t = off;
+  off += align256((size_t)rows * sizeof(L1Cache));
+  L.win = off;
+  off += align256((size_t)rows * kC23 * sizeof(WinHist));
   L.kc = off;
   off += align256((size_t)rows * 8 * sizeof(CountLine));
   L.status = off;
@@ -289,6 +298,7 @@ struct Args {
   Layout lay;
   int nb;          // workgroups per row of the histogram passes
   int64_t chunk;   // elements per histogram workgroup (multiple of 4)
+  int first;       // k_solve: the solve right after the statistics pass
   int32_t* idx;
   float* val;
   int64_t cap;
@@ -305,12 +315,13 @@ __device__ __forceinline__ RowCtl* ctl_of(const Args& a, int64_t r) {
 __device__ __forceinline__ Hist1* h1_of(const Args& a, int64_t r, int c = 0) {
   return reinterpret_cast<Hist1*>(a.ws + a.lay.h1) + r * kC1 + c;
 }
-__device__ __forceinline__ Hist2* h2_of(const Args& a, int64_t r, int c = 0) {
-  return reinterpret_cast<Hist2*>(a.ws + a.lay.h2) + r * kC23 + c;
+__device__ __forceinline__ L1Cache* l1t_of(const Args& a, int64_t r) {
+  return reinterpret_cast<L1Cache*>(a.ws + a.lay.l1t) + r;
 }
-__device__ __forceinline__ Hist3* h3_of(const Args& a, int64_t r, int c = 0) {
-  return reinterpret_cast<Hist3*>(a.ws + a.lay.h3) + r * kC23 + c;
+__device__ __forceinline__ WinHist* win_of(const Args& a, int64_t r, int c = 0) {
+  return reinterpret_cast<WinHist*>(a.ws + a.lay.win) + r * kC23 + c;
 }
+
 __device__ __forceinline__ CountLine* kc_of(const Args& a, int64_t r) {
   return reinterpret_cast<CountLine*>(a.ws + a.lay.kc) + r * 8;
 }
@@ -422,15 +433,8 @@ struct BinInfo {
   Fx Wb;
   uint32_t mx;
 };
-// The solver's working copies of the histograms, in LDS: level 1 with, per binade, the count and
-// exact sum of all keys in binades above it; the level-2 and level-3 windows when they exist.
-struct L1Cache {
-  uint64_t cnt[kB1];
-  uint64_t sig[kB1];
-  uint32_t mx[kB1];
-  uint64_t K[kB1];
-  Fx W[kB1];
-};
+// The solver's working copies of the histograms, in LDS: level 1 (L1Cache, kept in global memory
+// as well between solves); the level-2 and level-3 windows when they exist.
 template <int N>
 struct WinCache {
   uint32_t cnt[N];  // window counts never exceed d < 2^31
@@ -443,22 +447,19 @@ struct SolveLds {
   Fx sw[kB1 / 64];
   int ired[kNT / 64];
   BinInfo bi;
-  RowCtl c;  // working copy of the row's control block
   L1Cache l1;
   WinCache<kB2> w2;
   WinCache<kB3> w3;
-  uint32_t w2mn[kB2];  // level-2 bin minima (0xFFFFFFFF: empty)
-  uint64_t qcnt, qsig; // direct count and significand sum of keys >= c.qkey in the level-2 window
-  int w2ready;         // the level-2 window has been summed into w2 in this solve
+  uint64_t bcnt, bsig;  // a level-2 bin's totals, broadcast by its owner (greedy queries)
+  uint32_t bmx, bmn;
 };
 struct Hists {
   L1Cache* l1;         // LDS
   WinCache<kB2>* w2;   // LDS
   WinCache<kB3>* w3;   // LDS
-  uint32_t* w2mn;      // LDS
+  L1Cache* l1g;        // the row's level-1 table in global memory, written by the first solve
   const Hist1* h1g;    // the row's global copies, filled by the histogram passes
-  Hist2* h2g;
-  Hist3* h3g;
+  WinHist* wg;         // copies of the refinement window
 };
 
 GS_DI int block_max(SolveLds& s, int v) {
@@ -673,74 +674,100 @@ GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLd
   b2 = block_min(s, lowest);
 }
 
-GS_DI void sv_finalize(SolveLds& s, double lam, uint32_t tcap) {
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    s.c.lam = lam;
-    s.c.tcap = tcap;
-    s.c.inv_lam = (lam > 0.0 && lam < INFINITY) ? (float)(1.0 / lam) : 0.0f;
-    s.c.done = 1;
-    s.c.need = 0;
-  }
-  __syncthreads();
+// The solver's control flow runs in every thread of the workgroup on a private copy of the row's
+// control block: every decision depends only on data all threads see (the LDS tables and values
+// broadcast through LDS by the block-wide steps), so the copies stay identical and no barrier is
+// needed between scalar steps. Thread 0 writes the block back at the end.
+GS_DI void sv_finalize(RowCtl& c, double lam, uint32_t tcap) {
+  c.lam = lam;
+  c.tcap = tcap;
+  c.inv_lam = (lam > 0.0 && lam < INFINITY) ? (float)(1.0 / lam) : 0.0f;
+  c.done = 1;
+  c.need = 0;
 }
 
 // Ask for a histogram of binade E (level 2; the pass also counts the keys >= qkey directly, kNone
-// for none) or of keys [base, base + 2048) (level 3).
-GS_DI void sv_request(SolveLds& s, const Hists& H, int level, uint32_t E, uint32_t base, uint32_t qkey = kNone) {
-  __syncthreads();
-  // clear every copy of the requested level before the pass that fills it
-  for (int c = 0; c < kC23; ++c) {
-    if (level == 2) {
-      Hist2* h = H.h2g + c;
-      for (int b = threadIdx.x; b < kB2; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; h->mnc[b] = 0; }
-      if (threadIdx.x == 0) { h->qcnt = 0; h->qsig = 0; }
-    } else {
-      Hist3* h = H.h3g + c;
-      for (int b = threadIdx.x; b < kB3; b += kNT) { h->cnt[b] = 0; h->sig[b] = 0; h->mx[b] = 0; }
-    }
+// for none) or of keys [base, base + 2048) (level 3; wK and wW count and sum the keys above it).
+// Clears the window's copies (every thread of the workgroup takes part; the kernel boundary orders
+// the stores before the pass).
+GS_DI void sv_request(RowCtl& c, const Hists& H, int level, uint32_t E, uint32_t base, uint32_t qkey, uint64_t wK,
+                      const Fx& wW) {
+  uint4 z;
+  z.x = z.y = z.z = z.w = 0u;
+  uint4* w = reinterpret_cast<uint4*>(H.wg);
+  for (int i = threadIdx.x; i < (int)(kC23 * sizeof(WinHist) / 16); i += kNT) w[i] = z;
+  c.need = level;
+  if (level == 2) {
+    c.l2exp = E;
+    c.l3base = kNone;
+    c.qkey = qkey;
+  } else {
+    c.l3base = base;
+    c.wK = wK;
+    c.wW = wW;
   }
-  if (threadIdx.x == 0) {
-    s.c.need = level;
-    if (level == 2) {
-      s.c.l2exp = E;
-      s.c.l3base = kNone;
-      s.c.qkey = qkey;
-    } else {
-      s.c.l3base = base;
-    }
-  }
-  __syncthreads();
 }
 
-// Sums the level-2 copies (bins and minima) into the LDS window, once per solve.
-GS_DI void load_w2(SolveLds& s, const Hists& H) {
-  if (s.w2ready) return;
-  for (int b = threadIdx.x; b < kB2; b += kNT) {
-    uint64_t c = 0, sg = 0;
-    uint32_t m = 0, mc = 0;
-    for (int k = 0; k < kC23; ++k) {
-      c += H.h2g[k].cnt[b];
-      sg += H.h2g[k].sig[b];
-      m = max(m, H.h2g[k].mx[b]);
-      mc = max(mc, H.h2g[k].mnc[b]);
+// Count and significand sum of the level-2 window's keys in bins above sb, summed straight from the
+// global copies (thread t owns bins [t * per, t * per + per)); bin sb's own totals, maximum and
+// minimum go to s.bcnt, s.bsig, s.bmx, s.bmn.
+GS_DI void w2_above(SolveLds& s, const Hists& H, int sb, uint64_t& ka, uint64_t& sa) {
+  constexpr int per = kB2 / kNT;
+  const int b0 = threadIdx.x * per;
+  uint64_t c[per], g[per];
+#pragma unroll
+  for (int j = 0; j < per; ++j) {
+    c[j] = 0;
+    g[j] = 0;
+#pragma unroll
+    for (int q = 0; q < kC23; ++q) {
+      c[j] += H.wg[q].cnt[b0 + j];
+      g[j] += H.wg[q].sig[b0 + j];
     }
-    H.w2->cnt[b] = (uint32_t)c;
-    H.w2->sig[b] = sg;
-    H.w2->mx[b] = m;
-    H.w2mn[b] = ~mc;
+  }
+  uint64_t k = 0, sg = 0;
+#pragma unroll
+  for (int j = 0; j < per; ++j) {
+    if (b0 + j > sb) {
+      k += c[j];
+      sg += g[j];
+    } else if (b0 + j == sb) {
+      uint32_t mx = 0, mc = 0;
+      for (int q = 0; q < kC23; ++q) {
+        mx = max(mx, H.wg[q].mx[sb]);
+        mc = max(mc, H.wg[q].mnc[sb]);
+      }
+      s.bcnt = c[j];
+      s.bsig = g[j];
+      s.bmx = mx;
+      s.bmn = ~mc;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    k += __shfl_xor(k, o);
+    sg += __shfl_xor(sg, o);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    s.sk[threadIdx.x >> 6] = k;
+    s.ss[threadIdx.x >> 6] = sg;
   }
   __syncthreads();
-  if (threadIdx.x == 0) s.w2ready = 1;
+  ka = 0;
+  sa = 0;
+  for (int i = 0; i < kNT / 64; ++i) {
+    ka += s.sk[i];
+    sa += s.ss[i];
+  }
   __syncthreads();
 }
 
 // Greedy query: count K and exact sum W of the keys >= t. Resolved from level 1 when t's binade
 // is empty, lies below t or starts at t; else from the level-2 pass of that binade, which counted
-// the keys >= its qkey directly, or whose bin holding t has all its keys on one side of t (bin
-// minimum and maximum). Otherwise a level-2 pass of t's binade counting the keys >= t is
+// the keys >= its qkey directly (qcnt, qsig), or whose bin holding t has all its keys on one side
+// of t (bin minimum and maximum). Otherwise a level-2 pass of t's binade counting the keys >= t is
 // requested. Returns 0 when resolved, 2 after a request.
-GS_DI int sv_query(SolveLds& s, const Hists& H, uint32_t t, uint64_t& K, Fx& W) {
+GS_DI int sv_query(SolveLds& s, RowCtl& c, const Hists& H, uint64_t qcnt, uint64_t qsig, uint32_t t, uint64_t& K,
+                   Fx& W) {
   const int e = (int)(t >> 23);
   const BinInfo i1 = l1_info(H, e);
   if ((t & 0x7FFFFFu) == 0) {
@@ -751,173 +778,146 @@ GS_DI int sv_query(SolveLds& s, const Hists& H, uint32_t t, uint64_t& K, Fx& W) 
     K = i1.Kab; W = i1.Wab;
     return 0;
   }
-  if (s.c.l2exp == (uint32_t)e) {
-    if (s.c.qkey == t) {
-      K = i1.Kab + s.qcnt;
+  if (c.l2exp == (uint32_t)e) {
+    uint64_t kq = 0, sq = 0;
+    bool ok = false;
+    if (c.qkey == t) {
+      kq = qcnt;
+      sq = qsig;
+      ok = true;
+    } else {
+      uint64_t ka, sa;
+      w2_above(s, H, (int)((t >> 11) & (kB2 - 1)), ka, sa);
+      if (s.bcnt == 0 || s.bmx < t) {
+        kq = ka; sq = sa; ok = true;
+      } else if (s.bmn >= t) {
+        kq = ka + s.bcnt; sq = sa + s.bsig; ok = true;
+      }
+    }
+    if (ok) {
+      K = i1.Kab + kq;
       W = i1.Wab;
-      if (s.qsig) fx_add(W, fx_shifted(s.qsig, binade_shift(e)));
-      return 0;
-    }
-    load_w2(s, H);
-    const Lvl L2 = lvl2(H, (uint32_t)e, i1.Kab, i1.Wab);
-    Walk w2;
-    lvl_scan(L2, s, w2);
-    const int sb = (int)((t >> 11) & (kB2 - 1));
-    BinInfo i2;
-    lvl_bin_info(L2, w2, sb, s, i2);
-    if (i2.cnt == 0 || i2.mx < t) {
-      K = i2.Kab; W = i2.Wab;
-      return 0;
-    }
-    if (H.w2mn[sb] >= t) {
-      K = i2.Kab + i2.cnt; W = i2.Wab; fx_add(W, i2.Wb);
+      if (sq) fx_add(W, fx_shifted(sq, binade_shift(e)));
       return 0;
     }
   }
-  sv_request(s, H, 2, (uint32_t)e, 0, t);
+  sv_request(c, H, 2, (uint32_t)e, 0, t, 0, fx_zero());
   return 2;
 }
 
 // Algorithm 3 in scale form: lambda_{j+1} = (B - k_j) / U_j, stop when it does not grow.
-GS_DI void sv_greedy(SolveLds& s, const Hists& H) {
-  while (s.c.iter < s.c.T) {
-    const double lam = s.c.lam;
+GS_DI void sv_greedy(SolveLds& s, RowCtl& c, const Hists& H, uint64_t qcnt, uint64_t qsig) {
+  while (c.iter < c.T) {
+    const double lam = c.lam;
     uint64_t K;
     Fx W;
-    if (sv_query(s, H, cap_key(lam), K, W)) return;
-    const double U = fx_to_double(fx_sub(s.c.S, W));
+    if (sv_query(s, c, H, qcnt, qsig, cap_key(lam), K, W)) return;
+    const double U = fx_to_double(fx_sub(c.S, W));
     if (U == 0.0) break;
-    const double ln = (s.c.B - (double)K) / U;
+    const double ln = (c.B - (double)K) / U;
     if (!(ln > lam)) break;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      s.c.lam = ln;
-      s.c.iter += 1;
-    }
-    __syncthreads();
+    c.lam = ln;
+    c.iter += 1;
   }
-  const double lam = s.c.lam;
-  sv_finalize(s, lam, cap_key(lam));
+  sv_finalize(c, c.lam, cap_key(c.lam));
 }
 
-GS_DI void sv_exact_finish(SolveLds& s, uint64_t K, const Fx& W, uint32_t tcap) {
-  const double T1 = fx_to_double(fx_sub(s.c.S, W));
-  const double lam = (s.c.B - (double)K) / T1;
-  sv_finalize(s, lam, tcap);
+GS_DI void sv_exact_finish(RowCtl& c, uint64_t K, const Fx& W, uint32_t tcap) {
+  const double T1 = fx_to_double(fx_sub(c.S, W));
+  const double lam = (c.B - (double)K) / T1;
+  sv_finalize(c, lam, tcap);
 }
 
 // The exact solver descends levels: at each one it finds the highest bin whose maximum passes
 // the criterion (b1) and the lowest occupied bin above it (b2); the answer is b1's maximum
 // unless b2 holds two or more values that could still pass, in which case b2 is refined.
-GS_DI void sv_exact(SolveLds& s, const Hists& H) {
-  const int level = s.c.stage;
+GS_DI void sv_exact(SolveLds& s, RowCtl& c, const Hists& H) {
+  const int level = c.stage;
   int b1, b2;
   BinInfo c1, c2;  // the bins b1 and b2 at this level
   uint32_t E = 0;
   if (level == 1) {
-    l1_exact(H, s.c.B, s.c.S, s, b1, b2);
+    l1_exact(H, c.B, c.S, s, b1, b2);
     if (b1 >= 0) c1 = l1_info(H, b1);
     if (b2 != INT_MAX) c2 = l1_info(H, b2);
   } else {
-    E = s.c.l2exp;
-    const BinInfo iE = l1_info(H, (int)E);
-    const Lvl L2 = lvl2(H, E, iE.Kab, iE.Wab);
-    Walk w2;
-    lvl_scan(L2, s, w2);
-    Lvl L = L2;
-    Walk w = w2;
-    if (level == 3) {
-      BinInfo i2;
-      lvl_bin_info(L2, w2, (int)((s.c.l3base >> 11) & (kB2 - 1)), s, i2);
-      const Lvl L3 = lvl3(H, E, i2.Kab, i2.Wab);
-      Walk w3;
-      lvl_scan(L3, s, w3);
-      L = L3;
-      w = w3;
+    E = c.l2exp;
+    Lvl L;
+    if (level == 2) {
+      const BinInfo iE = l1_info(H, (int)E);
+      L = lvl2(H, E, iE.Kab, iE.Wab);
+    } else {
+      L = lvl3(H, E, c.wK, c.wW);
     }
-    lvl_exact(L, w, s.c.B, s.c.S, s, b1, b2);
+    Walk w;
+    lvl_scan(L, s, w);
+    lvl_exact(L, w, c.B, c.S, s, b1, b2);
     if (b1 >= 0) lvl_bin_info(L, w, b1, s, c1);
     if (b2 != INT_MAX) lvl_bin_info(L, w, b2, s, c2);
   }
   if (b1 < 0) {
     // no value in this window passes: the answer is the candidate found one level up
-    if (s.c.fbValid) {
-      const uint64_t K = s.c.fbK;
-      const Fx W = s.c.fbW;
-      const uint32_t tc = s.c.fbTcap;
-      sv_exact_finish(s, K, W, tc);
+    if (c.fbValid) {
+      sv_exact_finish(c, c.fbK, c.fbW, c.fbTcap);
     } else {
-      __syncthreads();
-      if (threadIdx.x == 0) s.c.flags |= kFlagInternal;
-      sv_finalize(s, NAN, kKeyInf);
+      c.flags |= kFlagInternal;
+      sv_finalize(c, NAN, kKeyInf);
     }
     return;
   }
   const uint32_t cand_tcap = c1.mx + 1;
   if (b2 != INT_MAX && level < 3 && c2.cnt >= 2) {
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      s.c.fbValid = 1;
-      s.c.fbK = c1.Kab;
-      s.c.fbW = c1.Wab;
-      s.c.fbTcap = cand_tcap;
-      s.c.stage = level + 1;
-    }
-    __syncthreads();
-    if (level == 1) sv_request(s, H, 2, (uint32_t)b2, 0);
-    else sv_request(s, H, 3, 0, (E << 23) | ((uint32_t)b2 << 11));
+    c.fbValid = 1;
+    c.fbK = c1.Kab;
+    c.fbW = c1.Wab;
+    c.fbTcap = cand_tcap;
+    c.stage = level + 1;
+    if (level == 1) sv_request(c, H, 2, (uint32_t)b2, 0, kNone, 0, fx_zero());
+    else sv_request(c, H, 3, 0, (E << 23) | ((uint32_t)b2 << 11), kNone, c2.Kab, c2.Wab);
     return;
   }
-  sv_exact_finish(s, c1.Kab, c1.Wab, cand_tcap);
+  sv_exact_finish(c, c1.Kab, c1.Wab, cand_tcap);
 }
 
-// First solve after the statistics pass: the level-1 cache, totals and the special cases.
-GS_DI void sv_start(SolveLds& s, const Hists& H, int64_t d) {
+// First solve after the statistics pass: totals and the special cases.
+GS_DI void sv_start(SolveLds& s, RowCtl& c, const Hists& H, int64_t d) {
   const BinInfo i0 = l1_info(H, 0);
   const BinInfo inf = l1_info(H, 255);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    // every finite key lies in binades 0..254; binade 255 counts only Inf/NaN
-    Fx tot = i0.Wab;
-    fx_add(tot, i0.Wb);
-    if (inf.cnt) {
-      tot = fx_sub(tot, inf.Wb);
-      s.c.flags |= GSPAR_FLAG_NONFINITE;
-    }
-    s.c.S = tot;
-    s.c.stage = 1;
+  // every finite key lies in binades 0..254; binade 255 counts only Inf/NaN
+  Fx tot = i0.Wab;
+  fx_add(tot, i0.Wb);
+  if (inf.cnt) {
+    tot = fx_sub(tot, inf.Wb);
+    c.flags |= GSPAR_FLAG_NONFINITE;
   }
-  __syncthreads();
-  const uint64_t nnz = (uint64_t)d - s.c.zeros;
-  if (s.c.flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO)) {
-    sv_finalize(s, NAN, kKeyInf);
+  c.S = tot;
+  c.stage = 1;
+  // zeros = d minus the histogram's population (every nonzero key, finite or not, is binned)
+  c.zeros = (uint64_t)d - (i0.Kab + i0.cnt);
+  const uint64_t nnz = (uint64_t)d - c.zeros;
+  if (c.flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO)) {
+    sv_finalize(c, NAN, kKeyInf);
     return;
   }
   if (nnz == 0) {
-    __syncthreads();
-    if (threadIdx.x == 0) s.c.flags |= GSPAR_FLAG_ALLZERO;
-    __syncthreads();
-    sv_finalize(s, INFINITY, 1);
+    c.flags |= GSPAR_FLAG_ALLZERO;
+    sv_finalize(c, INFINITY, 1);
     return;
   }
-  if (s.c.B >= (double)nnz) {
-    sv_finalize(s, INFINITY, 1);
+  if (c.B >= (double)nnz) {
+    sv_finalize(c, INFINITY, 1);
     return;
   }
-  if (s.c.B == 0.0) {
-    sv_finalize(s, 0.0, kKeyInf);
+  if (c.B == 0.0) {
+    sv_finalize(c, 0.0, kKeyInf);
     return;
   }
-  if (s.c.solver == GSPAR_GREEDY) {
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      s.c.lam = s.c.B / fx_to_double(s.c.S);
-      s.c.iter = 0;
-    }
-    __syncthreads();
-    sv_greedy(s, H);
+  if (c.solver == GSPAR_GREEDY) {
+    c.lam = c.B / fx_to_double(c.S);
+    c.iter = 0;
+    sv_greedy(s, c, H, 0, 0);
   } else {
-    sv_exact(s, H);
+    sv_exact(s, c, H);
   }
 }
 
@@ -941,52 +941,64 @@ GS_DI void reduce_into(const HistT* h, int copies, int nbins, CntT* cnt, uint64_
 
 // The row's solver, run by one workgroup per row after each histogram pass: it either finishes the
 // row (lambda and the capped threshold become final) or requests the next refinement window.
-GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d) {
-  if (threadIdx.x == 0) {
-    s.c = *gc;
-    s.w2ready = 0;
-  }
-  __syncthreads();
-  if (s.c.done) return;
-  // the histograms this solve may read: level 1 always; for the exact solver the level-2 /
-  // level-3 windows if any; for the greedy solver the direct count of the last level-2 pass (its
-  // bins are summed only if a query needs them)
-  reduce_into(H.h1g, kC1, kB1, H.l1->cnt, H.l1->sig, H.l1->mx);
-  if (s.c.solver != GSPAR_GREEDY) {
-    if (s.c.l2exp != kNone) reduce_into(H.h2g, kC23, kB2, H.w2->cnt, H.w2->sig, H.w2->mx);
-    if (s.c.l3base != kNone) reduce_into(H.h3g, kC23, kB3, H.w3->cnt, H.w3->sig, H.w3->mx);
-  } else if (threadIdx.x == 0 && s.c.l2exp != kNone) {
-    uint64_t qc = 0, qs = 0;
+// `first`: the solve right after the statistics pass.
+GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d, bool first) {
+  // The global reads of a solve are issued together, so they share one round trip: level 1
+  // (summed from its copies by the first solve, which also builds the suffix sums and keeps the
+  // table in global memory for the later solves) and the direct count of the last level-2 pass.
+  RowCtl c = *gc;
+  constexpr int n16 = (int)(sizeof(L1Cache) / 16);
+  constexpr int per16 = (n16 + kNT - 1) / kNT;
+  uint4 tab[per16];
+  uint64_t qcnt = 0, qsig = 0;
+  if (first) {
+    reduce_into(H.h1g, kC1, kB1, H.l1->cnt, H.l1->sig, H.l1->mx);
+  } else {
+    if (c.done) return;
+    const uint4* src = reinterpret_cast<const uint4*>(H.l1g);
+#pragma unroll
+    for (int j = 0; j < per16; ++j) {
+      const int i = threadIdx.x + j * kNT;
+      if (i < n16) tab[j] = src[i];
+    }
+#pragma unroll
     for (int k = 0; k < kC23; ++k) {
-      qc += H.h2g[k].qcnt;
-      qs += H.h2g[k].qsig;
+      qcnt += H.wg[k].qcnt;
+      qsig += H.wg[k].qsig;
     }
-    s.qcnt = qc;
-    s.qsig = qs;
   }
-  __syncthreads();
-  if (s.c.stage == 0) {
-    // zeros = d minus the histogram's population (every nonzero key, finite or not, is binned)
-    uint64_t n = threadIdx.x < kB1 ? H.l1->cnt[threadIdx.x] : 0;
-    for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o);
-    if ((threadIdx.x & 63) == 0) s.sk[threadIdx.x >> 6] = n;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint64_t tot = 0;
-      for (int i = 0; i < kNT / 64; ++i) tot += s.sk[i];
-      s.c.zeros = (uint64_t)d - tot;
-      s.c.need = 0;
+  if (c.done) return;
+  if (!first) {
+    uint4* dst = reinterpret_cast<uint4*>(H.l1);
+#pragma unroll
+    for (int j = 0; j < per16; ++j) {
+      const int i = threadIdx.x + j * kNT;
+      if (i < n16) dst[i] = tab[j];
     }
-  } else if (threadIdx.x == 0) {
-    s.c.need = 0;
   }
+  // for the exact solver the level-2 / level-3 window the last pass filled (for the greedy solver
+  // the bins of a level-2 window are read only if a query needs them)
+  if (c.solver != GSPAR_GREEDY) {
+    if (c.stage == 2) reduce_into(H.wg, kC23, kB2, H.w2->cnt, H.w2->sig, H.w2->mx);
+    if (c.stage == 3) reduce_into(H.wg, kC23, kB3, H.w3->cnt, H.w3->sig, H.w3->mx);
+  }
+  c.need = 0;
+  // every load above has returned before any thread can go on to clear the window it read
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  l1_build(s, H);
-  if (s.c.stage == 0) sv_start(s, H, d);
-  else if (s.c.solver == GSPAR_GREEDY) sv_greedy(s, H);
-  else sv_exact(s, H);
-  __syncthreads();
-  if (threadIdx.x == 0) *gc = s.c;
+  if (first) {
+    l1_build(s, H);
+    constexpr int n16 = (int)(sizeof(L1Cache) / 16);
+    const uint4* src = reinterpret_cast<const uint4*>(H.l1);
+    uint4* dst = reinterpret_cast<uint4*>(H.l1g);
+    for (int i = threadIdx.x; i < n16; i += kNT) dst[i] = src[i];
+    sv_start(s, c, H, d);
+  } else if (c.solver == GSPAR_GREEDY) {
+    sv_greedy(s, c, H, qcnt, qsig);
+  } else {
+    sv_exact(s, c, H);
+  }
+  if (threadIdx.x == 0) *gc = c;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1085,21 +1097,16 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   if (need != 2 && need != 3) return;
   uint32_t lo, shift;
   int nbins;
-  uint64_t *gcnt, *gsig;
-  uint32_t* gmx;
   const int cp = (int)(blk % kC23);
+  WinHist* h = win_of(a, row, cp);
   if (need == 2) {
     lo = ctl->l2exp << 23;
     shift = 11;
     nbins = kB2;
-    Hist2* h = h2_of(a, row, cp);
-    gcnt = h->cnt; gsig = h->sig; gmx = h->mx;
   } else {
     lo = ctl->l3base;
     shift = 0;
     nbins = kB3;
-    Hist3* h = h3_of(a, row, cp);
-    gcnt = h->cnt; gsig = h->sig; gmx = h->mx;
   }
   const uint32_t span = (uint32_t)nbins << shift;
   // level 2 also keeps bin minima and counts the window's keys >= qkey directly (qkey lies in the
@@ -1145,13 +1152,18 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
     }
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < nbins; b += kNT) {
+  // flush: workgroups start at different blocks of kNT bins, so they do not queue on the same
+  // addresses at the same time
+  static_assert(kB2 % kNT == 0 && kB3 % kNT == 0, "whole blocks of bins");
+  const int nblk = nbins / kNT;
+  for (int i = 0; i < nblk; ++i) {
+    const int b = ((i + (int)blk) % nblk) * kNT + threadIdx.x;
     const uint64_t p = sm.pk[b];
     if (p) {
-      atomicAdd((unsigned long long*)&gcnt[b], (unsigned long long)(p >> 44));
-      atomicAdd((unsigned long long*)&gsig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
-      atomicMax(&gmx[b], sm.mx[b]);
-      if (l2) atomicMax(&h2_of(a, row, cp)->mnc[b], sm.mnc[b]);
+      atomicAdd((unsigned long long*)&h->cnt[b], (unsigned long long)(p >> 44));
+      atomicAdd((unsigned long long*)&h->sig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
+      atomicMax(&h->mx[b], sm.mx[b]);
+      if (l2) atomicMax(&h->mnc[b], sm.mnc[b]);
     }
   }
   if (l2 && threadIdx.x == 0) {
@@ -1161,7 +1173,6 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
       ts += sm.qs[i];
     }
     if (tc) {
-      Hist2* h = h2_of(a, row, cp);
       atomicAdd((unsigned long long*)&h->qcnt, (unsigned long long)tc);
       atomicAdd((unsigned long long*)&h->qsig, (unsigned long long)ts);
     }
@@ -1172,8 +1183,8 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
 __global__ void __launch_bounds__(kNT) k_solve(Args a) {
   __shared__ SolveLds sm;
   const int64_t row = blockIdx.x;
-  const Hists H{&sm.l1, &sm.w2, &sm.w3, sm.w2mn, h1_of(a, row), h2_of(a, row), h3_of(a, row)};
-  solve_row(sm, ctl_of(a, row), H, a.d);
+  const Hists H{&sm.l1, &sm.w2, &sm.w3, l1t_of(a, row), h1_of(a, row), win_of(a, row)};
+  solve_row(sm, ctl_of(a, row), H, a.d, a.first != 0);
 }
 
 // Sampling, amplification and order-preserving compaction. Workgroup t handles tile t (kTileElems
@@ -1642,6 +1653,7 @@ static int launch_solve(Args& a, hipStream_t s) {
   if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
   else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
   time_after(1, s);
+  a.first = 1;
   time_before(3, s);
   hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
   time_after(3, s);
@@ -1649,6 +1661,7 @@ static int launch_solve(Args& a, hipStream_t s) {
   // exact solver at most a level-2 and a level-3 window
   const int R = a.solver == GSPAR_GREEDY ? a.T : 2;
   for (int r = 0; r < R; ++r) {
+    a.first = 0;
     time_before(4, s);
     if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
     else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
