@@ -179,13 +179,22 @@ GS_HD uint32_t cap_key(double lam) {
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32->64 products on
 // counter words 0 and 2, high halves crossed with words 1, 3 and the round key; the key advances
 // by the golden-ratio and sqrt(3)-1 Weyl increments after each round.
+// a ^ b ^ c (one three-input bitwise instruction on gfx950)
+GS_HD uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+#else
+  return a ^ b ^ c;
+#endif
+}
+
 GS_HD void philox10(uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3, uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     uint64_t m0 = (uint64_t)c0 * 0xD2511F53u;
     uint64_t m1 = (uint64_t)c2 * 0xCD9E8D57u;
-    uint32_t x0 = (uint32_t)(m1 >> 32) ^ c1 ^ k0;
-    uint32_t x2 = (uint32_t)(m0 >> 32) ^ c3 ^ k1;
+    uint32_t x0 = xor3((uint32_t)(m1 >> 32), c1, k0);
+    uint32_t x2 = xor3((uint32_t)(m0 >> 32), c3, k1);
     c1 = (uint32_t)m1;
     c3 = (uint32_t)m0;
     c0 = x0;
@@ -1194,7 +1203,12 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
 // that has not published after a long back-off is counted by the waiting wave itself, so no
 // ordering of workgroup dispatch is assumed and every wait ends.
 constexpr uint64_t kStAgg = 1ull << 62, kStInc = 2ull << 62, kStVal = (1ull << 62) - 1;
-constexpr int kPolls = 4096;
+// Look-back rounds before a waiting wave counts an unpublished predecessor itself (a build may
+// lower it to exercise that path).
+#ifndef GSPAR_LOOKBACK_POLLS
+#define GSPAR_LOOKBACK_POLLS 4096
+#endif
+constexpr int kPolls = GSPAR_LOOKBACK_POLLS;
 constexpr int kWaveElems = kTileElems / (kTileThreads / 64);  // coordinates per wave per tile
 
 struct TileCtx {
@@ -1286,13 +1300,18 @@ __device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double 
   uint32_t x0 = (uint32_t)q, x1 = (uint32_t)((uint64_t)q >> 32), x2 = 0, x3 = 0;
   philox10(x0, x1, x2, x3, k0, k1);
   const uint32_t xr[4] = {x0, x1, x2, x3};
+  double t[4];
   z = 0;
   cz = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const double t = lam32 * (double)fabsf(v[k]);
-    z |= (uint32_t)((double)xr[k] < t) << k;
-    cz |= (uint32_t)(t >= 0x1p32) << k;
+    t[k] = lam32 * (double)fabsf(v[k]);
+    z |= (uint32_t)((double)xr[k] < t[k]) << k;
+  }
+  // capped coordinates are rare: test the group's largest threshold first
+  if (fmax(fmax(t[0], t[1]), fmax(t[2], t[3])) >= 0x1p32) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) cz |= (uint32_t)(t[k] >= 0x1p32) << k;
   }
 }
 
@@ -1429,18 +1448,20 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
       while (true) {
         const int64_t i = look - lane;
         uint64_t sw = kStInc;
-        if (i >= first) {
-          int polls = 0;
-          sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          while ((sw >> 62) == 0 && ++polls < kPolls) {
-            __builtin_amdgcn_s_sleep(4);
-            sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
+        if (i >= first) sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // wait only for the predecessors between this tile and the nearest one whose inclusive
+        // prefix is published (that boundary can only move closer while waiting)
+        uint64_t incl_mask, missing;
+        int stop;
+        for (int polls = 0;; ++polls) {
+          incl_mask = __ballot((sw >> 62) == 2);
+          stop = incl_mask ? (__ffsll((unsigned long long)incl_mask) - 1) : 63;
+          missing = __ballot((sw >> 62) == 0 && lane <= stop);
+          if (!missing || polls == kPolls) break;
+          __builtin_amdgcn_s_sleep(4);
+          if ((sw >> 62) == 0 && lane <= stop) sw = __hip_atomic_load(&st[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        const uint64_t incl_mask = __ballot((sw >> 62) == 2);
-        const int stop = incl_mask ? (__ffsll((unsigned long long)incl_mask) - 1) : 63;
         // predecessors up to `stop` that never published: count them here
-        uint64_t missing = __ballot((sw >> 62) == 0 && lane <= stop);
         while (missing) {
           const int m = __ffsll((unsigned long long)missing) - 1;
           const uint64_t val = wave_tile_aggregate<VEC>(c, (look - m) - first, lane);

@@ -15,7 +15,8 @@ def build(asan: bool = False) -> str:
     if os.path.exists(out) and os.path.getmtime(out) > max(os.path.getmtime(SRC),
                                                          os.path.getmtime(os.path.join(HERE, "hip", "hip_runtime.h"))):
         return out
-    cmd = ["g++", "-std=c++20", "-O1", "-g", "-fPIC", "-shared", "-pthread", "-Wno-attributes",
+    # a short look-back wait keeps the emulated fallback test (every status hidden) quick
+    cmd = ["g++", "-std=c++20", "-O1", "-g", "-fPIC", "-shared", "-pthread", "-Wno-attributes", "-DGSPAR_LOOKBACK_POLLS=64",
            "-Wno-unknown-pragmas", "-I", HERE, "-I", os.path.join(ROOT, "include"), "-x", "c++", SRC,
            "-o", out + ".tmp"]
     if asan:
