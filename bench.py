@@ -13,6 +13,10 @@ largest HBM-bound kernel: algorithmic bytes = 4 B per input element + 8 B per su
 HIP events on its stream over the timed region), the time per step of every kernel class, and the
 oracle timed on a bounded sample on one host core as a CPU baseline.
 
+With --cells (and --workload all for every workload) it prints instead one line per (workload,
+solver, rho): the median time of one call warm and right after a 512 MiB scratch write that evicts
+the last-level cache, elements/s, the algorithmic HBM fraction and the oracle's one-core rate.
+
 Counter runs: with --copy-probe the run first copies a 512 MiB device buffer three times (a plain
 copy kernel of known size), so that two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) can be
 scaled to bytes; `bench.py --summarize-pmc FETCH_DIR WRITE_DIR` turns those two runs into bytes
@@ -38,7 +42,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5", "all"])
     ap.add_argument("--solver", default=None, help="restrict to one solver")
     ap.add_argument("--rho", type=float, default=None, help="restrict to one density")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -46,6 +50,9 @@ def parse():
     ap.add_argument("--copy-probe", action="store_true", help="copy a 512 MiB buffer 3 times first (counter scale)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
                     help="summarise two rocprofv3 --pmc runs of this benchmark into profiles/traffic.json")
+    ap.add_argument("--cells", action="store_true",
+                    help="one JSON line per (workload, solver, rho) cell instead of the step line: median call "
+                         "time warm and after evicting the caches, algorithmic HBM fraction, oracle rate")
     return ap.parse_args()
 
 
@@ -134,28 +141,93 @@ def cpu_baseline(wl, combos, target_s):
     target_s seconds of work; returns elements/s and what the sample was."""
     import oracle
 
-    t0 = time.perf_counter()
-    elems = 0
-    done = []
-    r = 0
-    prefix = min(wl.d, 1 << 24)  # rows longer than 2^24 are sampled by their leading 2^24 entries
-    while True:
-        row = wl.g[r % wl.rows][:prefix]
-        for solver, rho in combos:
-            sol = oracle.solve(row, rho, solver, wl.iters)
-            oracle.sample_compact(row, sol.p, wl.seeds[r % wl.rows])
-            elems += row.size
-        done.append(r % wl.rows)
-        r += 1
-        if time.perf_counter() - t0 >= target_s or r >= 4 * wl.rows:
-            break
-    dt = time.perf_counter() - t0
+    host_cores = len(os.sched_getaffinity(0))
+    keep = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {min(keep)})  # the oracle is single-threaded: time it on one core
+    try:
+        t0 = time.perf_counter()
+        elems = 0
+        r = 0
+        prefix = min(wl.d, 1 << 24)  # rows longer than 2^24 are sampled by their leading 2^24 entries
+        while True:
+            row = wl.g[r % wl.rows][:prefix]
+            for solver, rho in combos:
+                sol = oracle.solve(row, rho, solver, wl.iters)
+                oracle.sample_compact(row, sol.p, wl.seeds[r % wl.rows])
+                elems += row.size
+            r += 1
+            if time.perf_counter() - t0 >= target_s or r >= 4 * wl.rows:
+                break
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, keep)
     return {"value": elems / dt, "unit": "elements/s", "cores": 1, "kind": "oracle",
-            "sample": f"{r} rows of {prefix} of the workload's {wl.d} entries x {len(combos)} (solver, rho) "
-                      f"combos, {dt:.1f} s, fp64 oracle single thread"}
+            "sample": f"{r} row passes over {min(r, wl.rows)} distinct rows, each the leading {prefix} of the "
+                      f"row's {wl.d} entries, x {len(combos)} (solver, rho) combos; {dt:.1f} s of fp64 oracle "
+                      f"work on 1 of the host's {host_cores} cores"}
 
 
 KERNEL_CLASSES = {"k_init": 5, "k_stats": 1, "k_solve": 3, "k_refine": 4, "k_sample": 0}
+
+
+def cells(args):
+    """One JSON line per (workload, solver, rho): the median time of one call over 20 (inputs resident,
+    warm caches) and over 5 calls each made right after writing a 512 MiB scratch buffer (which evicts
+    the 256 MB last-level cache), elements/s for both, the algorithmic HBM fraction
+    (4 B per element + 8 B per survivor over the call time, against 8 TB/s), and the oracle's rate
+    on one host core on a bounded sample of the same rows."""
+    import numpy as np
+    import torch
+
+    import paper_1710_09854_amd as gs
+    import workloads
+
+    assert torch.cuda.is_available(), "needs a GPU"
+    dev = torch.device("cuda:0")
+    names = ["c1", "c2", "c3", "c4", "c5"] if args.workload == "all" else [args.workload]
+    scratch = torch.empty(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+    for name in names:
+        wl = workloads.CONFIGS[name]()
+        g = torch.from_numpy(wl.g).to(dev)
+        rows, d = wl.rows, wl.d
+        seeds = torch.tensor([s - (1 << 64) if s >= (1 << 63) else s for s in wl.seeds], dtype=torch.int64,
+                             device=dev)
+        for solver in ([args.solver] if args.solver else wl.solvers):
+            for rho in ([args.rho] if args.rho is not None else wl.rhos):
+                plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho))
+                rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
+                for _ in range(3):
+                    plan.run(g, rho_dev, seeds)
+                torch.cuda.synchronize()
+                fl = plan.flags.cpu().numpy()
+                assert not fl.any(), f"unexpected flags {fl}"
+
+                def timed(evict):
+                    if evict:
+                        scratch.fill_(0.5)
+                    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    s.record()
+                    plan.run(g, rho_dev, seeds)
+                    e.record()
+                    torch.cuda.synchronize()
+                    return s.elapsed_time(e) * 1e-3
+
+                warm = float(np.median([timed(False) for _ in range(20)]))
+                cold = float(np.median([timed(True) for _ in range(5)]))
+                nnz = int(plan.nnz.sum().item())
+                alg = 4.0 * rows * d + 8.0 * nnz
+                cell = {"workload": wl.name, "solver": solver, "rho": rho, "rows": rows, "d": d, "nnz": nnz,
+                        "lambda_row0": float(plan.lam[0].item()), "k_row0": int(plan.k[0].item()),
+                        "warm_us": warm * 1e6, "warm_elements_per_s": rows * d / warm,
+                        "cold_us": cold * 1e6, "cold_elements_per_s": rows * d / cold,
+                        "algorithmic_bytes": alg, "algorithmic_frac_warm": alg / warm / 1e9 / HBM_PEAK_GBS,
+                        "algorithmic_frac_cold": alg / cold / 1e9 / HBM_PEAK_GBS}
+                if not args.no_cpu_baseline:
+                    cell["cpu_baseline"] = cpu_baseline(wl, [(solver, rho)], args.cpu_seconds)
+                print(json.dumps(cell), flush=True)
+                del plan
+        del g
+        torch.cuda.empty_cache()
 
 
 def main():
@@ -168,6 +240,12 @@ def main():
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); multi-GPU runs are not part of "
               "this build", file=sys.stderr)
+        sys.exit(2)
+    if args.cells:
+        cells(args)
+        return
+    if args.workload == "all":
+        print("--workload all needs --cells", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
@@ -263,6 +341,19 @@ def main():
                      "algorithmic_bytes_per_launch": alg_bytes_per_step / len(plans),
                      "avg_launch_ms": avg_launch_ms, "launches": launches},
     }
+    # the whole path: algorithmic bytes (g read once, the output written once) and, when the counter
+    # summary matches this kernel source, the bytes the kernels actually moved, per step
+    path = {"algorithmic_bytes_per_step": alg_bytes_per_step,
+            "algorithmic_GBps": alg_bytes_per_step / (ms_per_step * 1e-3) / 1e9}
+    path["algorithmic_frac"] = path["algorithmic_GBps"] / HBM_PEAK_GBS
+    if traffic is not None:
+        per_kernel = {k: traffic_for(wl.name, k) for k in KERNEL_CLASSES}
+        if all(v is not None for v in per_kernel.values()):
+            moved = sum(per_kernel[k] * kernels[k]["launches_per_step"] for k in KERNEL_CLASSES)
+            path["measured_bytes_per_step"] = moved
+            path["measured_GBps"] = moved / (ms_per_step * 1e-3) / 1e9
+            path["measured_frac"] = path["measured_GBps"] / HBM_PEAK_GBS
+    line["path"] = path
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, combos, args.cpu_seconds)
     line["kernels"] = kernels
