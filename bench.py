@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--copy-probe", action="store_true", help="copy a 512 MiB buffer 3 times first (counter scale)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
                     help="summarise two rocprofv3 --pmc runs of this benchmark into profiles/traffic.json")
+    ap.add_argument("--hybrid", action="store_true",
+                    help="time the hybrid coding entry point (Q_A / Q_B lists) instead of the compaction")
+    ap.add_argument("--dense-q", action="store_true", help="with --hybrid, also write the dense ternary vector")
     ap.add_argument("--cells", action="store_true",
                     help="one JSON line per (workload, solver, rho) cell instead of the step line: median call "
                          "time warm and after evicting the caches, algorithmic HBM fraction, oracle rate")
@@ -194,7 +197,8 @@ def cells(args):
                              device=dev)
         for solver in ([args.solver] if args.solver else wl.solvers):
             for rho in ([args.rho] if args.rho is not None else wl.rhos):
-                plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho))
+                plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho),
+                               hybrid=args.hybrid, dense_q=args.dense_q)
                 rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
                 for _ in range(3):
                     plan.run(g, rho_dev, seeds)
@@ -214,10 +218,11 @@ def cells(args):
 
                 warm = float(np.median([timed(False) for _ in range(20)]))
                 cold = float(np.median([timed(True) for _ in range(5)]))
-                nnz = int(plan.nnz.sum().item())
-                alg = 4.0 * rows * d + 8.0 * nnz
+                nnz, out_bytes = plan.survivors_and_bytes()
+                alg = 4.0 * rows * d + out_bytes
                 cell = {"workload": wl.name, "solver": solver, "rho": rho, "rows": rows, "d": d, "nnz": nnz,
-                        "lambda_row0": float(plan.lam[0].item()), "k_row0": int(plan.k[0].item()),
+                        "entry": "hybrid" + ("+q" if args.dense_q else "") if args.hybrid else "compact",
+                        "lambda_row0": float(plan.lam[0].item()),
                         "warm_us": warm * 1e6, "warm_elements_per_s": rows * d / warm,
                         "cold_us": cold * 1e6, "cold_elements_per_s": rows * d / cold,
                         "algorithmic_bytes": alg, "algorithmic_frac_warm": alg / warm / 1e9 / HBM_PEAK_GBS,
@@ -264,7 +269,8 @@ def main():
     seeds = torch.tensor([s - (1 << 64) if s >= (1 << 63) else s for s in wl.seeds], dtype=torch.int64, device=dev)
     plans = []
     for solver, rho in combos:
-        plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho))
+        plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho),
+                       hybrid=args.hybrid, dense_q=args.dense_q)
         rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
         plans.append((plan, rho_dev))
 
@@ -297,8 +303,11 @@ def main():
     elapsed = time.perf_counter() - t0
     ksample_ms, launches = timer.read()
     timer.close()
+    out_bytes = 0
     for plan, _ in plans:
-        nnz_tot += int(plan.nnz.sum().item())
+        n, ob = plan.survivors_and_bytes()
+        nnz_tot += n
+        out_bytes += ob
     # time per step of every kernel class (separate short loops, one class bracketed at a time)
     kernels = {}
     reps = min(args.steps, 10)
@@ -313,10 +322,10 @@ def main():
     elements_per_step = rows * d * len(plans)
     ms_per_step = elapsed * 1e3 / args.steps
     value = elements_per_step / (elapsed / args.steps)
-    alg_bytes_per_step = 4.0 * elements_per_step + 8.0 * nnz_tot
+    alg_bytes_per_step = 4.0 * elements_per_step + out_bytes
     avg_launch_ms = ksample_ms / max(launches, 1)
     achieved = alg_bytes_per_step / len(plans) / (avg_launch_ms * 1e-3) / 1e9
-    traffic = traffic_for(wl.name) if (args.solver is None and args.rho is None) else None
+    traffic = traffic_for(wl.name) if (args.solver is None and args.rho is None and not args.hybrid) else None
     line = {
         "metric": METRIC,
         "value": value,
@@ -333,11 +342,15 @@ def main():
         "config": {"workload": wl.name, "rows": rows, "d": d,
                    "solvers": solvers, "rho": rhos, "greedy_iters": wl.iters,
                    "seeds": "per-row Philox keys " + ("1000+r" if args.workload == "c2" else str(wl.seeds[0])),
-                   "parallelism": "single GPU, rows batched in one call"},
+                   "parallelism": "single GPU, rows batched in one call",
+                   "output": ("hybrid coding Q_A (index, value) + Q_B (index | sign)" +
+                              (" + dense ternary vector" if args.dense_q else "")) if args.hybrid
+                   else "ascending (int32 index, fp32 value) pairs"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_sample (Philox sampling, amplification, compaction; the largest "
-                               "HBM-bound kernel, time per class in 'kernels')",
+                     "kernel": "k_sample (Philox sampling, amplification, " +
+                               ("hybrid Q_A / Q_B coding" if args.hybrid else "compaction") +
+                               "; the largest HBM-bound kernel, time per class in 'kernels')",
                      "algorithmic_bytes_per_launch": alg_bytes_per_step / len(plans),
                      "avg_launch_ms": avg_launch_ms, "launches": launches},
     }

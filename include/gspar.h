@@ -115,6 +115,48 @@ int sparsify_sample_compact_batched(const float* g, int64_t rows, int64_t d, int
                                     int64_t cap_per_row, int64_t* nnz, double* lambda, int64_t* k,
                                     uint32_t* flags, void* ws, size_t ws_bytes, void* stream);
 
+/* Hybrid coding of the sparsified gradient (Section 3.3, eqs. 9-10): the same solve and the same
+ * Bernoulli selection as sparsify_sample_compact (identical survivors for identical arguments),
+ * with the survivors split by the capped set S_k = {p_i = 1}:
+ *   Q_A: idx_a[r*cap_a ...] int32 ascending indices and val_a[...] fp32 values g_i of the capped
+ *        survivors (every capped coordinate survives); n_a[r] receives their true count, which is
+ *        also the capped count k;
+ *   Q_B: code_b[r*cap_b ...] int32 words (index | sign << 31), ascending by index, for every other
+ *        survivor, whose value is sign(g_i)/lambda; n_b[r] receives their true count;
+ *   inv_lambda [rows] fp32 (optional): the single float 1/lambda that Q_B's values share
+ *        (0 when lambda is 0 or +inf);
+ *   q [rows*ld] int8 (optional): the dense ternary vector of Section 3.3, 2 on S_k, sign(g_i) for
+ *        the other survivors, 0 elsewhere.
+ * rho [rows] fp64 and seeds [rows] uint64 are DEVICE arrays; lambda and flags are optional
+ * [rows] outputs. GSPAR_FLAG_OVERFLOW is set when n_a > cap_a or n_b > cap_b (the first cap_a /
+ * cap_b entries are written). code_b is required; idx_a and val_a may be NULL when cap_a = 0. */
+int sparsify_sample_hybrid_batched(const float* g, int64_t rows, int64_t d, int64_t ld,
+                                   const double* rho, int solver, int greedy_iters,
+                                   const uint64_t* seeds, int32_t* idx_a, float* val_a,
+                                   int64_t cap_a, int64_t* n_a, int32_t* code_b, int64_t cap_b,
+                                   int64_t* n_b, float* inv_lambda, int8_t* q, double* lambda,
+                                   uint32_t* flags, void* ws, size_t ws_bytes, void* stream);
+
+/* Single-row hybrid coding: rho and seed are host scalars; every array has one row (q has d
+ * entries); n_a and n_b are [1] DEVICE outputs. */
+int sparsify_sample_hybrid(const float* g, int64_t d, double rho, int solver, int greedy_iters,
+                           uint64_t seed, int32_t* idx_a, float* val_a, int64_t cap_a,
+                           int64_t* n_a, int32_t* code_b, int64_t cap_b, int64_t* n_b,
+                           float* inv_lambda, int8_t* q, double* lambda, uint32_t* flags,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/* Coding length in bits of one hybrid message of a d-coordinate gradient with n_a entries in Q_A,
+ * n_b in Q_B of which n_b_neg are negative, for floats of `float_bits` bits (host only, no GPU).
+ *   out[0]: sparse lists, n_a (b + log2 d) + n_b (log2 d + 1) + b (indices, values, signs, 1/lambda);
+ *   out[1]: entropy-coded ternary vector, sum over its four symbols of d_l log2(d / d_l), plus
+ *           n_a b for Q_A's values and b for 1/lambda (Section 3.3);
+ *   out[2]: the experiments' per-message cost (Section 5), n_a (b + log2 d) + min(2d, n_b log2 d)
+ *           + b, with the realised n_b in place of the expected sum of p over the uncapped set.
+ * Returns GSPAR_ERR_ARG for out = NULL, d < 1, negative counts, n_a + n_b > d, n_b_neg > n_b or
+ * float_bits < 1. */
+int gspar_coding_bits(int64_t d, int64_t n_a, int64_t n_b, int64_t n_b_neg, int float_bits,
+                      double* out);
+
 /* Human-readable name of a status code (static storage). */
 const char* gspar_status_string(int status);
 

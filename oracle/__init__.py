@@ -19,6 +19,11 @@ Functions and the passage each follows:
 * ``solve_greedy_scale``  -- Algorithm 3 rewritten through lambda (cross-check).
 * ``sample_compact``      -- Section 3's protocol: Z_i ~ Bernoulli(p_i), Q(g)_i = Z_i g_i / p_i,
   survivors in ascending index order.
+* ``sample_hybrid``       -- Section 3.3, eqs. (9)-(10): the survivors split into Q_A (the capped set
+  S_k, stored as index and value) and Q_B (index and sign; value sign(g_i)/lambda), plus the dense
+  ternary vector of the same section.
+* ``coding_bits``         -- coding lengths of one hybrid message: the sparse lists, the entropy-coded
+  ternary vector (Section 3.3), and the experiments' per-message formula (Section 5).
 """
 from __future__ import annotations
 
@@ -189,3 +194,47 @@ def sparsify(g, rho: float, solver: str = "greedy", iters: int = 2, seed: int = 
         return sol, np.zeros(0, np.int32), np.zeros(0, np.float32), 0
     idx, val, n = sample_compact(g, sol.p, seed)
     return sol, idx, val, n
+
+
+@dataclass
+class HybridMessage:
+    qa_idx: np.ndarray   # int32, ascending: the capped survivors (every i with p_i = 1 survives)
+    qa_val: np.ndarray   # float32 g_i (= g_i / p_i since p_i = 1)
+    qb_idx: np.ndarray   # int32, ascending: the other survivors
+    qb_neg: np.ndarray   # bool, g_i < 0 for each entry of qb_idx (Q_B's value is sign(g_i) / lambda)
+    q: np.ndarray        # int8 [d]: 2 on S_k, sign(g_i) on the other survivors, 0 elsewhere
+
+
+def sample_hybrid(g, p, seed: int) -> HybridMessage:
+    """Section 3.3, eqs. (9)-(10). The survivors are those of ``sample_compact`` (same generator, same
+    test Z_i = [x_i < p_i 2^32]); a survivor belongs to Q_A when p_i = 1 (the capped set S_k), to Q_B
+    otherwise. The dense vector q takes 2 on S_k and lambda Q(g_i) = sign(g_i) on Q_B's entries."""
+    g = _f32(g)
+    p = np.ascontiguousarray(p, dtype=np.float64)
+    idx, _, n = sample_compact(g, p, seed)
+    assert idx.size == n
+    capped = p[idx] == 1.0
+    qa_idx = idx[capped]
+    qb_idx = idx[~capped]
+    q = np.zeros(g.size, np.int8)
+    q[qa_idx] = 2
+    q[qb_idx] = np.where(g[qb_idx] < 0, -1, 1).astype(np.int8)
+    return HybridMessage(qa_idx, g[qa_idx].copy(), qb_idx, g[qb_idx] < 0, q)
+
+
+def coding_bits(d: int, n_a: int, n_b: int, n_b_neg: int, float_bits: int = 32):
+    """Bits of one hybrid message of a d-coordinate gradient (Section 3.3; Theorem 4's accounting):
+    (1) the sparse lists: each Q_A entry an index (log2 d bits) and a float, each Q_B entry an index
+        and a sign bit, plus the single float 1/lambda;
+    (2) the ternary vector with entropy coding, sum over its symbols l of d_l log2(d / d_l), plus a
+        float per Q_A entry and the float 1/lambda;
+    (3) the experiments' per-message cost, n_a (b + log2 d) + min(2d, n_b log2 d) + b, with the
+        realised |Q_B| standing in for the expected sum of p over the uncapped set."""
+    b = float(float_bits)
+    L = np.log2(float(d))
+    sparse = n_a * (b + L) + n_b * (L + 1.0) + b
+    counts = [n_a, n_b_neg, n_b - n_b_neg, d - n_a - n_b]
+    ent = sum(c * np.log2(d / c) for c in counts if c > 0)
+    ternary = ent + n_a * b + b
+    paper = n_a * (b + L) + min(2.0 * d, n_b * L) + b
+    return float(sparse), float(ternary), float(paper)

@@ -11,6 +11,9 @@ Entry points mirror the C ABI:
 * ``sparsify_sample_compact(g, rho, seed, solver, iters)``   -> Sparse(idx, val, nnz, lam, k, flags)
 * ``sparsify_probs_batched(g2d, rho, solver, iters)``
 * ``sparsify_sample_compact_batched(g2d, rho, seeds, ...)``
+* ``sparsify_sample_hybrid(g, rho, seed, ...)`` / ``sparsify_sample_hybrid_batched(g2d, rho, seeds, ...)``
+  -> Hybrid(idx_a, val_a, n_a, code_b, n_b, inv_lam, q, lam, flags): the Q_A / Q_B coding
+* ``coding_bits(d, n_a, n_b, n_b_neg, float_bits)`` -> (sparse lists, ternary entropy, paper formula)
 * ``Plan``: a preallocated batched sample/compact call for timing loops.
 """
 from __future__ import annotations
@@ -65,6 +68,14 @@ def lib():
     L.sparsify_sample_compact_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp, vp,
                                                   vp, vp, vp, ctypes.c_size_t, vp]
     L.sparsify_sample_compact_batched.restype = i32
+    L.sparsify_sample_hybrid_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp, vp, i64,
+                                                 vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_hybrid_batched.restype = i32
+    L.sparsify_sample_hybrid.argtypes = [vp, i64, f64, i32, i32, u64, vp, vp, i64, vp, vp, i64, vp, vp, vp, vp, vp,
+                                         vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_hybrid.restype = i32
+    L.gspar_coding_bits.argtypes = [i64, i64, i64, i64, i32, ctypes.POINTER(f64)]
+    L.gspar_coding_bits.restype = i32
     L.gspar_status_string.argtypes = [i32]
     L.gspar_status_string.restype = ctypes.c_char_p
     L.gspar_version.argtypes = []
@@ -214,6 +225,92 @@ def sparsify_sample_compact(g, rho: float, seed: int = 0, solver="greedy", iters
     return Sparse(idx[:cap], val[:cap], nnz, lam, k, fl)
 
 
+@dataclass
+class Hybrid:
+    """Section 3.3's coding: Q_A = (idx_a, val_a) for the capped survivors (n_a of them), Q_B =
+    code_b words (index | sign << 31) for the others (n_b), whose value is sign / lambda; inv_lam
+    is the fp32 1/lambda they share; q the optional dense ternary vector (2, +-1 or 0)."""
+    idx_a: torch.Tensor
+    val_a: torch.Tensor
+    n_a: torch.Tensor
+    code_b: torch.Tensor
+    n_b: torch.Tensor
+    inv_lam: torch.Tensor
+    q: torch.Tensor | None
+    lam: torch.Tensor
+    flags: torch.Tensor
+
+
+def sparsify_sample_hybrid(g, rho: float, seed: int = 0, solver="greedy", iters: int = 2,
+                           cap_a: int | None = None, cap_b: int | None = None, dense_q: bool = False,
+                           workspace=None, stream=None) -> Hybrid:
+    g = _as_row(g)
+    d = g.numel()
+    dev = g.device
+    cap_b = capacity_hint(d, rho) if cap_b is None else int(cap_b)
+    cap_a = cap_b if cap_a is None else int(cap_a)
+    idx_a = torch.empty(max(cap_a, 1), dtype=torch.int32, device=dev)
+    val_a = torch.empty(max(cap_a, 1), dtype=torch.float32, device=dev)
+    code_b = torch.empty(max(cap_b, 1), dtype=torch.int32, device=dev)
+    n_a = torch.empty(1, dtype=torch.int64, device=dev)
+    n_b = torch.empty(1, dtype=torch.int64, device=dev)
+    inv = torch.empty(1, dtype=torch.float32, device=dev)
+    q = torch.empty(d, dtype=torch.int8, device=dev) if dense_q else None
+    lam = torch.empty(1, dtype=torch.float64, device=dev)
+    fl = torch.empty(1, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid))
+    rc = lib().sparsify_sample_hybrid(g.data_ptr(), d, float(rho), sid, int(iters), int(seed) & 0xFFFFFFFFFFFFFFFF,
+                                      idx_a.data_ptr(), val_a.data_ptr(), cap_a, n_a.data_ptr(), code_b.data_ptr(),
+                                      cap_b, n_b.data_ptr(), inv.data_ptr(), _ptr(q), lam.data_ptr(), fl.data_ptr(),
+                                      buf.data_ptr(), nb, _stream(stream))
+    _check(rc, "sparsify_sample_hybrid")
+    return Hybrid(idx_a[:cap_a], val_a[:cap_a], n_a, code_b[:cap_b], n_b, inv, q, lam, fl)
+
+
+def sparsify_sample_hybrid_batched(g, rho, seeds, solver="greedy", iters: int = 2, cap_a: int | None = None,
+                                   cap_b: int | None = None, dense_q: bool = False, workspace=None,
+                                   stream=None) -> Hybrid:
+    g = _as_rows(g)
+    rows, d = g.shape
+    ld = _leading_dim(g)
+    dev = g.device
+    r = _rho_dev(rho, rows, dev)
+    s = _seeds_dev(seeds, rows, dev)
+    if cap_b is None:
+        rmax = float(r.max().item()) if rows else 0.0
+        cap_b = capacity_hint(d, min(max(rmax, 0.0), 1.0))
+    cap_b = int(cap_b)
+    cap_a = cap_b if cap_a is None else int(cap_a)
+    idx_a = torch.empty((rows, max(cap_a, 1)), dtype=torch.int32, device=dev)
+    val_a = torch.empty((rows, max(cap_a, 1)), dtype=torch.float32, device=dev)
+    code_b = torch.empty((rows, max(cap_b, 1)), dtype=torch.int32, device=dev)
+    n_a = torch.empty(rows, dtype=torch.int64, device=dev)
+    n_b = torch.empty(rows, dtype=torch.int64, device=dev)
+    inv = torch.empty(rows, dtype=torch.float32, device=dev)
+    q = torch.empty((rows, ld), dtype=torch.int8, device=dev) if dense_q else None
+    lam = torch.empty(rows, dtype=torch.float64, device=dev)
+    fl = torch.empty(rows, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid))
+    rc = lib().sparsify_sample_hybrid_batched(g.data_ptr(), rows, d, ld, r.data_ptr(), sid, int(iters), s.data_ptr(),
+                                              idx_a.data_ptr(), val_a.data_ptr(), cap_a, n_a.data_ptr(),
+                                              code_b.data_ptr(), cap_b, n_b.data_ptr(), inv.data_ptr(), _ptr(q),
+                                              lam.data_ptr(), fl.data_ptr(), buf.data_ptr(), nb, _stream(stream))
+    _check(rc, "sparsify_sample_hybrid_batched")
+    return Hybrid(idx_a[:, :cap_a], val_a[:, :cap_a], n_a, code_b[:, :cap_b], n_b, inv,
+                  None if q is None else q[:, :d], lam, fl)
+
+
+def coding_bits(d: int, n_a: int, n_b: int, n_b_neg: int, float_bits: int = 32):
+    """(sparse lists, entropy-coded ternary vector, the experiments' formula) in bits for one hybrid
+    message; see gspar_coding_bits in include/gspar.h."""
+    out = (ctypes.c_double * 3)()
+    rc = lib().gspar_coding_bits(int(d), int(n_a), int(n_b), int(n_b_neg), int(float_bits), out)
+    _check(rc, "gspar_coding_bits")
+    return out[0], out[1], out[2]
+
+
 def _rho_dev(rho, rows, dev):
     if isinstance(rho, torch.Tensor):
         r = rho.to(device=dev, dtype=torch.float64).contiguous()
@@ -263,13 +360,16 @@ class Plan:
     so a timing loop measures only the library's kernels."""
 
     def __init__(self, rows: int, d: int, ld: int | None = None, solver="greedy", iters: int = 2,
-                 cap_per_row: int | None = None, rho_for_cap: float = 1.0, device="cuda"):
+                 cap_per_row: int | None = None, rho_for_cap: float = 1.0, device="cuda", hybrid: bool = False,
+                 dense_q: bool = False):
         self.rows, self.d = rows, d
         self.ld = d if ld is None else ld
         self.sid = _solver_id(solver)
         self.iters = int(iters)
         self.cap = capacity_hint(d, rho_for_cap) if cap_per_row is None else int(cap_per_row)
+        self.hybrid = bool(hybrid)
         dev = torch.device(device)
+        # compaction: (idx, val) per survivor; hybrid coding: Q_A in (idx, val), Q_B in code_b
         self.idx = torch.empty((rows, max(self.cap, 1)), dtype=torch.int32, device=dev)
         self.val = torch.empty((rows, max(self.cap, 1)), dtype=torch.float32, device=dev)
         self.nnz = torch.empty(rows, dtype=torch.int64, device=dev)
@@ -277,14 +377,36 @@ class Plan:
         self.k = torch.empty(rows, dtype=torch.int64, device=dev)
         self.flags = torch.empty(rows, dtype=torch.int32, device=dev)
         self.ws = torch.empty(workspace_bytes(rows, d, self.sid), dtype=torch.uint8, device=dev)
+        if self.hybrid:
+            self.code_b = torch.empty((rows, max(self.cap, 1)), dtype=torch.int32, device=dev)
+            self.nnz_b = torch.empty(rows, dtype=torch.int64, device=dev)
+            self.inv = torch.empty(rows, dtype=torch.float32, device=dev)
+            self.q = torch.empty((rows, self.ld), dtype=torch.int8, device=dev) if dense_q else None
 
     def run(self, g, rho_dev, seeds_dev, stream=None):
+        if self.hybrid:
+            rc = lib().sparsify_sample_hybrid_batched(
+                g.data_ptr(), self.rows, self.d, self.ld, rho_dev.data_ptr(), self.sid, self.iters,
+                seeds_dev.data_ptr(), self.idx.data_ptr(), self.val.data_ptr(), self.cap, self.nnz.data_ptr(),
+                self.code_b.data_ptr(), self.cap, self.nnz_b.data_ptr(), self.inv.data_ptr(), _ptr(self.q),
+                self.lam.data_ptr(), self.flags.data_ptr(), self.ws.data_ptr(), self.ws.numel(), _stream(stream))
+            _check(rc, "sparsify_sample_hybrid_batched")
+            return
         rc = lib().sparsify_sample_compact_batched(
             g.data_ptr(), self.rows, self.d, self.ld, rho_dev.data_ptr(), self.sid, self.iters,
             seeds_dev.data_ptr(), self.idx.data_ptr(), self.val.data_ptr(), self.cap, self.nnz.data_ptr(),
             self.lam.data_ptr(), self.k.data_ptr(), self.flags.data_ptr(), self.ws.data_ptr(),
             self.ws.numel(), _stream(stream))
         _check(rc, "sparsify_sample_compact_batched")
+
+    def survivors_and_bytes(self):
+        """(survivors, output bytes) of the last run, summed over rows (host sync)."""
+        if self.hybrid:
+            na, nb = int(self.nnz.sum().item()), int(self.nnz_b.sum().item())
+            qb = self.rows * self.d if self.q is not None else 0
+            return na + nb, 8 * na + 4 * nb + qb
+        n = int(self.nnz.sum().item())
+        return n, 8 * n
 
 
 def sparsify_sample_compact_batched(g, rho, seeds, solver="greedy", iters: int = 2,

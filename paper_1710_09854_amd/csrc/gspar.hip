@@ -26,6 +26,7 @@
 #include <hip/hip_runtime.h>
 
 #include <climits>
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -308,10 +309,15 @@ struct Args {
   int nb;          // workgroups per row of the histogram passes
   int64_t chunk;   // elements per histogram workgroup (multiple of 4)
   int first;       // k_solve: the solve right after the statistics pass
-  int32_t* idx;
+  int32_t* idx;    // compaction: every survivor; hybrid coding: Q_A, the capped survivors
   float* val;
   int64_t cap;
   int64_t* nnz;
+  int32_t* code_b;  // hybrid coding: Q_B, index | sign << 31 of every other survivor
+  int64_t cap_b;
+  int64_t* nnz_b;
+  float* inv_out;   // hybrid coding: fp32 1/lambda per row
+  int8_t* q;        // hybrid coding: optional dense ternary vector, leading dimension ld
   double* lam_out;
   int64_t* k_out;
   uint32_t* flags_out;
@@ -1334,7 +1340,7 @@ __device__ __forceinline__ uint32_t wave_prefix_bits(uint32_t x, uint32_t& total
   return pre;
 }
 
-template <bool VEC>
+template <bool VEC, bool HYB>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   __shared__ float s_capv[kTileThreads / 64][kCapList];
   __shared__ alignas(16) uint8_t s_code[kTileElems / 4];  // per group: selection | sign << 4
@@ -1424,9 +1430,12 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     s_wcl[wv] = ncl;
   }
   __syncthreads();
-  uint32_t tsel = 0, tcp = 0, wbase = 0;
+  uint32_t tsel = 0, tcp = 0, wbase = 0, wbase_cap = 0;
   for (int i = 0; i < kTileThreads / 64; ++i) {
-    if (i < wv) wbase += s_wsel[i];
+    if (i < wv) {
+      wbase += s_wsel[i];
+      wbase_cap += s_wcap[i];
+    }
     tsel += s_wsel[i];
     tcp += s_wcap[i];
   }
@@ -1485,64 +1494,143 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
 
   // phase 2: thread tid owns tile groups [16 tid, 16 tid + 16) (bit b of its masks is tile
   // coordinate 64 tid + b)
+  const int64_t e0 = part * (int64_t)kTileElems + 64 * tid;
+  uint64_t sm = 0, nm = 0, cm = 0;  // selected, negative, capped-and-selected coordinates
+  uint32_t cr = 0;                  // rank of this thread's first capped survivor in its wave's list
   if (s_wsel[wv]) {
     const uint4 cw = *reinterpret_cast<const uint4*>(&s_code[16 * tid]);
     const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
-    uint64_t sm = 0, nm = 0;
 #pragma unroll
     for (int b = 0; b < 16; ++b) {
       const uint64_t byte = (words[b >> 2] >> (8 * (b & 3))) & 0xFF;
       sm |= (byte & 0xF) << (4 * b);
       nm |= (byte >> 4) << (4 * b);
     }
-    uint32_t wtot;
-    uint64_t pos = (excl & 0x7FFFFFFFull) + wbase + wave_prefix_bits<7>((uint32_t)__popcll(sm), wtot);
-    int32_t* __restrict__ oi = a.idx + row * a.cap;
-    float* __restrict__ ov = a.val + row * a.cap;
-    const int64_t e0 = part * (int64_t)kTileElems + 64 * tid;
-    auto emit = [&](auto from_lds) {
-      // capped survivors: their bits, and the rank of this thread's first one in the wave's list
-      uint64_t cm = 0;
-      uint32_t cr = 0;
-      if (s_wcap[wv]) {
-        const uint4 bw = *reinterpret_cast<const uint4*>(&s_capb[16 * tid]);
-        const uint32_t cwd[4] = {bw.x, bw.y, bw.z, bw.w};
+    if (s_wcap[wv]) {
+      const uint4 bw = *reinterpret_cast<const uint4*>(&s_capb[16 * tid]);
+      const uint32_t cwd[4] = {bw.x, bw.y, bw.z, bw.w};
 #pragma unroll
-        for (int b = 0; b < 16; ++b) cm |= (uint64_t)((cwd[b >> 2] >> (8 * (b & 3))) & 0xF) << (4 * b);
-        uint32_t ctot;
-        cr = wave_prefix_bits<7>((uint32_t)__popcll(cm), ctot);
+      for (int b = 0; b < 16; ++b) cm |= (uint64_t)((cwd[b >> 2] >> (8 * (b & 3))) & 0xF) << (4 * b);
+      uint32_t ctot;
+      cr = wave_prefix_bits<7>((uint32_t)__popcll(cm), ctot);
+    }
+    const bool lds_values = s_wcl[wv] <= (uint32_t)kCapList;
+    if constexpr (!HYB) {
+      uint32_t wtot;
+      uint64_t pos = (excl & 0x7FFFFFFFull) + wbase + wave_prefix_bits<7>((uint32_t)__popcll(sm), wtot);
+      int32_t* __restrict__ oi = a.idx + row * a.cap;
+      float* __restrict__ ov = a.val + row * a.cap;
+      auto emit = [&](auto from_lds) {
+        uint32_t r = cr;
+        uint64_t m = sm;
+        while (m) {
+          const int b = __ffsll((unsigned long long)m) - 1;
+          const uint64_t bit = 1ull << b;
+          float val = (nm & bit) ? -inv : inv;
+          if (cm & bit) {
+            if constexpr (decltype(from_lds)::value) val = s_capv[wv][r];
+            else val = c.row[e0 + b];
+            ++r;
+          }
+          if ((int64_t)pos < a.cap) {
+            oi[pos] = (int32_t)(e0 + b);
+            ov[pos] = val;
+          }
+          ++pos;
+          m &= m - 1;
+        }
+      };
+      if (lds_values) emit(std::true_type{});
+      else emit(std::false_type{});
+    } else {
+      // hybrid coding (Section 3.3, eqs. 9-10): capped survivors go to Q_A as (index, g_i), the
+      // others to Q_B as index | sign << 31 (their value is sign(g_i) / lambda)
+      const uint64_t bm = sm & ~cm;
+      uint32_t btot;
+      const uint64_t excl_cap = (excl >> 31) & 0x7FFFFFFFull;
+      uint64_t pa = excl_cap + wbase_cap + cr;
+      uint64_t pb = (excl & 0x7FFFFFFFull) - excl_cap + (wbase - wbase_cap) +
+                    wave_prefix_bits<7>((uint32_t)__popcll(bm), btot);
+      int32_t* __restrict__ oa = a.idx + row * a.cap;
+      float* __restrict__ va = a.val + row * a.cap;
+      int32_t* __restrict__ ob = a.code_b + row * a.cap_b;
+      auto emit_a = [&](auto from_lds) {
+        uint32_t r = cr;
+        uint64_t m = cm;
+        while (m) {
+          const int b = __ffsll((unsigned long long)m) - 1;
+          float val;
+          if constexpr (decltype(from_lds)::value) val = s_capv[wv][r];
+          else val = c.row[e0 + b];
+          ++r;
+          if ((int64_t)pa < a.cap) {
+            oa[pa] = (int32_t)(e0 + b);
+            va[pa] = val;
+          }
+          ++pa;
+          m &= m - 1;
+        }
+      };
+      if (cm) {
+        if (lds_values) emit_a(std::true_type{});
+        else emit_a(std::false_type{});
       }
-      uint64_t m = sm;
+      uint64_t m = bm;
       while (m) {
         const int b = __ffsll((unsigned long long)m) - 1;
-        const uint64_t bit = 1ull << b;
-        float val = (nm & bit) ? -inv : inv;
-        if (cm & bit) {
-          if constexpr (decltype(from_lds)::value) val = s_capv[wv][cr];
-          else val = c.row[e0 + b];
-          ++cr;
-        }
-        if ((int64_t)pos < a.cap) {
-          oi[pos] = (int32_t)(e0 + b);
-          ov[pos] = val;
-        }
-        ++pos;
+        if ((int64_t)pb < a.cap_b) ob[pb] = (int32_t)((uint32_t)(e0 + b) | (uint32_t)(((nm >> b) & 1) << 31));
+        ++pb;
         m &= m - 1;
       }
-    };
-    if (s_wcl[wv] <= (uint32_t)kCapList) emit(std::true_type{});
-    else emit(std::false_type{});
+    }
+  }
+  if constexpr (HYB) {
+    // dense ternary vector (Section 3.3): 2 on the capped set, sign(g_i) for the other
+    // survivors, 0 elsewhere; this thread's 64 coordinates
+    if (a.q && e0 < a.d) {
+      int8_t* __restrict__ qr = a.q + row * a.ld + e0;
+      uint32_t w[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        uint32_t x = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int b = 4 * j + k;
+          const uint32_t code = ((cm >> b) & 1) ? 2u : (((sm >> b) & 1) ? (((nm >> b) & 1) ? 0xFFu : 1u) : 0u);
+          x |= code << (8 * k);
+        }
+        w[j] = x;
+      }
+      if (e0 + 64 <= a.d && ((uintptr_t)qr & 15) == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint4 v;
+          v.x = w[4 * j]; v.y = w[4 * j + 1]; v.z = w[4 * j + 2]; v.w = w[4 * j + 3];
+          reinterpret_cast<uint4*>(qr)[j] = v;
+        }
+      } else {
+        const int64_t nb = min((int64_t)64, a.d - e0);
+        for (int64_t b = 0; b < nb; ++b) qr[b] = (int8_t)((w[b >> 2] >> (8 * (b & 3))) & 0xFF);
+      }
+    }
   }
   if (part == a.lay.tiles - 1 && tid == 0) {
     const uint64_t incl = excl + agg;
     const int64_t n = (int64_t)(incl & 0x7FFFFFFFull);
     const int64_t kc = (int64_t)((incl >> 31) & 0x7FFFFFFFull);
-    if (a.nnz) a.nnz[row] = n;
-    if (a.k_out) a.k_out[row] = kc;
-    if (a.lam_out) a.lam_out[row] = ctl->lam;
     uint32_t fl = ctl->flags;
     if (!ctl->done) fl |= kFlagInternal;
-    if (n > a.cap) fl |= GSPAR_FLAG_OVERFLOW;
+    if constexpr (!HYB) {
+      if (a.nnz) a.nnz[row] = n;
+      if (n > a.cap) fl |= GSPAR_FLAG_OVERFLOW;
+    } else {
+      a.nnz[row] = kc;
+      a.nnz_b[row] = n - kc;
+      if (a.inv_out) a.inv_out[row] = inv;
+      if (kc > a.cap || n - kc > a.cap_b) fl |= GSPAR_FLAG_OVERFLOW;
+    }
+    if (a.k_out) a.k_out[row] = kc;
+    if (a.lam_out) a.lam_out[row] = ctl->lam;
     if (a.flags_out) a.flags_out[row] = fl;
   }
 }
@@ -1701,8 +1789,13 @@ static int run_sample(Args& a, hipStream_t s) {
   const bool vec = vec_ok(a);
   const dim3 grid((unsigned)(a.rows * a.lay.tiles));
   time_before(0, s);
-  if (vec) hipLaunchKernelGGL(k_sample<true>, grid, dim3(kTileThreads), 0, s, a);
-  else hipLaunchKernelGGL(k_sample<false>, grid, dim3(kTileThreads), 0, s, a);
+  if (a.code_b) {
+    if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, true>), grid, dim3(kTileThreads), 0, s, a);
+    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, true>), grid, dim3(kTileThreads), 0, s, a);
+  } else {
+    if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, false>), grid, dim3(kTileThreads), 0, s, a);
+    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, false>), grid, dim3(kTileThreads), 0, s, a);
+  }
   time_after(0, s);
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
@@ -1785,6 +1878,76 @@ int sparsify_sample_compact(const float* g, int64_t d, double rho, int solver, i
   a.k_out = k;
   a.flags_out = flags;
   return run_sample(a, (hipStream_t)stream);
+}
+
+int sparsify_sample_hybrid_batched(const float* g, int64_t rows, int64_t d, int64_t ld, const double* rho,
+                                   int solver, int greedy_iters, const uint64_t* seeds, int32_t* idx_a, float* val_a,
+                                   int64_t cap_a, int64_t* n_a, int32_t* code_b, int64_t cap_b, int64_t* n_b,
+                                   float* inv_lambda, int8_t* q, double* lambda, uint32_t* flags, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  if (!rho || !seeds || !n_a || !n_b || cap_a < 0 || cap_b < 0 || (cap_a > 0 && (!idx_a || !val_a)) ||
+      !code_b)
+    return GSPAR_ERR_ARG;
+  int rc = check_common(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws);
+  a.rho_dev = rho;
+  a.seed_dev = seeds;
+  a.idx = idx_a;
+  a.val = val_a;
+  a.cap = cap_a;
+  a.nnz = n_a;
+  a.code_b = code_b;
+  a.cap_b = cap_b;
+  a.nnz_b = n_b;
+  a.inv_out = inv_lambda;
+  a.q = q;
+  a.lam_out = lambda;
+  a.flags_out = flags;
+  return run_sample(a, (hipStream_t)stream);
+}
+
+int sparsify_sample_hybrid(const float* g, int64_t d, double rho, int solver, int greedy_iters, uint64_t seed,
+                           int32_t* idx_a, float* val_a, int64_t cap_a, int64_t* n_a, int32_t* code_b, int64_t cap_b,
+                           int64_t* n_b, float* inv_lambda, int8_t* q, double* lambda, uint32_t* flags, void* ws,
+                           size_t ws_bytes, void* stream) {
+  if (!n_a || !n_b || cap_a < 0 || cap_b < 0 || (cap_a > 0 && (!idx_a || !val_a)) || !code_b || !rho_ok(rho))
+    return GSPAR_ERR_ARG;
+  int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws);
+  a.rho = rho;
+  a.seed = seed;
+  a.idx = idx_a;
+  a.val = val_a;
+  a.cap = cap_a;
+  a.nnz = n_a;
+  a.code_b = code_b;
+  a.cap_b = cap_b;
+  a.nnz_b = n_b;
+  a.inv_out = inv_lambda;
+  a.q = q;
+  a.lam_out = lambda;
+  a.flags_out = flags;
+  return run_sample(a, (hipStream_t)stream);
+}
+
+int gspar_coding_bits(int64_t d, int64_t n_a, int64_t n_b, int64_t n_b_neg, int float_bits, double* out) {
+  if (!out || d < 1 || n_a < 0 || n_b < 0 || n_b_neg < 0 || n_b_neg > n_b || n_a > d || n_b > d - n_a ||
+      float_bits < 1)
+    return GSPAR_ERR_ARG;
+  const double L = std::log2((double)d), b = (double)float_bits;
+  // Q_A: index and value per entry; Q_B: index and sign per entry; one float for 1/lambda
+  out[0] = (double)n_a * (b + L) + (double)n_b * (L + 1.0) + b;
+  // entropy-coded ternary vector (symbols 2, -1, +1, 0) plus the values of Q_A and 1/lambda
+  const double counts[4] = {(double)n_a, (double)n_b_neg, (double)(n_b - n_b_neg), (double)(d - n_a - n_b)};
+  double h = 0.0;
+  for (double c : counts)
+    if (c > 0.0) h += c * std::log2((double)d / c);
+  out[1] = h + (double)n_a * b + b;
+  // the experiments' per-message cost, with the realised |Q_B| for the expected sum of p over it
+  out[2] = (double)n_a * (b + L) + std::min(2.0 * (double)d, (double)n_b * L) + b;
+  return GSPAR_OK;
 }
 
 int sparsify_probs_batched(const float* g, int64_t rows, int64_t d, int64_t ld, const double* rho, int solver,

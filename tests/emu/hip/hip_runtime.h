@@ -279,3 +279,4 @@ void launch(K kernel, dim3 grid, dim3 block, A... args) {
 }  // namespace emu
 
 #define hipLaunchKernelGGL(kernel, grid, block, shmem, stream, ...) emu::launch(kernel, grid, block, __VA_ARGS__)
+#define HIP_KERNEL_NAME(...) __VA_ARGS__

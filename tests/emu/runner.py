@@ -26,6 +26,8 @@ def load(path):
     L.sparsify_probs.argtypes = [vp, i64, f64, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     L.sparsify_sample_compact_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp, vp,
                                                   vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_hybrid_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp, vp, i64,
+                                                 vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     return L
 
 
@@ -129,6 +131,70 @@ def batched(L, g2, rhos, seeds, solver, iters=2, cap=None, ld=None):
                                            k.ctypes.data, fl.ctypes.data, ws.ctypes.data, wsb, None)
     assert rc == 0, rc
     return idx, val, nnz, lam, k, fl
+
+
+def hybrid_batched(L, g2, rhos, seeds, solver, iters=2, cap=None, ld=None):
+    """The hybrid-coding entry point on host buffers: (idx_a, val_a, n_a, code_b, n_b, inv, q, lam, flags)."""
+    rows, d = g2.shape
+    ld = d if ld is None else ld
+    buf = np.zeros((rows, ld), np.float32)
+    buf[:, :d] = g2
+    cap = d if cap is None else cap
+    idx_a = np.zeros((rows, max(cap, 1)), np.int32)
+    val_a = np.zeros((rows, max(cap, 1)), np.float32)
+    code_b = np.zeros((rows, max(cap, 1)), np.int32)
+    n_a = np.zeros(rows, np.int64)
+    n_b = np.zeros(rows, np.int64)
+    inv = np.zeros(rows, np.float32)
+    q = np.full((rows, ld), 77, np.int8)
+    lam = np.zeros(rows)
+    fl = np.zeros(rows, np.uint32)
+    r = np.ascontiguousarray(rhos, np.float64)
+    s = np.array([int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds], np.uint64)
+    sid = 0 if solver == "greedy" else 1
+    wsb = L.gspar_workspace_bytes(rows, d, sid)
+    keep, ws = _aligned(wsb)
+    rc = L.sparsify_sample_hybrid_batched(buf.ctypes.data, rows, d, ld, r.ctypes.data, sid, iters, s.ctypes.data,
+                                          idx_a.ctypes.data, val_a.ctypes.data, cap, n_a.ctypes.data,
+                                          code_b.ctypes.data, cap, n_b.ctypes.data, inv.ctypes.data, q.ctypes.data,
+                                          lam.ctypes.data, fl.ctypes.data, ws.ctypes.data, wsb, None)
+    assert rc == 0, rc
+    return idx_a, val_a, n_a, code_b, n_b, inv, q[:, :d], lam, fl
+
+
+def check_hybrid(L, verbose=True):
+    """The hybrid coding against the compaction of the same call (identical survivors and values)
+    and against the oracle's split (Section 3.3)."""
+    rows, d = 3, 40003
+    rng = np.random.default_rng(81)
+    g2 = np.stack([W.t_mixture(d, 200 + r) * np.float32(10.0 ** rng.uniform(-3, 0)) for r in range(rows)])
+    g2[:, ::13] = 0
+    rhos, seeds = [0.02, 0.1, 0.4], [7, 8, 9]
+    for solver in ("greedy", "exact"):
+        idx, val, nnz, lam, k, fl = batched(L, g2, rhos, seeds, solver, ld=d + 5)
+        ia, va, na, cb, nb, inv, q, lam2, fl2 = hybrid_batched(L, g2, rhos, seeds, solver, ld=d + 5)
+        assert np.array_equal(lam, lam2) and not fl2.any()
+        for r in range(rows):
+            n = int(nnz[r])
+            A, B = int(na[r]), int(nb[r])
+            assert A + B == n and A == k[r]
+            bi = cb[r, :B] & 0x7FFFFFFF
+            neg = cb[r, :B] < 0
+            merged = np.concatenate([ia[r, :A], bi])
+            vals = np.concatenate([va[r, :A], np.where(neg, -inv[r], inv[r]).astype(np.float32)])
+            o = np.argsort(merged, kind="stable")
+            assert np.array_equal(merged[o], idx[r, :n]) and np.array_equal(vals[o], val[r, :n])
+            assert np.array_equal(neg, g2[r][bi] < 0)
+            assert np.all(q[r][ia[r, :A]] == 2) and np.array_equal(q[r][bi], np.where(neg, -1, 1).astype(np.int8))
+            assert np.count_nonzero(q[r]) == n
+            sol = oracle.solve(g2[r], rhos[r], solver, 2)
+            h = oracle.sample_hybrid(g2[r], sol.p, seeds[r])
+            if solver == "exact":  # identical lambda: identical capped set and survivors
+                assert np.array_equal(ia[r, :A], h.qa_idx) and np.array_equal(bi, h.qb_idx)
+                assert np.array_equal(q[r], h.q)
+    if verbose:
+        print("hybrid cases ok", flush=True)
+    return True
 
 
 def run_extra(path, verbose=True):

@@ -97,6 +97,53 @@ def test_argument_errors(L):
     assert L.gspar_status_string(gs.ERR_ARG) == b"invalid argument"
 
 
+def test_hybrid_argument_errors(L):
+    import paper_1710_09854_amd as gs
+
+    wsb = L.gspar_workspace_bytes(1, 1000, 0)
+
+    def one(**kw):
+        a = dict(g=FAKE, d=1000, rho=0.1, idx_a=FAKE, val_a=FAKE, cap_a=10, n_a=FAKE, code_b=FAKE, cap_b=10,
+                 n_b=FAKE, ws=FAKE)
+        a.update(kw)
+        return L.sparsify_sample_hybrid(a["g"], a["d"], a["rho"], 0, 2, 0, a["idx_a"], a["val_a"], a["cap_a"],
+                                        a["n_a"], a["code_b"], a["cap_b"], a["n_b"], None, None, None, None,
+                                        a["ws"], wsb, None)
+
+    assert one(code_b=None) == gs.ERR_ARG
+    assert one(n_a=None) == gs.ERR_ARG
+    assert one(n_b=None) == gs.ERR_ARG
+    assert one(cap_b=-1) == gs.ERR_ARG
+    assert one(idx_a=None) == gs.ERR_ARG
+    assert one(rho=2.0) == gs.ERR_ARG
+    assert one(ws=FAKE + 8) == gs.ERR_WORKSPACE
+    assert L.sparsify_sample_hybrid_batched(FAKE, 2, 1000, 1000, None, 0, 2, FAKE, FAKE, FAKE, 10, FAKE, FAKE, 10,
+                                            FAKE, None, None, None, None, FAKE, wsb, None) == gs.ERR_ARG
+
+
+def test_coding_bits_match_oracle(L):
+    """The library's host-side coding-length helper against the oracle's own statement."""
+    import oracle
+    import paper_1710_09854_amd as gs
+
+    rng = np.random.default_rng(3)
+    for _ in range(200):
+        d = int(rng.integers(1, 1 << 28))
+        n_a = int(rng.integers(0, min(d, 100000) + 1))
+        n_b = int(rng.integers(0, min(d - n_a, 1000000) + 1))
+        n_neg = int(rng.integers(0, n_b + 1))
+        bits = int(rng.choice([16, 32, 64]))
+        got = gs.coding_bits(d, n_a, n_b, n_neg, bits)
+        want = oracle.coding_bits(d, n_a, n_b, n_neg, bits)
+        for x, y in zip(got, want):
+            assert abs(x - y) <= 1e-12 * max(1.0, abs(y))
+    out = (ctypes.c_double * 3)()
+    assert L.gspar_coding_bits(10, 6, 5, 0, 32, out) == gs.ERR_ARG   # n_a + n_b > d
+    assert L.gspar_coding_bits(10, 1, 2, 3, 32, out) == gs.ERR_ARG   # more negatives than Q_B entries
+    assert L.gspar_coding_bits(10, 1, 2, 1, 0, out) == gs.ERR_ARG
+    assert L.gspar_coding_bits(10, 1, 2, 1, 32, None) == gs.ERR_ARG
+
+
 def _fx_limbs(v: int):
     return (ctypes.c_uint64 * 5)(*[(v >> (64 * i)) & 0xFFFFFFFFFFFFFFFF for i in range(5)])
 

@@ -28,6 +28,10 @@ def test_emulated_special_batched_overflow_unaligned(emu_lib):
     assert runner.run_extra(emu_lib, verbose=False)
 
 
+def test_emulated_hybrid_coding(emu_lib):
+    assert runner.check_hybrid(runner.load(emu_lib), verbose=False)
+
+
 def test_emulated_parity_subset(emu_lib):
     L = runner.load(emu_lib)
     import oracle

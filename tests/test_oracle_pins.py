@@ -456,6 +456,75 @@ def test_sampling_unbiased_and_second_moment():
     assert abs(sq.mean() - second) < 0.03 * second
 
 
+# ----------------------------------------------------------------------------- hybrid coding
+@pytest.mark.parametrize("maker,rho,solver", [(lambda: W.t_mixture(6000, 61), 0.05, "exact"),
+                                              (lambda: W.two_level(5000, 30, 80.0, 1.0, 62), 0.02, "greedy"),
+                                              (lambda: W.integer_ties(4000, 63), 0.3, "exact"),
+                                              (lambda: W.normal(3000, 64), 0.1, "greedy")])
+def test_hybrid_split(maker, rho, solver):
+    """Section 3.3, eqs. (9)-(10): Q_A is exactly the capped set S_k = {p_i = 1} (a capped coordinate
+    always survives), Q_B the other survivors; decoding Q_A with its values and Q_B with
+    sign(g_i)/lambda gives back the amplified vector Q(g); the ternary vector marks both."""
+    g = maker()
+    g[::11] = 0
+    sol = oracle.solve(g, rho, solver, 2)
+    h = oracle.sample_hybrid(g, sol.p, 5)
+    idx, val, n = oracle.sample_compact(g, sol.p, 5)
+    assert np.array_equal(h.qa_idx, np.flatnonzero(sol.p == 1))
+    assert np.array_equal(np.sort(np.concatenate([h.qa_idx, h.qb_idx])), idx)
+    assert np.array_equal(h.qa_val, g[h.qa_idx])
+    dec = np.zeros(g.size, np.float64)
+    dec[h.qa_idx] = h.qa_val
+    dec[h.qb_idx] = np.where(h.qb_neg, -1.0, 1.0) / sol.lam
+    assert np.allclose(dec[idx], val, rtol=1e-6, atol=0)
+    assert np.count_nonzero(dec) == n
+    assert np.array_equal(h.qb_neg, g[h.qb_idx] < 0)
+    vals, cnt = np.unique(h.q, return_counts=True)
+    want = {2: h.qa_idx.size, -1: int(h.qb_neg.sum()), 1: int((~h.qb_neg).sum()), 0: g.size - n}
+    assert {int(v): int(c) for v, c in zip(vals, cnt)} == {k: v for k, v in want.items() if v}
+
+
+def test_coding_bits_entropy_and_bounds():
+    """The ternary vector's entropy term is d times the base-2 Shannon entropy of its symbol
+    frequencies (a library routine here); four equally frequent symbols cost exactly 2 bits each and
+    a constant vector nothing; the sparse-list cost is linear in the list lengths."""
+    from scipy.stats import entropy
+    rng = np.random.default_rng(7)
+    b = 32
+    for _ in range(50):
+        d = int(rng.integers(8, 100000))
+        n_a = int(rng.integers(0, d // 3 + 1))
+        n_b = int(rng.integers(0, d - n_a + 1))
+        n_neg = int(rng.integers(0, n_b + 1))
+        sparse, ternary, paper = oracle.coding_bits(d, n_a, n_b, n_neg, b)
+        freq = np.array([n_a, n_neg, n_b - n_neg, d - n_a - n_b], np.float64) / d
+        assert abs((ternary - n_a * b - b) - d * entropy(freq, base=2)) <= 1e-9 * d
+        assert ternary - n_a * b - b <= 2 * d * (1 + 1e-12)
+        assert paper <= sparse + 1e-9  # min(2d, n_b log2 d) <= n_b (log2 d + 1)
+    d = 4096
+    assert abs(oracle.coding_bits(d, d // 4, d // 2, d // 4, b)[1] - (2 * d + (d // 4) * b + b)) < 1e-6
+    assert oracle.coding_bits(d, 0, 0, 0, b)[1] == b
+    s1 = oracle.coding_bits(d, 10, 100, 40, b)[0]
+    s2 = oracle.coding_bits(d, 11, 100, 40, b)[0]
+    s3 = oracle.coding_bits(d, 10, 101, 40, b)[0]
+    assert abs((s2 - s1) - (b + 12)) < 1e-9 and abs((s3 - s1) - 13) < 1e-9
+
+
+@pytest.mark.parametrize("s,rho_def,seed", [(20, 0.05, 1), (50, 0.2, 2), (5, 0.01, 3), (100, 0.5, 4)])
+def test_theorem4_coding_length_bound(s, rho_def, seed):
+    """Theorem 4: for a (rho, s)-approximately sparse g (Definition 2) and the sparsification of
+    Lemma 3 (variance budget eps = rho), the expected coding length, the sum over S_k of
+    p_i (b + log2 d) plus min(d, sum over the rest of p_i log2 d) plus b, is at most
+    s (b + log2 d) + min(rho s log2 d, d) + b."""
+    d, b = 4000, 32
+    g = W.approx_sparse(d, s, rho_def, seed)
+    sol = oracle.solve_variance(g, rho_def)
+    L = math.log2(d)
+    cap = sol.p == 1
+    expected = float(sol.p[cap].sum()) * (b + L) + min(d, float(sol.p[~cap].sum()) * L) + b
+    assert expected <= s * (b + L) + min(rho_def * s * L, d) + b + 1e-9
+
+
 # ----------------------------------------------------------------------------- generators
 def test_generators_shapes_and_determinism():
     w1 = W.c1()
