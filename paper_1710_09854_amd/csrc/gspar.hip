@@ -11,7 +11,8 @@
 //              finishes the row or asks for a refinement window.
 //   k_refine   (launched a fixed number of times, each followed by k_solve; exits at once unless
 //              the solver asked for it) histograms only the magnitudes inside one binade (4096
-//              sub-bins) or inside one sub-bin (2048 single bit patterns), so every threshold the
+//              sub-bins with their minima, and a direct count of the keys at or above the greedy
+//              query key) or inside one sub-bin (2048 single bit patterns), so every threshold the
 //              solvers need is resolved exactly.
 //   k_sample   one streaming pass: Philox4x32-10 per group of four coordinates, Bernoulli selection,
 //              amplification to g_i or sign(g_i)/lambda, order-preserving compaction with a
@@ -50,6 +51,12 @@ constexpr int kB3 = 2048;                   // level 3: one level-2 bin, one key
 constexpr int kTileThreads = 256;
 constexpr int kTileGroups = 16;             // float4 groups per thread per tile
 constexpr int kTileElems = kTileThreads * kTileGroups * 4;  // 16384 coordinates per tile
+// Sample tiles resident at once (256 CUs x 7); larger grids give each workgroup two tiles (a build
+// may lower the threshold to exercise that path on small inputs).
+#ifndef GSPAR_SAMPLE_RESIDENT
+#define GSPAR_SAMPLE_RESIDENT (256 * 7)
+#endif
+constexpr int64_t kSampleResident = GSPAR_SAMPLE_RESIDENT;
 constexpr int kMaxIters = 64;
 constexpr int64_t kMaxChunk = (1 << 20) - 4;  // LDS packing holds < 2^20 elements per workgroup
 
@@ -1340,19 +1347,22 @@ __device__ __forceinline__ uint32_t wave_prefix_bits(uint32_t x, uint32_t& total
   return pre;
 }
 
-template <bool VEC, bool HYB>
+template <bool VEC, bool HYB, int K>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
-  __shared__ float s_capv[kTileThreads / 64][kCapList];
-  __shared__ alignas(16) uint8_t s_code[kTileElems / 4];  // per group: selection | sign << 4
-  __shared__ alignas(16) uint8_t s_capb[kTileElems / 4];  // per group: capped-survivor bits
-  __shared__ uint32_t s_wsel[kTileThreads / 64];
-  __shared__ uint32_t s_wcap[kTileThreads / 64];
-  __shared__ uint32_t s_wcl[kTileThreads / 64];
+  __shared__ float s_capv[K][kTileThreads / 64][kCapList];
+  __shared__ alignas(16) uint8_t s_code[K][kTileElems / 4];  // per group: selection | sign << 4
+  __shared__ alignas(16) uint8_t s_capb[K][kTileElems / 4];  // per group: capped-survivor bits
+  __shared__ uint32_t s_wsel[K][kTileThreads / 64];
+  __shared__ uint32_t s_wcap[K][kTileThreads / 64];
+  __shared__ uint32_t s_wcl[K][kTileThreads / 64];
   __shared__ uint64_t s_excl;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int64_t t = blockIdx.x;
-  const int64_t row = t / a.lay.tiles;
-  const int64_t part = t % a.lay.tiles;
+  // workgroup -> K consecutive tiles [part0, part0 + nk) of one row
+  const int64_t wpr = (a.lay.tiles + K - 1) / K;  // workgroups per row
+  const int64_t row = blockIdx.x / wpr;
+  const int64_t part0 = (blockIdx.x % wpr) * K;
+  const int nk = (int)min((int64_t)K, a.lay.tiles - part0);
+  const int64_t t0 = row * a.lay.tiles + part0;  // status word of the first tile
   const RowCtl* ctl = ctl_of(a, row);
   TileCtx c;
   c.row = a.g + row * a.ld;
@@ -1364,94 +1374,99 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   c.k0 = (uint32_t)seed;
   c.k1 = (uint32_t)(seed >> 32);
   const float inv = ctl->inv_lam;
-  // phase 1: group j of this lane is tile group wv * (kWaveElems / 4) + 64 j + lane
+  const bool fast = c.live && (c.lam == 0.0 || c.lam >= kLamScaledMin);
+  const double lam32 = c.lam * 0x1p32;
+  uint64_t* st = status_of(a);
+  // group j of this lane in a tile is tile group wv * (kWaveElems / 4) + 64 j + lane
   const int tg0 = wv * (kWaveElems / 4) + lane;
-  const int64_t q0 = part * (kTileElems / 4) + tg0;
+  uint64_t agg[K];  // per tile: (capped survivors << 31) | survivors
 
-  uint32_t nsel = 0, ncap = 0;
-  uint32_t ncl = 0;  // capped survivors of this wave so far (the LDS list keeps the first kCapList)
-  auto record = [&](int j, const float v[4], uint32_t z, uint32_t cz) {
-    cz &= z;
-    uint32_t neg = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) neg |= (__float_as_uint(v[k]) >> 31) << k;
-    s_code[tg0 + 64 * j] = (uint8_t)(z | (neg << 4));
-    s_capb[tg0 + 64 * j] = (uint8_t)cz;
-    nsel += (uint32_t)__popc(z);
-    if (__ballot(cz != 0)) {
-      ncap += (uint32_t)__popc(cz);
-      uint32_t tot;
-      uint32_t p = ncl + wave_prefix_bits<3>((uint32_t)__popc(cz), tot);
+  for (int kk = 0; kk < K; ++kk) {
+    if (kk >= nk) break;
+    __builtin_amdgcn_sched_barrier(0);  // keep each tile's loads in its own iteration
+    // phase 1 of tile part0 + kk
+    const int64_t part = part0 + kk;
+    const int64_t q0 = part * (kTileElems / 4) + tg0;
+    uint32_t nsel = 0, ncap = 0;
+    uint32_t ncl = 0;  // capped survivors of this wave so far (the LDS list keeps the first kCapList)
+    auto record = [&](int j, const float v[4], uint32_t z, uint32_t cz) {
+      cz &= z;
+      uint32_t neg = 0;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if ((cz >> k) & 1) {
-          if (p < (uint32_t)kCapList) s_capv[wv][p] = v[k];
-          ++p;
+      for (int k = 0; k < 4; ++k) neg |= (__float_as_uint(v[k]) >> 31) << k;
+      s_code[kk][tg0 + 64 * j] = (uint8_t)(z | (neg << 4));
+      s_capb[kk][tg0 + 64 * j] = (uint8_t)cz;
+      nsel += (uint32_t)__popc(z);
+      if (__ballot(cz != 0)) {
+        ncap += (uint32_t)__popc(cz);
+        uint32_t tot;
+        uint32_t p = ncl + wave_prefix_bits<3>((uint32_t)__popc(cz), tot);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if ((cz >> k) & 1) {
+            if (p < (uint32_t)kCapList) s_capv[kk][wv][p] = v[k];
+            ++p;
+          }
+        }
+        ncl += tot;
+      }
+    };
+    if (VEC && fast && (part + 1) * (int64_t)kTileElems <= a.d) {
+      // whole tile inside the row: kSampleBatch unconditional loads in flight per lane
+#pragma unroll
+      for (int jb = 0; jb < kTileGroups; jb += kSampleBatch) {
+        float4 x[kSampleBatch];
+#pragma unroll
+        for (int u = 0; u < kSampleBatch; ++u)
+          x[u] = *reinterpret_cast<const float4*>(c.row + 4 * (q0 + 64 * (jb + u)));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kSampleBatch; ++u) {
+          const float v[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+          uint32_t z, cz;
+          decide_fast(q0 + 64 * (jb + u), v, lam32, c.k0, c.k1, z, cz);
+          record(jb + u, v, z, cz);
         }
       }
-      ncl += tot;
-    }
-  };
-  const bool fast = c.live && (c.lam == 0.0 || c.lam >= kLamScaledMin);
-  if (VEC && fast && (part + 1) * (int64_t)kTileElems <= a.d) {
-    // whole tile inside the row: kSampleBatch unconditional loads in flight per lane
-    const double lam32 = c.lam * 0x1p32;
-#pragma unroll
-    for (int jb = 0; jb < kTileGroups; jb += kSampleBatch) {
-      float4 x[kSampleBatch];
-#pragma unroll
-      for (int u = 0; u < kSampleBatch; ++u)
-        x[u] = *reinterpret_cast<const float4*>(c.row + 4 * (q0 + 64 * (jb + u)));
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int u = 0; u < kSampleBatch; ++u) {
-        const float v[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-        uint32_t z, cz;
-        decide_fast(q0 + 64 * (jb + u), v, lam32, c.k0, c.k1, z, cz);
-        record(jb + u, v, z, cz);
+    } else {
+      for (int j = 0; j < kTileGroups; ++j) {
+        float v[4];
+        uint32_t z = 0, cz = 0;
+        if (c.live) decide_group<VEC>(c, q0 + 64 * j, v, z, cz);
+        else v[0] = v[1] = v[2] = v[3] = 0.0f;
+        record(j, v, z, cz);
       }
     }
-  } else {
-    for (int j = 0; j < kTileGroups; ++j) {
-      float v[4];
-      uint32_t z = 0, cz = 0;
-      if (c.live) decide_group<VEC>(c, q0 + 64 * j, v, z, cz);
-      else v[0] = v[1] = v[2] = v[3] = 0.0f;
-      record(j, v, z, cz);
+    for (int o = 32; o > 0; o >>= 1) {
+      nsel += __shfl_xor(nsel, o);
+      ncap += __shfl_xor(ncap, o);
     }
-  }
-  for (int o = 32; o > 0; o >>= 1) {
-    nsel += __shfl_xor(nsel, o);
-    ncap += __shfl_xor(ncap, o);
-  }
-  if (lane == 0) {
-    s_wsel[wv] = nsel;
-    s_wcap[wv] = ncap;
-    s_wcl[wv] = ncl;
-  }
-  __syncthreads();
-  uint32_t tsel = 0, tcp = 0, wbase = 0, wbase_cap = 0;
-  for (int i = 0; i < kTileThreads / 64; ++i) {
-    if (i < wv) {
-      wbase += s_wsel[i];
-      wbase_cap += s_wcap[i];
+    if (lane == 0) {
+      s_wsel[kk][wv] = nsel;
+      s_wcap[kk][wv] = ncap;
+      s_wcl[kk][wv] = ncl;
     }
-    tsel += s_wsel[i];
-    tcp += s_wcap[i];
+    __syncthreads();
+    uint32_t tsel = 0, tcp = 0;
+    for (int i = 0; i < kTileThreads / 64; ++i) {
+      tsel += s_wsel[kk][i];
+      tcp += s_wcap[kk][i];
+    }
+    agg[kk] = ((uint64_t)tcp << 31) | tsel;
+    // publish at once: a row's first tile its inclusive prefix, every other tile its aggregate
+    if (tid == 0)
+      __hip_atomic_store(&st[t0 + kk], (part == 0 ? kStInc : kStAgg) | agg[kk], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
   }
-  const uint64_t agg = ((uint64_t)tcp << 31) | tsel;
 
-  // decoupled look-back for the tile's exclusive prefix within its row
-  uint64_t* st = status_of(a);
-  if (part == 0) {
-    if (tid == 0) {
-      __hip_atomic_store(&st[t], kStInc | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      s_excl = 0;
-    }
+  // decoupled look-back for the exclusive prefix of the first tile within its row
+  if (part0 == 0) {
+    if (tid == 0) s_excl = 0;
   } else {
-    if (tid == 0) __hip_atomic_store(&st[t], kStAgg | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (wv == 0) {
-      const int64_t first = t - part;
+      const int64_t t = t0;
+      const int64_t first = t - part0;
       int64_t look = t - 1;
       uint64_t ex = 0;
       while (true) {
@@ -1484,138 +1499,162 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         look -= 64;
       }
       if (lane == 0) {
-        __hip_atomic_store(&st[t], kStInc | (ex + agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_excl = ex;
+        uint64_t run = ex;
+        for (int kk = 0; kk < nk; ++kk) {
+          run += agg[kk];
+          __hip_atomic_store(&st[t0 + kk], kStInc | run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
       }
+    }
+  }
+  if (part0 == 0 && tid == 0) {
+    // the row's first workgroup: its later tiles' inclusive prefixes follow from its own aggregates
+    uint64_t run = agg[0];
+    for (int kk = 1; kk < nk; ++kk) {
+      run += agg[kk];
+      __hip_atomic_store(&st[t0 + kk], kStInc | run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
   __syncthreads();
-  const uint64_t excl = s_excl;
+  uint64_t excl = s_excl;
 
-  // phase 2: thread tid owns tile groups [16 tid, 16 tid + 16) (bit b of its masks is tile
-  // coordinate 64 tid + b)
-  const int64_t e0 = part * (int64_t)kTileElems + 64 * tid;
-  uint64_t sm = 0, nm = 0, cm = 0;  // selected, negative, capped-and-selected coordinates
-  uint32_t cr = 0;                  // rank of this thread's first capped survivor in its wave's list
-  if (s_wsel[wv]) {
-    const uint4 cw = *reinterpret_cast<const uint4*>(&s_code[16 * tid]);
-    const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
+  // phase 2, tile by tile: thread tid owns tile groups [16 tid, 16 tid + 16) (bit b of its masks
+  // is tile coordinate 64 tid + b)
 #pragma unroll
-    for (int b = 0; b < 16; ++b) {
-      const uint64_t byte = (words[b >> 2] >> (8 * (b & 3))) & 0xFF;
-      sm |= (byte & 0xF) << (4 * b);
-      nm |= (byte >> 4) << (4 * b);
+  for (int kk = 0; kk < K; ++kk) {
+    if (kk >= nk) break;
+    __builtin_amdgcn_sched_barrier(0);
+    const int64_t part = part0 + kk;
+    uint32_t wbase = 0, wbase_cap = 0;
+    for (int i = 0; i < wv; ++i) {
+      wbase += s_wsel[kk][i];
+      wbase_cap += s_wcap[kk][i];
     }
-    if (s_wcap[wv]) {
-      const uint4 bw = *reinterpret_cast<const uint4*>(&s_capb[16 * tid]);
-      const uint32_t cwd[4] = {bw.x, bw.y, bw.z, bw.w};
+    const int64_t e0 = part * (int64_t)kTileElems + 64 * tid;
+    uint64_t sm = 0, nm = 0, cm = 0;  // selected, negative, capped-and-selected coordinates
+    uint32_t cr = 0;                  // rank of this thread's first capped survivor in its wave's list
+    if (s_wsel[kk][wv]) {
+      const uint4 cw = *reinterpret_cast<const uint4*>(&s_code[kk][16 * tid]);
+      const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
 #pragma unroll
-      for (int b = 0; b < 16; ++b) cm |= (uint64_t)((cwd[b >> 2] >> (8 * (b & 3))) & 0xF) << (4 * b);
-      uint32_t ctot;
-      cr = wave_prefix_bits<7>((uint32_t)__popcll(cm), ctot);
-    }
-    const bool lds_values = s_wcl[wv] <= (uint32_t)kCapList;
-    if constexpr (!HYB) {
-      uint32_t wtot;
-      uint64_t pos = (excl & 0x7FFFFFFFull) + wbase + wave_prefix_bits<7>((uint32_t)__popcll(sm), wtot);
-      int32_t* __restrict__ oi = a.idx + row * a.cap;
-      float* __restrict__ ov = a.val + row * a.cap;
-      auto emit = [&](auto from_lds) {
-        uint32_t r = cr;
-        uint64_t m = sm;
-        while (m) {
-          const int b = __ffsll((unsigned long long)m) - 1;
-          const uint64_t bit = 1ull << b;
-          float val = (nm & bit) ? -inv : inv;
-          if (cm & bit) {
-            if constexpr (decltype(from_lds)::value) val = s_capv[wv][r];
+      for (int b = 0; b < 16; ++b) {
+        const uint64_t byte = (words[b >> 2] >> (8 * (b & 3))) & 0xFF;
+        sm |= (byte & 0xF) << (4 * b);
+        nm |= (byte >> 4) << (4 * b);
+      }
+      if (s_wcap[kk][wv]) {
+        const uint4 bw = *reinterpret_cast<const uint4*>(&s_capb[kk][16 * tid]);
+        const uint32_t cwd[4] = {bw.x, bw.y, bw.z, bw.w};
+#pragma unroll
+        for (int b = 0; b < 16; ++b) cm |= (uint64_t)((cwd[b >> 2] >> (8 * (b & 3))) & 0xF) << (4 * b);
+        uint32_t ctot;
+        cr = wave_prefix_bits<7>((uint32_t)__popcll(cm), ctot);
+      }
+      const bool lds_values = s_wcl[kk][wv] <= (uint32_t)kCapList;
+      if constexpr (!HYB) {
+        uint32_t wtot;
+        uint64_t pos = (excl & 0x7FFFFFFFull) + wbase + wave_prefix_bits<7>((uint32_t)__popcll(sm), wtot);
+        int32_t* __restrict__ oi = a.idx + row * a.cap;
+        float* __restrict__ ov = a.val + row * a.cap;
+        auto emit = [&](auto from_lds) {
+          uint32_t r = cr;
+          uint64_t m = sm;
+          while (m) {
+            const int b = __ffsll((unsigned long long)m) - 1;
+            const uint64_t bit = 1ull << b;
+            float val = (nm & bit) ? -inv : inv;
+            if (cm & bit) {
+              if constexpr (decltype(from_lds)::value) val = s_capv[kk][wv][r];
+              else val = c.row[e0 + b];
+              ++r;
+            }
+            if ((int64_t)pos < a.cap) {
+              oi[pos] = (int32_t)(e0 + b);
+              ov[pos] = val;
+            }
+            ++pos;
+            m &= m - 1;
+          }
+        };
+        if (lds_values) emit(std::true_type{});
+        else emit(std::false_type{});
+      } else {
+        // hybrid coding (Section 3.3, eqs. 9-10): capped survivors go to Q_A as (index, g_i), the
+        // others to Q_B as index | sign << 31 (their value is sign(g_i) / lambda)
+        const uint64_t bm = sm & ~cm;
+        uint32_t btot;
+        const uint64_t excl_cap = (excl >> 31) & 0x7FFFFFFFull;
+        uint64_t pa = excl_cap + wbase_cap + cr;
+        uint64_t pb = (excl & 0x7FFFFFFFull) - excl_cap + (wbase - wbase_cap) +
+                      wave_prefix_bits<7>((uint32_t)__popcll(bm), btot);
+        int32_t* __restrict__ oa = a.idx + row * a.cap;
+        float* __restrict__ va = a.val + row * a.cap;
+        int32_t* __restrict__ ob = a.code_b + row * a.cap_b;
+        auto emit_a = [&](auto from_lds) {
+          uint32_t r = cr;
+          uint64_t m = cm;
+          while (m) {
+            const int b = __ffsll((unsigned long long)m) - 1;
+            float val;
+            if constexpr (decltype(from_lds)::value) val = s_capv[kk][wv][r];
             else val = c.row[e0 + b];
             ++r;
+            if ((int64_t)pa < a.cap) {
+              oa[pa] = (int32_t)(e0 + b);
+              va[pa] = val;
+            }
+            ++pa;
+            m &= m - 1;
           }
-          if ((int64_t)pos < a.cap) {
-            oi[pos] = (int32_t)(e0 + b);
-            ov[pos] = val;
-          }
-          ++pos;
-          m &= m - 1;
+        };
+        if (cm) {
+          if (lds_values) emit_a(std::true_type{});
+          else emit_a(std::false_type{});
         }
-      };
-      if (lds_values) emit(std::true_type{});
-      else emit(std::false_type{});
-    } else {
-      // hybrid coding (Section 3.3, eqs. 9-10): capped survivors go to Q_A as (index, g_i), the
-      // others to Q_B as index | sign << 31 (their value is sign(g_i) / lambda)
-      const uint64_t bm = sm & ~cm;
-      uint32_t btot;
-      const uint64_t excl_cap = (excl >> 31) & 0x7FFFFFFFull;
-      uint64_t pa = excl_cap + wbase_cap + cr;
-      uint64_t pb = (excl & 0x7FFFFFFFull) - excl_cap + (wbase - wbase_cap) +
-                    wave_prefix_bits<7>((uint32_t)__popcll(bm), btot);
-      int32_t* __restrict__ oa = a.idx + row * a.cap;
-      float* __restrict__ va = a.val + row * a.cap;
-      int32_t* __restrict__ ob = a.code_b + row * a.cap_b;
-      auto emit_a = [&](auto from_lds) {
-        uint32_t r = cr;
-        uint64_t m = cm;
+        uint64_t m = bm;
         while (m) {
           const int b = __ffsll((unsigned long long)m) - 1;
-          float val;
-          if constexpr (decltype(from_lds)::value) val = s_capv[wv][r];
-          else val = c.row[e0 + b];
-          ++r;
-          if ((int64_t)pa < a.cap) {
-            oa[pa] = (int32_t)(e0 + b);
-            va[pa] = val;
-          }
-          ++pa;
+          if ((int64_t)pb < a.cap_b) ob[pb] = (int32_t)((uint32_t)(e0 + b) | (uint32_t)(((nm >> b) & 1) << 31));
+          ++pb;
           m &= m - 1;
         }
-      };
-      if (cm) {
-        if (lds_values) emit_a(std::true_type{});
-        else emit_a(std::false_type{});
-      }
-      uint64_t m = bm;
-      while (m) {
-        const int b = __ffsll((unsigned long long)m) - 1;
-        if ((int64_t)pb < a.cap_b) ob[pb] = (int32_t)((uint32_t)(e0 + b) | (uint32_t)(((nm >> b) & 1) << 31));
-        ++pb;
-        m &= m - 1;
       }
     }
-  }
-  if constexpr (HYB) {
-    // dense ternary vector (Section 3.3): 2 on the capped set, sign(g_i) for the other
-    // survivors, 0 elsewhere; this thread's 64 coordinates
-    if (a.q && e0 < a.d) {
-      int8_t* __restrict__ qr = a.q + row * a.ld + e0;
-      uint32_t w[16];
+    if constexpr (HYB) {
+      // dense ternary vector (Section 3.3): 2 on the capped set, sign(g_i) for the other
+      // survivors, 0 elsewhere; this thread's 64 coordinates
+      if (a.q && e0 < a.d) {
+        int8_t* __restrict__ qr = a.q + row * a.ld + e0;
+        uint32_t w[16];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        uint32_t x = 0;
+        for (int j = 0; j < 16; ++j) {
+          uint32_t x = 0;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int b = 4 * j + k;
-          const uint32_t code = ((cm >> b) & 1) ? 2u : (((sm >> b) & 1) ? (((nm >> b) & 1) ? 0xFFu : 1u) : 0u);
-          x |= code << (8 * k);
+          for (int k = 0; k < 4; ++k) {
+            const int b = 4 * j + k;
+            const uint32_t code = ((cm >> b) & 1) ? 2u : (((sm >> b) & 1) ? (((nm >> b) & 1) ? 0xFFu : 1u) : 0u);
+            x |= code << (8 * k);
+          }
+          w[j] = x;
         }
-        w[j] = x;
-      }
-      if (e0 + 64 <= a.d && ((uintptr_t)qr & 15) == 0) {
+        if (e0 + 64 <= a.d && ((uintptr_t)qr & 15) == 0) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          uint4 v;
-          v.x = w[4 * j]; v.y = w[4 * j + 1]; v.z = w[4 * j + 2]; v.w = w[4 * j + 3];
-          reinterpret_cast<uint4*>(qr)[j] = v;
+          for (int j = 0; j < 4; ++j) {
+            uint4 v;
+            v.x = w[4 * j]; v.y = w[4 * j + 1]; v.z = w[4 * j + 2]; v.w = w[4 * j + 3];
+            reinterpret_cast<uint4*>(qr)[j] = v;
+          }
+        } else {
+          const int64_t nb = min((int64_t)64, a.d - e0);
+          for (int64_t b = 0; b < nb; ++b) qr[b] = (int8_t)((w[b >> 2] >> (8 * (b & 3))) & 0xFF);
         }
-      } else {
-        const int64_t nb = min((int64_t)64, a.d - e0);
-        for (int64_t b = 0; b < nb; ++b) qr[b] = (int8_t)((w[b >> 2] >> (8 * (b & 3))) & 0xFF);
       }
     }
+    excl += agg[kk];
   }
-  if (part == a.lay.tiles - 1 && tid == 0) {
-    const uint64_t incl = excl + agg;
+  if (part0 + nk == a.lay.tiles && tid == 0) {
+    const uint64_t incl = excl;
     const int64_t n = (int64_t)(incl & 0x7FFFFFFFull);
     const int64_t kc = (int64_t)((incl >> 31) & 0x7FFFFFFFull);
     uint32_t fl = ctl->flags;
@@ -1782,20 +1821,28 @@ static int launch_solve(Args& a, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
 
+template <int K>
+static void launch_sample(const Args& a, bool vec, hipStream_t s) {
+  const dim3 grid((unsigned)(a.rows * ((a.lay.tiles + K - 1) / K)));
+  if (a.code_b) {
+    if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, true, K>), grid, dim3(kTileThreads), 0, s, a);
+    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, true, K>), grid, dim3(kTileThreads), 0, s, a);
+  } else {
+    if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, false, K>), grid, dim3(kTileThreads), 0, s, a);
+    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, false, K>), grid, dim3(kTileThreads), 0, s, a);
+  }
+}
+
 static int run_sample(Args& a, hipStream_t s) {
   plan(a);
   int rc = launch_solve(a, s);
   if (rc) return rc;
   const bool vec = vec_ok(a);
-  const dim3 grid((unsigned)(a.rows * a.lay.tiles));
   time_before(0, s);
-  if (a.code_b) {
-    if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, true>), grid, dim3(kTileThreads), 0, s, a);
-    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, true>), grid, dim3(kTileThreads), 0, s, a);
-  } else {
-    if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, false>), grid, dim3(kTileThreads), 0, s, a);
-    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, false>), grid, dim3(kTileThreads), 0, s, a);
-  }
+  // tiles per workgroup: 1 while every tile can be resident at once, else 2, so that a
+  // workgroup's wait for its predecessors' prefix overlaps the decide phase of its second tile
+  if (a.rows * a.lay.tiles <= kSampleResident) launch_sample<1>(a, vec, s);
+  else launch_sample<2>(a, vec, s);
   time_after(0, s);
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }

@@ -11,12 +11,16 @@ OUT_DIR = os.path.join(HERE, "_build")
 
 def build(asan: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
-    out = os.path.join(OUT_DIR, "libgspar_emu_asan.so" if asan else "libgspar_emu.so")
+    res = os.environ.get("GSPAR_EMU_RESIDENT")
+    out = os.path.join(OUT_DIR, ("libgspar_emu_asan" if asan else "libgspar_emu") + (f"_r{int(res)}" if res else "") + ".so")
     if os.path.exists(out) and os.path.getmtime(out) > max(os.path.getmtime(SRC),
                                                          os.path.getmtime(os.path.join(HERE, "hip", "hip_runtime.h"))):
         return out
-    # a short look-back wait keeps the emulated fallback test (every status hidden) quick
+    # a short look-back wait keeps the emulated fallback test (every status hidden) quick; a low
+    # residency threshold makes the small emulated inputs take the two-tiles-per-workgroup path too
+    # when GSPAR_EMU_RESIDENT is set
     cmd = ["g++", "-std=c++20", "-O1", "-g", "-fPIC", "-shared", "-pthread", "-Wno-attributes", "-DGSPAR_LOOKBACK_POLLS=64",
+           f"-DGSPAR_SAMPLE_RESIDENT={int(os.environ.get('GSPAR_EMU_RESIDENT', '1792'))}",
            "-Wno-unknown-pragmas", "-I", HERE, "-I", os.path.join(ROOT, "include"), "-x", "c++", SRC,
            "-o", out + ".tmp"]
     if asan:
