@@ -266,5 +266,7 @@ if __name__ == "__main__":
     which = sys.argv[2] if len(sys.argv) > 2 else "all"
     if which in ("all", "extra"):
         run_extra(sys.argv[1])
+    if which in ("all", "hybrid"):
+        check_hybrid(load(sys.argv[1]))
     if which in ("all", "main"):
         print("checked", run_all(sys.argv[1]))
