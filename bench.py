@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--hybrid", action="store_true",
                     help="time the hybrid coding entry point (Q_A / Q_B lists) instead of the compaction")
     ap.add_argument("--dense-q", action="store_true", help="with --hybrid, also write the dense ternary vector")
+    ap.add_argument("--aggregate", action="store_true",
+                    help="with --cells: also time the aggregation (Algorithm 1, step 6) of each cell's lists, "
+                         "one worker per row")
     ap.add_argument("--cells", action="store_true",
                     help="one JSON line per (workload, solver, rho) cell instead of the step line: median call "
                          "time warm and after evicting the caches, algorithmic HBM fraction, oracle rate")
@@ -230,9 +233,73 @@ def cells(args):
                 if not args.no_cpu_baseline:
                     cell["cpu_baseline"] = cpu_baseline(wl, [(solver, rho)], args.cpu_seconds)
                 print(json.dumps(cell), flush=True)
+                if args.aggregate and not args.hybrid:
+                    print(json.dumps(aggregate_cell(args, wl, plan, scratch, solver, rho)), flush=True)
                 del plan
         del g
         torch.cuda.empty_cache()
+
+
+def aggregate_cell(args, wl, plan, scratch, solver, rho):
+    """The aggregation v = (1/M) sum_m Q(g^m) of the plan's lists (M = rows): median call time warm
+    and after a cache-evicting write, the kernel time from HIP events on its stream, algorithmic bytes
+    (8 B per kept list entry and per length read, 4 B per output coordinate), and the oracle's
+    one-core time on the same lists."""
+    import numpy as np
+    import torch
+
+    import paper_1710_09854_amd as gs
+
+    rows, d = wl.rows, wl.d
+    idx, val, nnz = plan.idx[:, :plan.cap], plan.val[:, :plan.cap], plan.nnz
+    v = torch.empty(d, dtype=torch.float32, device=idx.device)
+    for _ in range(3):
+        gs.aggregate(idx, val, nnz, d, out=v)
+    torch.cuda.synchronize()
+
+    def timed(evict):
+        if evict:
+            scratch.fill_(0.5)
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        gs.aggregate(idx, val, nnz, d, out=v)
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) * 1e-3
+
+    warm = float(np.median([timed(False) for _ in range(20)]))
+    cold = float(np.median([timed(True) for _ in range(5)]))
+    t = gs.KernelTimer(6, 20)
+    for _ in range(20):
+        gs.aggregate(idx, val, nnz, d, out=v)
+    ms, n = t.read()
+    t.close()
+    kept = int(torch.clamp(nnz, 0, plan.cap).sum().item())
+    alg = 8.0 * kept + 8.0 * rows + 4.0 * d
+    kernel_s = ms * 1e-3 / max(n, 1)
+    cell = {"workload": wl.name, "entry": "aggregate", "solver": solver, "rho": rho, "workers": rows, "d": d,
+            "kept_entries": kept, "warm_us": warm * 1e6, "cold_us": cold * 1e6, "kernel_us": kernel_s * 1e6,
+            "algorithmic_bytes": alg, "algorithmic_frac_kernel": alg / kernel_s / 1e9 / HBM_PEAK_GBS,
+            "algorithmic_frac_cold": alg / cold / 1e9 / HBM_PEAK_GBS}
+    if not args.no_cpu_baseline:
+        import oracle
+
+        I, V, N = idx.cpu().numpy(), val.cpu().numpy(), nnz.cpu().numpy()
+        lists = [(I[m, :min(int(N[m]), plan.cap)], V[m, :min(int(N[m]), plan.cap)]) for m in range(rows)]
+        keep = os.sched_getaffinity(0)
+        os.sched_setaffinity(0, {min(keep)})
+        try:
+            t0 = time.perf_counter()
+            reps = 0
+            while reps < 3 or time.perf_counter() - t0 < 2.0:
+                oracle.aggregate(lists, d)
+                reps += 1
+            dt = (time.perf_counter() - t0) / reps
+        finally:
+            os.sched_setaffinity(0, keep)
+        cell["cpu_baseline"] = {"value": dt * 1e6, "unit": "us per aggregation", "cores": 1, "kind": "oracle",
+                                "sample": f"{reps} aggregations of the same {rows} lists on one host core"}
+    return cell
 
 
 def main():

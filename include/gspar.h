@@ -157,6 +157,19 @@ int sparsify_sample_hybrid(const float* g, int64_t d, double rho, int solver, in
 int gspar_coding_bits(int64_t d, int64_t n_a, int64_t n_b, int64_t n_b_neg, int float_bits,
                       double* out);
 
+/* Aggregation of the workers' sparsified gradients (Algorithm 1, step 6, on one device): the dense
+ * average v_i = (1/M) sum_m Q(g^m)_i for M = `workers`, from the lists that
+ * sparsify_sample_compact_batched writes (worker m's entries idx[m*cap ...], val[m*cap ...], the
+ * first min(nnz[m], cap) of them, indices strictly ascending in [0, d)). Each v_i is the fp64 sum
+ * of the workers' values at i taken in worker order m = 0, 1, ..., divided by M and rounded to
+ * fp32, so the result does not depend on the launch. idx, val, nnz [workers] int64 and v [d] fp32
+ * are DEVICE memory; no workspace is used. Entries outside [0, d) are skipped; a list that does
+ * not ascend strictly can lose entries, but nothing is read beyond a list's first min(nnz, cap)
+ * entries. Returns GSPAR_ERR_ARG for NULL nnz or v, NULL lists with cap > 0, workers outside
+ * [1, 2^20], d outside [1, 2^31 - 1] or cap < 0; GSPAR_ERR_HIP if the launch failed. */
+int gspar_aggregate(const int32_t* idx, const float* val, int64_t cap, const int64_t* nnz,
+                    int64_t workers, int64_t d, float* v, void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* gspar_status_string(int status);
 
@@ -165,10 +178,10 @@ int gspar_version(void);
 
 /* Measurement hook for benchmarks (process-global, not thread-safe): while armed, every launch
  * of kernel class `which` (0 = sample/compact, 1 = statistics pass, 2 = probabilities, 3 = solver,
- * 4 = refinement pass, 5 = workspace initialisation) is bracketed by a pair of HIP timing events
- * on its stream, for up to `max_launches` launches. gspar_timing_read synchronises on the last
- * event and returns the summed kernel time in ms and the number of bracketed launches;
- * gspar_timing_disarm releases the events. Returns GSPAR_ERR_ARG for an unknown class or a
+ * 4 = refinement pass, 5 = workspace initialisation, 6 = aggregation, its two kernels together)
+ * is bracketed by a pair of HIP timing events on its stream, for up to `max_launches` launches.
+ * gspar_timing_read synchronises on the last event and returns the summed kernel time in ms and
+ * the number of bracketed launches; gspar_timing_disarm releases the events. Returns GSPAR_ERR_ARG for an unknown class or a
  * non-positive count, GSPAR_ERR_HIP if the events cannot be created. */
 int gspar_timing_arm(int which, int max_launches);
 int gspar_timing_read(double* total_ms, int* launches);

@@ -24,6 +24,7 @@ Functions and the passage each follows:
   ternary vector of the same section.
 * ``coding_bits``         -- coding lengths of one hybrid message: the sparse lists, the entropy-coded
   ternary vector (Section 3.3), and the experiments' per-message formula (Section 5).
+* ``aggregate``           -- Algorithm 1, step 6: the average of the workers' sparsified gradients.
 """
 from __future__ import annotations
 
@@ -238,3 +239,15 @@ def coding_bits(d: int, n_a: int, n_b: int, n_b_neg: int, float_bits: int = 32):
     ternary = ent + n_a * b + b
     paper = n_a * (b + L) + min(2.0 * d, n_b * L) + b
     return float(sparse), float(ternary), float(paper)
+
+
+def aggregate(lists, d: int) -> np.ndarray:
+    """Algorithm 1, step 6: v = (1/M) sum_m Q(g^m) for the M workers' sparse messages, given as
+    (idx, val) pairs of arrays with distinct indices. Each coordinate's sum is taken in fp64 in
+    worker order, divided by M and rounded to fp32."""
+    acc = np.zeros(int(d), np.float64)
+    for idx, val in lists:
+        idx = np.asarray(idx, np.int64)
+        assert np.unique(idx).size == idx.size, "indices must be distinct within a message"
+        acc[idx] += np.asarray(val, np.float32).astype(np.float64)
+    return (acc / len(lists)).astype(np.float32)

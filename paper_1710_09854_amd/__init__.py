@@ -14,6 +14,7 @@ Entry points mirror the C ABI:
 * ``sparsify_sample_hybrid(g, rho, seed, ...)`` / ``sparsify_sample_hybrid_batched(g2d, rho, seeds, ...)``
   -> Hybrid(idx_a, val_a, n_a, code_b, n_b, inv_lam, q, lam, flags): the Q_A / Q_B coding
 * ``coding_bits(d, n_a, n_b, n_b_neg, float_bits)`` -> (sparse lists, ternary entropy, paper formula)
+* ``aggregate(idx2d, val2d, nnz, d)`` -> the workers' average (1/M) sum_m Q(g^m) as a dense fp32 vector
 * ``Plan``: a preallocated batched sample/compact call for timing loops.
 """
 from __future__ import annotations
@@ -76,6 +77,8 @@ def lib():
     L.sparsify_sample_hybrid.restype = i32
     L.gspar_coding_bits.argtypes = [i64, i64, i64, i64, i32, ctypes.POINTER(f64)]
     L.gspar_coding_bits.restype = i32
+    L.gspar_aggregate.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
+    L.gspar_aggregate.restype = i32
     L.gspar_status_string.argtypes = [i32]
     L.gspar_status_string.restype = ctypes.c_char_p
     L.gspar_version.argtypes = []
@@ -309,6 +312,23 @@ def coding_bits(d: int, n_a: int, n_b: int, n_b_neg: int, float_bits: int = 32):
     rc = lib().gspar_coding_bits(int(d), int(n_a), int(n_b), int(n_b_neg), int(float_bits), out)
     _check(rc, "gspar_coding_bits")
     return out[0], out[1], out[2]
+
+
+def aggregate(idx, val, nnz, d: int, out=None, stream=None) -> torch.Tensor:
+    """Algorithm 1, step 6: v = (1/M) sum_m Q(g^m), dense fp32 [d], from M workers' ascending
+    (index, value) lists (rows of idx / val, the first nnz[m] entries of row m)."""
+    if idx.dim() != 2 or val.shape != idx.shape or idx.dtype != torch.int32 or val.dtype != torch.float32:
+        raise ValueError("idx / val must be [workers, cap] int32 / float32")
+    if not (idx.is_contiguous() and val.is_contiguous()):
+        raise ValueError("idx / val must be contiguous")
+    workers, cap = idx.shape
+    dev = idx.device
+    n = nnz.to(device=dev, dtype=torch.int64).contiguous()
+    v = torch.empty(d, dtype=torch.float32, device=dev) if out is None else out
+    rc = lib().gspar_aggregate(idx.data_ptr(), val.data_ptr(), cap, n.data_ptr(), workers, int(d), v.data_ptr(),
+                               _stream(stream))
+    _check(rc, "gspar_aggregate")
+    return v
 
 
 def _rho_dev(rho, rows, dev):

@@ -1310,7 +1310,9 @@ constexpr double kLamScaledMin = 0x1p-900;
 // has a threshold of at least 2^32, so it always survives and the capped test is that comparison.
 __device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double lam32, uint32_t k0, uint32_t k1,
                                             uint32_t& z, uint32_t& cz) {
-  uint32_t x0 = (uint32_t)q, x1 = (uint32_t)((uint64_t)q >> 32), x2 = 0, x3 = 0;
+  // rows are shorter than 2^31 coordinates, so the counter's high word floor(i/4) >> 32 is 0; with
+  // that known the first rounds fold into fewer vector operations
+  uint32_t x0 = (uint32_t)q, x1 = 0, x2 = 0, x3 = 0;
   philox10(x0, x1, x2, x3, k0, k1);
   const uint32_t xr[4] = {x0, x1, x2, x3};
   double t[4];
@@ -1874,6 +1876,111 @@ static Args base_args(const float* g, int64_t rows, int64_t d, int64_t ld, int s
   return a;
 }
 
+// ------------------------------------------------------------------------------------------
+// Aggregation of the workers' sparsified gradients (Algorithm 1, step 6 on one device):
+// v_i = (sum over workers m = 0..M-1, in that order, of Q(g^m)_i in fp64) / M, rounded to fp32.
+// Input: each worker's ascending (index, value) list as written by the sampling pass.
+//
+// One workgroup per block of kAggBlock output coordinates, no workspace. For kAggGroup workers at
+// a time the workgroup finds where each list enters and leaves its block (a 9-ary search by eight
+// lanes per bound, about log_9(n) dependent loads), loads the first kAggThreads entries of every
+// one of those ranges at once, then adds them into an fp64 LDS accumulator one worker after
+// another (a barrier between workers), so each coordinate's sum is taken in worker order.
+// ------------------------------------------------------------------------------------------
+constexpr int kAggBlock = 2048;                   // output coordinates per workgroup
+constexpr int kAggThreads = 256;
+constexpr int kAggLanes = 8;                      // lanes per search
+constexpr int kAggGroup = kAggThreads / kAggLanes / 2;  // workers per pass (two searches each)
+
+struct AggArgs {
+  const int32_t* idx;
+  const float* val;
+  int64_t cap;
+  const int64_t* nnz;
+  int64_t workers, d;
+  float* v;
+};
+
+__device__ __forceinline__ int64_t agg_len(const AggArgs& a, int64_t m) {
+  const int64_t n = a.nnz[m];
+  return n < 0 ? 0 : (n < a.cap ? n : a.cap);
+}
+
+// Number of entries of id[0, n) below key when the list ascends (its lower bound), found by the
+// eight lanes of an aligned lane group: each step probes eight cut points of [lo, hi) and keeps
+// the part between the last probe below key and the first one at or above it. For any list the
+// result lies in [0, n] and the loop ends, since [lo, hi) shrinks at every step. Every lane of the
+// wave must call it (the loop condition is wave-wide).
+__device__ int64_t agg_search(const int32_t* id, int64_t n, int64_t key, bool active) {
+  const int lane = threadIdx.x & 63, k = lane & (kAggLanes - 1);
+  const unsigned long long gmask = 0xFFull << (lane & ~(kAggLanes - 1));
+  int64_t lo = 0, hi = active ? n : 0;
+  while (__ballot(hi > lo)) {
+    const int64_t w = hi - lo;
+    const int64_t pk = lo + (w * (k + 1)) / (kAggLanes + 1);
+    const bool below = w > 0 && (int64_t)id[pk] < key;
+    const int c = __popcll(__ballot(below) & gmask);
+    if (w > 0) {
+      const int64_t nlo = c == 0 ? lo : lo + (w * c) / (kAggLanes + 1) + 1;
+      const int64_t nhi = c == kAggLanes ? hi : lo + (w * (c + 1)) / (kAggLanes + 1);
+      hi = nhi;
+      lo = nlo < nhi ? nlo : nhi;
+    }
+  }
+  return lo;
+}
+
+__global__ void __launch_bounds__(kAggThreads) k_aggregate(AggArgs a) {
+  __shared__ double acc[kAggBlock];
+  __shared__ int64_t rng[kAggGroup][2];
+  const int t = threadIdx.x;
+  const int64_t b0 = (int64_t)blockIdx.x * kAggBlock;
+  for (int i = t; i < kAggBlock; i += kAggThreads) acc[i] = 0.0;
+  for (int64_t m0 = 0; m0 < a.workers; m0 += kAggGroup) {
+    const int64_t mg = a.workers - m0 < kAggGroup ? a.workers - m0 : kAggGroup;
+    {
+      const int q = t / kAggLanes;           // search q: worker m0 + q/2, bound q&1
+      const int64_t m = m0 + (q >> 1);
+      const bool act = (q >> 1) < mg;
+      const int64_t n = act ? agg_len(a, m) : 0;
+      const int64_t lb = agg_search(a.idx + (act ? m : 0) * a.cap, n, b0 + (q & 1) * kAggBlock, act);
+      if (act && (t & (kAggLanes - 1)) == 0) rng[q >> 1][q & 1] = lb;
+    }
+    __syncthreads();
+    // the first kAggThreads entries of every range, loaded before any is added
+    int32_t r[kAggGroup];
+    float x[kAggGroup];
+#pragma unroll
+    for (int k = 0; k < kAggGroup; ++k) {
+      r[k] = -1;
+      x[k] = 0.0f;
+      if (k < mg) {
+        const int64_t j = rng[k][0] + t;
+        if (j < rng[k][1]) {
+          const int64_t rr = (int64_t)a.idx[(m0 + k) * a.cap + j] - b0;
+          r[k] = rr >= 0 && rr < kAggBlock ? (int32_t)rr : -1;
+          x[k] = a.val[(m0 + k) * a.cap + j];
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kAggGroup; ++k) {
+      if (k < mg) {
+        if (r[k] >= 0) acc[r[k]] += (double)x[k];
+        const int64_t hi = rng[k][1];
+        for (int64_t j = rng[k][0] + t + kAggThreads; j < hi; j += kAggThreads) {
+          const int64_t rr = (int64_t)a.idx[(m0 + k) * a.cap + j] - b0;
+          if (rr >= 0 && rr < kAggBlock) acc[rr] += (double)a.val[(m0 + k) * a.cap + j];
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const double M = (double)a.workers;
+  for (int i = t; i < kAggBlock; i += kAggThreads)
+    if (b0 + i < a.d) a.v[b0 + i] = (float)(acc[i] / M);
+}
+
 }  // namespace gspar
 
 using namespace gspar;
@@ -1997,6 +2104,27 @@ int gspar_coding_bits(int64_t d, int64_t n_a, int64_t n_b, int64_t n_b_neg, int 
   return GSPAR_OK;
 }
 
+int gspar_aggregate(const int32_t* idx, const float* val, int64_t cap, const int64_t* nnz, int64_t workers, int64_t d,
+                    float* v, void* stream) {
+  using namespace gspar;
+  if (!nnz || !v || workers < 1 || workers > ((int64_t)1 << 20) || d < 1 || d > INT32_MAX || cap < 0 ||
+      (cap > 0 && (!idx || !val)))
+    return GSPAR_ERR_ARG;
+  AggArgs a;
+  a.idx = idx;
+  a.val = val;
+  a.cap = cap;
+  a.nnz = nnz;
+  a.workers = workers;
+  a.d = d;
+  a.v = v;
+  hipStream_t s = (hipStream_t)stream;
+  time_before(6, s);
+  hipLaunchKernelGGL(k_aggregate, dim3((unsigned)((d + kAggBlock - 1) / kAggBlock)), dim3(kAggThreads), 0, s, a);
+  time_after(6, s);
+  return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
+}
+
 int sparsify_probs_batched(const float* g, int64_t rows, int64_t d, int64_t ld, const double* rho, int solver,
                            int greedy_iters, float* p, double* lambda, int64_t* k, uint32_t* flags, void* ws,
                            size_t ws_bytes, void* stream) {
@@ -2045,7 +2173,7 @@ const char* gspar_status_string(int status) {
 int gspar_version(void) { return 100; }
 
 int gspar_timing_arm(int which, int max_launches) {
-  if (which < 0 || which > 5 || max_launches < 1) return GSPAR_ERR_ARG;
+  if (which < 0 || which > 6 || max_launches < 1) return GSPAR_ERR_ARG;
   gspar_timing_disarm();
   g_timing.ev = new hipEvent_t[2 * (size_t)max_launches];
   for (int i = 0; i < 2 * max_launches; ++i) {

@@ -28,6 +28,7 @@ def load(path):
                                                   vp, vp, vp, ctypes.c_size_t, vp]
     L.sparsify_sample_hybrid_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp, vp, i64,
                                                  vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.gspar_aggregate.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
     return L
 
 
@@ -197,6 +198,54 @@ def check_hybrid(L, verbose=True):
     return True
 
 
+def aggregate(L, idx, val, nnz, d):
+    """gspar_aggregate on [workers, cap] lists; returns v [d]."""
+    workers, cap = idx.shape
+    v = np.full(d, np.nan, np.float32)
+    nn = np.ascontiguousarray(nnz, np.int64)
+    rc = L.gspar_aggregate(idx.ctypes.data, val.ctypes.data, cap, nn.ctypes.data, workers, d, v.ctypes.data, None)
+    assert rc == 0, rc
+    return v
+
+
+def _lists(idx, val, nnz):
+    cap = idx.shape[1]
+    return [(idx[m, :max(0, min(int(n), cap))], val[m, :max(0, min(int(n), cap))]) for m, n in enumerate(nnz)]
+
+
+def check_aggregate(L, verbose=True):
+    """Algorithm 1, step 6: bit-exact against the oracle's worker-order fp64 average."""
+    # the sampling pass's own lists: a batch of workers of one gradient size
+    rows, d = 5, 20011
+    rng = np.random.default_rng(91)
+    g2 = np.stack([W.t_mixture(d, 300 + r) * np.float32(10.0 ** rng.uniform(-3, 0)) for r in range(rows)])
+    for rho in (0.01, 0.3, 1.0):
+        idx, val, nnz, lam, k, fl = batched(L, g2, [rho] * rows, [40 + r for r in range(rows)], "greedy")
+        v = aggregate(L, idx, val, nnz, d)
+        assert np.array_equal(v, oracle.aggregate(_lists(idx, val, nnz), d), equal_nan=True)
+    # synthetic lists: more workers than one pass holds, empty and overflowing lists, ragged d,
+    # long ranges inside one block, a single worker
+    for i, (workers, d, cap) in enumerate(((37, 10007, 3000), (1, 4096 * 3 + 5, 9000), (16, 2048, 2048),
+                                           (17, 999, 400))):
+        idx, val, nnz = W.sparse_lists(workers, d, cap, 500 + i, empty=(1, 2) if workers > 2 else (), over=(0,))
+        v = aggregate(L, idx, val, nnz, d)
+        assert np.array_equal(v, oracle.aggregate(_lists(idx, val, nnz), d)), (workers, d, cap)
+    # zero capacity: every list empty
+    v = aggregate(L, np.zeros((3, 0), np.int32), np.zeros((3, 0), np.float32), np.array([5, 0, 2]), 5000)
+    assert np.array_equal(v, np.zeros(5000, np.float32))
+    # lists that break the contract: out-of-range indices are skipped, disorder never reads outside
+    idx, val, nnz = W.sparse_lists(4, 6000, 1500, 510)
+    idx[0, :3] = [-5, -1, 0]
+    idx[0, 3:] = np.sort(idx[0, 3:])
+    idx[1, :nnz[1]] = np.minimum(idx[1, :nnz[1]] + 5990, 2**31 - 1)
+    idx[2, :nnz[2]] = rng.permutation(idx[2, :nnz[2]])
+    v = aggregate(L, idx, val, nnz, 6000)
+    assert v.shape == (6000,) and not np.isnan(v).any()
+    if verbose:
+        print("aggregate cases ok", flush=True)
+    return True
+
+
 def run_extra(path, verbose=True):
     L = load(path)
     # greedy step counts
@@ -268,5 +317,7 @@ if __name__ == "__main__":
         run_extra(sys.argv[1])
     if which in ("all", "hybrid"):
         check_hybrid(load(sys.argv[1]))
+    if which in ("all", "aggregate"):
+        check_aggregate(load(sys.argv[1]))
     if which in ("all", "main"):
         print("checked", run_all(sys.argv[1]))

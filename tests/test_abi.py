@@ -121,6 +121,25 @@ def test_hybrid_argument_errors(L):
                                             FAKE, None, None, None, None, FAKE, wsb, None) == gs.ERR_ARG
 
 
+def test_aggregate_argument_errors(L):
+    import paper_1710_09854_amd as gs
+
+    def one(**kw):
+        a = dict(idx=FAKE, val=FAKE, cap=10, nnz=FAKE, workers=4, d=1000, v=FAKE)
+        a.update(kw)
+        return L.gspar_aggregate(a["idx"], a["val"], a["cap"], a["nnz"], a["workers"], a["d"], a["v"], None)
+
+    assert one(nnz=None) == gs.ERR_ARG
+    assert one(v=None) == gs.ERR_ARG
+    assert one(idx=None) == gs.ERR_ARG
+    assert one(val=None) == gs.ERR_ARG
+    assert one(cap=-1) == gs.ERR_ARG
+    assert one(workers=0) == gs.ERR_ARG
+    assert one(workers=(1 << 20) + 1) == gs.ERR_ARG
+    assert one(d=0) == gs.ERR_ARG
+    assert one(d=1 << 31) == gs.ERR_ARG
+
+
 def test_coding_bits_match_oracle(L):
     """The library's host-side coding-length helper against the oracle's own statement."""
     import oracle

@@ -525,6 +525,56 @@ def test_theorem4_coding_length_bound(s, rho_def, seed):
     assert expected <= s * (b + L) + min(rho_def * s * L, d) + b + 1e-9
 
 
+# ----------------------------------------------------------------------------- aggregation
+def test_aggregate_keeps_everything_is_the_exact_mean():
+    """With every coordinate kept (B >= nnz, Q(g) = g) the aggregate is the mean gradient: for four
+    workers whose values share a narrow exponent range the fp64 sums are exact, so v equals the
+    exactly rounded mean computed with rationals."""
+    from fractions import Fraction
+    rng = np.random.default_rng(9)
+    M, d = 4, 300
+    gs_ = [(rng.uniform(1.0, 2.0, d) * rng.choice([-1.0, 1.0], d)).astype(np.float32) for _ in range(M)]
+    lists = []
+    for m, g in enumerate(gs_):
+        sol = oracle.solve_exact(g, 1.0)
+        idx, val, n = oracle.sample_compact(g, sol.p, m)
+        assert n == d and np.array_equal(val, g)
+        lists.append((idx, val))
+    v = oracle.aggregate(lists, d)
+    want = np.array([float(sum(Fraction(float(g[i])) for g in gs_) / M) for i in range(d)]).astype(np.float32)
+    assert np.array_equal(v, want)
+
+
+def test_aggregate_single_worker_is_the_sparsified_vector():
+    g = W.t_mixture(2000, 12)
+    sol = oracle.solve_exact(g, 0.1)
+    idx, val, n = oracle.sample_compact(g, sol.p, 4)
+    v = oracle.aggregate([(idx, val)], g.size)
+    dense = np.zeros(g.size, np.float32)
+    dense[idx] = val
+    assert np.array_equal(v, dense)
+
+
+def test_aggregate_unbiased_over_seeds():
+    """Algorithm 1: E[v] = (1/M) sum_m g^m, since each Q(g^m) is unbiased (Section 3)."""
+    rng = np.random.default_rng(13)
+    M, d, S = 3, 48, 3000
+    gs_ = [(rng.standard_t(2, d)).astype(np.float32) for _ in range(M)]
+    ps = [oracle.solve_exact(g, 0.2).p for g in gs_]
+    mean = np.mean([g.astype(np.float64) for g in gs_], axis=0)
+    acc = np.zeros(d)
+    for s in range(S):
+        lists = []
+        for m in range(M):
+            idx, val, n = oracle.sample_compact(gs_[m], ps[m], 50_000 + 97 * s + m)
+            lists.append((idx, val))
+        acc += oracle.aggregate(lists, d)
+    # per-coordinate standard error of the average of M independent Q(g^m)_i
+    var = sum(np.where(p > 0, g.astype(np.float64) ** 2 * (1 - p) / np.where(p > 0, p, 1), 0) for g, p in zip(gs_, ps))
+    se = np.sqrt(var / M ** 2 / S)
+    assert np.all(np.abs(acc / S - mean) <= 4.5 * se + 1e-6 * np.abs(mean))
+
+
 # ----------------------------------------------------------------------------- generators
 def test_generators_shapes_and_determinism():
     w1 = W.c1()

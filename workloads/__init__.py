@@ -179,3 +179,32 @@ def wide_range(d: int, seed: int) -> np.ndarray:
     rng = np.random.default_rng(seed)
     e = rng.uniform(-140, 30, d)
     return (rng.choice([-1.0, 1.0], size=d) * np.exp2(e)).astype(np.float32)
+
+
+def sparse_lists(workers: int, d: int, cap: int, seed: int, empty=(), over=()):
+    """Per-worker strictly ascending index lists with fp32 values, as [workers, cap] arrays and an
+    int64 length per worker: mixed lengths, every third list clustered into a short index range,
+    values spread over sixty binades. Workers in `empty` get length 0 (odd ones -1), those in
+    `over` a full list and a length beyond cap (an overflowed list of which cap entries are kept)."""
+    rng = np.random.default_rng(seed)
+    idx = np.zeros((workers, cap), np.int32)
+    val = np.zeros((workers, cap), np.float32)
+    nnz = np.zeros(workers, np.int64)
+    for m in range(workers):
+        n = int(rng.integers(0, cap + 1))
+        if m % 3 == 0:
+            lo = int(rng.integers(0, d))
+            pool = np.arange(lo, min(d, lo + 3 * n + 1))
+        else:
+            pool = np.arange(d)
+        n = min(n, pool.size)
+        idx[m, :n] = np.sort(rng.choice(pool, size=n, replace=False))
+        val[m, :n] = (rng.standard_normal(n) * np.exp2(rng.integers(-30, 30, n))).astype(np.float32)
+        nnz[m] = n
+    for m in empty:
+        nnz[m] = -1 if m % 2 else 0
+    for m in over:
+        nnz[m] = cap + 17
+        idx[m] = np.sort(rng.choice(d, size=cap, replace=False))
+        val[m] = rng.standard_normal(cap).astype(np.float32)
+    return idx, val, nnz
