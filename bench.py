@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--hybrid", action="store_true",
                     help="time the hybrid coding entry point (Q_A / Q_B lists) instead of the compaction")
     ap.add_argument("--dense-q", action="store_true", help="with --hybrid, also write the dense ternary vector")
+    ap.add_argument("--per-layer", action="store_true",
+                    help="c4 only: sparsify each of the 54 ResNet-50 layers on its own (one lambda per layer, "
+                         "Philox keys 4000 + layer) in one segmented call")
     ap.add_argument("--aggregate", action="store_true",
                     help="with --cells: also time the aggregation (Algorithm 1, step 6) of each cell's lists, "
                          "one worker per row")
@@ -142,7 +145,21 @@ def summarize_pmc(fetch_dir, write_dir, workload):
     print(json.dumps(data[workload], indent=1, sort_keys=True))
 
 
-def cpu_baseline(wl, combos, target_s):
+def layer_setup(args, wl, dev):
+    """Inputs of a per-layer run: the flat gradient, its segments and one Philox key per layer."""
+    import torch
+
+    import paper_1710_09854_amd as gs
+
+    if "segments" not in wl.meta:
+        raise SystemExit("--per-layer needs a workload with layer segments (c4)")
+    seg = gs.Segments.from_lengths(wl.meta["segments"], device=dev)
+    g = torch.from_numpy(wl.g[0]).to(dev)
+    seeds = torch.arange(4000, 4000 + seg.segs, dtype=torch.int64, device=dev)
+    return g, seg, seeds
+
+
+def cpu_baseline(wl, combos, target_s, per_layer=False):
     """The oracle as it stands (single thread), on whole rows of the same workload until about
     target_s seconds of work; returns elements/s and what the sample was."""
     import oracle
@@ -155,6 +172,26 @@ def cpu_baseline(wl, combos, target_s):
         elems = 0
         r = 0
         prefix = min(wl.d, 1 << 24)  # rows longer than 2^24 are sampled by their leading 2^24 entries
+        if per_layer:
+            # layer after layer of the flat gradient, each solved and sampled on its own
+            lens = wl.meta["segments"]
+            off = [0]
+            for n in lens:
+                off.append(off[-1] + n)
+            while True:
+                s = r % len(lens)
+                layer = wl.g[0][off[s]:off[s + 1]]
+                for solver, rho in combos:
+                    oracle.sparsify(layer, rho, solver, wl.iters, 4000 + s)
+                    elems += layer.size
+                r += 1
+                if time.perf_counter() - t0 >= target_s or r >= len(lens):
+                    break
+            dt = time.perf_counter() - t0
+            return {"value": elems / dt, "unit": "elements/s", "cores": 1, "kind": "oracle",
+                    "sample": f"the first {r} of the {len(lens)} layers, each solved and sampled on its own, x "
+                              f"{len(combos)} (solver, rho) combos; {dt:.1f} s of fp64 oracle work on 1 of the "
+                              f"host's {host_cores} cores"}
         while True:
             row = wl.g[r % wl.rows][:prefix]
             for solver, rho in combos:
@@ -194,14 +231,23 @@ def cells(args):
     scratch = torch.empty(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
     for name in names:
         wl = workloads.CONFIGS[name]()
-        g = torch.from_numpy(wl.g).to(dev)
-        rows, d = wl.rows, wl.d
-        seeds = torch.tensor([s - (1 << 64) if s >= (1 << 63) else s for s in wl.seeds], dtype=torch.int64,
-                             device=dev)
+        seg = None
+        if args.per_layer:
+            if "segments" not in wl.meta:
+                continue
+            g, seg, seeds = layer_setup(args, wl, dev)
+            rows, d = seg.segs, seg.max_len
+            n_elems = seg.total
+        else:
+            g = torch.from_numpy(wl.g).to(dev)
+            rows, d = wl.rows, wl.d
+            n_elems = rows * d
+            seeds = torch.tensor([s - (1 << 64) if s >= (1 << 63) else s for s in wl.seeds], dtype=torch.int64,
+                                 device=dev)
         for solver in ([args.solver] if args.solver else wl.solvers):
             for rho in ([args.rho] if args.rho is not None else wl.rhos):
                 plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho),
-                               hybrid=args.hybrid, dense_q=args.dense_q)
+                               hybrid=args.hybrid, dense_q=args.dense_q, segments=seg)
                 rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
                 for _ in range(3):
                     plan.run(g, rho_dev, seeds)
@@ -222,18 +268,20 @@ def cells(args):
                 warm = float(np.median([timed(False) for _ in range(20)]))
                 cold = float(np.median([timed(True) for _ in range(5)]))
                 nnz, out_bytes = plan.survivors_and_bytes()
-                alg = 4.0 * rows * d + out_bytes
+                alg = 4.0 * n_elems + out_bytes
+                entry = "hybrid" + ("+q" if args.dense_q else "") if args.hybrid else "compact"
                 cell = {"workload": wl.name, "solver": solver, "rho": rho, "rows": rows, "d": d, "nnz": nnz,
-                        "entry": "hybrid" + ("+q" if args.dense_q else "") if args.hybrid else "compact",
+                        "entry": entry + ("_per_layer" if args.per_layer else ""),
                         "lambda_row0": float(plan.lam[0].item()),
-                        "warm_us": warm * 1e6, "warm_elements_per_s": rows * d / warm,
-                        "cold_us": cold * 1e6, "cold_elements_per_s": rows * d / cold,
+                        "warm_us": warm * 1e6, "warm_elements_per_s": n_elems / warm,
+                        "cold_us": cold * 1e6, "cold_elements_per_s": n_elems / cold,
                         "algorithmic_bytes": alg, "algorithmic_frac_warm": alg / warm / 1e9 / HBM_PEAK_GBS,
                         "algorithmic_frac_cold": alg / cold / 1e9 / HBM_PEAK_GBS}
                 if not args.no_cpu_baseline:
-                    cell["cpu_baseline"] = cpu_baseline(wl, [(solver, rho)], args.cpu_seconds)
+                    cell["cpu_baseline"] = cpu_baseline(wl, [(solver, rho)], args.cpu_seconds,
+                                                        per_layer=args.per_layer)
                 print(json.dumps(cell), flush=True)
-                if args.aggregate and not args.hybrid:
+                if args.aggregate and not args.hybrid and not args.per_layer:
                     print(json.dumps(aggregate_cell(args, wl, plan, scratch, solver, rho)), flush=True)
                 del plan
         del g
@@ -331,13 +379,21 @@ def main():
     solvers = [args.solver] if args.solver else wl.solvers
     rhos = [args.rho] if args.rho is not None else wl.rhos
     combos = [(s, r) for s in solvers for r in rhos]
-    g = torch.from_numpy(wl.g).to(dev)
-    rows, d = wl.rows, wl.d
-    seeds = torch.tensor([s - (1 << 64) if s >= (1 << 63) else s for s in wl.seeds], dtype=torch.int64, device=dev)
+    seg = None
+    if args.per_layer:
+        g, seg, seeds = layer_setup(args, wl, dev)
+        rows, d = seg.segs, seg.max_len
+        n_elems = seg.total
+    else:
+        g = torch.from_numpy(wl.g).to(dev)
+        rows, d = wl.rows, wl.d
+        n_elems = rows * d
+        seeds = torch.tensor([s - (1 << 64) if s >= (1 << 63) else s for s in wl.seeds], dtype=torch.int64,
+                             device=dev)
     plans = []
     for solver, rho in combos:
         plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho),
-                       hybrid=args.hybrid, dense_q=args.dense_q)
+                       hybrid=args.hybrid, dense_q=args.dense_q, segments=seg)
         rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
         plans.append((plan, rho_dev))
 
@@ -386,13 +442,14 @@ def main():
         t.close()
         kernels[name] = {"us_per_step": 1e3 * ms / reps, "launches_per_step": n / reps}
     # survivors are identical in every step (same seeds), so per-step bytes are exact
-    elements_per_step = rows * d * len(plans)
+    elements_per_step = n_elems * len(plans)
     ms_per_step = elapsed * 1e3 / args.steps
     value = elements_per_step / (elapsed / args.steps)
     alg_bytes_per_step = 4.0 * elements_per_step + out_bytes
     avg_launch_ms = ksample_ms / max(launches, 1)
     achieved = alg_bytes_per_step / len(plans) / (avg_launch_ms * 1e-3) / 1e9
-    traffic = traffic_for(wl.name) if (args.solver is None and args.rho is None and not args.hybrid) else None
+    traffic = (traffic_for(wl.name) if (args.solver is None and args.rho is None and not args.hybrid
+                                         and not args.per_layer) else None)
     line = {
         "metric": METRIC,
         "value": value,
@@ -406,10 +463,12 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": wl.name, "rows": rows, "d": d,
+        "config": {"workload": wl.name + ("_per_layer" if args.per_layer else ""), "rows": rows, "d": d,
                    "solvers": solvers, "rho": rhos, "greedy_iters": wl.iters,
-                   "seeds": "per-row Philox keys " + ("1000+r" if args.workload == "c2" else str(wl.seeds[0])),
-                   "parallelism": "single GPU, rows batched in one call",
+                   "seeds": ("per-layer Philox keys 4000+layer" if args.per_layer else
+                             "per-row Philox keys " + ("1000+r" if args.workload == "c2" else str(wl.seeds[0]))),
+                   "parallelism": ("single GPU, 54 layers (rows: segments, d: the longest) in one segmented call"
+                                   if args.per_layer else "single GPU, rows batched in one call"),
                    "output": ("hybrid coding Q_A (index, value) + Q_B (index | sign)" +
                               (" + dense ternary vector" if args.dense_q else "")) if args.hybrid
                    else "ascending (int32 index, fp32 value) pairs"},
@@ -435,7 +494,7 @@ def main():
             path["measured_frac"] = path["measured_GBps"] / HBM_PEAK_GBS
     line["path"] = path
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, combos, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(wl, combos, args.cpu_seconds, per_layer=args.per_layer)
     line["kernels"] = kernels
     line["nnz_per_step"] = nnz_tot
     line["src_sha"] = src_hash()

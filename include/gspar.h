@@ -67,7 +67,9 @@ enum {
   GSPAR_FLAG_OVERFLOW = 2,  /* more survivors than capacity: the first `capacity` pairs are
                                written and nnz holds the true count                          */
   GSPAR_FLAG_ALLZERO = 4,   /* g is identically zero: nnz = 0                                 */
-  GSPAR_FLAG_BADRHO = 8     /* (batched) rho[r] outside [0, 1] or NaN: row skipped, nnz = 0  */
+  GSPAR_FLAG_BADRHO = 8,    /* (batched) rho[r] outside [0, 1] or NaN: row skipped, nnz = 0  */
+  GSPAR_FLAG_BADSEG = 32    /* (segmented) the device offsets of the segment disagree with the
+                               host offsets' bounds: segment skipped, nnz = 0                 */
 };
 
 /* Bytes of device workspace needed by a call on `rows` rows of length d with `solver`. The
@@ -156,6 +158,32 @@ int sparsify_sample_hybrid(const float* g, int64_t d, double rho, int solver, in
  * float_bits < 1. */
 int gspar_coding_bits(int64_t d, int64_t n_a, int64_t n_b, int64_t n_b_neg, int float_bits,
                       double* out);
+
+/* Per-layer sparsification (Section 5.2: each layer of a network is sparsified on its own).
+ * Segment s of the flat vector g is g[off[s] .. off[s+1]) and is treated as its own row: its own
+ * density rho[s] (budget rho[s] * length), its own lambda, capped set and Philox key seeds[s], with
+ * the Philox counter and the output indices taken within the segment, so the result of a segment
+ * equals a single-row call on it. off_host and off_dev hold the same segs + 1 offsets (int64), on the
+ * host (checked here: off[0] >= 0, nondecreasing, every length below 2^31; used to size the launch)
+ * and on the device (read by the kernels, which check each segment again against the host's bounds
+ * and flag one that disagrees GSPAR_FLAG_BADSEG); g holds off[segs] floats. Segments may be empty
+ * (then flagged GSPAR_FLAG_ALLZERO). Vector loads are used when g is 16-byte aligned and every
+ * offset is a multiple of 4. The workspace is gspar_workspace_bytes(segs, L, solver) with L the
+ * longest segment (at least 1). rho [segs] fp64 and seeds [segs] uint64 are DEVICE arrays.
+ * sparsify_sample_compact_segmented writes segment s's survivors to idx[s*cap_per_seg ...] and
+ * val[s*cap_per_seg ...] and its count to nnz[s]; sparsify_probs_segmented writes p in g's layout
+ * (p[off[s] + i]). lambda, k and flags are [segs] (optional where the batched calls allow it).
+ * Errors: those of the batched calls, and GSPAR_ERR_ARG for NULL or invalid offsets or segs outside
+ * [1, 2^24]. */
+int sparsify_sample_compact_segmented(const float* g, int64_t segs, const int64_t* off_host,
+                                      const int64_t* off_dev, const double* rho, int solver,
+                                      int greedy_iters, const uint64_t* seeds, int32_t* idx, float* val,
+                                      int64_t cap_per_seg, int64_t* nnz, double* lambda, int64_t* k,
+                                      uint32_t* flags, void* ws, size_t ws_bytes, void* stream);
+int sparsify_probs_segmented(const float* g, int64_t segs, const int64_t* off_host,
+                             const int64_t* off_dev, const double* rho, int solver, int greedy_iters,
+                             float* p, double* lambda, int64_t* k, uint32_t* flags, void* ws,
+                             size_t ws_bytes, void* stream);
 
 /* Aggregation of the workers' sparsified gradients (Algorithm 1, step 6, on one device): the dense
  * average v_i = (1/M) sum_m Q(g^m)_i for M = `workers`, from the lists that

@@ -25,6 +25,8 @@ Functions and the passage each follows:
 * ``coding_bits``         -- coding lengths of one hybrid message: the sparse lists, the entropy-coded
   ternary vector (Section 3.3), and the experiments' per-message formula (Section 5).
 * ``aggregate``           -- Algorithm 1, step 6: the average of the workers' sparsified gradients.
+* ``sparsify_segments``   -- per-layer sparsification (Section 5.2): every segment of a flat
+  gradient solved and sampled on its own.
 """
 from __future__ import annotations
 
@@ -251,3 +253,19 @@ def aggregate(lists, d: int) -> np.ndarray:
         assert np.unique(idx).size == idx.size, "indices must be distinct within a message"
         acc[idx] += np.asarray(val, np.float32).astype(np.float64)
     return (acc / len(lists)).astype(np.float32)
+
+
+def sparsify_segments(g, offsets, rhos, seeds, solver: str = "greedy", iters: int = 2):
+    """Section 5.2 sparsifies each layer independently: segment s = g[off[s]:off[s+1]] gets its own
+    budget rho[s] * length, its own solution and its own random words (key seeds[s], counters
+    counted within the segment). Returns one (Solution, idx, val, nnz) per segment, idx within the
+    segment."""
+    g = _f32(g)
+    out = []
+    for s_, (b, e) in enumerate(zip(offsets[:-1], offsets[1:])):
+        seg = g[int(b):int(e)]
+        if seg.size == 0:
+            out.append((None, np.zeros(0, np.int32), np.zeros(0, np.float32), 0))
+            continue
+        out.append(sparsify(seg, float(rhos[s_]), solver, iters, int(seeds[s_])))
+    return out

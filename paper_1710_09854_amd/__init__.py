@@ -35,6 +35,7 @@ FLAG_OVERFLOW = 2
 FLAG_ALLZERO = 4
 FLAG_BADRHO = 8
 FLAG_INTERNAL = 16
+FLAG_BADSEG = 32
 
 OK = 0
 ERR_ARG = -1
@@ -77,6 +78,11 @@ def lib():
     L.sparsify_sample_hybrid.restype = i32
     L.gspar_coding_bits.argtypes = [i64, i64, i64, i64, i32, ctypes.POINTER(f64)]
     L.gspar_coding_bits.restype = i32
+    L.sparsify_sample_compact_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, i64, vp, vp, vp,
+                                                    vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_compact_segmented.restype = i32
+    L.sparsify_probs_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_probs_segmented.restype = i32
     L.gspar_aggregate.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
     L.gspar_aggregate.restype = i32
     L.gspar_status_string.argtypes = [i32]
@@ -381,7 +387,14 @@ class Plan:
 
     def __init__(self, rows: int, d: int, ld: int | None = None, solver="greedy", iters: int = 2,
                  cap_per_row: int | None = None, rho_for_cap: float = 1.0, device="cuda", hybrid: bool = False,
-                 dense_q: bool = False):
+                 dense_q: bool = False, segments: "Segments | None" = None):
+        # with segments: one output row per segment (rows and d are then the segment count and the
+        # longest segment)
+        self.seg = segments
+        if segments is not None:
+            if hybrid:
+                raise ValueError("segmented calls write the compaction output")
+            rows, d = segments.segs, segments.max_len
         self.rows, self.d = rows, d
         self.ld = d if ld is None else ld
         self.sid = _solver_id(solver)
@@ -404,6 +417,14 @@ class Plan:
             self.q = torch.empty((rows, self.ld), dtype=torch.int8, device=dev) if dense_q else None
 
     def run(self, g, rho_dev, seeds_dev, stream=None):
+        if self.seg is not None:
+            rc = lib().sparsify_sample_compact_segmented(
+                g.data_ptr(), self.rows, self.seg.host.data_ptr(), self.seg.dev.data_ptr(), rho_dev.data_ptr(),
+                self.sid, self.iters, seeds_dev.data_ptr(), self.idx.data_ptr(), self.val.data_ptr(), self.cap,
+                self.nnz.data_ptr(), self.lam.data_ptr(), self.k.data_ptr(), self.flags.data_ptr(),
+                self.ws.data_ptr(), self.ws.numel(), _stream(stream))
+            _check(rc, "sparsify_sample_compact_segmented")
+            return
         if self.hybrid:
             rc = lib().sparsify_sample_hybrid_batched(
                 g.data_ptr(), self.rows, self.d, self.ld, rho_dev.data_ptr(), self.sid, self.iters,
@@ -455,6 +476,81 @@ def sparsify_sample_compact_batched(g, rho, seeds, solver="greedy", iters: int =
                                                _stream(stream))
     _check(rc, "sparsify_sample_compact_batched")
     return Sparse(idx[:, :cap], val[:, :cap], nnz, lam, k, fl)
+
+
+class Segments:
+    """Offsets of the segments (layers) of a flat gradient, kept on the host and on the device:
+    segment s is g[off[s]:off[s+1]]."""
+
+    def __init__(self, offsets, device="cuda"):
+        self.host = torch.as_tensor(offsets, dtype=torch.int64, device="cpu").contiguous().clone()
+        if self.host.dim() != 1 or self.host.numel() < 2:
+            raise ValueError("offsets need at least two entries")
+        self.dev = self.host.to(torch.device(device))
+        self.segs = self.host.numel() - 1
+        self.max_len = max(1, int((self.host[1:] - self.host[:-1]).max().item()))
+        self.total = int(self.host[-1].item())
+
+    @classmethod
+    def from_lengths(cls, lengths, device="cuda"):
+        lens = torch.as_tensor(lengths, dtype=torch.int64, device="cpu")
+        return cls(torch.cat([torch.zeros(1, dtype=torch.int64), torch.cumsum(lens, 0)]), device)
+
+
+def _flat(g, seg: Segments):
+    g = _as_row(g)
+    if g.numel() < seg.total:
+        raise ValueError("g is shorter than the last segment offset")
+    return g
+
+
+def sparsify_sample_compact_segmented(g, seg: Segments, rho, seeds, solver="greedy", iters: int = 2,
+                                      cap_per_seg: int | None = None, workspace=None, stream=None) -> Sparse:
+    """Per-layer sparsification: every segment of the flat gradient g gets its own lambda, density
+    and Philox key; row s of the outputs holds segment s's survivors, indexed within the segment."""
+    g = _flat(g, seg)
+    dev = g.device
+    rows = seg.segs
+    r = _rho_dev(rho, rows, dev)
+    s = _seeds_dev(seeds, rows, dev)
+    if cap_per_seg is None:
+        rmax = float(r.max().item())
+        cap_per_seg = capacity_hint(seg.max_len, min(max(rmax, 0.0), 1.0))
+    cap = int(cap_per_seg)
+    idx = torch.empty((rows, max(cap, 1)), dtype=torch.int32, device=dev)
+    val = torch.empty((rows, max(cap, 1)), dtype=torch.float32, device=dev)
+    nnz = torch.empty(rows, dtype=torch.int64, device=dev)
+    lam = torch.empty(rows, dtype=torch.float64, device=dev)
+    k = torch.empty(rows, dtype=torch.int64, device=dev)
+    fl = torch.empty(rows, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid))
+    rc = lib().sparsify_sample_compact_segmented(g.data_ptr(), rows, seg.host.data_ptr(), seg.dev.data_ptr(),
+                                                 r.data_ptr(), sid, int(iters), s.data_ptr(), idx.data_ptr(),
+                                                 val.data_ptr(), cap, nnz.data_ptr(), lam.data_ptr(), k.data_ptr(),
+                                                 fl.data_ptr(), buf.data_ptr(), nb, _stream(stream))
+    _check(rc, "sparsify_sample_compact_segmented")
+    return Sparse(idx[:, :cap], val[:, :cap], nnz, lam, k, fl)
+
+
+def sparsify_probs_segmented(g, seg: Segments, rho, solver="greedy", iters: int = 2, want_p: bool = True,
+                             workspace=None, stream=None) -> Probs:
+    """Per-layer probabilities: p in g's flat layout, lambda / k / flags per segment."""
+    g = _flat(g, seg)
+    dev = g.device
+    rows = seg.segs
+    r = _rho_dev(rho, rows, dev)
+    p = torch.zeros(seg.total, dtype=torch.float32, device=dev) if want_p else None
+    lam = torch.empty(rows, dtype=torch.float64, device=dev)
+    k = torch.empty(rows, dtype=torch.int64, device=dev)
+    fl = torch.empty(rows, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid))
+    rc = lib().sparsify_probs_segmented(g.data_ptr(), rows, seg.host.data_ptr(), seg.dev.data_ptr(), r.data_ptr(),
+                                        sid, int(iters), _ptr(p), lam.data_ptr(), k.data_ptr(), fl.data_ptr(),
+                                        buf.data_ptr(), nb, _stream(stream))
+    _check(rc, "sparsify_probs_segmented")
+    return Probs(p, lam, k, fl)
 
 
 class KernelTimer:

@@ -329,7 +329,28 @@ struct Args {
   int64_t* k_out;
   uint32_t* flags_out;
   float* p;
+  // segmented calls: row r is g[seg[r], seg[r + 1]) (device offsets), d the longest segment
+  const int64_t* seg;
+  int64_t seg_total;  // the host's last offset: no segment may end beyond it
+  int64_t seg_elems;  // the host's total segment length (sizes the histogram passes)
+  int seg_align;      // vector loads in use: every segment must start at a multiple of 4
 };
+
+// Start and length of row r: row r of a strided batch (offset r * ld, length d), or segment r of a
+// segmented call. A segment whose device offsets break the bounds the host checked (order, end,
+// length, alignment of the vector path) reads as empty and returns false.
+__device__ __forceinline__ bool row_span(const Args& a, int64_t r, int64_t& base, int64_t& len) {
+  if (!a.seg) {
+    base = r * a.ld;
+    len = a.d;
+    return true;
+  }
+  const int64_t b = a.seg[r], e = a.seg[r + 1];
+  const bool ok = b >= 0 && e >= b && e <= a.seg_total && e - b <= a.d && (!a.seg_align || (b & 3) == 0);
+  base = ok ? b : 0;
+  len = ok ? e - b : 0;
+  return ok;
+}
 
 __device__ __forceinline__ RowCtl* ctl_of(const Args& a, int64_t r) {
   return reinterpret_cast<RowCtl*>(a.ws + a.lay.ctl) + r;
@@ -1043,8 +1064,11 @@ __global__ void __launch_bounds__(256) k_init(Args a) {
     RowCtl c;
     memset(&c, 0, sizeof(c));
     const double rho = a.rho_dev ? a.rho_dev[r] : a.rho;
-    c.B = rho * (double)a.d;
+    int64_t base, len;
+    const bool ok = row_span(a, r, base, len);
+    c.B = rho * (double)len;
     if (!(rho >= 0.0 && rho <= 1.0)) c.flags = GSPAR_FLAG_BADRHO;
+    if (!ok) c.flags |= GSPAR_FLAG_BADSEG;
     c.l2exp = kNone;
     c.l3base = kNone;
     c.qkey = kNone;
@@ -1064,14 +1088,17 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   StatsLds& sm = sm_st;
   const int64_t row = blockIdx.x / a.nb;
   const int64_t blk = blockIdx.x % a.nb;
+  int64_t base, len;
+  row_span(a, row, base, len);
+  const int64_t beg = blk * a.chunk;
+  if (beg >= len) return;  // past the end of a shorter segment
   for (int b = threadIdx.x; b < kB1 * kLaneCopies; b += kNT) {
     sm.pk[b] = 0;
     sm.mx[b] = 0;
   }
   __syncthreads();
-  const float* __restrict__ gr = a.g + row * a.ld;
-  const int64_t beg = blk * a.chunk;
-  const int64_t end = min(a.d, beg + a.chunk);
+  const float* __restrict__ gr = a.g + base;
+  const int64_t end = min(len, beg + a.chunk);
   const uint32_t lc = threadIdx.x & (kLaneCopies - 1);
   stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) {
 #pragma unroll
@@ -1117,6 +1144,10 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   const RowCtl* ctl = ctl_of(a, row);
   const uint32_t need = ctl->need;
   if (need != 2 && need != 3) return;
+  int64_t base, len;
+  row_span(a, row, base, len);
+  const int64_t beg = blk * a.chunk;
+  if (beg >= len) return;  // past the end of a shorter segment
   uint32_t lo, shift;
   int nbins;
   const int cp = (int)(blk % kC23);
@@ -1141,9 +1172,8 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
     sm.mnc[b] = 0;
   }
   __syncthreads();
-  const float* __restrict__ gr = a.g + row * a.ld;
-  const int64_t beg = blk * a.chunk;
-  const int64_t end = min(a.d, beg + a.chunk);
+  const float* __restrict__ gr = a.g + base;
+  const int64_t end = min(len, beg + a.chunk);
   uint64_t qc = 0, qs = 0;
   stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) {
 #pragma unroll
@@ -1206,7 +1236,9 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
   __shared__ SolveLds sm;
   const int64_t row = blockIdx.x;
   const Hists H{&sm.l1, &sm.w2, &sm.w3, l1t_of(a, row), h1_of(a, row), win_of(a, row)};
-  solve_row(sm, ctl_of(a, row), H, a.d, a.first != 0);
+  int64_t base, len;
+  row_span(a, row, base, len);
+  solve_row(sm, ctl_of(a, row), H, len, a.first != 0);
 }
 
 // Sampling, amplification and order-preserving compaction. Workgroup t handles tile t (kTileElems
@@ -1367,11 +1399,12 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   const int64_t t0 = row * a.lay.tiles + part0;  // status word of the first tile
   const RowCtl* ctl = ctl_of(a, row);
   TileCtx c;
-  c.row = a.g + row * a.ld;
-  c.d = a.d;
+  int64_t base;
+  row_span(a, row, base, c.d);
+  c.row = a.g + base;
   c.lam = ctl->lam;
   c.tcap = ctl->tcap;
-  c.live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO));
+  c.live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO | GSPAR_FLAG_BADSEG));
   const uint64_t seed = a.seed_dev ? a.seed_dev[row] : a.seed;
   c.k0 = (uint32_t)seed;
   c.k1 = (uint32_t)(seed >> 32);
@@ -1414,7 +1447,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         ncl += tot;
       }
     };
-    if (VEC && fast && (part + 1) * (int64_t)kTileElems <= a.d) {
+    if (VEC && fast && (part + 1) * (int64_t)kTileElems <= c.d) {
       // whole tile inside the row: kSampleBatch unconditional loads in flight per lane
 #pragma unroll
       for (int jb = 0; jb < kTileGroups; jb += kSampleBatch) {
@@ -1435,7 +1468,9 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
       for (int j = 0; j < kTileGroups; ++j) {
         float v[4];
         uint32_t z = 0, cz = 0;
-        if (c.live) decide_group<VEC>(c, q0 + 64 * j, v, z, cz);
+        // groups past the row's end (the tail of the last tile, and whole tiles past the end of a
+        // shorter segment) hold no coordinates
+        if (c.live && 4 * (q0 + 64 * j) < c.d) decide_group<VEC>(c, q0 + 64 * j, v, z, cz);
         else v[0] = v[1] = v[2] = v[3] = 0.0f;
         record(j, v, z, cz);
       }
@@ -1626,8 +1661,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     if constexpr (HYB) {
       // dense ternary vector (Section 3.3): 2 on the capped set, sign(g_i) for the other
       // survivors, 0 elsewhere; this thread's 64 coordinates
-      if (a.q && e0 < a.d) {
-        int8_t* __restrict__ qr = a.q + row * a.ld + e0;
+      if (a.q && e0 < c.d) {
+        int8_t* __restrict__ qr = a.q + base + e0;
         uint32_t w[16];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
@@ -1640,7 +1675,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
           }
           w[j] = x;
         }
-        if (e0 + 64 <= a.d && ((uintptr_t)qr & 15) == 0) {
+        if (e0 + 64 <= c.d && ((uintptr_t)qr & 15) == 0) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             uint4 v;
@@ -1648,7 +1683,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             reinterpret_cast<uint4*>(qr)[j] = v;
           }
         } else {
-          const int64_t nb = min((int64_t)64, a.d - e0);
+          const int64_t nb = min((int64_t)64, c.d - e0);
           for (int64_t b = 0; b < nb; ++b) qr[b] = (int8_t)((w[b >> 2] >> (8 * (b & 3))) & 0xFF);
         }
       }
@@ -1686,11 +1721,14 @@ __global__ void __launch_bounds__(256) k_probs(Args a) {
   const RowCtl* ctl = ctl_of(a, row);
   const double lam = ctl->lam;
   const uint32_t tcap = ctl->tcap;
-  const bool live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO));
-  const float* __restrict__ gr = a.g + row * a.ld;
-  float* __restrict__ pr = a.p ? a.p + row * a.ld : nullptr;
+  const bool live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO | GSPAR_FLAG_BADSEG));
+  int64_t base, len;
+  row_span(a, row, base, len);
   const int64_t beg = blk * a.chunk;
-  const int64_t end = min(a.d, beg + a.chunk);
+  if (beg >= len) return;  // past the end of a shorter segment
+  const float* __restrict__ gr = a.g + base;
+  float* __restrict__ pr = a.p ? a.p + base : nullptr;
+  const int64_t end = min(len, beg + a.chunk);
   uint32_t kc = 0;
   stream_groups<VEC, 4, 256>(gr, beg, end, [&](int64_t q, const float v[4], uint32_t m) {
     float o[4];
@@ -1777,9 +1815,16 @@ static int check_common(const float* g, int64_t rows, int64_t d, int64_t ld, int
 static void plan(Args& a) {
   a.lay = layout_of(a.rows, a.d);
   const int64_t target = 512;
-  int64_t nbt = (target + a.rows - 1) / a.rows;
-  if (nbt < 1) nbt = 1;
-  int64_t chunk = (a.d + nbt - 1) / nbt;
+  int64_t chunk;
+  if (a.seg) {
+    // about `target` nonempty workgroups over all segments; a shorter segment's trailing
+    // workgroups find no coordinates and return at once
+    chunk = (a.seg_elems + target - 1) / target;
+  } else {
+    int64_t nbt = (target + a.rows - 1) / a.rows;
+    if (nbt < 1) nbt = 1;
+    chunk = (a.d + nbt - 1) / nbt;
+  }
   chunk = (chunk + 3) & ~(int64_t)3;
   if (chunk < 8192) chunk = 8192;
   if (chunk > kMaxChunk) chunk = kMaxChunk;
@@ -1787,7 +1832,10 @@ static void plan(Args& a) {
   a.nb = (int)((a.d + chunk - 1) / chunk);
 }
 
-static bool vec_ok(const Args& a) { return ((uintptr_t)a.g % 16 == 0) && (a.ld % 4 == 0); }
+static bool vec_ok(const Args& a) {
+  if (a.seg) return a.seg_align != 0;
+  return ((uintptr_t)a.g % 16 == 0) && (a.ld % 4 == 0);
+}
 
 static int launch_solve(Args& a, hipStream_t s) {
   const bool vec = vec_ok(a);
@@ -1837,6 +1885,7 @@ static void launch_sample(const Args& a, bool vec, hipStream_t s) {
 
 static int run_sample(Args& a, hipStream_t s) {
   plan(a);
+  if ((double)a.rows * (double)a.nb >= 2147483647.0) return GSPAR_ERR_ARG;
   int rc = launch_solve(a, s);
   if (rc) return rc;
   const bool vec = vec_ok(a);
@@ -1851,6 +1900,7 @@ static int run_sample(Args& a, hipStream_t s) {
 
 static int run_probs(Args& a, hipStream_t s) {
   plan(a);
+  if ((double)a.rows * (double)a.nb >= 2147483647.0) return GSPAR_ERR_ARG;
   int rc = launch_solve(a, s);
   if (rc) return rc;
   const bool vec = vec_ok(a) && (!a.p || (uintptr_t)a.p % 16 == 0);
@@ -2158,6 +2208,77 @@ int sparsify_sample_compact_batched(const float* g, int64_t rows, int64_t d, int
   a.k_out = k;
   a.flags_out = flags;
   return run_sample(a, (hipStream_t)stream);
+}
+
+// Host check of segment offsets (off[0] >= 0, nondecreasing, every length below 2^31): the longest
+// length (at least 1, the row length the workspace is sized for), the total length, and whether
+// vector loads may be used (g 16-byte aligned and every start a multiple of 4).
+static int check_segments(const float* g, const int64_t* off, const int64_t* off_dev, int64_t segs, int64_t& maxlen,
+                          int64_t& total, bool& aligned) {
+  if (!g || !off || !off_dev || segs < 1 || segs > ((int64_t)1 << 24) || off[0] < 0) return GSPAR_ERR_ARG;
+  maxlen = 1;
+  aligned = (uintptr_t)g % 16 == 0;
+  for (int64_t r = 0; r < segs; ++r) {
+    const int64_t len = off[r + 1] - off[r];
+    if (off[r + 1] < off[r] || len > INT32_MAX) return GSPAR_ERR_ARG;
+    if (len > maxlen) maxlen = len;
+    if (off[r] & 3) aligned = false;
+  }
+  total = off[segs] - off[0];
+  return GSPAR_OK;
+}
+
+static void set_segments(Args& a, const int64_t* off, const int64_t* off_dev, int64_t segs, int64_t total,
+                         bool aligned) {
+  a.seg = off_dev;
+  a.seg_total = off[segs];
+  a.seg_elems = total;
+  a.seg_align = aligned ? 1 : 0;
+}
+
+int sparsify_sample_compact_segmented(const float* g, int64_t segs, const int64_t* off, const int64_t* off_dev,
+                                      const double* rho, int solver, int greedy_iters, const uint64_t* seeds,
+                                      int32_t* idx, float* val, int64_t cap_per_seg, int64_t* nnz, double* lambda,
+                                      int64_t* k, uint32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!rho || !seeds || !nnz || cap_per_seg < 0 || (cap_per_seg > 0 && (!idx || !val))) return GSPAR_ERR_ARG;
+  int64_t maxlen, total;
+  bool aligned;
+  int rc = check_segments(g, off, off_dev, segs, maxlen, total, aligned);
+  if (rc) return rc;
+  rc = check_common(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws);
+  set_segments(a, off, off_dev, segs, total, aligned);
+  a.rho_dev = rho;
+  a.seed_dev = seeds;
+  a.idx = idx;
+  a.val = val;
+  a.cap = cap_per_seg;
+  a.nnz = nnz;
+  a.lam_out = lambda;
+  a.k_out = k;
+  a.flags_out = flags;
+  return run_sample(a, (hipStream_t)stream);
+}
+
+int sparsify_probs_segmented(const float* g, int64_t segs, const int64_t* off, const int64_t* off_dev,
+                             const double* rho, int solver, int greedy_iters, float* p, double* lambda, int64_t* k,
+                             uint32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!rho || !lambda) return GSPAR_ERR_ARG;
+  int64_t maxlen, total;
+  bool aligned;
+  int rc = check_segments(g, off, off_dev, segs, maxlen, total, aligned);
+  if (rc) return rc;
+  rc = check_common(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws);
+  set_segments(a, off, off_dev, segs, total, aligned);
+  a.rho_dev = rho;
+  a.p = p;
+  a.lam_out = lambda;
+  a.k_out = k;
+  a.flags_out = flags;
+  return run_probs(a, (hipStream_t)stream);
 }
 
 const char* gspar_status_string(int status) {

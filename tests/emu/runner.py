@@ -29,6 +29,9 @@ def load(path):
     L.sparsify_sample_hybrid_batched.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp, vp, i64,
                                                  vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     L.gspar_aggregate.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
+    L.sparsify_sample_compact_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, i64, vp, vp, vp,
+                                                    vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_probs_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     return L
 
 
@@ -198,6 +201,116 @@ def check_hybrid(L, verbose=True):
     return True
 
 
+def segmented(L, g, off, rhos, seeds, solver, iters=2, cap=None, off_dev=None, g_shift=0):
+    """sparsify_sample_compact_segmented on a flat host vector (placed g_shift floats past a
+    16-byte boundary); off_dev defaults to the host offsets."""
+    off = np.ascontiguousarray(off, np.int64)
+    od = off.copy() if off_dev is None else np.ascontiguousarray(off_dev, np.int64)
+    segs = off.size - 1
+    lens = np.diff(off)
+    maxlen = max(1, int(lens.max()))
+    raw = np.zeros(g.size + 8, np.float32)
+    base = (-raw.ctypes.data // 4) % 4 + g_shift
+    buf = raw[base:base + g.size]
+    buf[:] = g
+    cap = maxlen if cap is None else cap
+    idx = np.zeros((segs, max(cap, 1)), np.int32)
+    val = np.zeros((segs, max(cap, 1)), np.float32)
+    nnz = np.zeros(segs, np.int64)
+    lam = np.zeros(segs)
+    k = np.zeros(segs, np.int64)
+    fl = np.zeros(segs, np.uint32)
+    r = np.ascontiguousarray(rhos, np.float64)
+    s = np.array([int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds], np.uint64)
+    sid = 0 if solver == "greedy" else 1
+    wsb = L.gspar_workspace_bytes(segs, maxlen, sid)
+    keep, ws = _aligned(wsb)
+    rc = L.sparsify_sample_compact_segmented(buf.ctypes.data, segs, off.ctypes.data, od.ctypes.data, r.ctypes.data,
+                                             sid, iters, s.ctypes.data, idx.ctypes.data, val.ctypes.data, cap,
+                                             nnz.ctypes.data, lam.ctypes.data, k.ctypes.data, fl.ctypes.data,
+                                             ws.ctypes.data, wsb, None)
+    assert rc == 0, rc
+    return idx, val, nnz, lam, k, fl
+
+
+def probs_segmented(L, g, off, rhos, solver, iters=2):
+    off = np.ascontiguousarray(off, np.int64)
+    segs = off.size - 1
+    maxlen = max(1, int(np.diff(off).max()))
+    p = np.full(g.size, -1.0, np.float32)
+    lam = np.zeros(segs)
+    k = np.zeros(segs, np.int64)
+    fl = np.zeros(segs, np.uint32)
+    r = np.ascontiguousarray(rhos, np.float64)
+    sid = 0 if solver == "greedy" else 1
+    wsb = L.gspar_workspace_bytes(segs, maxlen, sid)
+    keep, ws = _aligned(wsb)
+    gg = np.ascontiguousarray(g, np.float32)
+    rc = L.sparsify_probs_segmented(gg.ctypes.data, segs, off.ctypes.data, off.ctypes.data, r.ctypes.data, sid,
+                                    iters, p.ctypes.data, lam.ctypes.data, k.ctypes.data, fl.ctypes.data,
+                                    ws.ctypes.data, wsb, None)
+    assert rc == 0, rc
+    return p, lam, k, fl
+
+
+def layered(lengths, seed):
+    """A flat gradient of layers with per-layer scales 10^U(-4, 0) and mixed shapes."""
+    rng = np.random.default_rng(seed)
+    parts = []
+    for i, n in enumerate(lengths):
+        mk = (W.t_mixture, W.normal, W.integer_ties)[i % 3]
+        parts.append(mk(n, seed + i) * np.float32(10.0 ** rng.uniform(-4, 0)) if n else np.zeros(0, np.float32))
+    return np.concatenate(parts).astype(np.float32), np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+
+
+def check_segmented(L, verbose=True):
+    """Per-layer sparsification (Section 5.2) against the oracle segment by segment, aligned and
+    unaligned offsets, empty and tiny layers, layers spanning several tiles, and device offsets
+    that disagree with the host's."""
+    for lengths, shift in (([3000, 0, 3, 16384 + 8, 1, 5000, 4], 0), ([4096, 16388, 12, 20000, 0, 8], 0),
+                           ([4096, 16388, 12, 20000, 0, 8], 1)):
+        g, off = layered(lengths, 600 + len(lengths))
+        segs = len(lengths)
+        rhos = [(0.01, 0.1, 0.5, 0.3, 1.0, 0.05, 0.2)[i % 7] for i in range(segs)]
+        seeds = [7000 + i for i in range(segs)]
+        for solver in ("greedy", "exact"):
+            idx, val, nnz, lam, k, fl = segmented(L, g, off, rhos, seeds, solver, g_shift=shift)
+            ref = oracle.sparsify_segments(g, off, rhos, seeds, solver)
+            for s_ in range(segs):
+                seg = g[off[s_]:off[s_ + 1]]
+                n = int(nnz[s_])
+                if seg.size == 0 or not np.any(seg):
+                    assert n == 0 and fl[s_] & 4, (s_, n, fl[s_])
+                    continue
+                assert fl[s_] == 0, (s_, fl[s_])
+                sol = ref[s_][0]
+                compare_sample(seg, sol.p, seeds[s_], idx[s_, :n], val[s_, :n], n, lam[s_], sol.lam)
+                if solver == "exact":
+                    assert lam[s_] == sol.lam and k[s_] == sol.k
+                if solver == "exact" and shift == 0:  # a segment equals a single-row call on it
+                    one = sample_row(L, np.ascontiguousarray(seg), rhos[s_], solver, seeds[s_])
+                    assert one[2] == n and np.array_equal(one[0], idx[s_, :n])
+                    assert np.array_equal(one[1], val[s_, :n])
+            if solver == "greedy":
+                continue
+            p, lam2, k2, fl2 = probs_segmented(L, g, off, rhos, "exact")
+            for s_ in range(segs):
+                seg = g[off[s_]:off[s_ + 1]]
+                if seg.size and np.any(seg):
+                    compare_probs(p[off[s_]:off[s_ + 1]], oracle.solve_exact(seg, rhos[s_]).p)
+    # device offsets that break the host's bounds: those segments are flagged and skipped
+    g, off = layered([4000, 8000, 4000], 650)
+    bad = off.copy()
+    bad[1] = 4001          # segment 0 longer, segment 1 misaligned for the vector path
+    bad[3] = off[3] + 400  # the last segment ends past the host's last offset
+    idx, val, nnz, lam, k, fl = segmented(L, g, off, [0.1] * 3, [1, 2, 3], "greedy", off_dev=bad)
+    assert fl[1] & 32 and fl[2] & 32 and nnz[1] == 0 and nnz[2] == 0
+    assert not fl[0] & 32 and nnz[0] > 0
+    if verbose:
+        print("segmented cases ok", flush=True)
+    return True
+
+
 def aggregate(L, idx, val, nnz, d):
     """gspar_aggregate on [workers, cap] lists; returns v [d]."""
     workers, cap = idx.shape
@@ -319,5 +432,7 @@ if __name__ == "__main__":
         check_hybrid(load(sys.argv[1]))
     if which in ("all", "aggregate"):
         check_aggregate(load(sys.argv[1]))
+    if which in ("all", "segmented"):
+        check_segmented(load(sys.argv[1]))
     if which in ("all", "main"):
         print("checked", run_all(sys.argv[1]))

@@ -121,6 +121,32 @@ def test_hybrid_argument_errors(L):
                                             FAKE, None, None, None, None, FAKE, wsb, None) == gs.ERR_ARG
 
 
+def test_segmented_argument_errors(L):
+    import paper_1710_09854_amd as gs
+
+    good = np.array([0, 400, 400, 1000], np.int64)
+    wsb = L.gspar_workspace_bytes(3, 600, 0)
+
+    def one(off=good, segs=3, off_dev=FAKE, rho=FAKE, ws=FAKE, wsb_=wsb, g=FAKE):
+        offp = None if off is None else np.ascontiguousarray(off, np.int64).ctypes.data
+        a = L.sparsify_sample_compact_segmented(g, segs, offp, off_dev, rho, 0, 2, FAKE, FAKE, FAKE, 10, FAKE,
+                                                None, None, None, ws, wsb_, None)
+        b = L.sparsify_probs_segmented(g, segs, offp, off_dev, rho, 0, 2, FAKE, FAKE, None, None, ws, wsb_, None)
+        assert a == b
+        return a
+
+    assert one(off=None) == gs.ERR_ARG
+    assert one(off_dev=None) == gs.ERR_ARG
+    assert one(g=None) == gs.ERR_ARG
+    assert one(rho=None) == gs.ERR_ARG
+    assert one(segs=0) == gs.ERR_ARG
+    assert one(off=[5, 3, 7, 9]) == gs.ERR_ARG           # decreasing
+    assert one(off=[-4, 0, 4, 8]) == gs.ERR_ARG          # negative start
+    assert one(off=[0, 1 << 31, 1 << 31, 1 << 31]) == gs.ERR_ARG  # a segment of 2^31 floats
+    assert one(ws=FAKE + 8) == gs.ERR_WORKSPACE
+    assert one(wsb_=wsb - 1) == gs.ERR_WORKSPACE         # sized for the longest segment (600)
+
+
 def test_aggregate_argument_errors(L):
     import paper_1710_09854_amd as gs
 

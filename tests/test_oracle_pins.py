@@ -525,6 +525,56 @@ def test_theorem4_coding_length_bound(s, rho_def, seed):
     assert expected <= s * (b + L) + min(rho_def * s * L, d) + b + 1e-9
 
 
+# ----------------------------------------------------------------------------- per-layer segments
+def _three_layers():
+    parts = [W.t_mixture(5000, 21), W.normal(3001, 22), W.integer_ties(4096, 23), np.zeros(0, np.float32)]
+    off = np.concatenate([[0], np.cumsum([p.size for p in parts])])
+    return np.concatenate(parts), off
+
+
+@pytest.mark.parametrize("solver", ["exact", "greedy"])
+def test_segments_scaling_one_layer_leaves_the_others(solver):
+    """Section 5.2 sparsifies layers independently: multiplying one layer by 2^5 divides its lambda
+    by 2^5 exactly (every sum scales exactly), keeps its survivors and multiplies their values by
+    2^5, and leaves every other layer's solution and samples unchanged. A single solve over the
+    whole vector would move every layer's probabilities."""
+    g, off = _three_layers()
+    rhos, seeds = [0.02, 0.1, 0.3, 0.5], [5, 6, 7, 8]
+    base = oracle.sparsify_segments(g, off, rhos, seeds, solver)
+    h = g.copy()
+    h[off[1]:off[2]] *= np.float32(32.0)
+    moved = oracle.sparsify_segments(h, off, rhos, seeds, solver)
+    for s_ in (0, 2):
+        assert base[s_][0].lam == moved[s_][0].lam
+        assert np.array_equal(base[s_][1], moved[s_][1]) and np.array_equal(base[s_][2], moved[s_][2])
+    assert moved[1][0].lam == base[1][0].lam / 32.0
+    assert np.array_equal(base[1][1], moved[1][1])
+    assert np.array_equal(moved[1][2], base[1][2] * np.float32(32.0))
+    assert base[3][3] == 0 and moved[3][3] == 0
+    # the whole-vector solve is not separable: scaling layer 1 changes layer 0's probabilities
+    pg = oracle.solve(g, 0.1, solver).p
+    ph = oracle.solve(h, 0.1, solver).p
+    assert not np.array_equal(pg[off[0]:off[1]], ph[off[0]:off[1]])
+
+
+def test_segments_budget_per_layer():
+    """With the exact solver every layer spends exactly its own budget: sum of p over segment s
+    equals rho_s times its length (Proposition 1, per layer)."""
+    g, off = _three_layers()
+    rhos = [0.02, 0.1, 0.3, 0.5]
+    res = oracle.sparsify_segments(g, off, rhos, [1, 2, 3, 4], "exact")
+    for s_ in range(3):
+        n = off[s_ + 1] - off[s_]
+        assert abs(res[s_][0].p.sum() - rhos[s_] * n) <= 1e-9 * rhos[s_] * n
+
+
+def test_one_segment_is_the_whole_vector():
+    g = W.t_mixture(7000, 31)
+    (sol, idx, val, n), = oracle.sparsify_segments(g, [0, g.size], [0.05], [99], "greedy")
+    ref = oracle.sparsify(g, 0.05, "greedy", 2, 99)
+    assert sol.lam == ref[0].lam and np.array_equal(idx, ref[1]) and np.array_equal(val, ref[2]) and n == ref[3]
+
+
 # ----------------------------------------------------------------------------- aggregation
 def test_aggregate_keeps_everything_is_the_exact_mean():
     """With every coordinate kept (B >= nnz, Q(g) = g) the aggregate is the mean gradient: for four
