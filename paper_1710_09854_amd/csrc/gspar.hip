@@ -277,9 +277,11 @@ struct alignas(128) CountLine {
 GS_HD size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctl, h1, l1t, win, kc, status, total;
+  size_t ctl, h1, l1t, win, kc, status, bmap, tmap, total;
   int64_t tiles;  // tiles per row of the sample pass
 };
+
+constexpr int64_t kMinChunk = 8192;  // fewest coordinates per histogram workgroup (but the row's)
 
 // Histogram copies: row r's copy c of level 1 is h1 + (r * kC1 + c), of a refinement window
 // win + (r * kC23 + c); the solve that requests a refinement pass clears the window's copies.
@@ -298,6 +300,12 @@ GS_HD Layout layout_of(int64_t rows, int64_t d) {
   L.kc = off;
   off += align256((size_t)rows * 8 * sizeof(CountLine));
   L.status = off;
+  off += align256((size_t)rows * (size_t)L.tiles * sizeof(uint64_t));
+  // segmented calls: workgroup -> (row, block) of the histogram passes and (row, first tile) of the
+  // sample pass, for the workgroups that hold coordinates only
+  L.bmap = off;
+  off += align256((size_t)rows * (size_t)((d + kMinChunk - 1) / kMinChunk) * sizeof(uint64_t));
+  L.tmap = off;
   off += align256((size_t)rows * (size_t)L.tiles * sizeof(uint64_t));
   L.total = off;
   return L;
@@ -332,7 +340,12 @@ struct Args {
   // segmented calls: row r is g[seg[r], seg[r + 1]) (device offsets), d the longest segment
   const int64_t* seg;
   int64_t seg_total;  // the host's last offset: no segment may end beyond it
-  int64_t seg_elems;  // the host's total segment length (sizes the histogram passes)
+  int64_t seg_elems;  // the host's total segment length
+  int64_t seg_chunk;  // host: histogram-pass chunk chosen from the segment lengths
+  int64_t seg_tiles;  // host: sample tiles that hold coordinates, over all segments
+  int64_t seg_blocks; // histogram-pass workgroups (the grid), from the host offsets
+  int64_t seg_wgs;    // sample-pass workgroups (the grid), from the host offsets
+  int seg_k;          // tiles per sample workgroup
   int seg_align;      // vector loads in use: every segment must start at a multiple of 4
 };
 
@@ -351,6 +364,11 @@ __device__ __forceinline__ bool row_span(const Args& a, int64_t r, int64_t& base
   len = ok ? e - b : 0;
   return ok;
 }
+
+// Segmented calls: the word k_init leaves in the workspace header, 1 when the workgroup maps built
+// from the device offsets have exactly the host's shape (the launched grids), 2 when they do not
+// (every segment is then flagged GSPAR_FLAG_BADSEG and skipped).
+__device__ __forceinline__ uint32_t* segok_of(const Args& a) { return reinterpret_cast<uint32_t*>(a.ws); }
 
 __device__ __forceinline__ RowCtl* ctl_of(const Args& a, int64_t r) {
   return reinterpret_cast<RowCtl*>(a.ws + a.lay.ctl) + r;
@@ -938,7 +956,7 @@ GS_DI void sv_start(SolveLds& s, RowCtl& c, const Hists& H, int64_t d) {
   // zeros = d minus the histogram's population (every nonzero key, finite or not, is binned)
   c.zeros = (uint64_t)d - (i0.Kab + i0.cnt);
   const uint64_t nnz = (uint64_t)d - c.zeros;
-  if (c.flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO)) {
+  if (c.flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO | GSPAR_FLAG_BADSEG)) {
     sv_finalize(c, NAN, kKeyInf);
     return;
   }
@@ -1047,7 +1065,81 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d, bool fi
 // ------------------------------------------------------------------------------------------
 // Kernels.
 // ------------------------------------------------------------------------------------------
+// Segmented calls: the workgroup maps of the histogram passes (row << 32 | block) and of the sample
+// pass (row << 32 | workgroup within the row), built by one workgroup of 256 threads from the
+// device offsets in row order, 256 rows at a time: an exclusive scan of the per-row counts, then
+// every thread fills map entries, finding each entry's row by a binary search of the scan. Also
+// the verdict whether the maps have exactly the launched (host) shape.
+__device__ void seg_maps(const Args& a) {
+  __shared__ int64_t s_tot[2][4];
+  __shared__ int64_t s_pre[2][257];  // exclusive prefixes of the batch's rows (+ the batch total)
+  uint64_t* bmap = reinterpret_cast<uint64_t*>(a.ws + a.lay.bmap);
+  uint64_t* tmap = reinterpret_cast<uint64_t*>(a.ws + a.lay.tmap);
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  int64_t cb = 0, cw = 0;  // workgroups of the rows before this batch
+  for (int64_t r0 = 0; r0 < a.rows; r0 += 256) {
+    const int64_t r = r0 + t;
+    int64_t nb = 0, nw = 0;
+    if (r < a.rows) {
+      int64_t base, len;
+      row_span(a, r, base, len);
+      nb = (len + a.chunk - 1) / a.chunk;
+      const int64_t rt = len > kTileElems ? (len + kTileElems - 1) / kTileElems : 1;
+      nw = (rt + a.seg_k - 1) / a.seg_k;
+    }
+    int64_t xb = nb, xw = nw;  // inclusive scans over the wave
+    for (int o = 1; o < 64; o <<= 1) {
+      const int64_t yb = __shfl_up(xb, o), yw = __shfl_up(xw, o);
+      if (lane >= o) {
+        xb += yb;
+        xw += yw;
+      }
+    }
+    if (lane == 63) {
+      s_tot[0][wv] = xb;
+      s_tot[1][wv] = xw;
+    }
+    __syncthreads();
+    int64_t pb = xb - nb, pw = xw - nw, tb = 0, tw = 0;
+    for (int w = 0; w < 4; ++w) {
+      if (w < wv) {
+        pb += s_tot[0][w];
+        pw += s_tot[1][w];
+      }
+      tb += s_tot[0][w];
+      tw += s_tot[1][w];
+    }
+    s_pre[0][t] = pb;
+    s_pre[1][t] = pw;
+    if (t == 0) {
+      s_pre[0][256] = tb;
+      s_pre[1][256] = tw;
+    }
+    __syncthreads();
+    // entry e of the batch belongs to the last row whose prefix is <= e (rows past the end have
+    // no entries and the prefix of a row with none equals the next row's)
+    for (int m = 0; m < 2; ++m) {
+      const int64_t tot = s_pre[m][256], c0 = m == 0 ? cb : cw, cap = m == 0 ? a.seg_blocks : a.seg_wgs;
+      uint64_t* map = m == 0 ? bmap : tmap;
+      for (int64_t e = t; e < tot && c0 + e < cap; e += 256) {
+        int lo = 0, hi = 255;  // the row lies in [lo, hi]
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (s_pre[m][mid] <= e) lo = mid;
+          else hi = mid - 1;
+        }
+        map[c0 + e] = ((uint64_t)(r0 + lo) << 32) | (uint64_t)(e - s_pre[m][lo]);
+      }
+    }
+    cb += tb;
+    cw += tw;
+    __syncthreads();
+  }
+  if (t == 0) *segok_of(a) = (cb == a.seg_blocks && cw == a.seg_wgs) ? 1u : 2u;
+}
+
 __global__ void __launch_bounds__(256) k_init(Args a) {
+  if (a.seg && blockIdx.x == 0) seg_maps(a);
   const int64_t tid = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   // level-1 histogram copies, capped-count lines, look-back status words
@@ -1078,6 +1170,21 @@ __global__ void __launch_bounds__(256) k_init(Args a) {
   }
 }
 
+// Row and block of a histogram-pass workgroup: rows * nb workgroups for a strided batch, the map
+// built by k_init for a segmented call (false: nothing to do).
+__device__ __forceinline__ bool hist_block(const Args& a, int64_t& row, int64_t& blk) {
+  if (!a.seg) {
+    row = blockIdx.x / a.nb;
+    blk = blockIdx.x % a.nb;
+    return true;
+  }
+  if (*segok_of(a) != 1) return false;
+  const uint64_t e = reinterpret_cast<const uint64_t*>(a.ws + a.lay.bmap)[blockIdx.x];
+  row = (int64_t)(e >> 32);
+  blk = (int64_t)(e & 0xFFFFFFFFu);
+  return true;
+}
+
 // Streaming statistics pass. Grid: rows * nb workgroups of kNT threads. Each builds an LDS
 // histogram over binades (count, exact significand sum, maximum key), kept in kLaneCopies copies
 // by lane to spread same-address LDS atomics, and adds its nonempty bins into one of the row's kC1
@@ -1086,8 +1193,8 @@ template <bool VEC>
 __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_stats(Args a) {
   __shared__ StatsLds sm_st;
   StatsLds& sm = sm_st;
-  const int64_t row = blockIdx.x / a.nb;
-  const int64_t blk = blockIdx.x % a.nb;
+  int64_t row, blk;
+  if (!hist_block(a, row, blk)) return;
   int64_t base, len;
   row_span(a, row, base, len);
   const int64_t beg = blk * a.chunk;
@@ -1139,8 +1246,8 @@ template <bool VEC>
 __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_refine(Args a) {
   __shared__ WinLds sm_w;
   WinLds& sm = sm_w;
-  const int64_t row = blockIdx.x / a.nb;
-  const int64_t blk = blockIdx.x % a.nb;
+  int64_t row, blk;
+  if (!hist_block(a, row, blk)) return;
   const RowCtl* ctl = ctl_of(a, row);
   const uint32_t need = ctl->need;
   if (need != 2 && need != 3) return;
@@ -1235,6 +1342,23 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
 __global__ void __launch_bounds__(kNT) k_solve(Args a) {
   __shared__ SolveLds sm;
   const int64_t row = blockIdx.x;
+  if (a.seg && *segok_of(a) != 1) {
+    // the workgroup maps of a segmented call do not have the launched shape: no histogram pass
+    // ran and the sample pass does nothing, so the first solve skips the row and writes its results
+    if (a.first && threadIdx.x == 0) {
+      RowCtl* gc = ctl_of(a, row);
+      RowCtl c = *gc;
+      c.flags |= GSPAR_FLAG_BADSEG;
+      sv_finalize(c, NAN, kKeyInf);
+      *gc = c;
+      if (a.nnz) a.nnz[row] = 0;
+      if (a.nnz_b) a.nnz_b[row] = 0;
+      if (a.k_out) a.k_out[row] = 0;
+      if (a.lam_out) a.lam_out[row] = c.lam;
+      if (a.flags_out) a.flags_out[row] = c.flags;
+    }
+    return;
+  }
   const Hists H{&sm.l1, &sm.w2, &sm.w3, l1t_of(a, row), h1_of(a, row), win_of(a, row)};
   int64_t base, len;
   row_span(a, row, base, len);
@@ -1391,16 +1515,31 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   __shared__ uint32_t s_wcl[K][kTileThreads / 64];
   __shared__ uint64_t s_excl;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  // workgroup -> K consecutive tiles [part0, part0 + nk) of one row
-  const int64_t wpr = (a.lay.tiles + K - 1) / K;  // workgroups per row
-  const int64_t row = blockIdx.x / wpr;
-  const int64_t part0 = (blockIdx.x % wpr) * K;
-  const int nk = (int)min((int64_t)K, a.lay.tiles - part0);
-  const int64_t t0 = row * a.lay.tiles + part0;  // status word of the first tile
-  const RowCtl* ctl = ctl_of(a, row);
+  // workgroup -> K consecutive tiles [part0, part0 + nk) of one row. A row has
+  // max(1, ceil(length / kTileElems)) tiles, all lay.tiles for rows of a strided batch; the
+  // workgroups past a shorter segment's tiles have nothing to do (no later tile of the row waits on
+  // them, and its last tile writes the row's results).
+  int64_t row, part0;
+  if (!a.seg) {
+    const int64_t wpr = (a.lay.tiles + K - 1) / K;  // workgroups per row
+    row = blockIdx.x / wpr;
+    part0 = (blockIdx.x % wpr) * K;
+  } else {
+    // the map built by k_init holds only workgroups with tiles; a map that does not have the
+    // launched shape leaves every row to the first solve
+    if (*segok_of(a) != 1) return;
+    const uint64_t e = reinterpret_cast<const uint64_t*>(a.ws + a.lay.tmap)[blockIdx.x];
+    row = (int64_t)(e >> 32);
+    part0 = (int64_t)(e & 0xFFFFFFFFu) * K;
+  }
   TileCtx c;
   int64_t base;
   row_span(a, row, base, c.d);
+  const int64_t rtiles = c.d > kTileElems ? (c.d + kTileElems - 1) / kTileElems : 1;
+  if (part0 >= rtiles) return;
+  const int nk = (int)min((int64_t)K, rtiles - part0);
+  const int64_t t0 = row * a.lay.tiles + part0;  // status word of the first tile
+  const RowCtl* ctl = ctl_of(a, row);
   c.row = a.g + base;
   c.lam = ctl->lam;
   c.tcap = ctl->tcap;
@@ -1690,7 +1829,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     }
     excl += agg[kk];
   }
-  if (part0 + nk == a.lay.tiles && tid == 0) {
+  if (part0 + nk == rtiles && tid == 0) {
     const uint64_t incl = excl;
     const int64_t n = (int64_t)(incl & 0x7FFFFFFFull);
     const int64_t kc = (int64_t)((incl >> 31) & 0x7FFFFFFFull);
@@ -1716,8 +1855,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
 template <bool VEC>
 __global__ void __launch_bounds__(256) k_probs(Args a) {
   __shared__ uint32_t s_cnt[4];
-  const int64_t row = blockIdx.x / a.nb;
-  const int64_t blk = blockIdx.x % a.nb;
+  int64_t row, blk;
+  if (!hist_block(a, row, blk)) return;
   const RowCtl* ctl = ctl_of(a, row);
   const double lam = ctl->lam;
   const uint32_t tcap = ctl->tcap;
@@ -1817,16 +1956,15 @@ static void plan(Args& a) {
   const int64_t target = 512;
   int64_t chunk;
   if (a.seg) {
-    // about `target` nonempty workgroups over all segments; a shorter segment's trailing
-    // workgroups find no coordinates and return at once
-    chunk = (a.seg_elems + target - 1) / target;
+    // chosen from the segment lengths so that the nonempty workgroups are resident at once
+    chunk = a.seg_chunk;
   } else {
     int64_t nbt = (target + a.rows - 1) / a.rows;
     if (nbt < 1) nbt = 1;
     chunk = (a.d + nbt - 1) / nbt;
   }
   chunk = (chunk + 3) & ~(int64_t)3;
-  if (chunk < 8192) chunk = 8192;
+  if (chunk < kMinChunk) chunk = kMinChunk;
   if (chunk > kMaxChunk) chunk = kMaxChunk;
   a.chunk = chunk;
   a.nb = (int)((a.d + chunk - 1) / chunk);
@@ -1846,10 +1984,15 @@ static int launch_solve(Args& a, hipStream_t s) {
   time_before(5, s);
   hipLaunchKernelGGL(k_init, dim3(ib), dim3(256), 0, s, a);
   time_after(5, s);
-  const dim3 grid((unsigned)(a.rows * a.nb));
+  // a segmented call launches only the workgroups that hold coordinates (none if every segment
+  // is empty)
+  const int64_t nblocks = a.seg ? a.seg_blocks : a.rows * a.nb;
+  const dim3 grid((unsigned)nblocks);
   time_before(1, s);
-  if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
-  else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
+  if (nblocks > 0) {
+    if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
+    else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
+  }
   time_after(1, s);
   a.first = 1;
   time_before(3, s);
@@ -1861,8 +2004,10 @@ static int launch_solve(Args& a, hipStream_t s) {
   for (int r = 0; r < R; ++r) {
     a.first = 0;
     time_before(4, s);
-    if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
-    else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
+    if (nblocks > 0) {
+      if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
+      else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
+    }
     time_after(4, s);
     time_before(3, s);
     hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
@@ -1873,7 +2018,7 @@ static int launch_solve(Args& a, hipStream_t s) {
 
 template <int K>
 static void launch_sample(const Args& a, bool vec, hipStream_t s) {
-  const dim3 grid((unsigned)(a.rows * ((a.lay.tiles + K - 1) / K)));
+  const dim3 grid((unsigned)(a.seg ? a.seg_wgs : a.rows * ((a.lay.tiles + K - 1) / K)));
   if (a.code_b) {
     if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, true, K>), grid, dim3(kTileThreads), 0, s, a);
     else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, true, K>), grid, dim3(kTileThreads), 0, s, a);
@@ -1892,7 +2037,8 @@ static int run_sample(Args& a, hipStream_t s) {
   time_before(0, s);
   // tiles per workgroup: 1 while every tile can be resident at once, else 2, so that a
   // workgroup's wait for its predecessors' prefix overlaps the decide phase of its second tile
-  if (a.rows * a.lay.tiles <= kSampleResident) launch_sample<1>(a, vec, s);
+  const int64_t tiles = a.seg ? a.seg_tiles : a.rows * a.lay.tiles;
+  if (a.seg ? a.seg_k == 1 : tiles <= kSampleResident) launch_sample<1>(a, vec, s);
   else launch_sample<2>(a, vec, s);
   time_after(0, s);
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
@@ -1904,10 +2050,13 @@ static int run_probs(Args& a, hipStream_t s) {
   int rc = launch_solve(a, s);
   if (rc) return rc;
   const bool vec = vec_ok(a) && (!a.p || (uintptr_t)a.p % 16 == 0);
-  const dim3 grid((unsigned)(a.rows * a.nb));
+  const int64_t nblocks = a.seg ? a.seg_blocks : a.rows * a.nb;
+  const dim3 grid((unsigned)nblocks);
   time_before(2, s);
-  if (vec) hipLaunchKernelGGL(k_probs<true>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_probs<false>, grid, dim3(256), 0, s, a);
+  if (nblocks > 0) {
+    if (vec) hipLaunchKernelGGL(k_probs<true>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_probs<false>, grid, dim3(256), 0, s, a);
+  }
   time_after(2, s);
   hipLaunchKernelGGL(k_probs_out, dim3((unsigned)((a.rows + 63) / 64)), dim3(64), 0, s, a);
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
@@ -2234,6 +2383,38 @@ static void set_segments(Args& a, const int64_t* off, const int64_t* off_dev, in
   a.seg_total = off[segs];
   a.seg_elems = total;
   a.seg_align = aligned ? 1 : 0;
+  // histogram passes: the smallest chunk (a multiple of 4, at least kMinChunk) for which the
+  // segments need at most 512 workgroups (two resident per CU); the grid holds exactly those
+  auto blocks = [&](int64_t ch) {
+    int64_t n = 0;
+    for (int64_t r = 0; r < segs; ++r) n += (off[r + 1] - off[r] + ch - 1) / ch;
+    return n;
+  };
+  int64_t lo = kMinChunk, hi = kMaxChunk & ~(int64_t)3;
+  if (blocks(lo) <= 512) {
+    hi = lo;
+  } else if (blocks(hi) <= 512) {
+    while (hi - lo > 4) {
+      const int64_t mid = ((lo + hi) / 2) & ~(int64_t)3;
+      if (blocks(mid) <= 512) hi = mid;
+      else lo = mid;
+    }
+  }
+  a.seg_chunk = hi;
+  a.seg_blocks = blocks(hi);
+  // sample pass: tiles per workgroup from the tiles that hold coordinates, and the workgroups
+  a.seg_tiles = 0;
+  for (int64_t r = 0; r < segs; ++r) {
+    const int64_t len = off[r + 1] - off[r];
+    a.seg_tiles += len > kTileElems ? (len + kTileElems - 1) / kTileElems : 1;
+  }
+  a.seg_k = a.seg_tiles <= kSampleResident ? 1 : 2;
+  a.seg_wgs = 0;
+  for (int64_t r = 0; r < segs; ++r) {
+    const int64_t len = off[r + 1] - off[r];
+    const int64_t rt = len > kTileElems ? (len + kTileElems - 1) / kTileElems : 1;
+    a.seg_wgs += (rt + a.seg_k - 1) / a.seg_k;
+  }
 }
 
 int sparsify_sample_compact_segmented(const float* g, int64_t segs, const int64_t* off, const int64_t* off_dev,

@@ -138,17 +138,25 @@ def test_probs_segmented(gs, layout):
 
 
 def test_device_offsets_that_disagree_are_flagged(gs):
-    """Segments whose device offsets break the host's bounds (a start that is not a multiple of 4 on
-    the vector path, an end past the host's last offset) are skipped and flagged; the rest run."""
+    """Device offsets that break the host's bounds (a start that is not a multiple of 4 on the
+    vector path, an end past the host's last offset) change the launch shape: every segment is
+    flagged and skipped, without reading outside the segments; the same workspace then serves a
+    call with the right offsets."""
     g, off = _layered([4000, 8000, 4000], 650)
     seg = gs.Segments(off)
+    good = seg.dev
     bad = off.copy()
     bad[1] = 4001
     bad[3] = off[3] + 400
     seg.dev = torch.from_numpy(bad).cuda()
+    gd = torch.from_numpy(g).cuda()
     _say("segmented bad device offsets")
-    out = gs.sparsify_sample_compact_segmented(torch.from_numpy(g).cuda(), seg, 0.1, [1, 2, 3], "greedy")
+    out = gs.sparsify_sample_compact_segmented(gd, seg, 0.1, [1, 2, 3], "greedy")
     fl = out.flags.cpu().numpy()
-    nnz = out.nnz.cpu().numpy()
-    assert fl[1] & gs.FLAG_BADSEG and fl[2] & gs.FLAG_BADSEG and nnz[1] == 0 and nnz[2] == 0
-    assert not fl[0] & gs.FLAG_BADSEG and nnz[0] > 0
+    assert np.all(fl & gs.FLAG_BADSEG) and not out.nnz.cpu().numpy().any()
+    assert np.isnan(out.lam.cpu().numpy()).all()
+    pr = gs.sparsify_probs_segmented(gd, seg, 0.1, "exact")
+    assert np.all(pr.flags.cpu().numpy() & gs.FLAG_BADSEG)
+    seg.dev = good
+    out = gs.sparsify_sample_compact_segmented(gd, seg, 0.1, [1, 2, 3], "greedy")
+    assert not out.flags.cpu().numpy().any() and np.all(out.nnz.cpu().numpy() > 0)
