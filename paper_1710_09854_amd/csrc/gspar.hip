@@ -3,7 +3,9 @@
 // Pipeline per call (all launches on the caller's stream, no host synchronisation). Workgroups
 // never wait on one another inside a histogram pass: every cross-workgroup hand-off is a kernel
 // boundary, because device-scope fences are expensive on a multi-XCD part.
-//   k_init     clears the per-call workspace and writes each row's budget B = rho*d.
+//   k_init     clears the per-call workspace and writes each row's budget B = rho*d (for a
+//              segmented call, one row per segment, also the maps that give each workgroup of the
+//              later passes its segment, so that only workgroups holding coordinates are launched).
 //   k_stats    one streaming pass over g: an LDS histogram over binades of the magnitude bit pattern
 //              (count, exact significand sum, max), added into per-row global copies.
 //   k_solve    one workgroup per row: sums the copies and runs the solver (Proposition 1;
@@ -19,6 +21,8 @@
 //              decoupled look-back across tiles.
 //   k_probs    (probabilities entry points) writes p_i = min(lambda |g_i|, 1); k_probs_out writes
 //              the per-row results.
+// Separately, k_aggregate averages M workers' sparse lists into one dense vector (Algorithm 1,
+// step 6), summing each coordinate in fp64 in worker order.
 //
 // Sums of magnitudes are exact: a magnitude's bit pattern (its "key") fixes its binade, bins never
 // straddle a binade, so per-bin sums of 24-bit significands are exact integers and are combined
