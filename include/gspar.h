@@ -180,6 +180,17 @@ int sparsify_sample_compact_segmented(const float* g, int64_t segs, const int64_
                                       int greedy_iters, const uint64_t* seeds, int32_t* idx, float* val,
                                       int64_t cap_per_seg, int64_t* nnz, double* lambda, int64_t* k,
                                       uint32_t* flags, void* ws, size_t ws_bytes, void* stream);
+/* Per-layer hybrid coding: the segmented call's solve and selection with the outputs of
+ * sparsify_sample_hybrid_batched, one row per segment (indices within the segment); q, when given,
+ * has g's layout (q[off[s] + i]). A call whose device offsets are rejected (GSPAR_FLAG_BADSEG on
+ * every segment) leaves q unwritten. */
+int sparsify_sample_hybrid_segmented(const float* g, int64_t segs, const int64_t* off_host,
+                                     const int64_t* off_dev, const double* rho, int solver,
+                                     int greedy_iters, const uint64_t* seeds, int32_t* idx_a,
+                                     float* val_a, int64_t cap_a, int64_t* n_a, int32_t* code_b,
+                                     int64_t cap_b, int64_t* n_b, float* inv_lambda, int8_t* q,
+                                     double* lambda, uint32_t* flags, void* ws, size_t ws_bytes,
+                                     void* stream);
 int sparsify_probs_segmented(const float* g, int64_t segs, const int64_t* off_host,
                              const int64_t* off_dev, const double* rho, int solver, int greedy_iters,
                              float* p, double* lambda, int64_t* k, uint32_t* flags, void* ws,

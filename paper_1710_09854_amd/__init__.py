@@ -82,6 +82,9 @@ def lib():
                                                     vp, vp, ctypes.c_size_t, vp]
     L.sparsify_sample_compact_segmented.restype = i32
     L.sparsify_probs_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_hybrid_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, i64, vp, vp, i64,
+                                                   vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_hybrid_segmented.restype = i32
     L.sparsify_probs_segmented.restype = i32
     L.gspar_aggregate.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
     L.gspar_aggregate.restype = i32
@@ -531,6 +534,41 @@ def sparsify_sample_compact_segmented(g, seg: Segments, rho, seeds, solver="gree
                                                  fl.data_ptr(), buf.data_ptr(), nb, _stream(stream))
     _check(rc, "sparsify_sample_compact_segmented")
     return Sparse(idx[:, :cap], val[:, :cap], nnz, lam, k, fl)
+
+
+def sparsify_sample_hybrid_segmented(g, seg: Segments, rho, seeds, solver="greedy", iters: int = 2,
+                                     cap_a: int | None = None, cap_b: int | None = None, dense_q: bool = False,
+                                     workspace=None, stream=None) -> Hybrid:
+    """Per-layer hybrid coding: row s of the outputs holds segment s's Q_A and Q_B; q (optional)
+    has g's flat layout."""
+    g = _flat(g, seg)
+    dev = g.device
+    rows = seg.segs
+    r = _rho_dev(rho, rows, dev)
+    s = _seeds_dev(seeds, rows, dev)
+    if cap_b is None:
+        rmax = float(r.max().item())
+        cap_b = capacity_hint(seg.max_len, min(max(rmax, 0.0), 1.0))
+    cap_b = int(cap_b)
+    cap_a = cap_b if cap_a is None else int(cap_a)
+    idx_a = torch.empty((rows, max(cap_a, 1)), dtype=torch.int32, device=dev)
+    val_a = torch.empty((rows, max(cap_a, 1)), dtype=torch.float32, device=dev)
+    code_b = torch.empty((rows, max(cap_b, 1)), dtype=torch.int32, device=dev)
+    n_a = torch.empty(rows, dtype=torch.int64, device=dev)
+    n_b = torch.empty(rows, dtype=torch.int64, device=dev)
+    inv = torch.empty(rows, dtype=torch.float32, device=dev)
+    q = torch.zeros(seg.total, dtype=torch.int8, device=dev) if dense_q else None
+    lam = torch.empty(rows, dtype=torch.float64, device=dev)
+    fl = torch.empty(rows, dtype=torch.int32, device=dev)
+    sid = _solver_id(solver)
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid))
+    rc = lib().sparsify_sample_hybrid_segmented(g.data_ptr(), rows, seg.host.data_ptr(), seg.dev.data_ptr(),
+                                                r.data_ptr(), sid, int(iters), s.data_ptr(), idx_a.data_ptr(),
+                                                val_a.data_ptr(), cap_a, n_a.data_ptr(), code_b.data_ptr(), cap_b,
+                                                n_b.data_ptr(), inv.data_ptr(), _ptr(q), lam.data_ptr(),
+                                                fl.data_ptr(), buf.data_ptr(), nb, _stream(stream))
+    _check(rc, "sparsify_sample_hybrid_segmented")
+    return Hybrid(idx_a[:, :cap_a], val_a[:, :cap_a], n_a, code_b[:, :cap_b], n_b, inv, q, lam, fl)
 
 
 def sparsify_probs_segmented(g, seg: Segments, rho, solver="greedy", iters: int = 2, want_p: bool = True,

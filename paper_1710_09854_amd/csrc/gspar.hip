@@ -1357,6 +1357,7 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
       *gc = c;
       if (a.nnz) a.nnz[row] = 0;
       if (a.nnz_b) a.nnz_b[row] = 0;
+      if (a.inv_out) a.inv_out[row] = c.inv_lam;
       if (a.k_out) a.k_out[row] = 0;
       if (a.lam_out) a.lam_out[row] = c.lam;
       if (a.flags_out) a.flags_out[row] = c.flags;
@@ -2442,6 +2443,38 @@ int sparsify_sample_compact_segmented(const float* g, int64_t segs, const int64_
   a.nnz = nnz;
   a.lam_out = lambda;
   a.k_out = k;
+  a.flags_out = flags;
+  return run_sample(a, (hipStream_t)stream);
+}
+
+int sparsify_sample_hybrid_segmented(const float* g, int64_t segs, const int64_t* off, const int64_t* off_dev,
+                                     const double* rho, int solver, int greedy_iters, const uint64_t* seeds,
+                                     int32_t* idx_a, float* val_a, int64_t cap_a, int64_t* n_a, int32_t* code_b,
+                                     int64_t cap_b, int64_t* n_b, float* inv_lambda, int8_t* q, double* lambda,
+                                     uint32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!rho || !seeds || !n_a || !n_b || cap_a < 0 || cap_b < 0 || (cap_a > 0 && (!idx_a || !val_a)) ||
+      !code_b)
+    return GSPAR_ERR_ARG;
+  int64_t maxlen, total;
+  bool aligned;
+  int rc = check_segments(g, off, off_dev, segs, maxlen, total, aligned);
+  if (rc) return rc;
+  rc = check_common(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
+  if (rc) return rc;
+  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws);
+  set_segments(a, off, off_dev, segs, total, aligned);
+  a.rho_dev = rho;
+  a.seed_dev = seeds;
+  a.idx = idx_a;
+  a.val = val_a;
+  a.cap = cap_a;
+  a.nnz = n_a;
+  a.code_b = code_b;
+  a.cap_b = cap_b;
+  a.nnz_b = n_b;
+  a.inv_out = inv_lambda;
+  a.q = q;
+  a.lam_out = lambda;
   a.flags_out = flags;
   return run_sample(a, (hipStream_t)stream);
 }

@@ -32,6 +32,8 @@ def load(path):
     L.sparsify_sample_compact_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, i64, vp, vp, vp,
                                                     vp, vp, ctypes.c_size_t, vp]
     L.sparsify_probs_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_sample_hybrid_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, i64, vp, vp, i64,
+                                                   vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     return L
 
 
@@ -233,6 +235,34 @@ def segmented(L, g, off, rhos, seeds, solver, iters=2, cap=None, off_dev=None, g
     return idx, val, nnz, lam, k, fl
 
 
+def hybrid_segmented(L, g, off, rhos, seeds, solver, iters=2):
+    off = np.ascontiguousarray(off, np.int64)
+    segs = off.size - 1
+    maxlen = max(1, int(np.diff(off).max()))
+    gg = np.ascontiguousarray(g, np.float32)
+    cap = maxlen
+    ia = np.zeros((segs, cap), np.int32)
+    va = np.zeros((segs, cap), np.float32)
+    cb = np.zeros((segs, cap), np.int32)
+    na = np.zeros(segs, np.int64)
+    nb = np.zeros(segs, np.int64)
+    inv = np.zeros(segs, np.float32)
+    q = np.full(g.size, 7, np.int8)
+    lam = np.zeros(segs)
+    fl = np.zeros(segs, np.uint32)
+    r = np.ascontiguousarray(rhos, np.float64)
+    sd = np.array([int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds], np.uint64)
+    sid = 0 if solver == "greedy" else 1
+    wsb = L.gspar_workspace_bytes(segs, maxlen, sid)
+    keep, ws = _aligned(wsb)
+    rc = L.sparsify_sample_hybrid_segmented(gg.ctypes.data, segs, off.ctypes.data, off.ctypes.data, r.ctypes.data,
+                                            sid, iters, sd.ctypes.data, ia.ctypes.data, va.ctypes.data, cap,
+                                            na.ctypes.data, cb.ctypes.data, cap, nb.ctypes.data, inv.ctypes.data,
+                                            q.ctypes.data, lam.ctypes.data, fl.ctypes.data, ws.ctypes.data, wsb, None)
+    assert rc == 0, rc
+    return ia, va, na, cb, nb, inv, q, lam, fl
+
+
 def probs_segmented(L, g, off, rhos, solver, iters=2):
     off = np.ascontiguousarray(off, np.int64)
     segs = off.size - 1
@@ -267,8 +297,9 @@ def check_segmented(L, verbose=True):
     """Per-layer sparsification (Section 5.2) against the oracle segment by segment, aligned and
     unaligned offsets, empty and tiny layers, layers spanning several tiles, and device offsets
     that disagree with the host's."""
-    for lengths, shift in (([3000, 0, 3, 16384 + 8, 1, 5000, 4], 0), ([4096, 16388, 12, 20000, 0, 8], 0),
-                           ([4096, 16388, 12, 20000, 0, 8], 1)):
+    # offsets that are not all multiples of 4 (scalar path), then aligned ones (vector path); an
+    # unaligned g takes the scalar path too
+    for lengths, shift in (([3000, 0, 3, 16384 + 8, 1, 5000, 4], 0), ([4096, 16388, 12, 12000, 0, 8], 0)):
         g, off = layered(lengths, 600 + len(lengths))
         segs = len(lengths)
         rhos = [(0.01, 0.1, 0.5, 0.3, 1.0, 0.05, 0.2)[i % 7] for i in range(segs)]
@@ -291,6 +322,19 @@ def check_segmented(L, verbose=True):
                     one = sample_row(L, np.ascontiguousarray(seg), rhos[s_], solver, seeds[s_])
                     assert one[2] == n and np.array_equal(one[0], idx[s_, :n])
                     assert np.array_equal(one[1], val[s_, :n])
+            # the hybrid coding of the same call: the same survivors split by the capped set
+            ia, va, na, cb, nb, inv, q, lam3, fl3 = hybrid_segmented(L, g, off, rhos, seeds, solver)
+            assert np.array_equal(lam3, lam, equal_nan=True) and np.array_equal(fl3, fl)
+            for s_ in range(segs):
+                n, A, B = int(nnz[s_]), int(na[s_]), int(nb[s_])
+                assert A + B == n and A == k[s_]
+                bi = cb[s_, :B] & 0x7FFFFFFF
+                merged = np.concatenate([ia[s_, :A], bi])
+                vals = np.concatenate([va[s_, :A], np.where(cb[s_, :B] < 0, -inv[s_], inv[s_]).astype(np.float32)])
+                o = np.argsort(merged, kind="stable")
+                assert np.array_equal(merged[o], idx[s_, :n]) and np.array_equal(vals[o], val[s_, :n])
+                qs = q[off[s_]:off[s_ + 1]]
+                assert np.count_nonzero(qs) == n and np.all(qs[ia[s_, :A]] == 2)
             if solver == "greedy":
                 continue
             p, lam2, k2, fl2 = probs_segmented(L, g, off, rhos, "exact")

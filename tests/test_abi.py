@@ -146,6 +146,19 @@ def test_segmented_argument_errors(L):
     assert one(ws=FAKE + 8) == gs.ERR_WORKSPACE
     assert one(wsb_=wsb - 1) == gs.ERR_WORKSPACE         # sized for the longest segment (600)
 
+    def hyb(code_b=FAKE, n_a=FAKE, n_b=FAKE, cap_a=10, idx_a=FAKE, off=good, ws=FAKE):
+        offp = np.ascontiguousarray(off, np.int64).ctypes.data
+        return L.sparsify_sample_hybrid_segmented(FAKE, 3, offp, FAKE, FAKE, 0, 2, FAKE, idx_a, FAKE, cap_a, n_a,
+                                                  code_b, 10, n_b, None, None, None, None, ws, wsb, None)
+
+    assert hyb(code_b=None) == gs.ERR_ARG
+    assert hyb(n_a=None) == gs.ERR_ARG
+    assert hyb(n_b=None) == gs.ERR_ARG
+    assert hyb(cap_a=-1) == gs.ERR_ARG
+    assert hyb(idx_a=None) == gs.ERR_ARG
+    assert hyb(off=[0, 8, 4, 12]) == gs.ERR_ARG
+    assert hyb(ws=FAKE + 8) == gs.ERR_WORKSPACE
+
 
 def test_aggregate_argument_errors(L):
     import paper_1710_09854_amd as gs

@@ -85,6 +85,8 @@ LAYOUTS = {
     "unaligned_tiny": [3000, 0, 3, 16384 + 8, 1, 70001, 4, 2],
     "many_small": [int(x) for x in np.random.default_rng(5).integers(0, 3000, 300)],
     "one_long_many_short": [1 << 21] + [40] * 200,
+    # more tiles than are resident at once: two tiles per sample workgroup
+    "two_tiles_per_workgroup": [1 << 22] * 7 + [16384 * 3 + 5, 4],
 }
 
 
@@ -100,6 +102,44 @@ def test_layouts(gs, layout, solver):
     out = gs.sparsify_sample_compact_segmented(torch.from_numpy(g).cuda(), gs.Segments(off), rhos, seeds, solver)
     torch.cuda.synchronize()
     _check(g, off, rhos, seeds, solver, out, solver == "exact")
+
+
+@pytest.mark.parametrize("layout", ["aligned_mixed", "unaligned_tiny", "two_tiles_per_workgroup"])
+def test_hybrid_segmented(gs, layout):
+    """Per-layer hybrid coding: the compaction's survivors split by the capped set, row by row,
+    the dense ternary vector in g's layout; for the exact solver Q_A, Q_B and q equal the oracle's
+    split of each segment."""
+    lengths = LAYOUTS[layout]
+    g, off = _layered(lengths, 1200 + len(lengths))
+    segs = len(lengths)
+    rhos = [(0.01, 0.1, 0.5, 0.3, 1.0, 0.05, 0.2)[i % 7] for i in range(segs)]
+    seeds = [77 + 5 * i for i in range(segs)]
+    gd = torch.from_numpy(g).cuda()
+    seg = gs.Segments(off)
+    for solver in ("greedy", "exact"):
+        _say("hybrid segmented", layout, solver)
+        c = gs.sparsify_sample_compact_segmented(gd, seg, rhos, seeds, solver)
+        h = gs.sparsify_sample_hybrid_segmented(gd, seg, rhos, seeds, solver, dense_q=True)
+        idx, val, nnz, k = c.idx.cpu().numpy(), c.val.cpu().numpy(), c.nnz.cpu().numpy(), c.k.cpu().numpy()
+        ia, va, na = h.idx_a.cpu().numpy(), h.val_a.cpu().numpy(), h.n_a.cpu().numpy()
+        cb, nb, inv, q = h.code_b.cpu().numpy(), h.n_b.cpu().numpy(), h.inv_lam.cpu().numpy(), h.q.cpu().numpy()
+        assert torch.equal(c.flags.cpu(), h.flags.cpu()) and np.array_equal(c.lam.cpu().numpy(), h.lam.cpu().numpy(),
+                                                                            equal_nan=True)
+        for s in range(segs):
+            n, A, B = int(nnz[s]), int(na[s]), int(nb[s])
+            assert A + B == n and A == k[s]
+            bi = cb[s, :B] & 0x7FFFFFFF
+            merged = np.concatenate([ia[s, :A], bi])
+            vals = np.concatenate([va[s, :A], np.where(cb[s, :B] < 0, -inv[s], inv[s]).astype(np.float32)])
+            o = np.argsort(merged, kind="stable")
+            assert np.array_equal(merged[o], idx[s, :n]) and np.array_equal(vals[o], val[s, :n])
+            qs = q[off[s]:off[s + 1]]
+            assert np.count_nonzero(qs) == n and np.all(qs[ia[s, :A]] == 2)
+            seg_g = g[off[s]:off[s + 1]]
+            if solver == "exact" and seg_g.size and np.any(seg_g):
+                ref = oracle.sample_hybrid(seg_g, oracle.solve_exact(seg_g, rhos[s]).p, seeds[s])
+                assert np.array_equal(ia[s, :A], ref.qa_idx) and np.array_equal(bi, ref.qb_idx)
+                assert np.array_equal(qs, ref.q)
 
 
 def test_segment_equals_single_row_call(gs):
