@@ -406,11 +406,13 @@ def check_aggregate(L, verbose=True):
     return True
 
 
-def run_extra(path, verbose=True):
+def run_extra(path, verbose=True, lite=False):
+    """Edge cases, batching, overflow and the unaligned path; `lite` (for reruns of the same cases
+    under other launch conditions) keeps one greedy step count and skips the single-row repeats."""
     L = load(path)
     # greedy step counts
     g = W.t_mixture(30001, 11)
-    for T in (0, 1, 3, 8):
+    for T in ((2,) if lite else (0, 1, 3, 8)):
         for rho in (0.01, 0.3):
             sol = oracle.solve_greedy(g, rho, T)
             idx, val, n, lam, k, fl = sample_row(L, g, rho, "greedy", 5, iters=T)
@@ -451,9 +453,10 @@ def run_extra(path, verbose=True):
             sol = oracle.solve(g2[r], rhos[r], solver, 2)
             n = int(nnz[r])
             compare_sample(g2[r], sol.p, seeds[r], idx[r, :n], val[r, :n], n, lam[r], sol.lam)
-            one = sample_row(L, np.ascontiguousarray(g2[r]), rhos[r], solver, seeds[r])
-            assert one[2] == n and np.array_equal(one[0], idx[r, :n]) and np.array_equal(one[1], val[r, :n])
-            assert one[3] == lam[r]
+            if not lite:
+                one = sample_row(L, np.ascontiguousarray(g2[r]), rhos[r], solver, seeds[r])
+                assert one[2] == n and np.array_equal(one[0], idx[r, :n]) and np.array_equal(one[1], val[r, :n])
+                assert one[3] == lam[r]
     idx, val, nnz, lam, k, fl = batched(L, g2[:2], [0.1, 1.5], [1, 2], "greedy")
     assert fl[1] & 8 and nnz[1] == 0 and fl[0] == 0 and nnz[0] > 0
     # unaligned row start (scalar-load path)
@@ -475,6 +478,8 @@ if __name__ == "__main__":
     which = sys.argv[2] if len(sys.argv) > 2 else "all"
     if which in ("all", "extra"):
         run_extra(sys.argv[1])
+    if which == "extra_lite":
+        run_extra(sys.argv[1], lite=True)
     if which in ("all", "hybrid"):
         check_hybrid(load(sys.argv[1]))
     if which in ("all", "aggregate"):

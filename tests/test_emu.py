@@ -77,7 +77,7 @@ def test_emulated_lookback_fallback():
     """Hide every published tile status so each look-back counts its predecessors itself."""
     lib = emu_build.build(asan=False)
     env = dict(os.environ, EMU_HIDE_STATUS="1", EMU_STALL_SECONDS="300")
-    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "extra"], env=env,
+    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "extra_lite"], env=env,
                        capture_output=True, text=True, timeout=1200)
     assert r.returncode == 0 and "extra cases ok" in r.stdout, (r.stdout[-2000:], r.stderr[-2000:])
 
@@ -89,7 +89,7 @@ def test_emulated_two_tiles_per_workgroup():
     env = dict(os.environ, GSPAR_EMU_RESIDENT="1")
     lib = subprocess.run([sys.executable, "-c", "import sys; sys.path.insert(0, %r); import build; print(build.build())"
                           % os.path.join(HERE, "emu")], env=env, capture_output=True, text=True, check=True).stdout.strip()
-    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "extra"], env=env,
+    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "extra_lite"], env=env,
                        capture_output=True, text=True, timeout=1200)
     assert r.returncode == 0 and "extra cases ok" in r.stdout, (r.stdout[-2000:], r.stderr[-2000:])
     r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "hybrid"], env=env,

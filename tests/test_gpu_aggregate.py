@@ -131,3 +131,23 @@ def test_aggregate_skips_out_of_range_entries(gs):
         keep = (i >= 0) & (i < 60000)
         lists.append((i[keep], x[keep]))
     assert np.array_equal(v, oracle.aggregate(lists, 60000))
+
+
+@pytest.mark.parametrize("solver", ["greedy", "exact"])
+def test_aggregate_then_sparsify_the_average(gs, c2_lists, solver):
+    """Algorithm 1 steps 6-7 on one device: the average of the workers' messages, sparsified again
+    before it is broadcast. The average is bit-exact, so the second sparsification is checked under
+    the parity rule against the oracle's sparsification of the oracle's average."""
+    from oracle.compare import compare_sample
+
+    I, V, N, d = c2_lists[0.1]
+    _say("aggregate then sparsify", solver)
+    v = gs.aggregate(torch.from_numpy(I).cuda(), torch.from_numpy(V).cuda(), torch.from_numpy(N).cuda(), d)
+    out = gs.sparsify_sample_compact(v, 0.01, 4242, solver)
+    torch.cuda.synchronize()
+    v_ref = oracle.aggregate(_lists(I, V, N), d)
+    assert np.array_equal(v.cpu().numpy(), v_ref)
+    sol = oracle.solve(v_ref, 0.01, solver, 2)
+    n = int(out.nnz[0].item())
+    compare_sample(v_ref, sol.p, 4242, out.idx[:n].cpu().numpy(), out.val[:n].cpu().numpy(), n, out.lam[0].item(),
+                   sol.lam)
