@@ -29,6 +29,12 @@
  *    never splitting ties) or GSPAR_GREEDY (Algorithm 3 for `greedy_iters` rescale steps; the
  *    paper's experiments use 2). Special cases: if B >= nnz(g), every nonzero is kept with
  *    probability one (lambda = +inf, Q(g) = g); if rho = 0 nothing is kept (lambda = 0).
+ *    GSPAR_VARIANCE is Algorithm 2 as printed, with the variance budget of problem (4): every rho
+ *    argument then carries eps (any finite eps >= 0), the capped set is {a > a_(k+1)} for the
+ *    smallest k with a_(k+1) T1 <= eps sum a^2 + T2 (eq. 6; T1, T2 the sum and the sum of squares
+ *    of the magnitudes not above a_(k+1)) and lambda = T1 / (eps sum a^2 + T2) (eq. 7), every sum
+ *    exact and rounded once; if no value satisfies the criterion (possible only through rounding
+ *    with eps = 0) every nonzero is capped (lambda = +inf). greedy_iters is ignored.
  *  - Random source: coordinate i of a row with seed s uses word (i mod 4) of Philox4x32-10 with
  *    key (s low 32, s high 32) and counter (floor(i/4) low 32, floor(i/4) high 32, 0, 0);
  *    Z_i = 1 iff word < p_i * 2^32 (Salmon et al., SC'11 for the generator).
@@ -36,7 +42,8 @@
  *    runs, launch geometries and streams.
  *  - Errors detectable on the host are returned synchronously before anything is enqueued:
  *    GSPAR_ERR_ARG (NULL required pointer, d < 1 or d > 2^31 - 1, rows < 1, ld < d, rho outside
- *    [0, 1] or NaN for scalar rho, greedy_iters outside [0, 64], unknown solver, negative
+ *    [0, 1] or NaN for scalar rho (eps negative, infinite or NaN for GSPAR_VARIANCE),
+ *    greedy_iters outside [0, 64], unknown solver, negative
  *    capacity), GSPAR_ERR_WORKSPACE (ws NULL or ws_bytes below gspar_workspace_bytes) and
  *    GSPAR_ERR_HIP (a launch failed). Data-dependent conditions are reported per row in `flags`.
  *  - Calls that share a workspace must be stream-ordered; concurrent calls need distinct
@@ -59,7 +66,7 @@ typedef enum {
   GSPAR_ERR_HIP = -3
 } gspar_status;
 
-typedef enum { GSPAR_GREEDY = 0, GSPAR_EXACT = 1 } gspar_solver;
+typedef enum { GSPAR_GREEDY = 0, GSPAR_EXACT = 1, GSPAR_VARIANCE = 2 } gspar_solver;
 
 /* Per-row flag bits written to `flags[r]`. */
 enum {
@@ -67,7 +74,7 @@ enum {
   GSPAR_FLAG_OVERFLOW = 2,  /* more survivors than capacity: the first `capacity` pairs are
                                written and nnz holds the true count                          */
   GSPAR_FLAG_ALLZERO = 4,   /* g is identically zero: nnz = 0                                 */
-  GSPAR_FLAG_BADRHO = 8,    /* (batched) rho[r] outside [0, 1] or NaN: row skipped, nnz = 0  */
+  GSPAR_FLAG_BADRHO = 8,    /* (batched) rho[r] outside [0, 1] or NaN (eps: negative, infinite or NaN): row skipped, nnz = 0 */
   GSPAR_FLAG_BADSEG = 32    /* (segmented) the device offsets of the segment disagree with the
                                host offsets' bounds: segment skipped, nnz = 0                 */
 };

@@ -168,10 +168,13 @@ def solve_greedy_scale(g, rho: float, iters: int = 2) -> Solution:
 
 
 def solve(g, rho: float, solver: str = "greedy", iters: int = 2) -> Solution:
+    """rho is the density for "greedy" and "exact", the variance budget eps for "variance"."""
     if solver == "greedy":
         return solve_greedy(g, rho, iters)
     if solver == "exact":
         return solve_exact(g, rho)
+    if solver == "variance":
+        return solve_variance(g, rho)
     raise ValueError(solver)
 
 

@@ -30,6 +30,7 @@ LIB_PATH = os.path.join(_HERE, "libgspar.so")
 
 GREEDY = 0
 EXACT = 1
+VARIANCE = 2  # the rho arguments then carry the variance budget eps
 FLAG_NONFINITE = 1
 FLAG_OVERFLOW = 2
 FLAG_ALLZERO = 4
@@ -107,6 +108,8 @@ def _solver_id(solver) -> int:
         return GREEDY
     if solver in ("exact", EXACT):
         return EXACT
+    if solver in ("variance", VARIANCE):
+        return VARIANCE
     raise ValueError(f"unknown solver {solver!r}")
 
 

@@ -152,6 +152,98 @@ GS_HD double fx_to_double(const Fx& a) {
 }
 
 // ------------------------------------------------------------------------------------------
+// 640-bit fixed point, value = x * 2^-298 (the square of the smallest subnormal float): exact sums
+// of squared magnitudes for the variance-budget solver.
+// ------------------------------------------------------------------------------------------
+constexpr int kQ = 10;
+struct Fq {
+  uint64_t w[kQ];
+};
+
+GS_HD Fq fq_zero() {
+  Fq r;
+  for (int i = 0; i < kQ; ++i) r.w[i] = 0;
+  return r;
+}
+GS_HD void fq_add(Fq& a, const Fq& b) {
+  uint64_t c = 0;
+  for (int i = 0; i < kQ; ++i) {
+    uint64_t s = a.w[i] + b.w[i];
+    uint64_t c1 = s < a.w[i];
+    uint64_t s2 = s + c;
+    uint64_t c2 = s2 < s;
+    a.w[i] = s2;
+    c = c1 | c2;
+  }
+}
+GS_HD Fq fq_sub(const Fq& a, const Fq& b) {  // requires a >= b
+  Fq r;
+  uint64_t br = 0;
+  for (int i = 0; i < kQ; ++i) {
+    uint64_t d1 = a.w[i] - b.w[i];
+    uint64_t b1 = a.w[i] < b.w[i];
+    uint64_t d2 = d1 - br;
+    uint64_t b2 = d1 < br;
+    r.w[i] = d2;
+    br = b1 | b2;
+  }
+  return r;
+}
+GS_HD uint64_t fq_limb(const Fq& a, int i) {
+  uint64_t r = 0;
+#pragma unroll
+  for (int j = 0; j < kQ; ++j) r = (j == i) ? a.w[j] : r;
+  return r;
+}
+// Squared significands summed per bin as qh * 2^24 + ql (each square m^2 < 2^48 split at bit 24;
+// qh, ql < 2^55 for at most 2^31 values), times 2^(2 shift): the bin's exact sum of squares.
+GS_HD Fq fq_squares(uint64_t qh, uint64_t ql, int shift) {
+  const uint64_t lo0 = qh << 24;
+  const uint64_t lo = lo0 + ql;
+  const uint64_t hi = (qh >> 40) + (lo < lo0 ? 1 : 0);
+  int sh = 2 * shift;
+  sh = sh < 0 ? 0 : (sh > 506 ? 506 : sh);
+  const int li = sh >> 6, off = sh & 63;
+  const uint64_t w0 = lo << off;
+  const uint64_t w1 = off ? ((lo >> (64 - off)) | (hi << off)) : hi;
+  const uint64_t w2 = off ? (hi >> (64 - off)) : 0;
+  Fq r;
+#pragma unroll
+  for (int j = 0; j < kQ; ++j) r.w[j] = j == li ? w0 : (j == li + 1 ? w1 : (j == li + 2 ? w2 : 0));
+  return r;
+}
+GS_HD bool fq_bit(const Fq& a, int k) { return (fq_limb(a, k >> 6) >> (k & 63)) & 1; }
+GS_HD bool fq_any_below(const Fq& a, int k) {
+  if (k <= 0) return false;
+  const int li = k >> 6, off = k & 63;
+  bool any = false;
+#pragma unroll
+  for (int j = 0; j < kQ; ++j) {
+    const uint64_t m = j < li ? ~0ull : ((j == li && off) ? ((1ull << off) - 1) : 0ull);
+    any = any || (a.w[j] & m) != 0;
+  }
+  return any;
+}
+// Round to the nearest double, ties to even.
+GS_HD double fq_to_double(const Fq& a) {
+  int top = -1;
+#pragma unroll
+  for (int i = 0; i < kQ; ++i)
+    if (a.w[i]) top = i * 64 + 63 - __builtin_clzll(a.w[i]);
+  if (top < 0) return 0.0;
+  if (top < 53) return ldexp((double)a.w[0], -298);
+  const int lo = top - 52;
+  const int li = lo >> 6, off = lo & 63;
+  uint64_t m = fq_limb(a, li) >> off;
+  if (off) m |= fq_limb(a, li + 1) << (64 - off);
+  m &= (1ull << 53) - 1;
+  const bool rnd = fq_bit(a, lo - 1);
+  const bool sticky = fq_any_below(a, lo - 1);
+  if (rnd && (sticky || (m & 1))) m += 1;
+  return ldexp((double)m, lo - 298);
+}
+
+// ------------------------------------------------------------------------------------------
 // Magnitude keys.
 // ------------------------------------------------------------------------------------------
 GS_HD uint32_t key_of(float x) {
@@ -272,6 +364,24 @@ struct alignas(16) L1Cache {
   Fx W[kB1];
 };
 static_assert(sizeof(L1Cache) % 16 == 0, "L1Cache is copied in 16-byte units");
+// Variance-budget solver: per-bin sums of squared significands (see fq_squares) of the level-1
+// histogram copies and of the level-2 window copies, and per row the exact total of squares and
+// the square sums that go with the solver's stored counts and sums (above the requested window,
+// and of the fallback candidate).
+struct H1Q {
+  uint64_t qh[kB1];
+  uint64_t ql[kB1];
+};
+struct alignas(256) WinQ {
+  uint64_t qh[kB2];
+  uint64_t ql[kB2];
+};
+struct alignas(256) VarCtl {
+  Fq A2;   // sum of a^2 over the row
+  Fq wH;   // square sum above the requested window
+  Fq fbH;  // square sum of the fallback candidate's capped set
+};
+
 // Per-row partial count of capped coordinates written by the probabilities pass, one per class.
 struct alignas(128) CountLine {
   unsigned long long v;
@@ -281,7 +391,7 @@ struct alignas(128) CountLine {
 GS_HD size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctl, h1, l1t, win, kc, status, bmap, tmap, total;
+  size_t ctl, h1, l1t, win, kc, status, bmap, tmap, h1q, winq, vctl, total;
   int64_t tiles;  // tiles per row of the sample pass
 };
 
@@ -311,6 +421,13 @@ GS_HD Layout layout_of(int64_t rows, int64_t d) {
   off += align256((size_t)rows * (size_t)((d + kMinChunk - 1) / kMinChunk) * sizeof(uint64_t));
   L.tmap = off;
   off += align256((size_t)rows * (size_t)L.tiles * sizeof(uint64_t));
+  // variance-budget solver only
+  L.h1q = off;
+  off += align256((size_t)rows * kC1 * sizeof(H1Q));
+  L.winq = off;
+  off += align256((size_t)rows * kC23 * sizeof(WinQ));
+  L.vctl = off;
+  off += align256((size_t)rows * sizeof(VarCtl));
   L.total = off;
   return L;
 }
@@ -385,6 +502,16 @@ __device__ __forceinline__ L1Cache* l1t_of(const Args& a, int64_t r) {
 }
 __device__ __forceinline__ WinHist* win_of(const Args& a, int64_t r, int c = 0) {
   return reinterpret_cast<WinHist*>(a.ws + a.lay.win) + r * kC23 + c;
+}
+
+__device__ __forceinline__ H1Q* h1q_of(const Args& a, int64_t r, int c = 0) {
+  return reinterpret_cast<H1Q*>(a.ws + a.lay.h1q) + r * kC1 + c;
+}
+__device__ __forceinline__ WinQ* winq_of(const Args& a, int64_t r, int c = 0) {
+  return reinterpret_cast<WinQ*>(a.ws + a.lay.winq) + r * kC23 + c;
+}
+__device__ __forceinline__ VarCtl* vctl_of(const Args& a, int64_t r) {
+  return reinterpret_cast<VarCtl*>(a.ws + a.lay.vctl) + r;
 }
 
 __device__ __forceinline__ CountLine* kc_of(const Args& a, int64_t r) {
@@ -482,6 +609,14 @@ struct StatsLds {
   unsigned long long pk[kB1 * kLaneCopies];
   uint32_t mx[kB1 * kLaneCopies];
 };
+// with the squared significands of the variance-budget solver (split at bit 24, see fq_squares)
+template <bool SQ>
+struct StatsLdsT : StatsLds {};
+template <>
+struct StatsLdsT<true> : StatsLds {
+  unsigned long long qh[kB1 * kLaneCopies];
+  unsigned long long ql[kB1 * kLaneCopies];
+};
 // LDS of a refinement pass: one window of at most kB2 bins, same packing, and for a level-2 window
 // the complemented bin minimum.
 struct WinLds {
@@ -490,6 +625,13 @@ struct WinLds {
   uint32_t mnc[kB2];
   uint64_t qc[kNT / 64];
   uint64_t qs[kNT / 64];
+};
+template <bool SQ>
+struct WinLdsT : WinLds {};
+template <>
+struct WinLdsT<true> : WinLds {
+  unsigned long long qh[kB2];
+  unsigned long long ql[kB2];
 };
 struct BinInfo {
   uint64_t Kab;  // count of keys strictly above the bin (including above the window)
@@ -517,6 +659,11 @@ struct SolveLds {
   WinCache<kB3> w3;
   uint64_t bcnt, bsig;  // a level-2 bin's totals, broadcast by its owner (greedy queries)
   uint32_t bmx, bmn;
+  // variance-budget solver: partial square sums of scans, and broadcasts of square sums
+  Fq sq[kB1 / 64];
+  Fq hq[2];
+  uint64_t sqh[kNT / 64];
+  uint64_t sql[kNT / 64];
 };
 struct Hists {
   L1Cache* l1;         // LDS
@@ -525,6 +672,9 @@ struct Hists {
   L1Cache* l1g;        // the row's level-1 table in global memory, written by the first solve
   const Hist1* h1g;    // the row's global copies, filled by the histogram passes
   WinHist* wg;         // copies of the refinement window
+  const H1Q* h1q;      // variance-budget solver: square sums of the level-1 copies
+  WinQ* wq;            // and of the level-2 window copies
+  VarCtl* vc;          // and its per-row state
 };
 
 GS_DI int block_max(SolveLds& s, int v) {
@@ -944,7 +1094,297 @@ GS_DI void sv_exact(SolveLds& s, RowCtl& c, const Hists& H) {
   sv_exact_finish(c, c1.Kab, c1.Wab, cand_tcap);
 }
 
+// ------------------------------------------------------------------------------------------
+// Variance-budget exact solver: Algorithm 2 as printed (budget (1 + eps) sum a^2 on the variance,
+// eqs. 6-7). With the magnitudes sorted decreasingly, k is the smallest index with
+// a_(k+1) T1_k <= eps A + T2_k, where A = sum a^2 and T1_k, T2_k are the sum and the sum of
+// squares of the magnitudes after the first k; lambda = T1_k / (eps A + T2_k) and the capped set
+// is {a > a_(k+1)}. Candidates are distinct values; moving down to the next smaller value never
+// turns the criterion from true to false, so the same three-level search as the density form
+// applies, with the square sums of the bins carried alongside the counts and sums.
+// ------------------------------------------------------------------------------------------
+GS_DI Fq wave_suffix(Fq x, int lane) {
+  for (int o = 1; o < 64; o <<= 1) {
+    Fq y;
+#pragma unroll
+    for (int i = 0; i < kQ; ++i) y.w[i] = __shfl_down(x.w[i], (unsigned)o);
+    if (lane + o < 64) fq_add(x, y);
+  }
+  return x;
+}
+
+// The criterion at a data value v, with W and H the exact sum and square sum of the magnitudes
+// above v: v * fl(S - W) <= fl(eps * fl(A2)) + fl(A2 - H), each operation rounded on its own (the
+// pragma keeps the compiler from fusing the product and the sum). T1 and the right-hand side are
+// returned for lambda.
+GS_DI bool v_criterion(double eps, const Fx& S, const Fq& A2, const Fx& W, const Fq& H, uint32_t vkey, double& T1,
+                       double& rhs) {
+#pragma clang fp contract(off)
+  T1 = fx_to_double(fx_sub(S, W));
+  const double T2 = fq_to_double(fq_sub(A2, H));
+  const double eA = eps * fq_to_double(A2);
+  rhs = eA + T2;
+  return key_value(vkey) * T1 <= rhs;
+}
+
+GS_DI void v_finish(RowCtl& c, const Fq& A2, const Fx& W, const Fq& H, uint32_t tcap) {
+  double T1, rhs;
+  v_criterion(c.B, c.S, A2, W, H, 1u, T1, rhs);
+  sv_finalize(c, T1 / rhs, tcap);
+}
+
+// A bin of a level: keys above it (count, sum, square sum), its own count and maximum key.
+struct VInfo {
+  uint64_t K;
+  Fx W;
+  Fq H;
+  uint64_t cnt;
+  uint32_t mx;
+};
+
+// Asks for a refinement window like sv_request, clears the window's square sums for level 2 and
+// keeps the square sum above the window.
+GS_DI void v_request(RowCtl& c, const Hists& H, int level, uint32_t E, uint32_t base, uint64_t wK, const Fx& wW,
+                     const Fq& wH) {
+  sv_request(c, H, level, E, base, kNone, wK, wW);
+  if (level == 2) {
+    uint4 z;
+    z.x = z.y = z.z = z.w = 0u;
+    uint4* w = reinterpret_cast<uint4*>(H.wq);
+    for (int i = threadIdx.x; i < (int)(kC23 * sizeof(WinQ) / 16); i += kNT) w[i] = z;
+  }
+  if (threadIdx.x == 0) H.vc->wH = wH;
+}
+
+// Level 1 (first solve): square sums of the binades from the global copies, the square sum above
+// each binade (exclusive suffix over binades), the total A2, then b1 = highest occupied binade whose
+// maximum passes the criterion and b2 = lowest occupied binade above b1.
+GS_DI void v_level1(SolveLds& s, const RowCtl& c, const Hists& H, Fq& A2, int& b1, int& b2, VInfo& i1, VInfo& i2) {
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  Fq q = fq_zero(), iq = fq_zero();
+  if (t < kB1) {  // whole waves
+    uint64_t qh = 0, ql = 0;
+    for (int k = 0; k < kC1; ++k) {
+      qh += H.h1q[k].qh[t];
+      ql += H.h1q[k].ql[t];
+    }
+    if (H.l1->cnt[t]) q = fq_squares(qh, ql, binade_shift(t));
+    iq = wave_suffix(q, lane);
+    if (lane == 0) s.sq[wv] = iq;
+  }
+  __syncthreads();
+  Fq above = fq_zero();
+  if (t < kB1) {
+    above = fq_sub(iq, q);
+    for (int i = wv + 1; i < kB1 / 64; ++i) fq_add(above, s.sq[i]);
+    if (t == 0) {
+      Fq tot = above;
+      fq_add(tot, q);
+      s.hq[0] = tot;
+    }
+  }
+  __syncthreads();
+  A2 = s.hq[0];
+  int best = -1, occupied = INT_MAX;
+  if (t < kB1 && H.l1->cnt[t]) {
+    double T1, rhs;
+    if (v_criterion(c.B, c.S, A2, H.l1->W[t], above, H.l1->mx[t], T1, rhs)) best = t;
+  }
+  b1 = block_max(s, best);
+  if (t < kB1 && t > b1 && H.l1->cnt[t]) occupied = t;
+  b2 = block_min(s, occupied);
+  if (t == b1) s.hq[0] = above;
+  if (t == b2) s.hq[1] = above;
+  __syncthreads();
+  if (b1 >= 0) {
+    i1.K = H.l1->K[b1];
+    i1.W = H.l1->W[b1];
+    i1.H = s.hq[0];
+    i1.cnt = H.l1->cnt[b1];
+    i1.mx = H.l1->mx[b1];
+  }
+  if (b2 != INT_MAX) {
+    i2.K = H.l1->K[b2];
+    i2.W = H.l1->W[b2];
+    i2.H = s.hq[1];
+    i2.cnt = H.l1->cnt[b2];
+    i2.mx = H.l1->mx[b2];
+  }
+  __syncthreads();
+}
+
+// Level 2 (a binade's 4096 bins, square sums from the global window copies) or level 3 (2048
+// single keys from `base`, whose square sums follow from the counts): b1 and b2 as at level 1, the
+// keys above the window given by (L.Kaw, L.Waw, Haw).
+GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, bool level2, uint32_t base,
+                   const Fq& A2, const Fq& Haw, int& b1, int& b2, VInfo& i1, VInfo& i2) {
+  constexpr int kPer = kB2 / kNT;  // the larger of the two levels' bins per thread
+  const int per = L.per, b0 = threadIdx.x * per;
+  uint64_t qh[kPer], ql[kPer];
+  uint64_t tk = 0, ts = 0, tqh = 0, tql = 0;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    qh[j] = 0;
+    ql[j] = 0;
+    const int b = b0 + j;
+    if (j < per && b < L.nbins) {
+      if (level2) {
+#pragma unroll
+        for (int k = 0; k < kC23; ++k) {
+          qh[j] += H.wq[k].qh[b];
+          ql[j] += H.wq[k].ql[b];
+        }
+      } else {
+        const uint64_t m = key_sig(base + (uint32_t)b), m2 = m * m, cnt = (uint64_t)L.cnt[b];
+        qh[j] = cnt * (m2 >> 24);
+        ql[j] = cnt * (m2 & 0xFFFFFFu);
+      }
+      tk += (uint64_t)L.cnt[b];
+      ts += (uint64_t)L.sig[b];
+      tqh += qh[j];
+      tql += ql[j];
+    }
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const uint64_t ik = wave_suffix(tk, lane), is = wave_suffix(ts, lane);
+  const uint64_t iqh = wave_suffix(tqh, lane), iql = wave_suffix(tql, lane);
+  if (lane == 0) {
+    s.sk[wv] = ik;
+    s.ss[wv] = is;
+    s.sqh[wv] = iqh;
+    s.sql[wv] = iql;
+  }
+  __syncthreads();
+  uint64_t K = ik - tk, Sg = is - ts, QH = iqh - tqh, QL = iql - tql;  // above this thread's bins
+  for (int i = wv + 1; i < kNT / 64; ++i) {
+    K += s.sk[i];
+    Sg += s.ss[i];
+    QH += s.sqh[i];
+    QL += s.sql[i];
+  }
+  __syncthreads();
+  // this thread's bins from the top: the first passing one, and every occupied bin's aggregates
+  int best = -1;
+  uint64_t aK[kPer], aS[kPer], aQH[kPer], aQL[kPer];
+#pragma unroll
+  for (int jj = 0; jj < kPer; ++jj) {
+    const int j = kPer - 1 - jj;
+    aK[j] = K;
+    aS[j] = Sg;
+    aQH[j] = QH;
+    aQL[j] = QL;
+    const int b = b0 + j;
+    if (j >= per || b >= L.nbins) continue;
+    const uint64_t cnt = (uint64_t)L.cnt[b];
+    if (cnt && best < 0) {
+      Fx W = L.Waw;
+      if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
+      Fq Hq = Haw;
+      fq_add(Hq, fq_squares(QH, QL, L.shift));
+      double T1, rhs;
+      if (v_criterion(c.B, c.S, A2, W, Hq, L.mx[b], T1, rhs)) best = b;
+    }
+    K += cnt;
+    Sg += (uint64_t)L.sig[b];
+    QH += qh[j];
+    QL += ql[j];
+  }
+  b1 = block_max(s, best);
+  int lowest = INT_MAX;
+  for (int j = 0; j < per; ++j) {
+    const int b = b0 + j;
+    if (b < L.nbins && b > b1 && (uint64_t)L.cnt[b]) {
+      lowest = b;
+      break;
+    }
+  }
+  b2 = block_min(s, lowest);
+  // the owners of b1 and b2 broadcast their aggregates
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    const int bb = w == 0 ? b1 : b2;
+    if (bb >= 0 && bb != INT_MAX && (int)threadIdx.x == bb / per) {
+      const int j = bb - b0;
+      uint64_t kk = 0, ssg = 0, qqh = 0, qql = 0;
+#pragma unroll
+      for (int jj = 0; jj < kPer; ++jj)
+        if (jj == j) {
+          kk = aK[jj];
+          ssg = aS[jj];
+          qqh = aQH[jj];
+          qql = aQL[jj];
+        }
+      s.bi.Kab = L.Kaw + kk;
+      Fx W = L.Waw;
+      if (ssg) fx_add(W, fx_shifted(ssg, L.shift));
+      s.bi.Wab = W;
+      Fq Hq = Haw;
+      fq_add(Hq, fq_squares(qqh, qql, L.shift));
+      s.hq[0] = Hq;
+      s.bi.cnt = (uint64_t)L.cnt[bb];
+      s.bi.mx = L.mx[bb];
+    }
+    __syncthreads();
+    if (bb >= 0 && bb != INT_MAX) {
+      VInfo& o = w == 0 ? i1 : i2;
+      o.K = s.bi.Kab;
+      o.W = s.bi.Wab;
+      o.H = s.hq[0];
+      o.cnt = s.bi.cnt;
+      o.mx = s.bi.mx;
+    }
+    __syncthreads();
+  }
+}
+
+GS_DI void sv_variance(SolveLds& s, RowCtl& c, const Hists& H) {
+  const int level = c.stage;
+  int b1, b2;
+  VInfo i1, i2;
+  Fq A2;
+  uint32_t E = 0;
+  if (level == 1) {
+    v_level1(s, c, H, A2, b1, b2, i1, i2);
+    if (threadIdx.x == 0) H.vc->A2 = A2;
+  } else {
+    A2 = H.vc->A2;
+    const Fq Haw = H.vc->wH;
+    E = c.l2exp;
+    if (level == 2) {
+      const BinInfo iE = l1_info(H, (int)E);
+      v_level(s, c, H, lvl2(H, E, iE.Kab, iE.Wab), true, 0, A2, Haw, b1, b2, i1, i2);
+    } else {
+      v_level(s, c, H, lvl3(H, E, c.wK, c.wW), false, c.l3base, A2, Haw, b1, b2, i1, i2);
+    }
+  }
+  // refine b2 when it holds two or more values, of which a smaller one may pass (also when
+  // nothing at this level passes: the lowest occupied bin may still hold a passing value)
+  if (b2 != INT_MAX && level < 3 && i2.cnt >= 2) {
+    if (b1 >= 0) {
+      c.fbValid = 1;
+      c.fbK = i1.K;
+      c.fbW = i1.W;
+      c.fbTcap = i1.mx + 1;
+      if (threadIdx.x == 0) H.vc->fbH = i1.H;
+    }
+    c.stage = level + 1;
+    if (level == 1) v_request(c, H, 2, (uint32_t)b2, 0, 0, fx_zero(), i2.H);
+    else v_request(c, H, 3, 0, (E << 23) | ((uint32_t)b2 << 11), i2.K, i2.W, i2.H);
+    return;
+  }
+  if (b1 >= 0) {
+    v_finish(c, A2, i1.W, i1.H, i1.mx + 1);
+  } else if (c.fbValid) {
+    const Fq fbH = H.vc->fbH;
+    v_finish(c, A2, c.fbW, fbH, c.fbTcap);
+  } else {
+    // no value passes (possible only through rounding with eps = 0): every nonzero is capped
+    sv_finalize(c, INFINITY, 1);
+  }
+}
+
 // First solve after the statistics pass: totals and the special cases.
+template <bool VAR>
 GS_DI void sv_start(SolveLds& s, RowCtl& c, const Hists& H, int64_t d) {
   const BinInfo i0 = l1_info(H, 0);
   const BinInfo inf = l1_info(H, 255);
@@ -967,6 +1407,10 @@ GS_DI void sv_start(SolveLds& s, RowCtl& c, const Hists& H, int64_t d) {
   if (nnz == 0) {
     c.flags |= GSPAR_FLAG_ALLZERO;
     sv_finalize(c, INFINITY, 1);
+    return;
+  }
+  if constexpr (VAR) {
+    sv_variance(s, c, H);
     return;
   }
   if (c.B >= (double)nnz) {
@@ -1007,6 +1451,9 @@ GS_DI void reduce_into(const HistT* h, int copies, int nbins, CntT* cnt, uint64_
 // The row's solver, run by one workgroup per row after each histogram pass: it either finishes the
 // row (lambda and the capped threshold become final) or requests the next refinement window.
 // `first`: the solve right after the statistics pass.
+// VAR: the variance-budget solver's instantiation (a kernel of its own, so that its registers do
+// not weigh on the density-budget solvers).
+template <bool VAR>
 GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d, bool first) {
   // The global reads of a solve are issued together, so they share one round trip: level 1
   // (summed from its copies by the first solve, which also builds the suffix sums and keeps the
@@ -1057,7 +1504,9 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d, bool fi
     const uint4* src = reinterpret_cast<const uint4*>(H.l1);
     uint4* dst = reinterpret_cast<uint4*>(H.l1g);
     for (int i = threadIdx.x; i < n16; i += kNT) dst[i] = src[i];
-    sv_start(s, c, H, d);
+    sv_start<VAR>(s, c, H, d);
+  } else if constexpr (VAR) {
+    sv_variance(s, c, H);
   } else if (c.solver == GSPAR_GREEDY) {
     sv_greedy(s, c, H, qcnt, qsig);
   } else {
@@ -1156,14 +1605,25 @@ __global__ void __launch_bounds__(256) k_init(Args a) {
   uint64_t* st = status_of(a);
   const int64_t ns = a.rows * a.lay.tiles;
   for (int64_t i = tid; i < ns; i += stride) st[i] = 0;
+  if (a.solver == GSPAR_VARIANCE) {
+    uint64_t* q = reinterpret_cast<uint64_t*>(a.ws + a.lay.h1q);
+    const int64_t nq = a.rows * kC1 * (int64_t)(sizeof(H1Q) / 8);
+    for (int64_t i = tid; i < nq; i += stride) q[i] = 0;
+  }
   for (int64_t r = tid; r < a.rows; r += stride) {
     RowCtl c;
     memset(&c, 0, sizeof(c));
     const double rho = a.rho_dev ? a.rho_dev[r] : a.rho;
     int64_t base, len;
     const bool ok = row_span(a, r, base, len);
-    c.B = rho * (double)len;
-    if (!(rho >= 0.0 && rho <= 1.0)) c.flags = GSPAR_FLAG_BADRHO;
+    if (a.solver == GSPAR_VARIANCE) {
+      // the variance budget eps (any finite eps >= 0) in place of the density
+      c.B = rho;
+      if (!(rho >= 0.0 && rho < INFINITY)) c.flags = GSPAR_FLAG_BADRHO;
+    } else {
+      c.B = rho * (double)len;
+      if (!(rho >= 0.0 && rho <= 1.0)) c.flags = GSPAR_FLAG_BADRHO;
+    }
     if (!ok) c.flags |= GSPAR_FLAG_BADSEG;
     c.l2exp = kNone;
     c.l3base = kNone;
@@ -1193,10 +1653,10 @@ __device__ __forceinline__ bool hist_block(const Args& a, int64_t& row, int64_t&
 // histogram over binades (count, exact significand sum, maximum key), kept in kLaneCopies copies
 // by lane to spread same-address LDS atomics, and adds its nonempty bins into one of the row's kC1
 // global copies (chosen by workgroup index) with atomics. k_solve runs next.
-template <bool VEC>
+template <bool VEC, bool SQ>
 __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_stats(Args a) {
-  __shared__ StatsLds sm_st;
-  StatsLds& sm = sm_st;
+  __shared__ StatsLdsT<SQ> sm_st;
+  StatsLdsT<SQ>& sm = sm_st;
   int64_t row, blk;
   if (!hist_block(a, row, blk)) return;
   int64_t base, len;
@@ -1206,6 +1666,10 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   for (int b = threadIdx.x; b < kB1 * kLaneCopies; b += kNT) {
     sm.pk[b] = 0;
     sm.mx[b] = 0;
+    if constexpr (SQ) {
+      sm.qh[b] = 0;
+      sm.ql[b] = 0;
+    }
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + base;
@@ -1220,6 +1684,11 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
         atomicAdd(&sm.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
         // the bin maximum only grows, so a plain read that already covers key skips the atomic
         if (key > sm.mx[f]) atomicMax(&sm.mx[f], key);
+        if constexpr (SQ) {
+          const uint64_t m = key_sig(key), m2 = m * m;
+          atomicAdd(&sm.qh[f], (unsigned long long)(m2 >> 24));
+          atomicAdd(&sm.ql[f], (unsigned long long)(m2 & 0xFFFFFFu));
+        }
       }
     }
   });
@@ -1241,15 +1710,26 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
       atomicAdd((unsigned long long*)&h->cnt[e], (unsigned long long)cnt);
       atomicAdd((unsigned long long*)&h->sig[e], (unsigned long long)sg);
       atomicMax(&h->mx[e], mx);
+      if constexpr (SQ) {
+        uint64_t qh = 0, ql = 0;
+#pragma unroll
+        for (int j = 0; j < kLaneCopies; ++j) {
+          qh += sm.qh[e * kLaneCopies + j];
+          ql += sm.ql[e * kLaneCopies + j];
+        }
+        H1Q* q = h1q_of(a, row, (int)(blk % kC1));
+        atomicAdd((unsigned long long*)&q->qh[e], (unsigned long long)qh);
+        atomicAdd((unsigned long long*)&q->ql[e], (unsigned long long)ql);
+      }
     }
   }
 }
 
 // Refinement pass over one window of keys, for the rows whose solver asked for one.
-template <bool VEC>
+template <bool VEC, bool SQ>
 __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_refine(Args a) {
-  __shared__ WinLds sm_w;
-  WinLds& sm = sm_w;
+  __shared__ WinLdsT<SQ> sm_w;
+  WinLdsT<SQ>& sm = sm_w;
   int64_t row, blk;
   if (!hist_block(a, row, blk)) return;
   const RowCtl* ctl = ctl_of(a, row);
@@ -1277,10 +1757,17 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   // window when set; kNone matches no key)
   const bool l2 = need == 2;
   const uint32_t qkey = l2 ? ctl->qkey : kNone;
+  // the variance-budget solver's level-2 windows also sum squared significands (level 3 has one
+  // key per bin, whose square follows from the count)
+  const bool sq2 = SQ && l2;
   for (int b = threadIdx.x; b < nbins; b += kNT) {
     sm.pk[b] = 0;
     sm.mx[b] = 0;
     sm.mnc[b] = 0;
+    if constexpr (SQ) {
+      sm.qh[b] = 0;
+      sm.ql[b] = 0;
+    }
   }
   __syncthreads();
   const float* __restrict__ gr = a.g + base;
@@ -1300,6 +1787,13 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
         if (key >= qkey) {
           ++qc;
           qs += sg;
+        }
+        if constexpr (SQ) {
+          if (sq2) {
+            const uint64_t m2 = sg * sg;
+            atomicAdd(&sm.qh[b], (unsigned long long)(m2 >> 24));
+            atomicAdd(&sm.ql[b], (unsigned long long)(m2 & 0xFFFFFFu));
+          }
         }
       }
     }
@@ -1327,6 +1821,13 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
       atomicAdd((unsigned long long*)&h->sig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
       atomicMax(&h->mx[b], sm.mx[b]);
       if (l2) atomicMax(&h->mnc[b], sm.mnc[b]);
+      if constexpr (SQ) {
+        if (sq2) {
+          WinQ* q = winq_of(a, row, cp);
+          atomicAdd((unsigned long long*)&q->qh[b], (unsigned long long)sm.qh[b]);
+          atomicAdd((unsigned long long*)&q->ql[b], (unsigned long long)sm.ql[b]);
+        }
+      }
     }
   }
   if (l2 && threadIdx.x == 0) {
@@ -1343,6 +1844,7 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
 }
 
 // The solver: one workgroup per row, after the statistics pass and after every refinement pass.
+template <bool VAR>
 __global__ void __launch_bounds__(kNT) k_solve(Args a) {
   __shared__ SolveLds sm;
   const int64_t row = blockIdx.x;
@@ -1364,10 +1866,11 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
     }
     return;
   }
-  const Hists H{&sm.l1, &sm.w2, &sm.w3, l1t_of(a, row), h1_of(a, row), win_of(a, row)};
+  const Hists H{&sm.l1, &sm.w2, &sm.w3, l1t_of(a, row), h1_of(a, row), win_of(a, row),
+                h1q_of(a, row), winq_of(a, row), vctl_of(a, row)};
   int64_t base, len;
   row_span(a, row, base, len);
-  solve_row(sm, ctl_of(a, row), H, len, a.first != 0);
+  solve_row<VAR>(sm, ctl_of(a, row), H, len, a.first != 0);
 }
 
 // Sampling, amplification and order-preserving compaction. Workgroup t handles tile t (kTileElems
@@ -1940,12 +2443,15 @@ static void time_after(int which, hipStream_t s) {
   }
 }
 
-static bool rho_ok(double rho) { return rho >= 0.0 && rho <= 1.0; }
+// a density in [0, 1], or for the variance-budget solver a finite eps >= 0
+static bool rho_ok(double rho, int solver = GSPAR_EXACT) {
+  return solver == GSPAR_VARIANCE ? (rho >= 0.0 && rho < INFINITY) : (rho >= 0.0 && rho <= 1.0);
+}
 
 static int check_common(const float* g, int64_t rows, int64_t d, int64_t ld, int solver, int iters,
                         void* ws, size_t ws_bytes) {
   if (!g || rows < 1 || d < 1 || d > INT32_MAX || ld < d) return GSPAR_ERR_ARG;
-  if (solver != GSPAR_GREEDY && solver != GSPAR_EXACT) return GSPAR_ERR_ARG;
+  if (solver != GSPAR_GREEDY && solver != GSPAR_EXACT && solver != GSPAR_VARIANCE) return GSPAR_ERR_ARG;
   if (iters < 0 || iters > kMaxIters) return GSPAR_ERR_ARG;
   if (rows > (int64_t)1 << 24) return GSPAR_ERR_ARG;
   const Layout L = layout_of(rows, d);
@@ -1983,6 +2489,7 @@ static bool vec_ok(const Args& a) {
 static int launch_solve(Args& a, hipStream_t s) {
   const bool vec = vec_ok(a);
   const int64_t zero_items = a.rows * kC1 * (int64_t)(sizeof(Hist1) / 8) + a.rows * a.lay.tiles;
+  const bool sq = a.solver == GSPAR_VARIANCE;  // histogram passes that also sum squares
   int ib = (int)((zero_items + 255) / 256);
   if (ib > 1024) ib = 1024;
   if (ib < 1) ib = 1;
@@ -1995,27 +2502,39 @@ static int launch_solve(Args& a, hipStream_t s) {
   const dim3 grid((unsigned)nblocks);
   time_before(1, s);
   if (nblocks > 0) {
-    if (vec) hipLaunchKernelGGL(k_stats<true>, grid, dim3(kNT), 0, s, a);
-    else hipLaunchKernelGGL(k_stats<false>, grid, dim3(kNT), 0, s, a);
+    if (sq) {
+      if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_stats<true, true>), grid, dim3(kNT), 0, s, a);
+      else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_stats<false, true>), grid, dim3(kNT), 0, s, a);
+    } else {
+      if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_stats<true, false>), grid, dim3(kNT), 0, s, a);
+      else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_stats<false, false>), grid, dim3(kNT), 0, s, a);
+    }
   }
   time_after(1, s);
   a.first = 1;
   time_before(3, s);
-  hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
+  if (sq) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_solve<true>), dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
+  else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_solve<false>), dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
   time_after(3, s);
   // each greedy step needs at most one level-2 pass (which counts its query key directly), the
   // exact solver at most a level-2 and a level-3 window
-  const int R = a.solver == GSPAR_GREEDY ? a.T : 2;
+  const int R = a.solver == GSPAR_GREEDY ? a.T : 2;  // the variance form also needs at most two
   for (int r = 0; r < R; ++r) {
     a.first = 0;
     time_before(4, s);
     if (nblocks > 0) {
-      if (vec) hipLaunchKernelGGL(k_refine<true>, grid, dim3(kNT), 0, s, a);
-      else hipLaunchKernelGGL(k_refine<false>, grid, dim3(kNT), 0, s, a);
+      if (sq) {
+        if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_refine<true, true>), grid, dim3(kNT), 0, s, a);
+        else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_refine<false, true>), grid, dim3(kNT), 0, s, a);
+      } else {
+        if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_refine<true, false>), grid, dim3(kNT), 0, s, a);
+        else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_refine<false, false>), grid, dim3(kNT), 0, s, a);
+      }
     }
     time_after(4, s);
     time_before(3, s);
-    hipLaunchKernelGGL(k_solve, dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
+    if (sq) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_solve<true>), dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
+    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_solve<false>), dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
     time_after(3, s);
   }
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
@@ -2207,7 +2726,7 @@ int64_t gspar_capacity_hint(int64_t d, double rho) {
 
 int sparsify_probs(const float* g, int64_t d, double rho, int solver, int greedy_iters, float* p,
                    double* lambda, int64_t* k, uint32_t* flags, void* ws, size_t ws_bytes, void* stream) {
-  if (!lambda || !rho_ok(rho)) return GSPAR_ERR_ARG;
+  if (!lambda || !rho_ok(rho, solver)) return GSPAR_ERR_ARG;
   int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
   Args a = base_args(g, 1, d, d, solver, greedy_iters, ws);
@@ -2222,7 +2741,7 @@ int sparsify_probs(const float* g, int64_t d, double rho, int solver, int greedy
 int sparsify_sample_compact(const float* g, int64_t d, double rho, int solver, int greedy_iters, uint64_t seed,
                             int32_t* idx, float* val, int64_t capacity, int64_t* nnz, double* lambda, int64_t* k,
                             uint32_t* flags, void* ws, size_t ws_bytes, void* stream) {
-  if (!nnz || capacity < 0 || (capacity > 0 && (!idx || !val)) || !rho_ok(rho)) return GSPAR_ERR_ARG;
+  if (!nnz || capacity < 0 || (capacity > 0 && (!idx || !val)) || !rho_ok(rho, solver)) return GSPAR_ERR_ARG;
   int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
   Args a = base_args(g, 1, d, d, solver, greedy_iters, ws);
@@ -2269,7 +2788,8 @@ int sparsify_sample_hybrid(const float* g, int64_t d, double rho, int solver, in
                            int32_t* idx_a, float* val_a, int64_t cap_a, int64_t* n_a, int32_t* code_b, int64_t cap_b,
                            int64_t* n_b, float* inv_lambda, int8_t* q, double* lambda, uint32_t* flags, void* ws,
                            size_t ws_bytes, void* stream) {
-  if (!n_a || !n_b || cap_a < 0 || cap_b < 0 || (cap_a > 0 && (!idx_a || !val_a)) || !code_b || !rho_ok(rho))
+  if (!n_a || !n_b || cap_a < 0 || cap_b < 0 || (cap_a > 0 && (!idx_a || !val_a)) || !code_b ||
+      !rho_ok(rho, solver))
     return GSPAR_ERR_ARG;
   int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;

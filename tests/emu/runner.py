@@ -52,7 +52,7 @@ def sample_row(L, g, rho, solver, seed, iters=2, cap=None):
     lam = np.zeros(1)
     k = np.zeros(1, np.int64)
     fl = np.zeros(1, np.uint32)
-    sid = 0 if solver == "greedy" else 1
+    sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
     wsb = L.gspar_workspace_bytes(1, d, sid)
     keep, ws = _aligned(wsb)
     rc = L.sparsify_sample_compact(g.ctypes.data, d, rho, sid, iters, seed, idx.ctypes.data, val.ctypes.data, cap,
@@ -70,7 +70,7 @@ def probs_row(L, g, rho, solver, iters=2):
     lam = np.zeros(1)
     k = np.zeros(1, np.int64)
     fl = np.zeros(1, np.uint32)
-    sid = 0 if solver == "greedy" else 1
+    sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
     wsb = L.gspar_workspace_bytes(1, d, sid)
     keep, ws = _aligned(wsb)
     rc = L.sparsify_probs(g.ctypes.data, d, rho, sid, iters, p.ctypes.data, lam.ctypes.data, k.ctypes.data,
@@ -129,7 +129,7 @@ def batched(L, g2, rhos, seeds, solver, iters=2, cap=None, ld=None):
     fl = np.zeros(rows, np.uint32)
     r = np.ascontiguousarray(rhos, np.float64)
     s = np.array([int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds], np.uint64)
-    sid = 0 if solver == "greedy" else 1
+    sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
     wsb = L.gspar_workspace_bytes(rows, d, sid)
     keep, ws = _aligned(wsb)
     rc = L.sparsify_sample_compact_batched(buf.ctypes.data, rows, d, ld, r.ctypes.data, sid, iters, s.ctypes.data,
@@ -157,7 +157,7 @@ def hybrid_batched(L, g2, rhos, seeds, solver, iters=2, cap=None, ld=None):
     fl = np.zeros(rows, np.uint32)
     r = np.ascontiguousarray(rhos, np.float64)
     s = np.array([int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds], np.uint64)
-    sid = 0 if solver == "greedy" else 1
+    sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
     wsb = L.gspar_workspace_bytes(rows, d, sid)
     keep, ws = _aligned(wsb)
     rc = L.sparsify_sample_hybrid_batched(buf.ctypes.data, rows, d, ld, r.ctypes.data, sid, iters, s.ctypes.data,
@@ -224,7 +224,7 @@ def segmented(L, g, off, rhos, seeds, solver, iters=2, cap=None, off_dev=None, g
     fl = np.zeros(segs, np.uint32)
     r = np.ascontiguousarray(rhos, np.float64)
     s = np.array([int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds], np.uint64)
-    sid = 0 if solver == "greedy" else 1
+    sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
     wsb = L.gspar_workspace_bytes(segs, maxlen, sid)
     keep, ws = _aligned(wsb)
     rc = L.sparsify_sample_compact_segmented(buf.ctypes.data, segs, off.ctypes.data, od.ctypes.data, r.ctypes.data,
@@ -252,7 +252,7 @@ def hybrid_segmented(L, g, off, rhos, seeds, solver, iters=2):
     fl = np.zeros(segs, np.uint32)
     r = np.ascontiguousarray(rhos, np.float64)
     sd = np.array([int(x) & 0xFFFFFFFFFFFFFFFF for x in seeds], np.uint64)
-    sid = 0 if solver == "greedy" else 1
+    sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
     wsb = L.gspar_workspace_bytes(segs, maxlen, sid)
     keep, ws = _aligned(wsb)
     rc = L.sparsify_sample_hybrid_segmented(gg.ctypes.data, segs, off.ctypes.data, off.ctypes.data, r.ctypes.data,
@@ -272,7 +272,7 @@ def probs_segmented(L, g, off, rhos, solver, iters=2):
     k = np.zeros(segs, np.int64)
     fl = np.zeros(segs, np.uint32)
     r = np.ascontiguousarray(rhos, np.float64)
-    sid = 0 if solver == "greedy" else 1
+    sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
     wsb = L.gspar_workspace_bytes(segs, maxlen, sid)
     keep, ws = _aligned(wsb)
     gg = np.ascontiguousarray(g, np.float32)
@@ -355,6 +355,29 @@ def check_segmented(L, verbose=True):
     assert not fl.any() and np.all(nnz > 0)
     if verbose:
         print("segmented cases ok", flush=True)
+    return True
+
+
+def check_variance(L, verbose=True):
+    """Algorithm 2 with the variance budget: lambda and k bit for bit, the sample under the parity
+    rule, p within 1e-6."""
+    cases = [("normal", W.normal(20001, 1)), ("tmix", W.t_mixture(30001, 2)), ("ties", W.integer_ties(12001, 3)),
+             ("two_level", W.two_level(8001, 40, 50.0, 1.0, 5)), ("wide", W.wide_range(10000, 4)),
+             ("approx_sparse", W.approx_sparse(9000, 60, 0.05, 6)), ("tiny", W.normal(7, 7))]
+    for name, g in cases:
+        g = np.ascontiguousarray(g, np.float32)
+        for eps in (0.0, 0.05, 0.5, 5.0):
+            sol = oracle.solve_variance(g, eps)
+            idx, val, n, lam, k, fl = sample_row(L, g, eps, "variance", 31)
+            assert fl == 0, (name, eps, fl)
+            assert lam == sol.lam and k == sol.k, (name, eps, lam, sol.lam, k, sol.k)
+            compare_sample(g, sol.p, 31, idx, val, n, lam, sol.lam)
+            if eps > 0:
+                p, lam2, k2, fl2 = probs_row(L, g, eps, "variance")
+                assert lam2 == sol.lam
+                compare_probs(p, sol.p)
+    if verbose:
+        print("variance cases ok", flush=True)
     return True
 
 
@@ -484,6 +507,8 @@ if __name__ == "__main__":
         check_hybrid(load(sys.argv[1]))
     if which in ("all", "aggregate"):
         check_aggregate(load(sys.argv[1]))
+    if which in ("all", "variance"):
+        check_variance(load(sys.argv[1]))
     if which in ("all", "segmented"):
         check_segmented(load(sys.argv[1]))
     if which in ("all", "main"):

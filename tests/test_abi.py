@@ -69,7 +69,12 @@ def test_argument_errors(L):
     assert _sc(L, rho=-0.1) == gs.ERR_ARG
     assert _sc(L, rho=1.5) == gs.ERR_ARG
     assert _sc(L, rho=float("nan")) == gs.ERR_ARG
-    assert _sc(L, solver=2) == gs.ERR_ARG
+    assert _sc(L, solver=3) == gs.ERR_ARG
+    # the variance-budget solver takes any finite eps >= 0 in place of rho
+    assert _sc(L, solver=2, rho=-0.1) == gs.ERR_ARG
+    assert _sc(L, solver=2, rho=float("inf")) == gs.ERR_ARG
+    assert _sc(L, solver=2, rho=float("nan")) == gs.ERR_ARG
+    assert _sc(L, solver=2, rho=5.0, ws=FAKE + 8) == gs.ERR_WORKSPACE  # eps = 5 passes the eps check
     assert _sc(L, iters=-1) == gs.ERR_ARG
     assert _sc(L, iters=65) == gs.ERR_ARG
     assert _sc(L, cap=-1) == gs.ERR_ARG

@@ -32,6 +32,10 @@ def test_emulated_hybrid_coding(emu_lib):
     assert runner.check_hybrid(runner.load(emu_lib), verbose=False)
 
 
+def test_emulated_variance_solver(emu_lib):
+    assert runner.check_variance(runner.load(emu_lib), verbose=False)
+
+
 def test_emulated_segmented(emu_lib):
     assert runner.check_segmented(runner.load(emu_lib), verbose=False)
 
