@@ -43,8 +43,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5", "all"])
-    ap.add_argument("--solver", default=None, help="restrict to one solver")
-    ap.add_argument("--rho", type=float, default=None, help="restrict to one density")
+    ap.add_argument("--solver", default=None, choices=["greedy", "exact", "variance"],
+                    help="restrict to one solver ('variance': Algorithm 2 with the variance budget eps)")
+    ap.add_argument("--rho", type=float, default=None,
+                    help="restrict to one density (with --solver variance: one eps; default eps 0.1 and 1)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
     ap.add_argument("--copy-probe", action="store_true", help="copy a 512 MiB buffer 3 times first (counter scale)")
@@ -143,6 +145,15 @@ def summarize_pmc(fetch_dir, write_dir, workload):
     with open(TRAFFIC_JSON, "w") as fh:
         json.dump(data, fh, indent=1, sort_keys=True)
     print(json.dumps(data[workload], indent=1, sort_keys=True))
+
+
+VARIANCE_EPS = [0.1, 1.0]
+
+
+def capacity(gs, d, solver, rho):
+    """Output capacity per row: from the density, or every coordinate for the variance budget
+    (whose expected survivor count is not known before the solve)."""
+    return d if solver == "variance" else gs.capacity_hint(d, rho)
 
 
 def layer_setup(args, wl, dev):
@@ -245,8 +256,8 @@ def cells(args):
             seeds = torch.tensor([s - (1 << 64) if s >= (1 << 63) else s for s in wl.seeds], dtype=torch.int64,
                                  device=dev)
         for solver in ([args.solver] if args.solver else wl.solvers):
-            for rho in ([args.rho] if args.rho is not None else wl.rhos):
-                plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho),
+            for rho in ([args.rho] if args.rho is not None else (VARIANCE_EPS if solver == "variance" else wl.rhos)):
+                plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=capacity(gs, d, solver, rho),
                                hybrid=args.hybrid, dense_q=args.dense_q, segments=seg)
                 rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
                 for _ in range(3):
@@ -377,8 +388,9 @@ def main():
     dev = torch.device("cuda:0")
     wl = workloads.CONFIGS[args.workload]()
     solvers = [args.solver] if args.solver else wl.solvers
-    rhos = [args.rho] if args.rho is not None else wl.rhos
-    combos = [(s, r) for s in solvers for r in rhos]
+    combos = [(s, r) for s in solvers
+              for r in ([args.rho] if args.rho is not None else (VARIANCE_EPS if s == "variance" else wl.rhos))]
+    rhos = sorted({r for _, r in combos})
     seg = None
     if args.per_layer:
         g, seg, seeds = layer_setup(args, wl, dev)
@@ -392,7 +404,7 @@ def main():
                              device=dev)
     plans = []
     for solver, rho in combos:
-        plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=gs.capacity_hint(d, rho),
+        plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=capacity(gs, d, solver, rho),
                        hybrid=args.hybrid, dense_q=args.dense_q, segments=seg)
         rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
         plans.append((plan, rho_dev))

@@ -1216,29 +1216,41 @@ GS_DI void v_level1(SolveLds& s, const RowCtl& c, const Hists& H, Fq& A2, int& b
 // Level 2 (a binade's 4096 bins, square sums from the global window copies) or level 3 (2048
 // single keys from `base`, whose square sums follow from the counts): b1 and b2 as at level 1, the
 // keys above the window given by (L.Kaw, L.Waw, Haw).
+// The square-sum parts (see fq_squares) of bin b of a level: level 2 from the global window copies,
+// level 3 (one key per bin) the count times the key's squared significand.
+GS_DI void v_bin_squares(const Hists& H, const Lvl& L, bool level2, uint32_t base, int b, uint64_t& qh,
+                         uint64_t& ql) {
+  if (level2) {
+    qh = 0;
+    ql = 0;
+#pragma unroll
+    for (int k = 0; k < kC23; ++k) {
+      qh += H.wq[k].qh[b];
+      ql += H.wq[k].ql[b];
+    }
+  } else {
+    const uint64_t m = key_sig(base + (uint32_t)b), m2 = m * m, cnt = (uint64_t)L.cnt[b];
+    qh = cnt * (m2 >> 24);
+    ql = cnt * (m2 & 0xFFFFFFu);
+  }
+}
+
+// Level 2 (a binade's 4096 bins, square sums from the global window copies) or level 3 (2048
+// single keys from `base`): b1 and b2 as at level 1, the keys above the window given by (L.Kaw,
+// L.Waw, Haw). The thread's bins are walked again where needed instead of being held in registers.
 GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, bool level2, uint32_t base,
                    const Fq& A2, const Fq& Haw, int& b1, int& b2, VInfo& i1, VInfo& i2) {
   constexpr int kPer = kB2 / kNT;  // the larger of the two levels' bins per thread
   const int per = L.per, b0 = threadIdx.x * per;
-  uint64_t qh[kPer], ql[kPer];
   uint64_t tk = 0, ts = 0, tqh = 0, tql = 0;
+  uint64_t qh[kPer], ql[kPer];  // the thread's bins' square parts, loaded together
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     qh[j] = 0;
     ql[j] = 0;
     const int b = b0 + j;
     if (j < per && b < L.nbins) {
-      if (level2) {
-#pragma unroll
-        for (int k = 0; k < kC23; ++k) {
-          qh[j] += H.wq[k].qh[b];
-          ql[j] += H.wq[k].ql[b];
-        }
-      } else {
-        const uint64_t m = key_sig(base + (uint32_t)b), m2 = m * m, cnt = (uint64_t)L.cnt[b];
-        qh[j] = cnt * (m2 >> 24);
-        ql[j] = cnt * (m2 & 0xFFFFFFu);
-      }
+      v_bin_squares(H, L, level2, base, b, qh[j], ql[j]);
       tk += (uint64_t)L.cnt[b];
       ts += (uint64_t)L.sig[b];
       tqh += qh[j];
@@ -1255,39 +1267,37 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
     s.sql[wv] = iql;
   }
   __syncthreads();
-  uint64_t K = ik - tk, Sg = is - ts, QH = iqh - tqh, QL = iql - tql;  // above this thread's bins
+  uint64_t eK = ik - tk, eS = is - ts, eQH = iqh - tqh, eQL = iql - tql;  // above this thread's bins
   for (int i = wv + 1; i < kNT / 64; ++i) {
-    K += s.sk[i];
-    Sg += s.ss[i];
-    QH += s.sqh[i];
-    QL += s.sql[i];
+    eK += s.sk[i];
+    eS += s.ss[i];
+    eQH += s.sqh[i];
+    eQL += s.sql[i];
   }
   __syncthreads();
-  // this thread's bins from the top: the first passing one, and every occupied bin's aggregates
+  // this thread's bins from the top: the first (highest) passing one
   int best = -1;
-  uint64_t aK[kPer], aS[kPer], aQH[kPer], aQL[kPer];
+  {
+    uint64_t K = eK, Sg = eS, QH = eQH, QL = eQL;
 #pragma unroll
-  for (int jj = 0; jj < kPer; ++jj) {
-    const int j = kPer - 1 - jj;
-    aK[j] = K;
-    aS[j] = Sg;
-    aQH[j] = QH;
-    aQL[j] = QL;
-    const int b = b0 + j;
-    if (j >= per || b >= L.nbins) continue;
-    const uint64_t cnt = (uint64_t)L.cnt[b];
-    if (cnt && best < 0) {
-      Fx W = L.Waw;
-      if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
-      Fq Hq = Haw;
-      fq_add(Hq, fq_squares(QH, QL, L.shift));
-      double T1, rhs;
-      if (v_criterion(c.B, c.S, A2, W, Hq, L.mx[b], T1, rhs)) best = b;
+    for (int jj = 0; jj < kPer; ++jj) {
+      const int j = kPer - 1 - jj;
+      const int b = b0 + j;
+      if (j >= per || b >= L.nbins || best >= 0) continue;
+      const uint64_t cnt = (uint64_t)L.cnt[b];
+      if (cnt) {
+        Fx W = L.Waw;
+        if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
+        Fq Hq = Haw;
+        fq_add(Hq, fq_squares(QH, QL, L.shift));
+        double T1, rhs;
+        if (v_criterion(c.B, c.S, A2, W, Hq, L.mx[b], T1, rhs)) best = b;
+      }
+      K += cnt;
+      Sg += (uint64_t)L.sig[b];
+      QH += qh[j];
+      QL += ql[j];
     }
-    K += cnt;
-    Sg += (uint64_t)L.sig[b];
-    QH += qh[j];
-    QL += ql[j];
   }
   b1 = block_max(s, best);
   int lowest = INT_MAX;
@@ -1299,39 +1309,41 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
     }
   }
   b2 = block_min(s, lowest);
-  // the owners of b1 and b2 broadcast their aggregates
-#pragma unroll
+  // the owners of b1 and b2 broadcast the aggregates above their bin
   for (int w = 0; w < 2; ++w) {
     const int bb = w == 0 ? b1 : b2;
     if (bb >= 0 && bb != INT_MAX && (int)threadIdx.x == bb / per) {
-      const int j = bb - b0;
-      uint64_t kk = 0, ssg = 0, qqh = 0, qql = 0;
+      uint64_t K = eK, Sg = eS, QH = eQH, QL = eQL;
 #pragma unroll
-      for (int jj = 0; jj < kPer; ++jj)
-        if (jj == j) {
-          kk = aK[jj];
-          ssg = aS[jj];
-          qqh = aQH[jj];
-          qql = aQL[jj];
-        }
-      s.bi.Kab = L.Kaw + kk;
+      for (int jj = 0; jj < kPer; ++jj) {
+        const int j = kPer - 1 - jj;
+        const int b = b0 + j;
+        if (j >= per || b >= L.nbins || b <= bb) continue;
+        K += (uint64_t)L.cnt[b];
+        Sg += (uint64_t)L.sig[b];
+        QH += qh[j];
+        QL += ql[j];
+      }
+      s.bi.Kab = L.Kaw + K;
       Fx W = L.Waw;
-      if (ssg) fx_add(W, fx_shifted(ssg, L.shift));
+      if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
       s.bi.Wab = W;
       Fq Hq = Haw;
-      fq_add(Hq, fq_squares(qqh, qql, L.shift));
+      fq_add(Hq, fq_squares(QH, QL, L.shift));
       s.hq[0] = Hq;
       s.bi.cnt = (uint64_t)L.cnt[bb];
       s.bi.mx = L.mx[bb];
     }
     __syncthreads();
     if (bb >= 0 && bb != INT_MAX) {
-      VInfo& o = w == 0 ? i1 : i2;
+      VInfo o;
       o.K = s.bi.Kab;
       o.W = s.bi.Wab;
       o.H = s.hq[0];
       o.cnt = s.bi.cnt;
       o.mx = s.bi.mx;
+      if (w == 0) i1 = o;
+      else i2 = o;
     }
     __syncthreads();
   }
