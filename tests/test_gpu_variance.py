@@ -113,3 +113,20 @@ def test_variance_bad_eps_is_flagged(gs):
     out = gs.sparsify_sample_compact_batched(g, [0.1, -1.0], [1, 2], "variance", cap_per_row=5000)
     fl = out.flags.cpu().numpy()
     assert fl[0] == 0 and fl[1] & gs.FLAG_BADRHO and int(out.nnz[1].item()) == 0
+
+
+def test_variance_hybrid_split(gs):
+    """The hybrid coding with the variance-budget solver: Q_A is the capped set {a > v*}, Q_A and
+    Q_B together are the compaction's survivors, and both match the oracle's split."""
+    g = np.ascontiguousarray(W.t_mixture(150001, 8), np.float32)
+    gd = torch.from_numpy(g).cuda()
+    _say("variance hybrid")
+    for eps in (0.1, 2.0):
+        sol = oracle.solve_variance(g, eps)
+        h = gs.sparsify_sample_hybrid(gd, eps, 17, "variance", cap_a=g.size, cap_b=g.size, dense_q=True)
+        A, B = int(h.n_a[0].item()), int(h.n_b[0].item())
+        assert h.lam[0].item() == sol.lam and A == sol.k
+        ref = oracle.sample_hybrid(g, sol.p, 17)
+        assert np.array_equal(h.idx_a[:A].cpu().numpy(), ref.qa_idx)
+        assert np.array_equal(h.code_b[:B].cpu().numpy() & 0x7FFFFFFF, ref.qb_idx)
+        assert np.array_equal(h.q.cpu().numpy(), ref.q)
