@@ -1240,22 +1240,17 @@ GS_DI void v_bin_squares(const Hists& H, const Lvl& L, bool level2, uint32_t bas
 // L.Waw, Haw). The thread's bins are walked again where needed instead of being held in registers.
 GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, bool level2, uint32_t base,
                    const Fq& A2, const Fq& Haw, int& b1, int& b2, VInfo& i1, VInfo& i2) {
-  constexpr int kPer = kB2 / kNT;  // the larger of the two levels' bins per thread
   const int per = L.per, b0 = threadIdx.x * per;
   uint64_t tk = 0, ts = 0, tqh = 0, tql = 0;
-  uint64_t qh[kPer], ql[kPer];  // the thread's bins' square parts, loaded together
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    qh[j] = 0;
-    ql[j] = 0;
+  for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
-    if (j < per && b < L.nbins) {
-      v_bin_squares(H, L, level2, base, b, qh[j], ql[j]);
-      tk += (uint64_t)L.cnt[b];
-      ts += (uint64_t)L.sig[b];
-      tqh += qh[j];
-      tql += ql[j];
-    }
+    if (b >= L.nbins) break;
+    uint64_t qh, ql;
+    v_bin_squares(H, L, level2, base, b, qh, ql);
+    tk += (uint64_t)L.cnt[b];
+    ts += (uint64_t)L.sig[b];
+    tqh += qh;
+    tql += ql;
   }
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const uint64_t ik = wave_suffix(tk, lane), is = wave_suffix(ts, lane);
@@ -1275,28 +1270,34 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
     eQL += s.sql[i];
   }
   __syncthreads();
-  // this thread's bins from the top: the first (highest) passing one
+  // this thread's bins from the top: the first (highest) passing one (a loop that is not unrolled:
+  // the criterion's wide arithmetic is long, and one copy of it keeps the code in the instruction
+  // cache)
   int best = -1;
   {
     uint64_t K = eK, Sg = eS, QH = eQH, QL = eQL;
-#pragma unroll
-    for (int jj = 0; jj < kPer; ++jj) {
-      const int j = kPer - 1 - jj;
+#pragma unroll 1
+    for (int j = per - 1; j >= 0; --j) {
       const int b = b0 + j;
-      if (j >= per || b >= L.nbins || best >= 0) continue;
+      if (b >= L.nbins) continue;
       const uint64_t cnt = (uint64_t)L.cnt[b];
+      uint64_t qh, ql;
+      v_bin_squares(H, L, level2, base, b, qh, ql);
       if (cnt) {
         Fx W = L.Waw;
         if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
         Fq Hq = Haw;
         fq_add(Hq, fq_squares(QH, QL, L.shift));
         double T1, rhs;
-        if (v_criterion(c.B, c.S, A2, W, Hq, L.mx[b], T1, rhs)) best = b;
+        if (v_criterion(c.B, c.S, A2, W, Hq, L.mx[b], T1, rhs)) {
+          best = b;
+          break;
+        }
       }
       K += cnt;
       Sg += (uint64_t)L.sig[b];
-      QH += qh[j];
-      QL += ql[j];
+      QH += qh;
+      QL += ql;
     }
   }
   b1 = block_max(s, best);
@@ -1310,19 +1311,21 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
   }
   b2 = block_min(s, lowest);
   // the owners of b1 and b2 broadcast the aggregates above their bin
+#pragma unroll 1
   for (int w = 0; w < 2; ++w) {
     const int bb = w == 0 ? b1 : b2;
     if (bb >= 0 && bb != INT_MAX && (int)threadIdx.x == bb / per) {
       uint64_t K = eK, Sg = eS, QH = eQH, QL = eQL;
-#pragma unroll
-      for (int jj = 0; jj < kPer; ++jj) {
-        const int j = kPer - 1 - jj;
+#pragma unroll 1
+      for (int j = per - 1; b0 + j > bb; --j) {
         const int b = b0 + j;
-        if (j >= per || b >= L.nbins || b <= bb) continue;
+        if (b >= L.nbins) continue;
+        uint64_t qh, ql;
+        v_bin_squares(H, L, level2, base, b, qh, ql);
         K += (uint64_t)L.cnt[b];
         Sg += (uint64_t)L.sig[b];
-        QH += qh[j];
-        QL += ql[j];
+        QH += qh;
+        QL += ql;
       }
       s.bi.Kab = L.Kaw + K;
       Fx W = L.Waw;
@@ -1362,12 +1365,14 @@ GS_DI void sv_variance(SolveLds& s, RowCtl& c, const Hists& H) {
     A2 = H.vc->A2;
     const Fq Haw = H.vc->wH;
     E = c.l2exp;
+    Lvl L;
     if (level == 2) {
       const BinInfo iE = l1_info(H, (int)E);
-      v_level(s, c, H, lvl2(H, E, iE.Kab, iE.Wab), true, 0, A2, Haw, b1, b2, i1, i2);
+      L = lvl2(H, E, iE.Kab, iE.Wab);
     } else {
-      v_level(s, c, H, lvl3(H, E, c.wK, c.wW), false, c.l3base, A2, Haw, b1, b2, i1, i2);
+      L = lvl3(H, E, c.wK, c.wW);
     }
+    v_level(s, c, H, L, level == 2, level == 2 ? 0u : c.l3base, A2, Haw, b1, b2, i1, i2);
   }
   // refine b2 when it holds two or more values, of which a smaller one may pass (also when
   // nothing at this level passes: the lowest occupied bin may still hold a passing value)
@@ -1384,11 +1389,21 @@ GS_DI void sv_variance(SolveLds& s, RowCtl& c, const Hists& H) {
     else v_request(c, H, 3, 0, (E << 23) | ((uint32_t)b2 << 11), i2.K, i2.W, i2.H);
     return;
   }
-  if (b1 >= 0) {
-    v_finish(c, A2, i1.W, i1.H, i1.mx + 1);
-  } else if (c.fbValid) {
-    const Fq fbH = H.vc->fbH;
-    v_finish(c, A2, c.fbW, fbH, c.fbTcap);
+  if (b1 >= 0 || c.fbValid) {
+    // b1's maximum, else the candidate found one level up
+    Fx W;
+    Fq Hq;
+    uint32_t tcap;
+    if (b1 >= 0) {
+      W = i1.W;
+      Hq = i1.H;
+      tcap = i1.mx + 1;
+    } else {
+      W = c.fbW;
+      Hq = H.vc->fbH;
+      tcap = c.fbTcap;
+    }
+    v_finish(c, A2, W, Hq, tcap);
   } else {
     // no value passes (possible only through rounding with eps = 0): every nonzero is capped
     sv_finalize(c, INFINITY, 1);
