@@ -1127,6 +1127,20 @@ GS_DI bool v_criterion(double eps, const Fx& S, const Fq& A2, const Fx& W, const
   return key_value(vkey) * T1 <= rhs;
 }
 
+// A double-precision screen of the criterion from approximate sums (each within a few units of
+// rounding of the exact value, all terms non-negative): 1 or 0 when the margin exceeds 2^-44 of
+// v*S + (1 + eps)*A2, far above every rounding of either evaluation, so the exact criterion
+// decides the same way; -1 when the exact evaluation must decide.
+GS_DI int v_screen(double eps, double Sd, double A2d, double Wd, double Hd, double v) {
+#pragma clang fp contract(off)
+  const double lhs = v * (Sd - Wd);
+  const double rhs = eps * A2d + (A2d - Hd);
+  const double tol = 0x1p-44 * (v * Sd + (1.0 + eps) * A2d);
+  if (lhs <= rhs - tol) return 1;
+  if (lhs >= rhs + tol) return 0;
+  return -1;
+}
+
 GS_DI void v_finish(RowCtl& c, const Fq& A2, const Fx& W, const Fq& H, uint32_t tcap) {
   double T1, rhs;
   v_criterion(c.B, c.S, A2, W, H, 1u, T1, rhs);
@@ -1272,9 +1286,11 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
   __syncthreads();
   // this thread's bins from the top: the first (highest) passing one (a loop that is not unrolled:
   // the criterion's wide arithmetic is long, and one copy of it keeps the code in the instruction
-  // cache)
+  // cache). The double-precision screen decides all but the bins next to the threshold.
   int best = -1;
   {
+    const double Sd = fx_to_double(c.S), A2d = fq_to_double(A2);
+    const double Wawd = fx_to_double(L.Waw), Hawd = fq_to_double(Haw);
     uint64_t K = eK, Sg = eS, QH = eQH, QL = eQL;
 #pragma unroll 1
     for (int j = per - 1; j >= 0; --j) {
@@ -1284,12 +1300,18 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
       uint64_t qh, ql;
       v_bin_squares(H, L, level2, base, b, qh, ql);
       if (cnt) {
-        Fx W = L.Waw;
-        if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
-        Fq Hq = Haw;
-        fq_add(Hq, fq_squares(QH, QL, L.shift));
-        double T1, rhs;
-        if (v_criterion(c.B, c.S, A2, W, Hq, L.mx[b], T1, rhs)) {
+        const double Wd = Wawd + ldexp((double)Sg, L.shift - 149);
+        const double Hd = Hawd + ldexp((double)QH, 2 * L.shift - 298 + 24) + ldexp((double)QL, 2 * L.shift - 298);
+        int pass = v_screen(c.B, Sd, A2d, Wd, Hd, key_value(L.mx[b]));
+        if (pass < 0) {
+          Fx W = L.Waw;
+          if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
+          Fq Hq = Haw;
+          fq_add(Hq, fq_squares(QH, QL, L.shift));
+          double T1, rhs;
+          pass = v_criterion(c.B, c.S, A2, W, Hq, L.mx[b], T1, rhs) ? 1 : 0;
+        }
+        if (pass) {
           best = b;
           break;
         }
