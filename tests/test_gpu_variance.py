@@ -130,3 +130,21 @@ def test_variance_hybrid_split(gs):
         assert np.array_equal(h.idx_a[:A].cpu().numpy(), ref.qa_idx)
         assert np.array_equal(h.code_b[:B].cpu().numpy() & 0x7FFFFFFF, ref.qb_idx)
         assert np.array_equal(h.q.cpu().numpy(), ref.q)
+
+
+def test_variance_full_size_student_t(gs):
+    """The 2^28-coordinate Student-t(2) gradient with 1 % outliers at eps = 1, in the launch the
+    benchmark times (one call, output capacity d): lambda and k bit for bit, every survivor under
+    the parity rule."""
+    w = W.c5()
+    g = w.g[0]
+    _say("variance 2^28 student-t eps 1")
+    gd = torch.from_numpy(g).cuda()
+    out = gs.sparsify_sample_compact_batched(gd.view(1, -1), [1.0], w.seeds, "variance", cap_per_row=w.d)
+    lam, k, n = out.lam[0].item(), int(out.k[0].item()), int(out.nnz[0].item())
+    idx, val = out.idx[0, :n].cpu().numpy(), out.val[0, :n].cpu().numpy()
+    del out, gd
+    torch.cuda.empty_cache()
+    sol = oracle.solve_variance(g, 1.0)
+    assert lam == sol.lam and k == sol.k, (lam, sol.lam, k, sol.k)
+    compare_sample(g, sol.p, w.seeds[0], idx, val, n, lam, sol.lam)
