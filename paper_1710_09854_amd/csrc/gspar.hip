@@ -2013,6 +2013,7 @@ __device__ __forceinline__ uint32_t wave_prefix_small(uint32_t n, int lane, uint
 // LDS list's capacity (a separate instantiation).
 constexpr int kCapList = 256;    // capped survivor values kept per wave
 constexpr int kSampleBatch = 8;  // float4 loads in flight per lane in the sampling pass
+constexpr int kDenseEmit = 1024;  // survivors of a wave's quarter tile (of 4096) above which emission goes by groups
 static_assert(kTileGroups % kSampleBatch == 0 && kTileGroups == 16, "tile shape");
 // Below this lambda, lambda * 2^32 * |g| could round differently from (lambda * |g|) * 2^32.
 constexpr double kLamScaledMin = 0x1p-900;
@@ -2310,8 +2311,46 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             m &= m - 1;
           }
         };
-        if (lds_values) emit(std::true_type{});
-        else emit(std::false_type{});
+        if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
+          // many survivors: lane l takes the wave's groups 64 j + l (the order of phase 1 and of
+          // the capped-value list), one step j at a time, so the stores of a step fall on a few
+          // consecutive lines instead of one line per lane
+          const uint64_t base0 = (excl & 0x7FFFFFFFull) + wbase;
+          uint32_t carry = 0, ccarry = 0;
+          for (int j = 0; j < kTileGroups; ++j) {
+            const int q = wv * (kWaveElems / 4) + 64 * j + lane;  // tile group
+            const uint32_t code = s_code[kk][q];
+            const uint32_t sel = code & 0xFu, neg = code >> 4;
+            const uint32_t cap = (uint32_t)s_capb[kk][q] & sel;
+            uint32_t stot, ctot;
+            const uint32_t sp = wave_prefix_bits<3>((uint32_t)__popc(sel), stot);
+            const uint32_t cp = wave_prefix_bits<3>((uint32_t)__popc(cap), ctot);
+            uint64_t p = base0 + carry + sp;
+            uint32_t r = ccarry + cp;
+            const int64_t eq = part * (int64_t)kTileElems + 4 * (int64_t)q;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              if ((sel >> k) & 1) {
+                float val = ((neg >> k) & 1) ? -inv : inv;
+                if ((cap >> k) & 1) {
+                  val = lds_values ? s_capv[kk][wv][r] : c.row[eq + k];
+                  ++r;
+                }
+                if ((int64_t)p < a.cap) {
+                  oi[p] = (int32_t)(eq + k);
+                  ov[p] = val;
+                }
+                ++p;
+              }
+            }
+            carry += stot;
+            ccarry += ctot;
+          }
+        } else if (lds_values) {
+          emit(std::true_type{});
+        } else {
+          emit(std::false_type{});
+        }
       } else {
         // hybrid coding (Section 3.3, eqs. 9-10): capped survivors go to Q_A as (index, g_i), the
         // others to Q_B as index | sign << 31 (their value is sign(g_i) / lambda)
