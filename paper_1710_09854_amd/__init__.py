@@ -136,6 +136,14 @@ def capacity_hint(d: int, rho: float) -> int:
     return int(lib().gspar_capacity_hint(d, rho))
 
 
+def _default_cap(d: int, rho: float, solver) -> int:
+    """Output capacity per row when the caller gives none: from the density, or every coordinate
+    for the variance budget (its survivor count is not known before the solve)."""
+    if _solver_id(solver) == VARIANCE:
+        return int(d)
+    return capacity_hint(d, min(max(float(rho), 0.0), 1.0))
+
+
 class Workspace:
     """Grow-only device workspace (the library itself never allocates)."""
 
@@ -223,7 +231,7 @@ def sparsify_sample_compact(g, rho: float, seed: int = 0, solver="greedy", iters
     g = _as_row(g)
     d = g.numel()
     dev = g.device
-    cap = capacity_hint(d, rho) if capacity is None else int(capacity)
+    cap = _default_cap(d, rho, solver) if capacity is None else int(capacity)
     idx = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
     val = torch.empty(max(cap, 1), dtype=torch.float32, device=dev)
     nnz = torch.empty(1, dtype=torch.int64, device=dev)
@@ -262,7 +270,7 @@ def sparsify_sample_hybrid(g, rho: float, seed: int = 0, solver="greedy", iters:
     g = _as_row(g)
     d = g.numel()
     dev = g.device
-    cap_b = capacity_hint(d, rho) if cap_b is None else int(cap_b)
+    cap_b = _default_cap(d, rho, solver) if cap_b is None else int(cap_b)
     cap_a = cap_b if cap_a is None else int(cap_a)
     idx_a = torch.empty(max(cap_a, 1), dtype=torch.int32, device=dev)
     val_a = torch.empty(max(cap_a, 1), dtype=torch.float32, device=dev)
@@ -294,7 +302,7 @@ def sparsify_sample_hybrid_batched(g, rho, seeds, solver="greedy", iters: int = 
     s = _seeds_dev(seeds, rows, dev)
     if cap_b is None:
         rmax = float(r.max().item()) if rows else 0.0
-        cap_b = capacity_hint(d, min(max(rmax, 0.0), 1.0))
+        cap_b = _default_cap(d, rmax, solver)
     cap_b = int(cap_b)
     cap_a = cap_b if cap_a is None else int(cap_a)
     idx_a = torch.empty((rows, max(cap_a, 1)), dtype=torch.int32, device=dev)
@@ -405,7 +413,7 @@ class Plan:
         self.ld = d if ld is None else ld
         self.sid = _solver_id(solver)
         self.iters = int(iters)
-        self.cap = capacity_hint(d, rho_for_cap) if cap_per_row is None else int(cap_per_row)
+        self.cap = _default_cap(d, rho_for_cap, solver) if cap_per_row is None else int(cap_per_row)
         self.hybrid = bool(hybrid)
         dev = torch.device(device)
         # compaction: (idx, val) per survivor; hybrid coding: Q_A in (idx, val), Q_B in code_b
@@ -466,7 +474,7 @@ def sparsify_sample_compact_batched(g, rho, seeds, solver="greedy", iters: int =
     s = _seeds_dev(seeds, rows, dev)
     if cap_per_row is None:
         rmax = float(r.max().item()) if rows else 0.0
-        cap_per_row = capacity_hint(d, min(max(rmax, 0.0), 1.0))
+        cap_per_row = _default_cap(d, rmax, solver)
     cap = int(cap_per_row)
     idx = torch.empty((rows, max(cap, 1)), dtype=torch.int32, device=dev)
     val = torch.empty((rows, max(cap, 1)), dtype=torch.float32, device=dev)
@@ -521,7 +529,7 @@ def sparsify_sample_compact_segmented(g, seg: Segments, rho, seeds, solver="gree
     s = _seeds_dev(seeds, rows, dev)
     if cap_per_seg is None:
         rmax = float(r.max().item())
-        cap_per_seg = capacity_hint(seg.max_len, min(max(rmax, 0.0), 1.0))
+        cap_per_seg = _default_cap(seg.max_len, rmax, solver)
     cap = int(cap_per_seg)
     idx = torch.empty((rows, max(cap, 1)), dtype=torch.int32, device=dev)
     val = torch.empty((rows, max(cap, 1)), dtype=torch.float32, device=dev)
@@ -551,7 +559,7 @@ def sparsify_sample_hybrid_segmented(g, seg: Segments, rho, seeds, solver="greed
     s = _seeds_dev(seeds, rows, dev)
     if cap_b is None:
         rmax = float(r.max().item())
-        cap_b = capacity_hint(seg.max_len, min(max(rmax, 0.0), 1.0))
+        cap_b = _default_cap(seg.max_len, rmax, solver)
     cap_b = int(cap_b)
     cap_a = cap_b if cap_a is None else int(cap_a)
     idx_a = torch.empty((rows, max(cap_a, 1)), dtype=torch.int32, device=dev)
