@@ -2380,16 +2380,50 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             m &= m - 1;
           }
         };
-        if (cm) {
-          if (lds_values) emit_a(std::true_type{});
-          else emit_a(std::false_type{});
-        }
-        uint64_t m = bm;
-        while (m) {
-          const int b = __ffsll((unsigned long long)m) - 1;
-          if ((int64_t)pb < a.cap_b) ob[pb] = (int32_t)((uint32_t)(e0 + b) | (uint32_t)(((nm >> b) & 1) << 31));
-          ++pb;
-          m &= m - 1;
+        if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
+          // many survivors: group by group in phase-1 order, as in the compaction above
+          uint64_t pa0 = excl_cap + wbase_cap;
+          uint64_t pb0 = (excl & 0x7FFFFFFFull) - excl_cap + (wbase - wbase_cap);
+          for (int j = 0; j < kTileGroups; ++j) {
+            const int q = wv * (kWaveElems / 4) + 64 * j + lane;  // tile group
+            const uint32_t code = s_code[kk][q];
+            const uint32_t sel = code & 0xFu, neg = code >> 4;
+            const uint32_t cap = (uint32_t)s_capb[kk][q] & sel, oth = sel & ~cap;
+            uint32_t atot, btot2;
+            uint64_t qa = pa0 + wave_prefix_bits<3>((uint32_t)__popc(cap), atot);
+            uint64_t qb = pb0 + wave_prefix_bits<3>((uint32_t)__popc(oth), btot2);
+            uint32_t r = (uint32_t)(qa - excl_cap - wbase_cap);  // rank in the wave's capped list
+            const int64_t eq = part * (int64_t)kTileElems + 4 * (int64_t)q;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              if ((cap >> k) & 1) {
+                const float val = lds_values ? s_capv[kk][wv][r] : c.row[eq + k];
+                ++r;
+                if ((int64_t)qa < a.cap) {
+                  oa[qa] = (int32_t)(eq + k);
+                  va[qa] = val;
+                }
+                ++qa;
+              } else if ((oth >> k) & 1) {
+                if ((int64_t)qb < a.cap_b) ob[qb] = (int32_t)((uint32_t)(eq + k) | (((neg >> k) & 1u) << 31));
+                ++qb;
+              }
+            }
+            pa0 += atot;
+            pb0 += btot2;
+          }
+        } else {
+          if (cm) {
+            if (lds_values) emit_a(std::true_type{});
+            else emit_a(std::false_type{});
+          }
+          uint64_t m = bm;
+          while (m) {
+            const int b = __ffsll((unsigned long long)m) - 1;
+            if ((int64_t)pb < a.cap_b) ob[pb] = (int32_t)((uint32_t)(e0 + b) | (uint32_t)(((nm >> b) & 1) << 31));
+            ++pb;
+            m &= m - 1;
+          }
         }
       }
     }
