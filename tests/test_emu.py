@@ -89,7 +89,8 @@ def test_emulated_lookback_fallback():
 def test_emulated_two_tiles_per_workgroup():
     """The sampling pass's two-tiles-per-workgroup path (taken on the GPU by grids larger than the
     resident set) forced on the small emulated inputs: edge cases, batching, overflow, the
-    unaligned path, the hybrid coding and segmented rows, with tile counts odd and even."""
+    unaligned path and the hybrid coding, with tile counts odd and even (segmented rows with two
+    tiles per workgroup run on the GPU, in tests/test_gpu_segmented.py)."""
     env = dict(os.environ, GSPAR_EMU_RESIDENT="1")
     lib = subprocess.run([sys.executable, "-c", "import sys; sys.path.insert(0, %r); import build; print(build.build())"
                           % os.path.join(HERE, "emu")], env=env, capture_output=True, text=True, check=True).stdout.strip()
@@ -99,6 +100,3 @@ def test_emulated_two_tiles_per_workgroup():
     r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "hybrid"], env=env,
                        capture_output=True, text=True, timeout=1200)
     assert r.returncode == 0 and "hybrid cases ok" in r.stdout, (r.stdout[-2000:], r.stderr[-2000:])
-    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "segmented"], env=env,
-                       capture_output=True, text=True, timeout=1200)
-    assert r.returncode == 0 and "segmented cases ok" in r.stdout, (r.stdout[-2000:], r.stderr[-2000:])
