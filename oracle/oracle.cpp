@@ -218,8 +218,10 @@ double orc_exact_sum(const double* x, int64_t n) {
 // T_k = sum_{i>k} a_(i), take the smallest k with (B - k) * a_(k+1) <= T_k, then
 // lambda = (B - k) / T_k. The criterion is monotone in k and never holds strictly inside a run of
 // equal magnitudes in exact arithmetic, so it is evaluated only where a_(k) > a_(k+1) (or k = 0);
-// this keeps tied coordinates together in floating point as well. The capped set is then
-// {i : a_i > a_(k+1)}. Uses partial sorting (the top floor(B)+1 magnitudes), as the paper notes.
+// this keeps tied coordinates together in floating point as well. Then p_i = 1 for a_i > a_(k+1)
+// and p_i = min(lambda * a_i, 1) otherwise; the capped set is {p_i = 1}, which also holds the run of
+// magnitudes equal to a_(k+1) when the criterion holds with equality (lambda * a_(k+1) = 1).
+// Uses partial sorting (the top floor(B)+1 magnitudes), as the paper notes.
 int orc_exact_density(const float* g, int64_t d, double rho, double* p, double* lam, int64_t* kout,
                       uint32_t* flags) {
   std::vector<double> a;
@@ -251,11 +253,15 @@ int orc_exact_density(const float* g, int64_t d, double rho, double* p, double* 
     }
     if (kstar < 0) return -1;
     double vstar = nz[kstar];
-    s.k = kstar;
     s.lambda = (B - (double)kstar) / T;
+    // k is the size of the capped set {p_i = 1} of Proposition 1: the kstar magnitudes above
+    // vstar, plus any others whose product lambda * a_i reaches 1 (a run of ties at vstar when the
+    // criterion holds with equality)
+    s.k = 0;
     for (int64_t i = 0; i < d; ++i) {
       if (a[i] > vstar) p[i] = 1.0;
       else p[i] = std::min(s.lambda * a[i], 1.0);
+      s.k += (p[i] == 1.0);
     }
   }
   *lam = s.lambda;
@@ -301,12 +307,14 @@ int orc_exact_variance(const float* g, int64_t d, double eps, double* p, double*
     p2.add(nz[k] * nz[k]);
   }
   double vstar = kstar < nnz ? nz[kstar] : 0.0;
+  int64_t kcap = 0;  // the capped set {p_i = 1}, as in the density form
   for (int64_t i = 0; i < d; ++i) {
     if (a[i] > vstar) p[i] = 1.0;
     else p[i] = std::min(lamv * a[i], 1.0);
+    kcap += (p[i] == 1.0);
   }
   *lam = lamv;
-  *kout = kstar;
+  *kout = kcap;
   return 0;
 }
 

@@ -106,6 +106,46 @@ def test_philox_matches_independent_engine():
                 assert np.array_equal(oracle.words(seed, 4 * nq).astype(np.uint64), want)
 
 
+def _words_at_pin(fn) -> bool:
+    """True when fn(seed, idx) gives word (i mod 4) of Philox4x32-10 keyed by (seed low 32, seed high
+    32) at counter (floor(i/4) low 32, floor(i/4) high 32, 0, 0) for every i in idx: against
+    ``words`` (itself pinned by the known answers and the independent engine) on ragged, unsorted,
+    repeated indices covering every i mod 4, and against the known-answer-pinned block function
+    directly for indices whose counter needs the high word."""
+    rng = np.random.default_rng(31)
+    d = 100003
+    for seed in (0, 1000, (1 << 32) + 1, 0xDEADBEEFCAFEF00D):
+        full = oracle.words(seed, d)
+        idx = np.concatenate([rng.integers(0, d, 997), np.arange(8), [d - 1, d - 2, d - 3, d - 4, 5, 5]])
+        if not np.array_equal(fn(seed, idx), full[idx]):
+            return False
+        big = np.array([(1 << 31) - 1, 1 << 32, (1 << 32) + 7, (1 << 40) + 2, (1 << 62) + 3], np.int64)
+        want = []
+        for i in big.tolist():
+            q = i >> 2
+            blk = oracle.philox4x32_10([q & 0xFFFFFFFF, q >> 32, 0, 0], [seed & 0xFFFFFFFF, seed >> 32])
+            want.append(int(blk[i & 3]))
+        if fn(seed, big).tolist() != want:
+            return False
+    return True
+
+
+def test_words_at_matches_the_generator_layout():
+    """``words_at`` decides which index differences the parity rule excuses, so its index mapping
+    is pinned on its own; plausible mistakes (neighbouring word, next counter, swapped key halves,
+    counter high word dropped) each fail the pin."""
+    assert _words_at_pin(oracle.words_at)
+    mutants = {
+        "neighbouring word": lambda s, i: oracle.words_at(s, np.asarray(i, np.int64) ^ 1),
+        "next counter": lambda s, i: oracle.words_at(s, np.asarray(i, np.int64) + 4),
+        "swapped key halves": lambda s, i: oracle.words_at(((s & 0xFFFFFFFF) << 32) | (s >> 32), i),
+        "counter high word dropped": lambda s, i: oracle.words_at(
+            s, np.asarray(i, np.int64) & ((1 << 34) - 1)),
+    }
+    for name, fn in mutants.items():
+        assert not _words_at_pin(fn), name
+
+
 def test_philox_top_byte_uniform():
     x = oracle.words(12345, 1 << 20)
     counts = np.bincount(x >> 24, minlength=256)
@@ -264,6 +304,29 @@ def test_exact_two_level_closed_form(s, hi, lo, rho):
     sol = oracle.solve_exact(g, rho)
     assert sol.k == k
     assert abs(sol.lam - lam) <= 1e-14 * lam
+
+
+def test_exact_criterion_equality_caps_the_tied_run():
+    """Two-level vector at the boundary of the closed form: B * A_hi equals the total, so the
+    criterion holds at k = 0 with equality, lambda = B / total and lambda * A_hi = 1 exactly. Then
+    p = 1 on the s large entries (Proposition 1's min(lambda a, 1)), and the capped set {p_i = 1}
+    holds all of them, for both budget forms."""
+    d, s_hi, s_zero = 40000, 3000, 3000
+    g = np.ones(d, np.float32)
+    g[:s_hi] = 2.0
+    g[s_hi:s_hi + s_zero] = 0.0
+    g[1::2] *= -1
+    # B = 0.5 * 40000 = 20000; total = 3000 * 2 + 34000 * 1 = 40000; B * 2 = total
+    sol = oracle.solve_exact(g, 0.5)
+    assert sol.lam == 0.5 and sol.k == s_hi
+    assert np.all(sol.p[:s_hi] == 1.0) and np.all(sol.p[s_hi + s_zero:] == 0.5)
+    assert sol.p.sum() == 20000.0
+    # variance budget with the same answer: eps = sum(g^2 / p) / sum(g^2) - 1
+    A = 3000 * 4.0 + 34000 * 1.0
+    eps = (3000 * 4.0 + 34000 * 1.0 / 0.5) / A - 1.0
+    sv = oracle.solve_variance(g, eps)
+    assert sv.k == s_hi and np.all(sv.p[:s_hi] == 1.0)
+    assert abs(sv.lam - 0.5) <= 1e-15
 
 
 def test_exact_uncapped_regime_is_budget_over_l1():
@@ -508,6 +571,58 @@ def test_coding_bits_entropy_and_bounds():
     s2 = oracle.coding_bits(d, 11, 100, 40, b)[0]
     s3 = oracle.coding_bits(d, 10, 101, 40, b)[0]
     assert abs((s2 - s1) - (b + 12)) < 1e-9 and abs((s3 - s1) - 13) < 1e-9
+
+
+# Per-message costs worked by hand from Section 5's formula n_A (b + log2 d) + min(2d, n_B log2 d) + b
+# (n_B the realised |Q_B|) and from the sparse-list count n_A (b + log2 d) + n_B (log2 d + 1) + b:
+#   d = 1024 (log2 d = 10), b = 32, n_A = 3, n_B = 150: 3*42 + min(2048, 1500) + 32 = 1658;
+#       lists 3*42 + 150*11 + 32 = 1808
+#   d = 1024, n_A = 3, n_B = 300: 3*42 + min(2048, 3000) + 32 = 2206; lists 126 + 3300 + 32 = 3458
+#   d = 1024, n_A = 0, n_B = 50: 0 + min(2048, 500) + 32 = 532; lists 550 + 32 = 582
+#   d = 256 (log2 d = 8), n_A = 5, n_B = 40: 5*40 + min(512, 320) + 32 = 552; lists 200 + 360 + 32 = 592
+#   d = 2^20 (log2 d = 20), n_A = 1000, n_B = 60000: 1000*52 + min(2097152, 1200000) + 32 = 1252032;
+#       lists 52000 + 1260000 + 32 = 1312032
+#   d = 1024, b = 64, n_A = 2, n_B = 120: 2*74 + min(2048, 1200) + 64 = 1412; lists 148 + 1320 + 64 = 1532
+# In the first, fourth, fifth and sixth cases n_B log2 d lies between d and 2d, so min(d, .) and
+# min(2d, .) differ, and n_A > 0 exercises the b + log2 d term.
+_CODING_HAND = [  # (d, n_a, n_b, b, sparse lists, per-message cost)
+    (1024, 3, 150, 32, 1808.0, 1658.0),
+    (1024, 3, 300, 32, 3458.0, 2206.0),
+    (1024, 0, 50, 32, 582.0, 532.0),
+    (256, 5, 40, 32, 592.0, 552.0),
+    (1 << 20, 1000, 60000, 32, 1312032.0, 1252032.0),
+    (1024, 2, 120, 64, 1532.0, 1412.0),
+]
+
+
+def _coding_pin(fn) -> bool:
+    for d, n_a, n_b, b, lists, paper in _CODING_HAND:
+        out = fn(d, n_a, n_b, n_b // 3, b)
+        if abs(out[0] - lists) > 1e-9 * lists or abs(out[2] - paper) > 1e-9 * paper:
+            return False
+    return True
+
+
+def test_coding_bits_per_message_cost_hand_values():
+    """The sparse-list and per-message costs against values worked by hand; copies of the formula
+    with min(d, .) for min(2d, .), the trailing float dropped, Q_A's index bits dropped, or a sign
+    bit added per Q_B entry each fail the pin (Theorem 4's proof bounds the index part by
+    min(d, .), Section 5 by min(2d, .); 2d is taken, see the reading of the coding length)."""
+    assert _coding_pin(oracle.coding_bits)
+
+    def mutant(kind):
+        def fn(d, n_a, n_b, n_neg, b):
+            L = math.log2(d)
+            lists = n_a * (b + L) + n_b * (L + 1) + b
+            cap = d if kind == "min_d" else 2 * d
+            qa = n_a * b if kind == "no_qa_index" else n_a * (b + L)
+            qb = n_b * (L + 1) if kind == "qb_sign" else n_b * L
+            tail = 0.0 if kind == "no_float" else b
+            return lists, 0.0, qa + min(cap, qb) + tail
+        return fn
+
+    for kind in ("min_d", "no_float", "no_qa_index", "qb_sign"):
+        assert not _coding_pin(mutant(kind)), kind
 
 
 @pytest.mark.parametrize("s,rho_def,seed", [(20, 0.05, 1), (50, 0.2, 2), (5, 0.01, 3), (100, 0.5, 4)])
