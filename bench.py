@@ -3,15 +3,20 @@
 A step sparsifies one batch of synthetic gradients with every (solver, density) the workload lists:
 solve (exact threshold or Algorithm 3), Philox Bernoulli sampling, amplification and compaction
 into (int32 index, fp32 value) pairs, for all rows. Inputs, outputs and the workspace stay resident
-in HBM; the timed region holds exactly K steps between two device synchronisations.
+in HBM; the timed region holds exactly K steps between two device synchronisations, with no timer
+armed (product library).
 
-Default workload: 16 rows x 2^20 (one per simulated worker), Laplace(0,1) times a per-row scale
-10^U(-3,0), greedy solver with two rescale steps, densities 0.01 and 0.1, Philox seeds 1000 + r.
+Default workload: one gradient of 2^28 coordinates (1 GiB), Student-t(2) with 1% of the entries
+multiplied by 100, the exact and the greedy (two rescale steps) solvers at densities 0.001, 0.01
+and 0.1 (six calls per step), Philox seed 5. --workload c2 selects 16 rows x 2^20 (Laplace times a
+per-row scale 10^U(-3,0), greedy, densities 0.01 and 0.1, seeds 1000 + r), and so on.
 
-Prints ONE JSON line with the metric, a roofline object for the sampling / compaction pass (the
-largest HBM-bound kernel: algorithmic bytes = 4 B per input element + 8 B per survivor, timed with
-HIP events on its stream over the timed region), the time per step of every kernel class, and the
-oracle timed on a bounded sample on one host core as a CPU baseline.
+Prints ONE JSON line with the metric, a roofline object for the sampling / compaction pass
+(algorithmic bytes = 4 B per input element + 8 B per survivor over its average kernel time), the
+time per step of every kernel class, and the oracle timed on a bounded sample on one host core as
+a CPU baseline. Kernel times come from a second loop of the same steps through the measurement
+build of the library (libgspar_instr.so, the same kernels), whose launches carry HIP events
+stamped by the dispatch itself at the kernel's start and end.
 
 With --cells (and --workload all for every workload) it prints instead one line per (workload,
 solver, rho): the median time of one call warm and right after a 512 MiB scratch write that evicts
@@ -42,7 +47,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5", "all"])
+    ap.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5", "all"])
     ap.add_argument("--solver", default=None, choices=["greedy", "exact", "variance"],
                     help="restrict to one solver ('variance': Algorithm 2 with the variance budget eps)")
     ap.add_argument("--rho", type=float, default=None,
@@ -55,6 +60,9 @@ def parse():
     ap.add_argument("--hybrid", action="store_true",
                     help="time the hybrid coding entry point (Q_A / Q_B lists) instead of the compaction")
     ap.add_argument("--dense-q", action="store_true", help="with --hybrid, also write the dense ternary vector")
+    ap.add_argument("--probs", action="store_true",
+                    help="time the probabilities entry point (p = min(lambda |g|, 1) written in full: 8 B per "
+                         "coordinate) instead of the compaction")
     ap.add_argument("--per-layer", action="store_true",
                     help="c4 only: sparsify each of the 54 ResNet-50 layers on its own (one lambda per layer, "
                          "Philox keys 4000 + layer) in one segmented call")
@@ -104,8 +112,8 @@ def _pmc_rows(path):
 
 
 def _kernel_class(name: str):
-    for k in ("k_sample", "k_stats", "k_refine", "k_solve", "k_init", "k_probs"):
-        if "gspar::" + k in name:
+    for k in ("k_probs_out", "k_sample", "k_stats", "k_refine", "k_solve", "k_init", "k_probs", "k_aggregate"):
+        if "gspar::" + k + "<" in name or "gspar::" + k + "(" in name:
             return k
     if "copyBuffer" in name:  # the runtime's device-to-device copy kernel (the probe)
         return "copy"
@@ -170,7 +178,7 @@ def layer_setup(args, wl, dev):
     return g, seg, seeds
 
 
-def cpu_baseline(wl, combos, target_s, per_layer=False):
+def cpu_baseline(wl, combos, target_s, per_layer=False, probs=False):
     """The oracle as it stands (single thread), on whole rows of the same workload until about
     target_s seconds of work; returns elements/s and what the sample was."""
     import oracle
@@ -207,7 +215,8 @@ def cpu_baseline(wl, combos, target_s, per_layer=False):
             row = wl.g[r % wl.rows][:prefix]
             for solver, rho in combos:
                 sol = oracle.solve(row, rho, solver, wl.iters)
-                oracle.sample_compact(row, sol.p, wl.seeds[r % wl.rows])
+                if not probs:
+                    oracle.sample_compact(row, sol.p, wl.seeds[r % wl.rows])
                 elems += row.size
             r += 1
             if time.perf_counter() - t0 >= target_s or r >= 4 * wl.rows:
@@ -217,11 +226,15 @@ def cpu_baseline(wl, combos, target_s, per_layer=False):
         os.sched_setaffinity(0, keep)
     return {"value": elems / dt, "unit": "elements/s", "cores": 1, "kind": "oracle",
             "sample": f"{r} row passes over {min(r, wl.rows)} distinct rows, each the leading {prefix} of the "
-                      f"row's {wl.d} entries, x {len(combos)} (solver, rho) combos; {dt:.1f} s of fp64 oracle "
+                      f"row's {wl.d} entries, x {len(combos)} (solver, rho) combos"
+                      f"{' (solve and p only)' if probs else ''}; {dt:.1f} s of fp64 oracle "
                       f"work on 1 of the host's {host_cores} cores"}
 
 
-KERNEL_CLASSES = {"k_init": 5, "k_stats": 1, "k_solve": 3, "k_refine": 4, "k_sample": 0}
+def _class_order():
+    import paper_1710_09854_amd as gs
+
+    return gs.PROF_CLASSES
 
 
 def cells(args):
@@ -258,7 +271,7 @@ def cells(args):
         for solver in ([args.solver] if args.solver else wl.solvers):
             for rho in ([args.rho] if args.rho is not None else (VARIANCE_EPS if solver == "variance" else wl.rhos)):
                 plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=capacity(gs, d, solver, rho),
-                               hybrid=args.hybrid, dense_q=args.dense_q, segments=seg)
+                               hybrid=args.hybrid, dense_q=args.dense_q, segments=seg, probs=args.probs)
                 rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
                 for _ in range(3):
                     plan.run(g, rho_dev, seeds)
@@ -280,17 +293,33 @@ def cells(args):
                 cold = float(np.median([timed(True) for _ in range(5)]))
                 nnz, out_bytes = plan.survivors_and_bytes()
                 alg = 4.0 * n_elems + out_bytes
-                entry = "hybrid" + ("+q" if args.dense_q else "") if args.hybrid else "compact"
+                entry = ("probs" if args.probs else
+                         "hybrid" + ("+q" if args.dense_q else "") if args.hybrid else "compact")
+                # kernel times of the same call through the measurement build
+                iplan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=capacity(gs, d, solver, rho),
+                                hybrid=args.hybrid, dense_q=args.dense_q, segments=seg, probs=args.probs,
+                                library=gs.instr_lib())
+                iplan.run(g, rho_dev, seeds)
+                torch.cuda.synchronize()
+                prof = gs.KernelProfiler(10 * 16)
+                for _ in range(10):
+                    iplan.run(g, rho_dev, seeds)
+                kt = prof.read()
+                prof.close()
+                del iplan
+                kernels = {k: {"us_per_call": 100.0 * ms, "launches_per_call": n / 10}
+                           for k, (ms, n) in kt.items() if n}
                 cell = {"workload": wl.name, "solver": solver, "rho": rho, "rows": rows, "d": d, "nnz": nnz,
                         "entry": entry + ("_per_layer" if args.per_layer else ""),
                         "lambda_row0": float(plan.lam[0].item()),
                         "warm_us": warm * 1e6, "warm_elements_per_s": n_elems / warm,
                         "cold_us": cold * 1e6, "cold_elements_per_s": n_elems / cold,
                         "algorithmic_bytes": alg, "algorithmic_frac_warm": alg / warm / 1e9 / HBM_PEAK_GBS,
-                        "algorithmic_frac_cold": alg / cold / 1e9 / HBM_PEAK_GBS}
+                        "algorithmic_frac_cold": alg / cold / 1e9 / HBM_PEAK_GBS, "kernels": kernels}
                 if not args.no_cpu_baseline:
                     cell["cpu_baseline"] = cpu_baseline(wl, [(solver, rho)], args.cpu_seconds,
-                                                        per_layer=args.per_layer)
+                                                        per_layer=args.per_layer and not args.probs,
+                                                        probs=args.probs)
                 print(json.dumps(cell), flush=True)
                 if args.aggregate and not args.hybrid and not args.per_layer:
                     print(json.dumps(aggregate_cell(args, wl, plan, scratch, solver, rho)), flush=True)
@@ -328,10 +357,13 @@ def aggregate_cell(args, wl, plan, scratch, solver, rho):
 
     warm = float(np.median([timed(False) for _ in range(20)]))
     cold = float(np.median([timed(True) for _ in range(5)]))
-    t = gs.KernelTimer(6, 20)
+    L = gs.instr_lib()
+    gs.aggregate(idx, val, nnz, d, out=v, library=L)
+    torch.cuda.synchronize()
+    t = gs.KernelProfiler(20)
     for _ in range(20):
-        gs.aggregate(idx, val, nnz, d, out=v)
-    ms, n = t.read()
+        gs.aggregate(idx, val, nnz, d, out=v, library=L)
+    ms, n = t.read()["k_aggregate"]
     t.close()
     kept = int(torch.clamp(nnz, 0, plan.cap).sum().item())
     alg = 8.0 * kept + 8.0 * rows + 4.0 * d
@@ -402,15 +434,19 @@ def main():
         n_elems = rows * d
         seeds = torch.tensor([s - (1 << 64) if s >= (1 << 63) else s for s in wl.seeds], dtype=torch.int64,
                              device=dev)
-    plans = []
-    for solver, rho in combos:
-        plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=capacity(gs, d, solver, rho),
-                       hybrid=args.hybrid, dense_q=args.dense_q, segments=seg)
-        rho_dev = torch.full((rows,), rho, dtype=torch.float64, device=dev)
-        plans.append((plan, rho_dev))
+    def make_plans(library):
+        out = []
+        for solver, rho in combos:
+            plan = gs.Plan(rows, d, solver=solver, iters=wl.iters, cap_per_row=capacity(gs, d, solver, rho),
+                           hybrid=args.hybrid, dense_q=args.dense_q, segments=seg, library=library,
+                           probs=args.probs)
+            out.append((plan, torch.full((rows,), rho, dtype=torch.float64, device=dev)))
+        return out
 
-    def step():
-        for plan, rho_dev in plans:
+    plans = make_plans(None)  # the product library
+
+    def step(ps):
+        for plan, rho_dev in ps:
             plan.run(g, rho_dev, seeds)
 
     if args.copy_probe:
@@ -422,46 +458,65 @@ def main():
         del src, dst
 
     for _ in range(args.warmup):
-        step()
+        step(plans)
     torch.cuda.synchronize()
     for plan, _ in plans:
         fl = plan.flags.cpu().numpy()
         assert not (fl & ~gs.FLAG_OVERFLOW).any(), f"unexpected flags {fl}"
 
-    timer = gs.KernelTimer(0, args.steps * len(plans))
-    nnz_tot = 0
+    # the timed region: K steps through the product library, no timer armed
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        step(plans)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    ksample_ms, launches = timer.read()
-    timer.close()
-    out_bytes = 0
+    nnz_tot, out_bytes = 0, 0
     for plan, _ in plans:
         n, ob = plan.survivors_and_bytes()
         nnz_tot += n
         out_bytes += ob
-    # time per step of every kernel class (separate short loops, one class bracketed at a time)
+
+    # kernel times: the same steps through the measurement build (same kernels), every launch
+    # stamped at its start and end by its own dispatch
+    iplans = make_plans(gs.instr_lib())
+    step(iplans)
+    torch.cuda.synchronize()
+    for (a, _), (b, _) in zip(plans, iplans):
+        assert torch.equal(a.lam, b.lam) and torch.equal(a.nnz, b.nnz), "the two builds disagree"
+    reps = args.steps
+    prof = gs.KernelProfiler(reps * len(iplans) * 16)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        step(iplans)
+    ktimes = prof.read()
+    prof.close()
+    del iplans
     kernels = {}
-    reps = min(args.steps, 10)
-    for name, which in KERNEL_CLASSES.items():
-        t = gs.KernelTimer(which, reps * len(plans) * 16)
-        for _ in range(reps):
-            step()
-        ms, n = t.read()
-        t.close()
-        kernels[name] = {"us_per_step": 1e3 * ms / reps, "launches_per_step": n / reps}
+    for name in _class_order():
+        ms, n = ktimes[name]
+        if n:
+            kernels[name] = {"us_per_step": 1e3 * ms / reps, "launches_per_step": n / reps,
+                             "avg_us": 1e3 * ms / n}
+    kernel_us_per_step = sum(v["us_per_step"] for v in kernels.values())
     # survivors are identical in every step (same seeds), so per-step bytes are exact
     elements_per_step = n_elems * len(plans)
     ms_per_step = elapsed * 1e3 / args.steps
     value = elements_per_step / (elapsed / args.steps)
     alg_bytes_per_step = 4.0 * elements_per_step + out_bytes
-    avg_launch_ms = ksample_ms / max(launches, 1)
-    achieved = alg_bytes_per_step / len(plans) / (avg_launch_ms * 1e-3) / 1e9
-    traffic = (traffic_for(wl.name) if (args.solver is None and args.rho is None and not args.hybrid
-                                         and not args.per_layer) else None)
+    # the roofline kernel: the sampling / compaction pass (or the probabilities pass), whose
+    # algorithmic bytes are the whole step's (g read once, the output written once)
+    rk = "k_probs" if args.probs else "k_sample"
+    rk_ms, rk_n = ktimes[rk]
+    avg_launch_ms = rk_ms / max(rk_n, 1)
+    alg_per_launch = alg_bytes_per_step / len(plans)
+    achieved = alg_per_launch / (avg_launch_ms * 1e-3) / 1e9
+    default_cells = args.solver is None and args.rho is None and not (args.hybrid or args.per_layer or args.probs)
+    traffic = traffic_for(wl.name, rk) if default_cells else None
+    entry = ("probabilities p = min(lambda |g|, 1)" if args.probs else
+             ("hybrid coding Q_A (index, value) + Q_B (index | sign)" + (" + dense ternary vector" if args.dense_q
+                                                                        else "")) if args.hybrid
+             else "ascending (int32 index, fp32 value) pairs")
     line = {
         "metric": METRIC,
         "value": value,
@@ -476,37 +531,44 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wl.name + ("_per_layer" if args.per_layer else ""), "rows": rows, "d": d,
-                   "solvers": solvers, "rho": rhos, "greedy_iters": wl.iters,
+                   "solvers": solvers, "rho": rhos, "greedy_iters": wl.iters, "calls_per_step": len(plans),
                    "seeds": ("per-layer Philox keys 4000+layer" if args.per_layer else
                              "per-row Philox keys " + ("1000+r" if args.workload == "c2" else str(wl.seeds[0]))),
                    "parallelism": ("single GPU, 54 layers (rows: segments, d: the longest) in one segmented call"
                                    if args.per_layer else "single GPU, rows batched in one call"),
-                   "output": ("hybrid coding Q_A (index, value) + Q_B (index | sign)" +
-                              (" + dense ternary vector" if args.dense_q else "")) if args.hybrid
-                   else "ascending (int32 index, fp32 value) pairs"},
+                   "output": entry},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_sample (Philox sampling, amplification, " +
-                               ("hybrid Q_A / Q_B coding" if args.hybrid else "compaction") +
-                               "; the largest HBM-bound kernel, time per class in 'kernels')",
-                     "algorithmic_bytes_per_launch": alg_bytes_per_step / len(plans),
-                     "avg_launch_ms": avg_launch_ms, "launches": launches},
+                     "kernel": rk + (" (probabilities: 4 B read + 4 B written per coordinate)" if args.probs else
+                                     " (Philox sampling, amplification, " +
+                                     ("hybrid Q_A / Q_B coding" if args.hybrid else "compaction") +
+                                     "; 4 B read per coordinate + the output)"),
+                     "algorithmic_bytes_per_launch": alg_per_launch,
+                     "avg_launch_ms": avg_launch_ms, "launches": rk_n,
+                     "timing": "HIP start/stop events stamped by each launch's dispatch (hipExtLaunchKernelGGL), "
+                               "measurement build, averaged over the launches of %d steps" % reps},
     }
-    # the whole path: algorithmic bytes (g read once, the output written once) and, when the counter
-    # summary matches this kernel source, the bytes the kernels actually moved, per step
+    # the whole path: algorithmic bytes (g read once, the output written once) over the step time
+    # and over the summed kernel time, and, when the counter summary matches this kernel source,
+    # the bytes the kernels actually moved
     path = {"algorithmic_bytes_per_step": alg_bytes_per_step,
-            "algorithmic_GBps": alg_bytes_per_step / (ms_per_step * 1e-3) / 1e9}
+            "algorithmic_GBps": alg_bytes_per_step / (ms_per_step * 1e-3) / 1e9,
+            "kernel_us_per_step": kernel_us_per_step}
     path["algorithmic_frac"] = path["algorithmic_GBps"] / HBM_PEAK_GBS
-    if traffic is not None:
-        per_kernel = {k: traffic_for(wl.name, k) for k in KERNEL_CLASSES}
+    path["algorithmic_frac_kernel_time"] = alg_bytes_per_step / (kernel_us_per_step * 1e-6) / 1e9 / HBM_PEAK_GBS
+    if default_cells:
+        per_kernel = {k: traffic_for(wl.name, k) for k in kernels}
         if all(v is not None for v in per_kernel.values()):
-            moved = sum(per_kernel[k] * kernels[k]["launches_per_step"] for k in KERNEL_CLASSES)
+            moved = sum(per_kernel[k] * kernels[k]["launches_per_step"] for k in kernels)
             path["measured_bytes_per_step"] = moved
             path["measured_GBps"] = moved / (ms_per_step * 1e-3) / 1e9
             path["measured_frac"] = path["measured_GBps"] / HBM_PEAK_GBS
+            path["measured_GBps_kernel_time"] = moved / (kernel_us_per_step * 1e-6) / 1e9
+            path["measured_frac_kernel_time"] = path["measured_GBps_kernel_time"] / HBM_PEAK_GBS
     line["path"] = path
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, combos, args.cpu_seconds, per_layer=args.per_layer)
+        line["cpu_baseline"] = cpu_baseline(wl, combos, args.cpu_seconds, per_layer=args.per_layer and not args.probs,
+                                            probs=args.probs)
     line["kernels"] = kernels
     line["nnz_per_step"] = nnz_tot
     line["src_sha"] = src_hash()

@@ -27,10 +27,11 @@
  *  - Budget: B = rho * d computed in double. rho must lie in [0, 1].
  *  - Solvers: GSPAR_EXACT (the lambda solving sum_i min(lambda|g_i|, 1) = B exactly, capped set
  *    never splitting ties) or GSPAR_GREEDY (Algorithm 3 for `greedy_iters` rescale steps; the
- *    paper's experiments use 2). Special cases: if B >= nnz(g), every nonzero is kept with
+ *    paper's experiments use 2). For every solver the capped set is {p_i = 1} (Proposition 1,
+ *    Section 3.3's S_k): every pass, every output and the capped count k use that one set. Special cases: if B >= nnz(g), every nonzero is kept with
  *    probability one (lambda = +inf, Q(g) = g); if rho = 0 nothing is kept (lambda = 0).
  *    GSPAR_VARIANCE is Algorithm 2 as printed, with the variance budget of problem (4): every rho
- *    argument then carries eps (any finite eps >= 0), the capped set is {a > a_(k+1)} for the
+ *    argument then carries eps (any finite eps >= 0), p_i = 1 on {a > a_(k+1)} for the
  *    smallest k with a_(k+1) T1 <= eps sum a^2 + T2 (eq. 6; T1, T2 the sum and the sum of squares
  *    of the magnitudes not above a_(k+1)) and lambda = T1 / (eps sum a^2 + T2) (eq. 7), every sum
  *    exact and rounded once; if no value satisfies the criterion (possible only through rounding
@@ -47,7 +48,13 @@
  *    capacity), GSPAR_ERR_WORKSPACE (ws NULL or ws_bytes below gspar_workspace_bytes) and
  *    GSPAR_ERR_HIP (a launch failed). Data-dependent conditions are reported per row in `flags`.
  *  - Calls that share a workspace must be stream-ordered; concurrent calls need distinct
- *    workspaces. The library keeps no other state (apart from the optional timing hook below).
+ *    workspaces. The library keeps no state of its own: it is re-entrant, and its exported
+ *    symbols are exactly the functions declared here.
+ *  - Per-row parameters of the batched, segmented and hybrid calls (rho or eps, Philox seeds)
+ *    are DEVICE arrays, read by the kernels: a call then enqueues its work without any host to
+ *    device copy (which would order the call after host work and, from pageable memory,
+ *    synchronise), and the values may themselves be produced on the device. The single-row calls
+ *    take them as host scalars.
  */
 #ifndef GSPAR_H
 #define GSPAR_H
@@ -58,6 +65,8 @@
 #ifdef __cplusplus
 extern "C" {
 #endif
+
+#pragma GCC visibility push(default)
 
 typedef enum {
   GSPAR_OK = 0,
@@ -75,6 +84,8 @@ enum {
                                written and nnz holds the true count                          */
   GSPAR_FLAG_ALLZERO = 4,   /* g is identically zero: nnz = 0                                 */
   GSPAR_FLAG_BADRHO = 8,    /* (batched) rho[r] outside [0, 1] or NaN (eps: negative, infinite or NaN): row skipped, nnz = 0 */
+  GSPAR_FLAG_INTERNAL = 16, /* an internal invariant of the solver's exact arithmetic failed (a
+                               library fault, never expected): row skipped, nnz = 0, lambda = NaN */
   GSPAR_FLAG_BADSEG = 32    /* (segmented) the device offsets of the segment disagree with the
                                host offsets' bounds: segment skipped, nnz = 0                 */
 };
@@ -108,14 +119,18 @@ int sparsify_sample_compact(const float* g, int64_t d, double rho, int solver, i
                             int64_t* nnz, double* lambda, int64_t* k, uint32_t* flags, void* ws,
                             size_t ws_bytes, void* stream);
 
-/* Batched keep probabilities: rows x d gradients with leading dimension ld.
+/* Batched keep probabilities: rows x d gradients with leading dimension ld, one row per worker
+ * (Algorithm 1, steps 4-5: every worker sparsifies its own gradient); row r is Proposition 1 with
+ * rho[r] and is bit-identical to sparsify_probs on that row.
  *   rho [rows] fp64 DEVICE array; p [rows*ld] or NULL; lambda [rows] (required), k [rows] and
  *   flags [rows] optional. */
 int sparsify_probs_batched(const float* g, int64_t rows, int64_t d, int64_t ld, const double* rho,
                            int solver, int greedy_iters, float* p, double* lambda, int64_t* k,
                            uint32_t* flags, void* ws, size_t ws_bytes, void* stream);
 
-/* Batched solve + sample + compact. rho [rows] fp64 and seeds [rows] uint64 are DEVICE arrays.
+/* Batched solve + sample + compact, one row per worker (Algorithm 1, steps 4-5: each worker m
+ * computes Q(g^m) from its own gradient; Section 3's selection and amplification per row).
+ * rho [rows] fp64 and seeds [rows] uint64 are DEVICE arrays.
  * Row r writes its survivors to idx[r*cap_per_row ...] and val[r*cap_per_row ...] and its count
  * to nnz[r]; lambda, k and flags ([rows] each) are optional. */
 int sparsify_sample_compact_batched(const float* g, int64_t rows, int64_t d, int64_t ld,
@@ -222,16 +237,8 @@ const char* gspar_status_string(int status);
 /* Library version as major*10000 + minor*100 + patch. */
 int gspar_version(void);
 
-/* Measurement hook for benchmarks (process-global, not thread-safe): while armed, every launch
- * of kernel class `which` (0 = sample/compact, 1 = statistics pass, 2 = probabilities, 3 = solver,
- * 4 = refinement pass, 5 = workspace initialisation, 6 = aggregation, its two kernels together)
- * is bracketed by a pair of HIP timing events on its stream, for up to `max_launches` launches.
- * gspar_timing_read synchronises on the last event and returns the summed kernel time in ms and
- * the number of bracketed launches; gspar_timing_disarm releases the events. Returns GSPAR_ERR_ARG for an unknown class or a
- * non-positive count, GSPAR_ERR_HIP if the events cannot be created. */
-int gspar_timing_arm(int which, int max_launches);
-int gspar_timing_read(double* total_ms, int* launches);
-int gspar_timing_disarm(void);
+
+#pragma GCC visibility pop
 
 #ifdef __cplusplus
 }

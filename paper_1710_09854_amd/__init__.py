@@ -43,18 +43,14 @@ ERR_ARG = -1
 ERR_WORKSPACE = -2
 ERR_HIP = -3
 
+INSTR_LIB_PATH = os.path.join(_HERE, "libgspar_instr.so")
+
 _lib = None
+_instr = None
 
 
-def lib():
-    """The loaded C library; raises if it was never built."""
-    global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(LIB_PATH):
-        raise RuntimeError(f"{LIB_PATH} is missing: build the HIP library first "
-                           "(python -m paper_1710_09854_amd.build)")
-    L = ctypes.CDLL(LIB_PATH)
+def _bind(L):
+    """Argument types of the C ABI of include/gspar.h on a loaded library."""
     vp, i64, u64, f64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_int
     L.gspar_workspace_bytes.argtypes = [i64, i64, i32]
     L.gspar_workspace_bytes.restype = ctypes.c_size_t
@@ -83,24 +79,52 @@ def lib():
                                                     vp, vp, ctypes.c_size_t, vp]
     L.sparsify_sample_compact_segmented.restype = i32
     L.sparsify_probs_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparsify_probs_segmented.restype = i32
     L.sparsify_sample_hybrid_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, i64, vp, vp, i64,
                                                    vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     L.sparsify_sample_hybrid_segmented.restype = i32
-    L.sparsify_probs_segmented.restype = i32
     L.gspar_aggregate.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
     L.gspar_aggregate.restype = i32
     L.gspar_status_string.argtypes = [i32]
     L.gspar_status_string.restype = ctypes.c_char_p
     L.gspar_version.argtypes = []
     L.gspar_version.restype = i32
-    L.gspar_timing_arm.argtypes = [i32, i32]
-    L.gspar_timing_arm.restype = i32
-    L.gspar_timing_read.argtypes = [ctypes.POINTER(f64), ctypes.POINTER(i32)]
-    L.gspar_timing_read.restype = i32
-    L.gspar_timing_disarm.argtypes = []
-    L.gspar_timing_disarm.restype = i32
-    _lib = L
     return L
+
+
+def _open(path):
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build the HIP library first "
+                           "(python -m paper_1710_09854_amd.build)")
+    return _bind(ctypes.CDLL(path))
+
+
+def lib():
+    """The loaded product library (libgspar.so); raises if it was never built."""
+    global _lib
+    if _lib is None:
+        _lib = _open(LIB_PATH)
+    return _lib
+
+
+PROF_CLASSES = ("k_sample", "k_stats", "k_probs", "k_solve", "k_refine", "k_init", "k_aggregate", "k_probs_out")
+
+
+def instr_lib():
+    """The measurement build (libgspar_instr.so: the same kernels, plus the launch timer and the
+    host-compiled arithmetic checks of include/gspar_instr.h). For the benchmark and the tests."""
+    global _instr
+    if _instr is None:
+        L = _open(INSTR_LIB_PATH)
+        i32, f64 = ctypes.c_int, ctypes.c_double
+        L.gspar_prof_arm.argtypes = [i32]
+        L.gspar_prof_arm.restype = i32
+        L.gspar_prof_read.argtypes = [ctypes.POINTER(f64), ctypes.POINTER(i32)]
+        L.gspar_prof_read.restype = i32
+        L.gspar_prof_disarm.argtypes = []
+        L.gspar_prof_disarm.restype = i32
+        _instr = L
+    return _instr
 
 
 def _solver_id(solver) -> int:
@@ -145,25 +169,39 @@ def _default_cap(d: int, rho: float, solver) -> int:
 
 
 class Workspace:
-    """Grow-only device workspace (the library itself never allocates)."""
+    """Grow-only device workspace (the library itself never allocates). Calls that share one must
+    be ordered on one stream; the buffer is allocated on that stream, so a buffer dropped when the
+    workspace grows is reused by the caching allocator only after the stream's earlier work."""
 
-    def __init__(self, device=None):
+    def __init__(self, device=None, stream=None):
         self.device = torch.device("cuda" if device is None else device)
+        self.stream = stream
         self.buf = None
 
     def get(self, nbytes: int) -> torch.Tensor:
         if self.buf is None or self.buf.numel() < nbytes:
-            self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+            if self.stream is None:
+                self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+            else:
+                with torch.cuda.stream(self.stream):
+                    self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         return self.buf
 
 
 _default_ws: dict = {}
 
 
-def _ws(ws, device, nbytes):
+def _ws(ws, device, nbytes, stream=None):
+    """The caller's workspace, or the default one of (device, stream): calls on different streams
+    never share a default workspace."""
     if ws is None:
-        key = torch.device(device).index if torch.device(device).index is not None else torch.cuda.current_device()
-        ws = _default_ws.setdefault(key, Workspace(device))
+        dev = torch.device(device)
+        idx = dev.index if dev.index is not None else torch.cuda.current_device()
+        s = torch.cuda.current_stream(idx) if stream is None else stream
+        key = (idx, s.cuda_stream)
+        if key not in _default_ws:
+            _default_ws[key] = Workspace(torch.device("cuda", idx), s)
+        ws = _default_ws[key]
     buf = ws.get(nbytes)
     return buf, buf.numel()
 
@@ -219,7 +257,7 @@ def sparsify_probs(g, rho: float, solver="greedy", iters: int = 2, want_p: bool 
     k = torch.empty(1, dtype=torch.int64, device=dev)
     fl = torch.empty(1, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid), stream)
     rc = lib().sparsify_probs(g.data_ptr(), d, float(rho), sid, int(iters), _ptr(p), lam.data_ptr(),
                               k.data_ptr(), fl.data_ptr(), buf.data_ptr(), nb, _stream(stream))
     _check(rc, "sparsify_probs")
@@ -239,7 +277,7 @@ def sparsify_sample_compact(g, rho: float, seed: int = 0, solver="greedy", iters
     k = torch.empty(1, dtype=torch.int64, device=dev)
     fl = torch.empty(1, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid), stream)
     rc = lib().sparsify_sample_compact(g.data_ptr(), d, float(rho), sid, int(iters),
                                        int(seed) & 0xFFFFFFFFFFFFFFFF, idx.data_ptr(), val.data_ptr(), cap,
                                        nnz.data_ptr(), lam.data_ptr(), k.data_ptr(), fl.data_ptr(),
@@ -282,7 +320,7 @@ def sparsify_sample_hybrid(g, rho: float, seed: int = 0, solver="greedy", iters:
     lam = torch.empty(1, dtype=torch.float64, device=dev)
     fl = torch.empty(1, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(1, d, sid), stream)
     rc = lib().sparsify_sample_hybrid(g.data_ptr(), d, float(rho), sid, int(iters), int(seed) & 0xFFFFFFFFFFFFFFFF,
                                       idx_a.data_ptr(), val_a.data_ptr(), cap_a, n_a.data_ptr(), code_b.data_ptr(),
                                       cap_b, n_b.data_ptr(), inv.data_ptr(), _ptr(q), lam.data_ptr(), fl.data_ptr(),
@@ -315,7 +353,7 @@ def sparsify_sample_hybrid_batched(g, rho, seeds, solver="greedy", iters: int = 
     lam = torch.empty(rows, dtype=torch.float64, device=dev)
     fl = torch.empty(rows, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid), stream)
     rc = lib().sparsify_sample_hybrid_batched(g.data_ptr(), rows, d, ld, r.data_ptr(), sid, int(iters), s.data_ptr(),
                                               idx_a.data_ptr(), val_a.data_ptr(), cap_a, n_a.data_ptr(),
                                               code_b.data_ptr(), cap_b, n_b.data_ptr(), inv.data_ptr(), _ptr(q),
@@ -334,7 +372,7 @@ def coding_bits(d: int, n_a: int, n_b: int, n_b_neg: int, float_bits: int = 32):
     return out[0], out[1], out[2]
 
 
-def aggregate(idx, val, nnz, d: int, out=None, stream=None) -> torch.Tensor:
+def aggregate(idx, val, nnz, d: int, out=None, stream=None, library=None) -> torch.Tensor:
     """Algorithm 1, step 6: v = (1/M) sum_m Q(g^m), dense fp32 [d], from M workers' ascending
     (index, value) lists (rows of idx / val, the first nnz[m] entries of row m)."""
     if idx.dim() != 2 or val.shape != idx.shape or idx.dtype != torch.int32 or val.dtype != torch.float32:
@@ -345,7 +383,8 @@ def aggregate(idx, val, nnz, d: int, out=None, stream=None) -> torch.Tensor:
     dev = idx.device
     n = nnz.to(device=dev, dtype=torch.int64).contiguous()
     v = torch.empty(d, dtype=torch.float32, device=dev) if out is None else out
-    rc = lib().gspar_aggregate(idx.data_ptr(), val.data_ptr(), cap, n.data_ptr(), workers, int(d), v.data_ptr(),
+    L = lib() if library is None else library
+    rc = L.gspar_aggregate(idx.data_ptr(), val.data_ptr(), cap, n.data_ptr(), workers, int(d), v.data_ptr(),
                                _stream(stream))
     _check(rc, "gspar_aggregate")
     return v
@@ -387,7 +426,7 @@ def sparsify_probs_batched(g, rho, solver="greedy", iters: int = 2, want_p: bool
     k = torch.empty(rows, dtype=torch.int64, device=dev)
     fl = torch.empty(rows, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid), stream)
     rc = lib().sparsify_probs_batched(g.data_ptr(), rows, d, ld, r.data_ptr(), sid, int(iters), _ptr(p),
                                       lam.data_ptr(), k.data_ptr(), fl.data_ptr(), buf.data_ptr(), nb,
                                       _stream(stream))
@@ -396,14 +435,17 @@ def sparsify_probs_batched(g, rho, solver="greedy", iters: int = 2, want_p: bool
 
 
 class Plan:
-    """Preallocated batched solve + sample + compact: inputs, outputs and workspace stay resident,
-    so a timing loop measures only the library's kernels."""
+    """Preallocated batched solve + sample + compact (or, with probs=True, the probabilities
+    entry point): inputs, outputs and workspace stay resident, so a timing loop measures only the
+    library's kernels."""
 
     def __init__(self, rows: int, d: int, ld: int | None = None, solver="greedy", iters: int = 2,
                  cap_per_row: int | None = None, rho_for_cap: float = 1.0, device="cuda", hybrid: bool = False,
-                 dense_q: bool = False, segments: "Segments | None" = None):
+                 dense_q: bool = False, segments: "Segments | None" = None, library=None, probs: bool = False):
         # with segments: one output row per segment (rows and d are then the segment count and the
-        # longest segment)
+        # longest segment); `library`: the loaded library to call (default the product library;
+        # the benchmark's timing loop passes the measurement build)
+        self.L = lib() if library is None else library
         self.seg = segments
         if segments is not None:
             if hybrid:
@@ -415,7 +457,14 @@ class Plan:
         self.iters = int(iters)
         self.cap = _default_cap(d, rho_for_cap, solver) if cap_per_row is None else int(cap_per_row)
         self.hybrid = bool(hybrid)
+        self.probs = bool(probs)
         dev = torch.device(device)
+        if self.probs:
+            if hybrid:
+                raise ValueError("the probabilities entry point has no hybrid output")
+            self.cap = 0
+            self.p = torch.empty(segments.total if segments is not None else (rows, self.ld), dtype=torch.float32,
+                                 device=dev)
         # compaction: (idx, val) per survivor; hybrid coding: Q_A in (idx, val), Q_B in code_b
         self.idx = torch.empty((rows, max(self.cap, 1)), dtype=torch.int32, device=dev)
         self.val = torch.empty((rows, max(self.cap, 1)), dtype=torch.float32, device=dev)
@@ -431,8 +480,21 @@ class Plan:
             self.q = torch.empty((rows, self.ld), dtype=torch.int8, device=dev) if dense_q else None
 
     def run(self, g, rho_dev, seeds_dev, stream=None):
+        if self.probs:
+            if self.seg is not None:
+                rc = self.L.sparsify_probs_segmented(
+                    g.data_ptr(), self.rows, self.seg.host.data_ptr(), self.seg.dev.data_ptr(), rho_dev.data_ptr(),
+                    self.sid, self.iters, self.p.data_ptr(), self.lam.data_ptr(), self.k.data_ptr(),
+                    self.flags.data_ptr(), self.ws.data_ptr(), self.ws.numel(), _stream(stream))
+            else:
+                rc = self.L.sparsify_probs_batched(
+                    g.data_ptr(), self.rows, self.d, self.ld, rho_dev.data_ptr(), self.sid, self.iters,
+                    self.p.data_ptr(), self.lam.data_ptr(), self.k.data_ptr(), self.flags.data_ptr(),
+                    self.ws.data_ptr(), self.ws.numel(), _stream(stream))
+            _check(rc, "sparsify_probs")
+            return
         if self.seg is not None:
-            rc = lib().sparsify_sample_compact_segmented(
+            rc = self.L.sparsify_sample_compact_segmented(
                 g.data_ptr(), self.rows, self.seg.host.data_ptr(), self.seg.dev.data_ptr(), rho_dev.data_ptr(),
                 self.sid, self.iters, seeds_dev.data_ptr(), self.idx.data_ptr(), self.val.data_ptr(), self.cap,
                 self.nnz.data_ptr(), self.lam.data_ptr(), self.k.data_ptr(), self.flags.data_ptr(),
@@ -440,14 +502,14 @@ class Plan:
             _check(rc, "sparsify_sample_compact_segmented")
             return
         if self.hybrid:
-            rc = lib().sparsify_sample_hybrid_batched(
+            rc = self.L.sparsify_sample_hybrid_batched(
                 g.data_ptr(), self.rows, self.d, self.ld, rho_dev.data_ptr(), self.sid, self.iters,
                 seeds_dev.data_ptr(), self.idx.data_ptr(), self.val.data_ptr(), self.cap, self.nnz.data_ptr(),
                 self.code_b.data_ptr(), self.cap, self.nnz_b.data_ptr(), self.inv.data_ptr(), _ptr(self.q),
                 self.lam.data_ptr(), self.flags.data_ptr(), self.ws.data_ptr(), self.ws.numel(), _stream(stream))
             _check(rc, "sparsify_sample_hybrid_batched")
             return
-        rc = lib().sparsify_sample_compact_batched(
+        rc = self.L.sparsify_sample_compact_batched(
             g.data_ptr(), self.rows, self.d, self.ld, rho_dev.data_ptr(), self.sid, self.iters,
             seeds_dev.data_ptr(), self.idx.data_ptr(), self.val.data_ptr(), self.cap, self.nnz.data_ptr(),
             self.lam.data_ptr(), self.k.data_ptr(), self.flags.data_ptr(), self.ws.data_ptr(),
@@ -455,7 +517,11 @@ class Plan:
         _check(rc, "sparsify_sample_compact_batched")
 
     def survivors_and_bytes(self):
-        """(survivors, output bytes) of the last run, summed over rows (host sync)."""
+        """(survivors, output bytes) of the last run, summed over rows (host sync); for the
+        probabilities entry point (capped coordinates, the 4 B per coordinate of p)."""
+        if self.probs:
+            n = self.seg.total if self.seg is not None else self.rows * self.d
+            return int(self.k.sum().item()), 4 * n
         if self.hybrid:
             na, nb = int(self.nnz.sum().item()), int(self.nnz_b.sum().item())
             qb = self.rows * self.d if self.q is not None else 0
@@ -483,7 +549,7 @@ def sparsify_sample_compact_batched(g, rho, seeds, solver="greedy", iters: int =
     k = torch.empty(rows, dtype=torch.int64, device=dev)
     fl = torch.empty(rows, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, d, sid), stream)
     rc = lib().sparsify_sample_compact_batched(g.data_ptr(), rows, d, ld, r.data_ptr(), sid, int(iters),
                                                s.data_ptr(), idx.data_ptr(), val.data_ptr(), cap, nnz.data_ptr(),
                                                lam.data_ptr(), k.data_ptr(), fl.data_ptr(), buf.data_ptr(), nb,
@@ -538,7 +604,7 @@ def sparsify_sample_compact_segmented(g, seg: Segments, rho, seeds, solver="gree
     k = torch.empty(rows, dtype=torch.int64, device=dev)
     fl = torch.empty(rows, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid), stream)
     rc = lib().sparsify_sample_compact_segmented(g.data_ptr(), rows, seg.host.data_ptr(), seg.dev.data_ptr(),
                                                  r.data_ptr(), sid, int(iters), s.data_ptr(), idx.data_ptr(),
                                                  val.data_ptr(), cap, nnz.data_ptr(), lam.data_ptr(), k.data_ptr(),
@@ -572,7 +638,7 @@ def sparsify_sample_hybrid_segmented(g, seg: Segments, rho, seeds, solver="greed
     lam = torch.empty(rows, dtype=torch.float64, device=dev)
     fl = torch.empty(rows, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid), stream)
     rc = lib().sparsify_sample_hybrid_segmented(g.data_ptr(), rows, seg.host.data_ptr(), seg.dev.data_ptr(),
                                                 r.data_ptr(), sid, int(iters), s.data_ptr(), idx_a.data_ptr(),
                                                 val_a.data_ptr(), cap_a, n_a.data_ptr(), code_b.data_ptr(), cap_b,
@@ -594,7 +660,7 @@ def sparsify_probs_segmented(g, seg: Segments, rho, solver="greedy", iters: int 
     k = torch.empty(rows, dtype=torch.int64, device=dev)
     fl = torch.empty(rows, dtype=torch.int32, device=dev)
     sid = _solver_id(solver)
-    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid))
+    buf, nb = _ws(workspace, dev, workspace_bytes(rows, seg.max_len, sid), stream)
     rc = lib().sparsify_probs_segmented(g.data_ptr(), rows, seg.host.data_ptr(), seg.dev.data_ptr(), r.data_ptr(),
                                         sid, int(iters), _ptr(p), lam.data_ptr(), k.data_ptr(), fl.data_ptr(),
                                         buf.data_ptr(), nb, _stream(stream))
@@ -602,18 +668,21 @@ def sparsify_probs_segmented(g, seg: Segments, rho, solver="greedy", iters: int 
     return Probs(p, lam, k, fl)
 
 
-class KernelTimer:
-    """Brackets every launch of one kernel (0 sample/compact, 1 statistics, 2 probabilities) with
-    HIP events on its stream; ``read()`` returns (total ms, launches)."""
+class KernelProfiler:
+    """Kernel times per class from the measurement build (libgspar_instr.so): every launch made
+    through that library while armed carries HIP start / stop events stamped by its dispatch.
+    ``read()`` returns {class name: (total ms, launches)}; ``close()`` disarms."""
 
-    def __init__(self, which: int, max_launches: int):
-        _check(lib().gspar_timing_arm(which, max_launches), "gspar_timing_arm")
+    def __init__(self, max_launches: int):
+        self.L = instr_lib()
+        _check(self.L.gspar_prof_arm(int(max_launches)), "gspar_prof_arm")
 
     def read(self):
-        ms = ctypes.c_double()
-        n = ctypes.c_int()
-        _check(lib().gspar_timing_read(ctypes.byref(ms), ctypes.byref(n)), "gspar_timing_read")
-        return ms.value, n.value
+        n = len(PROF_CLASSES)
+        ms = (ctypes.c_double * n)()
+        cnt = (ctypes.c_int * n)()
+        _check(self.L.gspar_prof_read(ms, cnt), "gspar_prof_read")
+        return {name: (ms[i], cnt[i]) for i, name in enumerate(PROF_CLASSES)}
 
     def close(self):
-        lib().gspar_timing_disarm()
+        self.L.gspar_prof_disarm()

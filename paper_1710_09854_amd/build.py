@@ -1,33 +1,53 @@
-"""Builds libgspar.so (HIP, gfx950) in-tree: python -m paper_1710_09854_amd.build"""
+"""Builds the HIP library for gfx950 in-tree: python -m paper_1710_09854_amd.build
+
+libgspar.so        the product library; its exports are exactly include/gspar.h.
+libgspar_instr.so  the same source with GSPAR_INSTRUMENT: gspar.h plus the measurement and
+                   host-check hooks of include/gspar_instr.h (benchmark and tests only).
+"""
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc", "gspar.hip")
 OUT = os.path.join(HERE, "libgspar.so")
+OUT_INSTR = os.path.join(HERE, "libgspar_instr.so")
+MAP = os.path.join(HERE, "csrc", "gspar.map")
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",
     # keep the compiler from emitting packed FP32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # only the C ABI of the headers is exported
+    "-fvisibility=hidden", "-fvisibility-inlines-hidden",
     "-Wall",
 ]
 
 
-def build(verbose: bool = False) -> str:
+def _compile(out, defines, verbose):
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = OUT + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, SRC]
+    tmp = out + ".tmp"
+    cmd = [hipcc, *HIPCC_FLAGS, *defines, "-Wl,--version-script=" + MAP, "-I", os.path.join(ROOT, "include"),
+           "-o", tmp, SRC]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if verbose or r.returncode != 0:
         lines = [l for l in (r.stdout + r.stderr).splitlines() if "packed-fp32-ops" not in l]
         sys.stderr.write("\n".join(lines) + "\n")
     if r.returncode != 0:
-        raise RuntimeError("hipcc failed for " + SRC)
-    os.replace(tmp, OUT)
-    return OUT
+        raise RuntimeError("hipcc failed for " + out)
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    with ThreadPoolExecutor(2) as ex:
+        a = ex.submit(_compile, OUT, [], verbose)
+        b = ex.submit(_compile, OUT_INSTR, ["-DGSPAR_INSTRUMENT"], verbose)
+        out = a.result()
+        b.result()
+    return out
 
 
 if __name__ == "__main__":

@@ -38,6 +38,11 @@
 #include <type_traits>
 
 #include "gspar.h"
+#ifdef GSPAR_INSTRUMENT
+#include <hip/hip_ext.h>
+
+#include "gspar_instr.h"
+#endif
 
 #define GS_HD __host__ __device__ __forceinline__
 
@@ -110,8 +115,14 @@ GS_HD uint64_t fx_limb(const Fx& a, int i) {
   for (int j = 0; j < 5; ++j) r = (j == i) ? a.w[j] : r;
   return r;
 }
-GS_HD Fx fx_shifted(uint64_t v, int s) {  // v * 2^s, s in [0, 253]
-  s = s < 0 ? 0 : (s > 255 ? 255 : s);
+// v * 2^s for s in [0, 255] (every v < 2^64 then fits). A shift outside that range breaks an
+// invariant of the callers (a binade index outside [0, 255]): it sets kFlagInternal in *err and
+// gives 0, so the row is reported instead of being solved with a wrong sum.
+GS_HD Fx fx_shifted(uint64_t v, int s, uint32_t* err) {
+  if ((unsigned)s > 255u) {
+    *err |= kFlagInternal;
+    return fx_zero();
+  }
   const int li = s >> 6, off = s & 63;
   const uint64_t lo = v << off;
   const uint64_t hi = off ? (v >> (64 - off)) : 0;
@@ -196,13 +207,18 @@ GS_HD uint64_t fq_limb(const Fq& a, int i) {
   return r;
 }
 // Squared significands summed per bin as qh * 2^24 + ql (each square m^2 < 2^48 split at bit 24;
-// qh, ql < 2^55 for at most 2^31 values), times 2^(2 shift): the bin's exact sum of squares.
-GS_HD Fq fq_squares(uint64_t qh, uint64_t ql, int shift) {
+// qh, ql < 2^55 for at most 2^31 values), times 2^(2 shift): the bin's exact sum of squares. The
+// sum is below 2^80, so 2 shift in [0, 511] keeps it inside the 640 bits; any other shift sets
+// kFlagInternal in *err and gives 0, like fx_shifted.
+GS_HD Fq fq_squares(uint64_t qh, uint64_t ql, int shift, uint32_t* err) {
+  const int sh = 2 * shift;
+  if ((unsigned)sh > 511u) {
+    *err |= kFlagInternal;
+    return fq_zero();
+  }
   const uint64_t lo0 = qh << 24;
   const uint64_t lo = lo0 + ql;
   const uint64_t hi = (qh >> 40) + (lo < lo0 ? 1 : 0);
-  int sh = 2 * shift;
-  sh = sh < 0 ? 0 : (sh > 506 ? 506 : sh);
   const int li = sh >> 6, off = sh & 63;
   const uint64_t w0 = lo << off;
   const uint64_t w1 = off ? ((lo >> (64 - off)) | (hi << off)) : hi;
@@ -657,6 +673,7 @@ struct SolveLds {
   L1Cache l1;
   WinCache<kB2> w2;
   WinCache<kB3> w3;
+  uint32_t err;         // kFlagInternal when a wide-arithmetic invariant broke during this solve
   uint64_t bcnt, bsig;  // a level-2 bin's totals, broadcast by its owner (greedy queries)
   uint32_t bmx, bmn;
   // variance-budget solver: partial square sums of scans, and broadcasts of square sums
@@ -666,6 +683,7 @@ struct SolveLds {
   uint64_t sql[kNT / 64];
 };
 struct Hists {
+  uint32_t* err;       // LDS word collecting kFlagInternal from the wide-arithmetic helpers
   L1Cache* l1;         // LDS
   WinCache<kB2>* w2;   // LDS
   WinCache<kB3>* w3;   // LDS
@@ -723,7 +741,7 @@ GS_DI void l1_build(SolveLds& s, const Hists& H) {
   Fx w = fx_zero(), iw = fx_zero();
   if (t < kB1) {  // whole waves
     k = H.l1->cnt[t];
-    if (k) w = fx_shifted(H.l1->sig[t], binade_shift(t));
+    if (k) w = fx_shifted(H.l1->sig[t], binade_shift(t), H.err);
     ik = wave_suffix(k, lane);
     iw = wave_suffix(w, lane);
     if (lane == 0) {
@@ -750,7 +768,7 @@ GS_DI BinInfo l1_info(const Hists& H, int e) {
   i.Kab = H.l1->K[e];
   i.Wab = H.l1->W[e];
   i.cnt = H.l1->cnt[e];
-  i.Wb = i.cnt ? fx_shifted(H.l1->sig[e], binade_shift(e)) : fx_zero();
+  i.Wb = i.cnt ? fx_shifted(H.l1->sig[e], binade_shift(e), H.err) : fx_zero();
   i.mx = H.l1->mx[e];
   return i;
 }
@@ -765,6 +783,7 @@ struct Lvl {
   int shift;     // binade_shift(E): value = significand * 2^shift (units of 2^-149)
   uint64_t Kaw;  // count of keys above the window
   Fx Waw;        // their exact sum
+  uint32_t* err; // as in Hists
 };
 struct Walk {
   uint64_t exK;  // count above this thread's bins, inside the window
@@ -774,13 +793,13 @@ struct Walk {
 GS_DI Lvl lvl2(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
   Lvl L;
   L.cnt = H.w2->cnt; L.sig = H.w2->sig; L.mx = H.w2->mx;
-  L.nbins = kB2; L.per = kB2 / kNT; L.shift = binade_shift((int)E); L.Kaw = Kaw; L.Waw = Waw;
+  L.nbins = kB2; L.per = kB2 / kNT; L.shift = binade_shift((int)E); L.Kaw = Kaw; L.Waw = Waw; L.err = H.err;
   return L;
 }
 GS_DI Lvl lvl3(const Hists& H, uint32_t E, uint64_t Kaw, const Fx& Waw) {
   Lvl L;
   L.cnt = H.w3->cnt; L.sig = H.w3->sig; L.mx = H.w3->mx;
-  L.nbins = kB3; L.per = kB3 / kNT; L.shift = binade_shift((int)E); L.Kaw = Kaw; L.Waw = Waw;
+  L.nbins = kB3; L.per = kB3 / kNT; L.shift = binade_shift((int)E); L.Kaw = Kaw; L.Waw = Waw; L.err = H.err;
   return L;
 }
 
@@ -816,7 +835,7 @@ GS_DI void lvl_scan(const Lvl& L, SolveLds& s, Walk& w) {
 GS_DI Fx lvl_total(const Lvl& L, uint64_t K, uint64_t S, uint64_t& Kout) {
   Kout = L.Kaw + K;
   Fx W = L.Waw;
-  if (S) fx_add(W, fx_shifted(S, L.shift));
+  if (S) fx_add(W, fx_shifted(S, L.shift, L.err));
   return W;
 }
 
@@ -832,7 +851,7 @@ GS_DI void lvl_bin_info(const Lvl& L, const Walk& w, int b, SolveLds& s, BinInfo
       if (bb == b) {
         s.bi.Wab = lvl_total(L, K, S, s.bi.Kab);
         s.bi.cnt = c;
-        s.bi.Wb = c ? fx_shifted(sg, L.shift) : fx_zero();
+        s.bi.Wb = c ? fx_shifted(sg, L.shift, L.err) : fx_zero();
         s.bi.mx = L.mx[bb];
         break;
       }
@@ -1012,7 +1031,7 @@ GS_DI int sv_query(SolveLds& s, RowCtl& c, const Hists& H, uint64_t qcnt, uint64
     if (ok) {
       K = i1.Kab + kq;
       W = i1.Wab;
-      if (sq) fx_add(W, fx_shifted(sq, binade_shift(e)));
+      if (sq) fx_add(W, fx_shifted(sq, binade_shift(e), H.err));
       return 0;
     }
   }
@@ -1037,10 +1056,19 @@ GS_DI void sv_greedy(SolveLds& s, RowCtl& c, const Hists& H, uint64_t qcnt, uint
   sv_finalize(c, c.lam, cap_key(c.lam));
 }
 
+// The capped set of Proposition 1 is {p_i = 1}: the magnitudes above the criterion's value v
+// (keys >= tcap = key(v) + 1) and, should fl(lambda * a) reach 1 below them (a tied run at v when
+// the criterion holds with equality), those too. Both sets are {key >= t} for some t, so the union
+// is the smaller threshold; every pass tests key >= the final tcap.
+GS_DI uint32_t capped_threshold(double lam, uint32_t tcap) {
+  const uint32_t t = cap_key(lam);
+  return t < tcap ? t : tcap;
+}
+
 GS_DI void sv_exact_finish(RowCtl& c, uint64_t K, const Fx& W, uint32_t tcap) {
   const double T1 = fx_to_double(fx_sub(c.S, W));
   const double lam = (c.B - (double)K) / T1;
-  sv_finalize(c, lam, tcap);
+  sv_finalize(c, lam, capped_threshold(lam, tcap));
 }
 
 // The exact solver descends levels: at each one it finds the highest bin whose maximum passes
@@ -1144,7 +1172,8 @@ GS_DI int v_screen(double eps, double Sd, double A2d, double Wd, double Hd, doub
 GS_DI void v_finish(RowCtl& c, const Fq& A2, const Fx& W, const Fq& H, uint32_t tcap) {
   double T1, rhs;
   v_criterion(c.B, c.S, A2, W, H, 1u, T1, rhs);
-  sv_finalize(c, T1 / rhs, tcap);
+  const double lam = T1 / rhs;
+  sv_finalize(c, lam, capped_threshold(lam, tcap));
 }
 
 // A bin of a level: keys above it (count, sum, square sum), its own count and maximum key.
@@ -1182,7 +1211,7 @@ GS_DI void v_level1(SolveLds& s, const RowCtl& c, const Hists& H, Fq& A2, int& b
       qh += H.h1q[k].qh[t];
       ql += H.h1q[k].ql[t];
     }
-    if (H.l1->cnt[t]) q = fq_squares(qh, ql, binade_shift(t));
+    if (H.l1->cnt[t]) q = fq_squares(qh, ql, binade_shift(t), H.err);
     iq = wave_suffix(q, lane);
     if (lane == 0) s.sq[wv] = iq;
   }
@@ -1305,9 +1334,9 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
         int pass = v_screen(c.B, Sd, A2d, Wd, Hd, key_value(L.mx[b]));
         if (pass < 0) {
           Fx W = L.Waw;
-          if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
+          if (Sg) fx_add(W, fx_shifted(Sg, L.shift, L.err));
           Fq Hq = Haw;
-          fq_add(Hq, fq_squares(QH, QL, L.shift));
+          fq_add(Hq, fq_squares(QH, QL, L.shift, L.err));
           double T1, rhs;
           pass = v_criterion(c.B, c.S, A2, W, Hq, L.mx[b], T1, rhs) ? 1 : 0;
         }
@@ -1351,10 +1380,10 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
       }
       s.bi.Kab = L.Kaw + K;
       Fx W = L.Waw;
-      if (Sg) fx_add(W, fx_shifted(Sg, L.shift));
+      if (Sg) fx_add(W, fx_shifted(Sg, L.shift, L.err));
       s.bi.Wab = W;
       Fq Hq = Haw;
-      fq_add(Hq, fq_squares(QH, QL, L.shift));
+      fq_add(Hq, fq_squares(QH, QL, L.shift, L.err));
       s.hq[0] = Hq;
       s.bi.cnt = (uint64_t)L.cnt[bb];
       s.bi.mx = L.mx[bb];
@@ -1544,6 +1573,7 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d, bool fi
     if (c.stage == 3) reduce_into(H.wg, kC23, kB3, H.w3->cnt, H.w3->sig, H.w3->mx);
   }
   c.need = 0;
+  if (threadIdx.x == 0) s.err = 0;
   // every load above has returned before any thread can go on to clear the window it read
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -1561,7 +1591,15 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d, bool fi
   } else {
     sv_exact(s, c, H);
   }
-  if (threadIdx.x == 0) *gc = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (s.err) {
+      // a broken invariant of the exact arithmetic: the row is reported, not sampled
+      c.flags |= s.err;
+      sv_finalize(c, NAN, kKeyInf);
+    }
+    *gc = c;
+  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1915,7 +1953,7 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
     }
     return;
   }
-  const Hists H{&sm.l1, &sm.w2, &sm.w3, l1t_of(a, row), h1_of(a, row), win_of(a, row),
+  const Hists H{&sm.err, &sm.l1, &sm.w2, &sm.w3, l1t_of(a, row), h1_of(a, row), win_of(a, row),
                 h1q_of(a, row), winq_of(a, row), vctl_of(a, row)};
   int64_t base, len;
   row_span(a, row, base, len);
@@ -2018,29 +2056,24 @@ static_assert(kTileGroups % kSampleBatch == 0 && kTileGroups == 16, "tile shape"
 // Below this lambda, lambda * 2^32 * |g| could round differently from (lambda * |g|) * 2^32.
 constexpr double kLamScaledMin = 0x1p-900;
 
-// Whole-tile decisions with the scaled threshold: coordinate i survives iff
+// Whole-tile decisions with the scaled threshold: an uncapped coordinate i survives iff
 // x_i < fl(lambda * 2^32 * |g_i|), which equals the comparison x_i < fl(lambda * |g_i|) * 2^32
 // (exact scaling by a power of two) for lambda = 0 or lambda >= kLamScaledMin; a capped coordinate
-// has a threshold of at least 2^32, so it always survives and the capped test is that comparison.
-__device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double lam32, uint32_t k0, uint32_t k1,
-                                            uint32_t& z, uint32_t& cz) {
+// (key >= tcap, p_i = 1) always survives.
+__device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double lam32, uint32_t tcap, uint32_t k0,
+                                            uint32_t k1, uint32_t& z, uint32_t& cz) {
   // rows are shorter than 2^31 coordinates, so the counter's high word floor(i/4) >> 32 is 0; with
   // that known the first rounds fold into fewer vector operations
   uint32_t x0 = (uint32_t)q, x1 = 0, x2 = 0, x3 = 0;
   philox10(x0, x1, x2, x3, k0, k1);
   const uint32_t xr[4] = {x0, x1, x2, x3};
-  double t[4];
   z = 0;
   cz = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    t[k] = lam32 * (double)fabsf(v[k]);
-    z |= (uint32_t)((double)xr[k] < t[k]) << k;
-  }
-  // capped coordinates are rare: test the group's largest threshold first
-  if (fmax(fmax(t[0], t[1]), fmax(t[2], t[3])) >= 0x1p32) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) cz |= (uint32_t)(t[k] >= 0x1p32) << k;
+    const bool capped = key_of(v[k]) >= tcap;  // tcap >= 1, so zeros are never capped
+    z |= (uint32_t)(capped || (double)xr[k] < lam32 * (double)fabsf(v[k])) << k;
+    cz |= (uint32_t)capped << k;
   }
 }
 
@@ -2101,7 +2134,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   c.row = a.g + base;
   c.lam = ctl->lam;
   c.tcap = ctl->tcap;
-  c.live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO | GSPAR_FLAG_BADSEG));
+  c.live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO | GSPAR_FLAG_BADSEG | kFlagInternal));
   const uint64_t seed = a.seed_dev ? a.seed_dev[row] : a.seed;
   c.k0 = (uint32_t)seed;
   c.k1 = (uint32_t)(seed >> 32);
@@ -2157,7 +2190,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         for (int u = 0; u < kSampleBatch; ++u) {
           const float v[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
           uint32_t z, cz;
-          decide_fast(q0 + 64 * (jb + u), v, lam32, c.k0, c.k1, z, cz);
+          decide_fast(q0 + 64 * (jb + u), v, lam32, c.tcap, c.k0, c.k1, z, cz);
           record(jb + u, v, z, cz);
         }
       }
@@ -2490,7 +2523,8 @@ __global__ void __launch_bounds__(256) k_probs(Args a) {
   const RowCtl* ctl = ctl_of(a, row);
   const double lam = ctl->lam;
   const uint32_t tcap = ctl->tcap;
-  const bool live = ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO | GSPAR_FLAG_BADSEG));
+  const bool live =
+      ctl->done && !(ctl->flags & (GSPAR_FLAG_NONFINITE | GSPAR_FLAG_BADRHO | GSPAR_FLAG_BADSEG | kFlagInternal));
   int64_t base, len;
   row_span(a, row, base, len);
   const int64_t beg = blk * a.chunk;
@@ -2547,22 +2581,34 @@ __global__ void __launch_bounds__(64) k_probs_out(Args a) {
 // ------------------------------------------------------------------------------------------
 // Host side.
 // ------------------------------------------------------------------------------------------
+// Kernel classes, in the order the instrumented build reports them.
+enum KernelClass { kcSample = 0, kcStats, kcProbs, kcSolve, kcRefine, kcInit, kcAggregate, kcProbsOut, kcCount };
+
+#ifdef GSPAR_INSTRUMENT
+// Measurement build only: while armed, each launch records a pair of HIP events taken by the
+// dispatch itself (hipExtLaunchKernelGGL's start and stop events, the kernel's own execution
+// interval), filed under its class.
 struct Timing {
-  int which = -1;
   int max = 0;
   int n = 0;
   hipEvent_t* ev = nullptr;
+  int* cls = nullptr;
 };
 static Timing g_timing;
+#endif
 
-static void time_before(int which, hipStream_t s) {
-  if (g_timing.which == which && g_timing.n < g_timing.max) (void)hipEventRecord(g_timing.ev[2 * g_timing.n], s);
-}
-static void time_after(int which, hipStream_t s) {
-  if (g_timing.which == which && g_timing.n < g_timing.max) {
-    (void)hipEventRecord(g_timing.ev[2 * g_timing.n + 1], s);
-    g_timing.n += 1;
+template <typename... KArgs, typename... Args>
+static void launch(int cls, void (*kern)(KArgs...), dim3 grid, dim3 block, hipStream_t s, Args... args) {
+#ifdef GSPAR_INSTRUMENT
+  if (g_timing.ev && g_timing.n < g_timing.max) {
+    const int i = g_timing.n++;
+    g_timing.cls[i] = cls;
+    hipExtLaunchKernelGGL(kern, grid, block, 0, s, g_timing.ev[2 * i], g_timing.ev[2 * i + 1], 0, args...);
+    return;
   }
+#endif
+  (void)cls;
+  hipLaunchKernelGGL(kern, grid, block, 0, s, args...);
 }
 
 // a density in [0, 1], or for the variance-budget solver a finite eps >= 0
@@ -2615,49 +2661,27 @@ static int launch_solve(Args& a, hipStream_t s) {
   int ib = (int)((zero_items + 255) / 256);
   if (ib > 1024) ib = 1024;
   if (ib < 1) ib = 1;
-  time_before(5, s);
-  hipLaunchKernelGGL(k_init, dim3(ib), dim3(256), 0, s, a);
-  time_after(5, s);
+  launch(kcInit, k_init, dim3(ib), dim3(256), s, a);
   // a segmented call launches only the workgroups that hold coordinates (none if every segment
   // is empty)
   const int64_t nblocks = a.seg ? a.seg_blocks : a.rows * a.nb;
   const dim3 grid((unsigned)nblocks);
-  time_before(1, s);
   if (nblocks > 0) {
-    if (sq) {
-      if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_stats<true, true>), grid, dim3(kNT), 0, s, a);
-      else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_stats<false, true>), grid, dim3(kNT), 0, s, a);
-    } else {
-      if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_stats<true, false>), grid, dim3(kNT), 0, s, a);
-      else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_stats<false, false>), grid, dim3(kNT), 0, s, a);
-    }
+    if (sq) launch(kcStats, vec ? k_stats<true, true> : k_stats<false, true>, grid, dim3(kNT), s, a);
+    else launch(kcStats, vec ? k_stats<true, false> : k_stats<false, false>, grid, dim3(kNT), s, a);
   }
-  time_after(1, s);
   a.first = 1;
-  time_before(3, s);
-  if (sq) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_solve<true>), dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
-  else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_solve<false>), dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
-  time_after(3, s);
+  launch(kcSolve, sq ? k_solve<true> : k_solve<false>, dim3((unsigned)a.rows), dim3(kNT), s, a);
   // each greedy step needs at most one level-2 pass (which counts its query key directly), the
   // exact solver at most a level-2 and a level-3 window
   const int R = a.solver == GSPAR_GREEDY ? a.T : 2;  // the variance form also needs at most two
   for (int r = 0; r < R; ++r) {
     a.first = 0;
-    time_before(4, s);
     if (nblocks > 0) {
-      if (sq) {
-        if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_refine<true, true>), grid, dim3(kNT), 0, s, a);
-        else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_refine<false, true>), grid, dim3(kNT), 0, s, a);
-      } else {
-        if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_refine<true, false>), grid, dim3(kNT), 0, s, a);
-        else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_refine<false, false>), grid, dim3(kNT), 0, s, a);
-      }
+      if (sq) launch(kcRefine, vec ? k_refine<true, true> : k_refine<false, true>, grid, dim3(kNT), s, a);
+      else launch(kcRefine, vec ? k_refine<true, false> : k_refine<false, false>, grid, dim3(kNT), s, a);
     }
-    time_after(4, s);
-    time_before(3, s);
-    if (sq) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_solve<true>), dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
-    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_solve<false>), dim3((unsigned)a.rows), dim3(kNT), 0, s, a);
-    time_after(3, s);
+    launch(kcSolve, sq ? k_solve<true> : k_solve<false>, dim3((unsigned)a.rows), dim3(kNT), s, a);
   }
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
@@ -2665,13 +2689,8 @@ static int launch_solve(Args& a, hipStream_t s) {
 template <int K>
 static void launch_sample(const Args& a, bool vec, hipStream_t s) {
   const dim3 grid((unsigned)(a.seg ? a.seg_wgs : a.rows * ((a.lay.tiles + K - 1) / K)));
-  if (a.code_b) {
-    if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, true, K>), grid, dim3(kTileThreads), 0, s, a);
-    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, true, K>), grid, dim3(kTileThreads), 0, s, a);
-  } else {
-    if (vec) hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<true, false, K>), grid, dim3(kTileThreads), 0, s, a);
-    else hipLaunchKernelGGL(HIP_KERNEL_NAME(k_sample<false, false, K>), grid, dim3(kTileThreads), 0, s, a);
-  }
+  if (a.code_b) launch(kcSample, vec ? k_sample<true, true, K> : k_sample<false, true, K>, grid, dim3(kTileThreads), s, a);
+  else launch(kcSample, vec ? k_sample<true, false, K> : k_sample<false, false, K>, grid, dim3(kTileThreads), s, a);
 }
 
 static int run_sample(Args& a, hipStream_t s) {
@@ -2680,13 +2699,11 @@ static int run_sample(Args& a, hipStream_t s) {
   int rc = launch_solve(a, s);
   if (rc) return rc;
   const bool vec = vec_ok(a);
-  time_before(0, s);
   // tiles per workgroup: 1 while every tile can be resident at once, else 2, so that a
   // workgroup's wait for its predecessors' prefix overlaps the decide phase of its second tile
   const int64_t tiles = a.seg ? a.seg_tiles : a.rows * a.lay.tiles;
   if (a.seg ? a.seg_k == 1 : tiles <= kSampleResident) launch_sample<1>(a, vec, s);
   else launch_sample<2>(a, vec, s);
-  time_after(0, s);
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
 
@@ -2698,13 +2715,8 @@ static int run_probs(Args& a, hipStream_t s) {
   const bool vec = vec_ok(a) && (!a.p || (uintptr_t)a.p % 16 == 0);
   const int64_t nblocks = a.seg ? a.seg_blocks : a.rows * a.nb;
   const dim3 grid((unsigned)nblocks);
-  time_before(2, s);
-  if (nblocks > 0) {
-    if (vec) hipLaunchKernelGGL(k_probs<true>, grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(k_probs<false>, grid, dim3(256), 0, s, a);
-  }
-  time_after(2, s);
-  hipLaunchKernelGGL(k_probs_out, dim3((unsigned)((a.rows + 63) / 64)), dim3(64), 0, s, a);
+  if (nblocks > 0) launch(kcProbs, vec ? k_probs<true> : k_probs<false>, grid, dim3(256), s, a);
+  launch(kcProbsOut, k_probs_out, dim3((unsigned)((a.rows + 63) / 64)), dim3(64), s, a);
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
 
@@ -2965,9 +2977,7 @@ int gspar_aggregate(const int32_t* idx, const float* val, int64_t cap, const int
   a.d = d;
   a.v = v;
   hipStream_t s = (hipStream_t)stream;
-  time_before(6, s);
-  hipLaunchKernelGGL(k_aggregate, dim3((unsigned)((d + kAggBlock - 1) / kAggBlock)), dim3(kAggThreads), 0, s, a);
-  time_after(6, s);
+  launch(kcAggregate, k_aggregate, dim3((unsigned)((d + kAggBlock - 1) / kAggBlock)), dim3(kAggThreads), s, a);
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
 
@@ -3153,65 +3163,84 @@ const char* gspar_status_string(int status) {
 
 int gspar_version(void) { return 100; }
 
-int gspar_timing_arm(int which, int max_launches) {
-  if (which < 0 || which > 6 || max_launches < 1) return GSPAR_ERR_ARG;
-  gspar_timing_disarm();
+#ifdef GSPAR_INSTRUMENT
+int gspar_prof_arm(int max_launches) {
+  if (max_launches < 1) return GSPAR_ERR_ARG;
+  gspar_prof_disarm();
   g_timing.ev = new hipEvent_t[2 * (size_t)max_launches];
+  g_timing.cls = new int[(size_t)max_launches];
   for (int i = 0; i < 2 * max_launches; ++i) {
     if (hipEventCreate(&g_timing.ev[i]) != hipSuccess) {
       for (int j = 0; j < i; ++j) (void)hipEventDestroy(g_timing.ev[j]);
       delete[] g_timing.ev;
-      g_timing.ev = nullptr;
+      delete[] g_timing.cls;
+      g_timing = Timing();
       return GSPAR_ERR_HIP;
     }
   }
-  g_timing.which = which;
   g_timing.max = max_launches;
   g_timing.n = 0;
   return GSPAR_OK;
 }
 
-int gspar_timing_read(double* total_ms, int* launches) {
-  if (!total_ms || !launches) return GSPAR_ERR_ARG;
-  *total_ms = 0.0;
-  *launches = g_timing.n;
+int gspar_prof_read(double* ms, int* launches) {
+  if (!ms || !launches) return GSPAR_ERR_ARG;
+  for (int c = 0; c < kcCount; ++c) {
+    ms[c] = 0.0;
+    launches[c] = 0;
+  }
   if (!g_timing.ev || g_timing.n == 0) return GSPAR_OK;
   if (hipEventSynchronize(g_timing.ev[2 * g_timing.n - 1]) != hipSuccess) return GSPAR_ERR_HIP;
-  double tot = 0.0;
   for (int i = 0; i < g_timing.n; ++i) {
-    float ms = 0.f;
-    if (hipEventElapsedTime(&ms, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]) != hipSuccess) return GSPAR_ERR_HIP;
-    tot += ms;
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]) != hipSuccess) return GSPAR_ERR_HIP;
+    ms[g_timing.cls[i]] += t;
+    launches[g_timing.cls[i]] += 1;
   }
-  *total_ms = tot;
   return GSPAR_OK;
 }
 
-int gspar_timing_disarm(void) {
+int gspar_prof_disarm(void) {
   if (g_timing.ev) {
     for (int i = 0; i < 2 * g_timing.max; ++i) (void)hipEventDestroy(g_timing.ev[i]);
     delete[] g_timing.ev;
+    delete[] g_timing.cls;
   }
   g_timing = Timing();
   return GSPAR_OK;
 }
 
-// Host-side checks of the device arithmetic (same source, compiled for the host): rounding of the
-// exact accumulator, the capped-threshold search and the random generator.
+// Host-side checks of the device arithmetic (the same source compiled for the host): rounding of
+// the exact accumulator, the shift invariant, the capped-threshold search and the generator.
 double gspar_check_fx_round(const uint64_t* limbs5) {
   Fx f;
   for (int i = 0; i < 5; ++i) f.w[i] = limbs5[i];
   return fx_to_double(f);
 }
 
+uint32_t gspar_check_fx_shifted(uint64_t v, int s, uint64_t* limbs5) {
+  uint32_t err = 0;
+  const Fx f = fx_shifted(v, s, &err);
+  for (int i = 0; i < 5; ++i) limbs5[i] = f.w[i];
+  return err;
+}
+
+uint32_t gspar_check_fq_squares(uint64_t qh, uint64_t ql, int shift, uint64_t* limbs10) {
+  uint32_t err = 0;
+  const Fq f = fq_squares(qh, ql, shift, &err);
+  for (int i = 0; i < kQ; ++i) limbs10[i] = f.w[i];
+  return err;
+}
+
 double gspar_check_exact_sum(const float* x, int64_t n) {
   Fx acc = fx_zero();
+  uint32_t err = 0;
   for (int64_t i = 0; i < n; ++i) {
     const uint32_t key = key_of(x[i]);
     if (key == 0 || key >= kKeyInf) continue;
-    fx_add(acc, fx_shifted(key_sig(key), binade_shift((int)(key >> 23))));
+    fx_add(acc, fx_shifted(key_sig(key), binade_shift((int)(key >> 23)), &err));
   }
-  return fx_to_double(acc);
+  return err ? NAN : fx_to_double(acc);
 }
 
 uint32_t gspar_check_cap_key(double lam) { return cap_key(lam); }
@@ -3221,5 +3250,6 @@ void gspar_check_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out)
   philox10(c0, c1, c2, c3, key[0], key[1]);
   out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
 }
+#endif  // GSPAR_INSTRUMENT
 
 }  // extern "C"

@@ -203,6 +203,58 @@ def check_hybrid(L, verbose=True):
     return True
 
 
+def tied_boundary(d=40000, n_hi=3000, n_zero=3000, seed=5):
+    """A vector whose exact solution at rho = 0.5 meets Algorithm 2's criterion with equality:
+    n_hi entries of +-2, n_zero zeros and the rest +-1 at seeded positions (so ties fall in full
+    and partial sample tiles), giving lambda = 0.5 and lambda * 2 = 1: the whole tied run of 2s has
+    p_i = 1 and forms the capped set."""
+    rng = np.random.default_rng(seed)
+    g = np.where(rng.random(d) < 0.5, -1.0, 1.0).astype(np.float32)
+    pos = rng.permutation(d)
+    g[pos[:n_hi]] *= 2
+    g[pos[n_hi:n_hi + n_zero]] = 0
+    return g
+
+
+def check_ties(L, verbose=True):
+    """One capped test everywhere: the compaction (fast and scalar paths), the probabilities, the
+    hybrid coding and the look-back's own recount all treat a coordinate with p_i = 1 as capped."""
+    g = tied_boundary()
+    hi = np.flatnonzero(np.abs(g) == 2)
+    A = 3000.0 * 4 + 34000.0
+    for solver, rho in (("exact", 0.5), ("variance", (3000.0 * 4 + 34000.0 / 0.5) / A - 1.0)):
+        sol = oracle.solve(g, rho, solver)
+        assert sol.k == hi.size
+        idx, val, n, lam, k, fl = sample_row(L, g, rho, solver, 13)
+        assert fl == 0 and lam == sol.lam and k == sol.k, (solver, lam, sol.lam, k, sol.k)
+        compare_sample(g, sol.p, 13, idx, val, n, lam, sol.lam)
+        assert np.all(np.isin(hi, idx))  # every capped coordinate survives
+        # the same row at an unaligned start (scalar decisions everywhere)
+        buf = np.zeros(g.size + 16, np.float32)
+        base = (-buf.ctypes.data // 4) % 4 + 1
+        view = buf[base:base + g.size]
+        view[:] = g
+        a = sample_row(L, view, rho, solver, 13)
+        assert a[2] == n and a[4] == k and np.array_equal(a[0], idx) and np.array_equal(a[1], val)
+        p, lam2, k2, fl2 = probs_row(L, g, rho, solver)
+        assert k2 == sol.k and lam2 == sol.lam
+        compare_probs(p, sol.p)
+        ia, va, na, cb, nb, inv, q, lam3, fl3 = hybrid_batched(L, g[None, :], [rho], [13], solver)
+        A_, B_ = int(na[0]), int(nb[0])
+        assert not fl3.any() and A_ == hi.size and A_ + B_ == n
+        assert np.array_equal(ia[0, :A_], hi) and np.array_equal(va[0, :A_], g[hi])
+        bi = cb[0, :B_] & 0x7FFFFFFF
+        assert np.all(np.diff(bi) > 0)
+        merged = np.sort(np.concatenate([ia[0, :A_], bi]))
+        assert np.array_equal(merged, idx)
+        h = oracle.sample_hybrid(g, sol.p, 13)
+        assert np.array_equal(ia[0, :A_], h.qa_idx) and np.array_equal(bi, h.qb_idx)
+        assert np.array_equal(q[0], h.q)
+    if verbose:
+        print("tie cases ok", flush=True)
+    return True
+
+
 def segmented(L, g, off, rhos, seeds, solver, iters=2, cap=None, off_dev=None, g_shift=0):
     """sparsify_sample_compact_segmented on a flat host vector (placed g_shift floats past a
     16-byte boundary); off_dev defaults to the host offsets."""
@@ -505,6 +557,8 @@ if __name__ == "__main__":
         run_extra(sys.argv[1], lite=True)
     if which in ("all", "hybrid"):
         check_hybrid(load(sys.argv[1]))
+    if which in ("all", "ties"):
+        check_ties(load(sys.argv[1]))
     if which in ("all", "aggregate"):
         check_aggregate(load(sys.argv[1]))
     if which in ("all", "variance"):

@@ -11,6 +11,8 @@ import numpy as np
 import pytest
 
 import ctypes
+import shutil
+import subprocess
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "gspar.h")
@@ -20,17 +22,31 @@ HEADER = os.path.join(ROOT, "include", "gspar.h")
 def L():
     import paper_1710_09854_amd as gs
 
-    if not os.path.exists(gs.LIB_PATH):
+    if not (os.path.exists(gs.LIB_PATH) and os.path.exists(gs.INSTR_LIB_PATH)):
         from paper_1710_09854_amd import build
 
         build.build()
     return gs.lib()
 
 
-def declared_functions():
-    src = open(HEADER).read()
+@pytest.fixture(scope="module")
+def LI(L):
+    """The measurement build: the same source with the host-compiled arithmetic checks."""
+    import paper_1710_09854_amd as gs
+
+    return gs.instr_lib()
+
+
+def declared_functions(header=HEADER):
+    src = open(header).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", src)) - {"defined"})
+    src = "\n".join(l for l in src.splitlines() if not l.lstrip().startswith("#"))  # preprocessor lines
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", src)))
+
+
+def exported_functions(path):
+    out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True, check=True).stdout
+    return sorted(line.split()[-1] for line in out.splitlines() if line.strip())
 
 
 def test_exports_every_declared_symbol(L):
@@ -38,6 +54,17 @@ def test_exports_every_declared_symbol(L):
     assert "sparsify_probs" in names and "sparsify_sample_compact_batched" in names
     for n in names:
         assert hasattr(L, n), f"symbol {n} declared in gspar.h is not exported"
+
+
+@pytest.mark.skipif(not shutil.which("nm"), reason="needs nm")
+def test_exports_are_exactly_the_header(L):
+    """The product library exports the functions of gspar.h and nothing else (no kernel handles,
+    no measurement hooks); the measurement build adds exactly gspar_instr.h's."""
+    import paper_1710_09854_amd as gs
+
+    assert exported_functions(gs.LIB_PATH) == declared_functions()
+    instr = sorted(declared_functions() + declared_functions(os.path.join(ROOT, "include", "gspar_instr.h")))
+    assert exported_functions(gs.INSTR_LIB_PATH) == instr
 
 
 def test_workspace_and_capacity(L):
@@ -211,7 +238,8 @@ def _fx_limbs(v: int):
     return (ctypes.c_uint64 * 5)(*[(v >> (64 * i)) & 0xFFFFFFFFFFFFFFFF for i in range(5)])
 
 
-def test_fixed_point_rounding_is_correct(L):
+def test_fixed_point_rounding_is_correct(LI):
+    L = LI
     L.gspar_check_fx_round.argtypes = [ctypes.c_uint64 * 5]
     L.gspar_check_fx_round.restype = ctypes.c_double
     rng = np.random.default_rng(3)
@@ -230,7 +258,8 @@ def test_fixed_point_rounding_is_correct(L):
         assert L.gspar_check_fx_round(_fx_limbs(v)) == want, hex(v)
 
 
-def test_exact_sum_matches_fsum(L):
+def test_exact_sum_matches_fsum(LI):
+    L = LI
     L.gspar_check_exact_sum.argtypes = [np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS"), ctypes.c_int64]
     L.gspar_check_exact_sum.restype = ctypes.c_double
     rng = np.random.default_rng(4)
@@ -240,7 +269,8 @@ def test_exact_sum_matches_fsum(L):
         assert L.gspar_check_exact_sum(x, x.size) == math.fsum(np.abs(x.astype(np.float64)))
 
 
-def test_cap_key_is_smallest_capped_pattern(L):
+def test_cap_key_is_smallest_capped_pattern(LI):
+    L = LI
     L.gspar_check_cap_key.argtypes = [ctypes.c_double]
     L.gspar_check_cap_key.restype = ctypes.c_uint32
     rng = np.random.default_rng(5)
@@ -262,7 +292,8 @@ def test_cap_key_is_smallest_capped_pattern(L):
     assert L.gspar_check_cap_key(float("nan")) == 0x7F800000
 
 
-def test_device_philox_known_answers(L):
+def test_device_philox_known_answers(LI):
+    L = LI
     u32p = np.ctypeslib.ndpointer(np.uint32, flags="C_CONTIGUOUS")
     L.gspar_check_philox.argtypes = [u32p, u32p, u32p]
     L.gspar_check_philox.restype = None
@@ -277,6 +308,38 @@ def test_device_philox_known_answers(L):
         assert out.tolist() == v[6:10]
         n += 1
     assert n == 3
+
+
+def test_shift_out_of_range_is_flagged(LI):
+    """The exact accumulators' shifts: in range they place v * 2^s exactly; out of range (a broken
+    invariant of the solver) they report the internal flag (16) and give zero, never a clamped
+    shift."""
+    L = LI
+    L.gspar_check_fx_shifted.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.c_uint64 * 5]
+    L.gspar_check_fx_shifted.restype = ctypes.c_uint32
+    L.gspar_check_fq_squares.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int, ctypes.c_uint64 * 10]
+    L.gspar_check_fq_squares.restype = ctypes.c_uint32
+
+    def fx(v, sh):
+        out = (ctypes.c_uint64 * 5)()
+        err = L.gspar_check_fx_shifted(v, sh, out)
+        return err, sum(int(out[i]) << (64 * i) for i in range(5))
+
+    def fq(qh, ql, sh):
+        out = (ctypes.c_uint64 * 10)()
+        err = L.gspar_check_fq_squares(qh, ql, sh, out)
+        return err, sum(int(out[i]) << (64 * i) for i in range(10))
+
+    v = 0xFEDCBA9876543210
+    for sh in (0, 1, 63, 64, 65, 127, 200, 254, 255):
+        assert fx(v, sh) == (0, v << sh), sh
+    for sh in (-1, -64, 256, 300, 1 << 20):
+        assert fx(v, sh) == (16, 0), sh
+    qh, ql = (1 << 55) - 3, (1 << 55) - 5
+    for sh in (0, 1, 100, 254, 255):
+        assert fq(qh, ql, sh) == (0, ((qh << 24) + ql) << (2 * sh)), sh
+    for sh in (-1, 256, 1000):
+        assert fq(qh, ql, sh) == (16, 0), sh
 
 
 def test_no_cpu_fallback_in_binding():

@@ -32,6 +32,10 @@ def test_emulated_hybrid_coding(emu_lib):
     assert runner.check_hybrid(runner.load(emu_lib), verbose=False)
 
 
+def test_emulated_capped_ties(emu_lib):
+    assert runner.check_ties(runner.load(emu_lib), verbose=False)
+
+
 def test_emulated_variance_solver(emu_lib):
     assert runner.check_variance(runner.load(emu_lib), verbose=False)
 
@@ -84,6 +88,9 @@ def test_emulated_lookback_fallback():
     r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "extra_lite"], env=env,
                        capture_output=True, text=True, timeout=1200)
     assert r.returncode == 0 and "extra cases ok" in r.stdout, (r.stdout[-2000:], r.stderr[-2000:])
+    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "ties"], env=env,
+                       capture_output=True, text=True, timeout=1200)
+    assert r.returncode == 0 and "tie cases ok" in r.stdout, (r.stdout[-2000:], r.stderr[-2000:])
 
 
 def test_emulated_two_tiles_per_workgroup():

@@ -9,7 +9,9 @@ batched entry point, inputs resident on the device), for every (solver, rho) eac
 
 Every row is checked element by element against the oracle under the parity rule (index sets
 equal except where |u_i - p_i| <= 1e-6, values to rel 1e-5, lambda to rel 1e-9 and, for the exact
-solver, bit for bit, with the same capped count)."""
+solver, bit for bit, with the same capped count). For c2, c4 and c5 the probabilities entry point
+(Proposition 1's p, written in full) is checked too: every p_i within 1e-6 of the oracle's, the
+capped count equal to the oracle's {p_i = 1}."""
 import sys
 import time
 
@@ -41,23 +43,40 @@ def gs():
 
 
 _cache = {}
+_sols = {}
 
 
 def _workload(name):
     if name not in _cache:
         _cache.clear()  # keep one workload resident at a time (c5 is 1 GiB)
+        _sols.clear()
         t0 = time.perf_counter()
         _cache[name] = W.CONFIGS[name]()
         _say(f"[configs] generated {name} in {time.perf_counter() - t0:.1f} s")
     return _cache[name]
 
 
+def _solution(wl, r, solver, rho):
+    """The oracle's solution of row r, kept while the same (solver, rho) is being checked."""
+    key = (wl.name, r, solver, rho)
+    if key not in _sols:
+        if _sols and next(iter(_sols))[2:] != (solver, rho):
+            _sols.clear()
+        _sols[key] = oracle.solve(wl.g[r], rho, solver, wl.iters)
+    return _sols[key]
+
+
 CASES = [(name, solver, rho) for name in ("c1", "c2", "c3", "c4", "c5")
          for solver in W.CONFIG_SOLVERS[name] for rho in W.CONFIG_RHOS[name]]
+PROB_CASES = [c for c in CASES if c[0] in ("c2", "c4", "c5")]
+ALL = [(n, s_, r, e) for (n, s_, r) in CASES for e in (("compact", "probs") if (n, s_, r) in PROB_CASES else
+                                                      ("compact",))]
 
 
-@pytest.mark.parametrize("name,solver,rho", CASES)
-def test_full_size_parity(gs, name, solver, rho):
+@pytest.mark.parametrize("name,solver,rho,entry", ALL)
+def test_full_size_parity(gs, name, solver, rho, entry):
+    if entry == "probs":
+        return _probs_parity(gs, name, solver, rho)
     wl = _workload(name)
     rows, d = wl.rows, wl.d
     _say(f"[configs] {name} rows={rows} d={d} solver={solver} rho={rho}")
@@ -77,7 +96,7 @@ def test_full_size_parity(gs, name, solver, rho):
     del g
     for r in range(rows):
         t1 = time.perf_counter()
-        sol = oracle.solve(wl.g[r], rho, solver, wl.iters)
+        sol = _solution(wl, r, solver, rho)
         n = int(nnz[r])
         rep = compare_sample(wl.g[r], sol.p, wl.seeds[r], out.idx[r, :n].cpu().numpy(), out.val[r, :n].cpu().numpy(),
                              n, float(lam[r]), sol.lam)
@@ -91,3 +110,38 @@ def test_full_size_parity(gs, name, solver, rho):
         if r == 0 or r == rows - 1:
             _say(f"   row {r}: nnz={n} oracle={rep['nnz_oracle']} excused={rep['excused']} lambda={float(lam[r]):.12g} "
                  f"k={int(k[r])} ({time.perf_counter() - t1:.1f} s oracle)")
+
+
+def _probs_parity(gs, name, solver, rho):
+    """sparsify_probs_batched at full size: p against the oracle's to 1e-6 absolute, lambda (bit for
+    bit for the exact solver), and k = #{p_i = 1}."""
+    wl = _workload(name)
+    rows, d = wl.rows, wl.d
+    _say(f"[configs-probs] {name} rows={rows} d={d} solver={solver} rho={rho}")
+    g = torch.from_numpy(wl.g).cuda()
+    out = gs.sparsify_probs_batched(g, [rho] * rows, solver=solver, iters=wl.iters)
+    torch.cuda.synchronize()
+    fl = out.flags.cpu().numpy()
+    assert not fl.any(), fl
+    lam = out.lam.cpu().numpy()
+    k = out.k.cpu().numpy()
+    del g
+    for r in range(rows):
+        sol = _solution(wl, r, solver, rho)
+        p = out.p[r].cpu().numpy()
+        err = 0.0
+        for c0 in range(0, d, 1 << 24):  # in chunks: the oracle's p is fp64
+            e = np.abs(p[c0:c0 + (1 << 24)].astype(np.float64) - sol.p[c0:c0 + (1 << 24)])
+            err = max(err, float(e.max()))
+        assert err <= 1e-6, (r, err)
+        assert lam_close(float(lam[r]), sol.lam)
+        lp = float(lam[r]) * np.abs(wl.g[r].astype(np.float64))
+        if solver == "exact":
+            assert float(lam[r]) == sol.lam and int(k[r]) == sol.k, (float(lam[r]), sol.lam, int(k[r]), sol.k)
+        else:
+            assert int(k[r]) == int(np.count_nonzero(lp >= 1.0))
+        # p_i = 1 on the capped set; elsewhere only a value within 2^-24 of 1 rounds to 1 in fp32
+        n1 = int(np.count_nonzero(p == 1.0))
+        assert int(k[r]) <= n1 <= int(k[r]) + int(np.count_nonzero((lp >= 1.0 - 2.0 ** -24) & (lp < 1.0)))
+        if r == 0 or r == rows - 1:
+            _say(f"   row {r}: max |p - p_oracle| = {err:.3g} k={int(k[r])} lambda={float(lam[r]):.12g}")

@@ -110,6 +110,54 @@ def test_probs_parity(gs, solver):
         assert int(out.flags.item()) == 0
 
 
+def _tied_boundary(d, n_hi, seed):
+    """+-1 entries with n_hi entries of +-2 and n_hi zeros at seeded positions: at rho = 0.5 the
+    total is 2 B, so Algorithm 2's criterion holds at k = 0 with equality, lambda = 0.5 and the
+    tied run of 2s has p_i = 1 (the capped set)."""
+    rng = np.random.default_rng(seed)
+    g = np.where(rng.random(d) < 0.5, -1.0, 1.0).astype(np.float32)
+    pos = rng.permutation(d)
+    g[pos[:n_hi]] *= 2
+    g[pos[n_hi:2 * n_hi]] = 0
+    return g
+
+
+@pytest.mark.parametrize("d,n_hi", [(40000, 3000), (1000003, 77777), ((1 << 25) + 5, 1 << 20)])
+def test_capped_ties_one_rule(gs, d, n_hi):
+    """Every pass takes the same capped set {p_i = 1}: compaction (whole tiles and the partial last
+    tile; one and two tiles per workgroup), probabilities and the hybrid coding. Closed form:
+    lambda = 0.5, k = n_hi, every 2 kept with value g_i."""
+    g = _tied_boundary(d, n_hi, 17)
+    hi = np.flatnonzero(np.abs(g) == 2)
+    gd = torch.from_numpy(g).cuda()
+    _say(f"[ties] d={d} n_hi={n_hi}")
+    out = gs.sparsify_sample_compact(gd, 0.5, seed=3, solver="exact", capacity=d)
+    h = gs.sparsify_sample_hybrid(gd, 0.5, seed=3, solver="exact", cap_a=d, cap_b=d, dense_q=True)
+    pr = gs.sparsify_probs(gd, 0.5, solver="exact")
+    torch.cuda.synchronize()
+    n = int(out.nnz.item())
+    idx, val = out.idx[:n].cpu().numpy(), out.val[:n].cpu().numpy()
+    assert float(out.lam.item()) == 0.5 and int(out.k.item()) == n_hi and int(out.flags.item()) == 0
+    assert np.all(np.isin(hi, idx)) and np.array_equal(val[np.isin(idx, hi)], g[hi])
+    A, B = int(h.n_a.item()), int(h.n_b.item())
+    assert A == n_hi and A + B == n and int(h.flags.item()) == 0
+    ia = h.idx_a[:A].cpu().numpy()
+    bi = h.code_b[:B].cpu().numpy() & 0x7FFFFFFF
+    assert np.array_equal(ia, hi) and np.all(np.diff(bi) > 0)
+    assert np.array_equal(np.sort(np.concatenate([ia, bi])), idx)
+    q = h.q.cpu().numpy()
+    assert np.array_equal(np.flatnonzero(q == 2), hi)
+    p = pr.p.cpu().numpy()
+    assert int(pr.k.item()) == n_hi and float(pr.lam.item()) == 0.5
+    assert np.all(p[hi] == 1.0) and np.count_nonzero(p == 1.0) == n_hi
+    if d <= 1000003:  # the oracle's sample under the parity rule
+        sol = oracle.solve_exact(g, 0.5)
+        assert sol.lam == 0.5 and sol.k == n_hi
+        compare_sample(g, sol.p, 3, idx, val, n, 0.5, sol.lam)
+        compare_probs(p, sol.p)
+    _say(f"   ok nnz={n}")
+
+
 def test_special_cases(gs):
     d = 50000
     z = np.zeros(d, np.float32)
