@@ -72,7 +72,8 @@ typedef enum {
   GSPAR_OK = 0,
   GSPAR_ERR_ARG = -1,
   GSPAR_ERR_WORKSPACE = -2,
-  GSPAR_ERR_HIP = -3
+  GSPAR_ERR_HIP = -3,
+  GSPAR_ERR_TOO_LARGE = -4 /* the call needs more scratch than the library's fixed array holds */
 } gspar_status;
 
 typedef enum { GSPAR_GREEDY = 0, GSPAR_EXACT = 1, GSPAR_VARIANCE = 2 } gspar_solver;
@@ -230,6 +231,25 @@ int sparsify_probs_segmented(const float* g, int64_t segs, const int64_t* off_ho
  * [1, 2^20], d outside [1, 2^31 - 1] or cap < 0; GSPAR_ERR_HIP if the launch failed. */
 int gspar_aggregate(const int32_t* idx, const float* val, int64_t cap, const int64_t* nnz,
                     int64_t workers, int64_t d, float* v, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): sparsify_sample_compact_batched without the workspace
+ * arguments. The scratch memory the kernels need comes from a fixed array inside the library,
+ * GSPAR_SCRATCH_BYTES on every GPU the library runs on, held until the process ends; the call
+ * allocates nothing (no hipMalloc, no hipFree, no allocating library routine). Its results are
+ * bit-identical to sparsify_sample_compact_batched's for the same arguments.
+ *   Returns GSPAR_ERR_TOO_LARGE, enqueuing nothing, when gspar_workspace_bytes(rows, d, solver)
+ * exceeds GSPAR_SCRATCH_BYTES; GSPAR_ERR_HIP if the array's address cannot be obtained on the
+ * current device; otherwise the errors of sparsify_sample_compact_batched.
+ *   Every call on one GPU uses that GPU's one array, which keeps the last call's contents (each
+ * call clears what it needs cleared): calls that may overlap in time on one GPU race and must be
+ * ordered, for instance on one stream. */
+#define GSPAR_SCRATCH_BYTES ((size_t)32 << 20)
+int sparsify_sample_compact_batched_noalloc(const float* g, int64_t rows, int64_t d, int64_t ld,
+                                            const double* rho, int solver, int greedy_iters,
+                                            const uint64_t* seeds, int32_t* idx, float* val,
+                                            int64_t cap_per_row, int64_t* nnz, double* lambda,
+                                            int64_t* k, uint32_t* flags, void* stream);
 
 /* Human-readable name of a status code (static storage). */
 const char* gspar_status_string(int status);

@@ -42,6 +42,7 @@ OK = 0
 ERR_ARG = -1
 ERR_WORKSPACE = -2
 ERR_HIP = -3
+ERR_TOO_LARGE = -4
 
 INSTR_LIB_PATH = os.path.join(_HERE, "libgspar_instr.so")
 
@@ -83,6 +84,9 @@ def _bind(L):
     L.sparsify_sample_hybrid_segmented.argtypes = [vp, i64, vp, vp, vp, i32, i32, vp, vp, vp, i64, vp, vp, i64,
                                                    vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     L.sparsify_sample_hybrid_segmented.restype = i32
+    L.sparsify_sample_compact_batched_noalloc.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, vp, vp, i64, vp,
+                                                          vp, vp, vp, vp]
+    L.sparsify_sample_compact_batched_noalloc.restype = i32
     L.gspar_aggregate.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
     L.gspar_aggregate.restype = i32
     L.gspar_status_string.argtypes = [i32]
@@ -556,6 +560,26 @@ def sparsify_sample_compact_batched(g, rho, seeds, solver="greedy", iters: int =
                                                _stream(stream))
     _check(rc, "sparsify_sample_compact_batched")
     return Sparse(idx[:, :cap], val[:, :cap], nnz, lam, k, fl)
+
+
+def sparsify_sample_compact_batched_noalloc(g, rho_dev, seeds_dev, idx, val, nnz, lam=None, k=None, flags=None,
+                                            solver="greedy", iters: int = 2, stream=None):
+    """The no-allocation entry point: every argument is a preallocated device tensor (rho_dev
+    [rows] float64, seeds_dev [rows] int64, idx / val [rows, cap], nnz [rows], optional lam, k,
+    flags [rows]); the library uses its own fixed scratch array instead of a workspace and
+    allocates nothing. Returns the status code (OK, or ERR_TOO_LARGE when the call does not fit
+    the array)."""
+    g = _as_rows(g)
+    rows, d = g.shape
+    cap = idx.shape[1]
+    if val.shape != idx.shape or idx.dtype != torch.int32 or val.dtype != torch.float32:
+        raise ValueError("idx / val must be [rows, cap] int32 / float32")
+    if rho_dev.dtype != torch.float64 or seeds_dev.dtype != torch.int64:
+        raise ValueError("rho_dev must be float64 and seeds_dev int64 device tensors")
+    return int(lib().sparsify_sample_compact_batched_noalloc(
+        g.data_ptr(), rows, d, _leading_dim(g), rho_dev.data_ptr(), _solver_id(solver), int(iters),
+        seeds_dev.data_ptr(), idx.data_ptr(), val.data_ptr(), cap, nnz.data_ptr(), _ptr(lam), _ptr(k), _ptr(flags),
+        _stream(stream)))
 
 
 class Segments:

@@ -32,6 +32,7 @@
 
 #include <climits>
 #include <algorithm>
+#include <mutex>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -2838,6 +2839,28 @@ __global__ void __launch_bounds__(kAggThreads) k_aggregate(AggArgs a) {
     if (b0 + i < a.d) a.v[b0 + i] = (float)(acc[i] / M);
 }
 
+// Scratch memory of the no-allocation entry point: one fixed array per GPU, in the code object's
+// device memory. Host code never passes the name `scratch` to a kernel (on the host it is only a
+// stand-in for the symbol): the array's device address is looked up once per device and kept.
+static __device__ __align__(256) unsigned char scratch[GSPAR_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static void* g_scratch_ptr[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+// Device address of the current device's scratch array (nullptr if it cannot be obtained).
+static void* scratch_of_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace gspar
 
 using namespace gspar;
@@ -3016,6 +3039,18 @@ int sparsify_sample_compact_batched(const float* g, int64_t rows, int64_t d, int
   return run_sample(a, (hipStream_t)stream);
 }
 
+int sparsify_sample_compact_batched_noalloc(const float* g, int64_t rows, int64_t d, int64_t ld, const double* rho,
+                                            int solver, int greedy_iters, const uint64_t* seeds, int32_t* idx,
+                                            float* val, int64_t cap_per_row, int64_t* nnz, double* lambda, int64_t* k,
+                                            uint32_t* flags, void* stream) {
+  if (rows < 1 || d < 1) return GSPAR_ERR_ARG;
+  if (layout_of(rows, d).total > GSPAR_SCRATCH_BYTES) return GSPAR_ERR_TOO_LARGE;
+  void* ws = scratch_of_current_device();
+  if (!ws) return GSPAR_ERR_HIP;
+  return sparsify_sample_compact_batched(g, rows, d, ld, rho, solver, greedy_iters, seeds, idx, val, cap_per_row,
+                                         nnz, lambda, k, flags, ws, GSPAR_SCRATCH_BYTES, stream);
+}
+
 // Host check of segment offsets (off[0] >= 0, nondecreasing, every length below 2^31): the longest
 // length (at least 1, the row length the workspace is sized for), the total length, and whether
 // vector loads may be used (g 16-byte aligned and every start a multiple of 4).
@@ -3157,6 +3192,7 @@ const char* gspar_status_string(int status) {
     case GSPAR_ERR_ARG: return "invalid argument";
     case GSPAR_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case GSPAR_ERR_HIP: return "HIP launch failed";
+    case GSPAR_ERR_TOO_LARGE: return "problem too large for the library's fixed scratch array";
     default: return "unknown status";
   }
 }
