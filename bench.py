@@ -112,7 +112,8 @@ def _pmc_rows(path):
 
 
 def _kernel_class(name: str):
-    for k in ("k_probs_out", "k_sample", "k_stats", "k_refine", "k_solve", "k_init", "k_probs", "k_aggregate"):
+    for k in ("k_probs_out", "k_presample", "k_sample", "k_stats", "k_refine", "k_solve", "k_init", "k_probs",
+              "k_aggregate"):
         if "gspar::" + k + "<" in name or "gspar::" + k + "(" in name:
             return k
     if "copyBuffer" in name:  # the runtime's device-to-device copy kernel (the probe)

@@ -18,8 +18,9 @@ extern "C" {
 
 /* Kernel classes reported by gspar_prof_read, in this order (GSPAR_PROF_CLASSES of them):
  * 0 sampling / compaction, 1 statistics pass, 2 probabilities, 3 solver, 4 refinement pass,
- * 5 workspace initialisation, 6 aggregation, 7 per-row outputs of the probabilities calls. */
-#define GSPAR_PROF_CLASSES 8
+ * 5 workspace initialisation, 6 aggregation, 7 per-row outputs of the probabilities calls,
+ * 8 row sample for the candidate band. */
+#define GSPAR_PROF_CLASSES 9
 
 /* Arms the launch timer: each of the next `max_launches` kernel launches (any entry point, any
  * stream) is made with hipExtLaunchKernelGGL and a pair of HIP events that the dispatch itself

@@ -111,7 +111,8 @@ def lib():
     return _lib
 
 
-PROF_CLASSES = ("k_sample", "k_stats", "k_probs", "k_solve", "k_refine", "k_init", "k_aggregate", "k_probs_out")
+PROF_CLASSES = ("k_sample", "k_stats", "k_probs", "k_solve", "k_refine", "k_init", "k_aggregate", "k_probs_out",
+                "k_presample")
 
 
 def instr_lib():

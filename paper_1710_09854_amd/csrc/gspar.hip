@@ -345,15 +345,22 @@ struct alignas(256) RowCtl {
   uint32_t need;     // 0: none; 2 / 3: a level-2 / level-3 pass is requested
   uint32_t done;     // 1 once lambda and tcap are final
   uint32_t qkey;     // greedy: key whose count and sum above the level-2 pass also counts directly
-  uint32_t spare2;
+  uint32_t src;      // 1: the requested window lies in the candidate band, its pass reads the candidates
   uint32_t l2exp;    // binade of the level-2 window (kNone: none)
   uint32_t l3base;   // first key of the level-3 window (kNone: none)
   int32_t iter;      // greedy rescale steps taken
   int32_t stage;     // 0 before the first solve; exact solver: next level to examine
   int32_t solver;
   int32_t T;
+  uint32_t band_lo;  // candidate band [band_lo, band_hi) of keys (whole binades) the statistics pass
+  uint32_t band_hi;  // collected, written by its first workgroup (equal bounds: no band)
+  uint64_t cand_n;   // candidates collected (first solve; above the capacity: incomplete, unused)
 };
 static_assert(sizeof(RowCtl) == 256, "RowCtl layout");
+// offsets read by the tests to see which source a refinement pass used
+static_assert(offsetof(RowCtl, src) == 192 && offsetof(RowCtl, band_lo) == 220 && offsetof(RowCtl, band_hi) == 224 &&
+                  offsetof(RowCtl, cand_n) == 232,
+              "RowCtl offsets known to the tests");
 
 struct Hist1 {
   uint64_t cnt[kB1];
@@ -405,18 +412,63 @@ struct alignas(128) CountLine {
   unsigned long long pad[15];
 };
 
+// Per-row histogram over binades of a systematic sample of the row (count and significand sum),
+// from which every statistics workgroup predicts the band of keys the solvers will refine.
+struct PreHist {
+  uint64_t cnt[kB1];
+  uint64_t sig[kB1];
+};
+
 GS_HD size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctl, h1, l1t, win, kc, status, bmap, tmap, h1q, winq, vctl, total;
-  int64_t tiles;  // tiles per row of the sample pass
+  size_t ctl, h1, l1t, win, kc, status, bmap, tmap, h1q, winq, vctl, pre, ccnt, cand, total;
+  int64_t tiles;     // tiles per row of the sample pass
+  int64_t cand_cap;  // candidate keys per row (0: no candidate band)
 };
 
 constexpr int64_t kMinChunk = 8192;  // fewest coordinates per histogram workgroup (but the row's)
 
+// Candidate band: rows of at least kCandMinRow coordinates predict, from a sample of the row, the
+// binades holding every threshold the solvers will refine, and the statistics pass copies the keys
+// inside them to a per-row buffer, so refinement passes read those keys instead of the row.
+// (a build may lower the row-length threshold to exercise the band on small inputs)
+#ifndef GSPAR_CAND_MIN_ROW
+#define GSPAR_CAND_MIN_ROW (1 << 22)
+#endif
+constexpr int64_t kCandMinRow = GSPAR_CAND_MIN_ROW;
+static_assert(kCandMinRow >= 1024, "a row must hold at least 64 whole lines to be sampled");
+constexpr int kPreWG = 64;              // sample workgroups per row
+#ifndef GSPAR_PRE_LINES
+#define GSPAR_PRE_LINES 256
+#endif
+constexpr int kPreLines = GSPAR_PRE_LINES;  // 64-byte lines sampled per workgroup (16384 per row)
+// Lines of a row of length len that the sample reads: every line when the row has fewer.
+GS_HD int64_t pre_lines(int64_t len) {
+  const int64_t nl = len / 16, ns = (int64_t)kPreWG * kPreLines;
+  return nl < ns ? nl : ns;
+}
+// Refinement over candidates: at least kCandShare keys per workgroup (each workgroup adds its whole
+// window into the global copies, so fewer, fuller workgroups cost fewer global atomics), read
+// kCandLoads float4 per thread at a time.
+constexpr int64_t kCandShare = 1 << 14;
+constexpr int kCandLoads = 8;
+// keys a wave buffers in LDS (flushed above kCandWave - 256); sized so that the statistics
+// workgroup stays within a quarter of the LDS (four resident per compute unit)
+constexpr int kCandWave = 496;
+// Candidate capacity per row a full workspace provides.
+GS_HD int64_t cand_cap_full(int64_t d) {
+  if (d < kCandMinRow) return 0;
+  int64_t c = d / 16;
+  if (c < ((int64_t)1 << 20)) c = (int64_t)1 << 20;
+  return (c < d ? c : d) & ~(int64_t)63;  // whole 256-byte blocks
+}
+
 // Histogram copies: row r's copy c of level 1 is h1 + (r * kC1 + c), of a refinement window
 // win + (r * kC23 + c); the solve that requests a refinement pass clears the window's copies.
-GS_HD Layout layout_of(int64_t rows, int64_t d) {
+// cand_cap: candidate keys per row (the workspace ends with the candidate buffers, so a smaller
+// capacity changes no other offset).
+GS_HD Layout layout_of(int64_t rows, int64_t d, int64_t cand_cap) {
   Layout L;
   L.tiles = (d + kTileElems - 1) / kTileElems;
   size_t off = 256;  // header (reserved)
@@ -445,6 +497,14 @@ GS_HD Layout layout_of(int64_t rows, int64_t d) {
   off += align256((size_t)rows * kC23 * sizeof(WinQ));
   L.vctl = off;
   off += align256((size_t)rows * sizeof(VarCtl));
+  // candidate band
+  L.pre = off;
+  off += align256((size_t)rows * sizeof(PreHist));
+  L.ccnt = off;  // per row: keys collected (reserved in the compact list)
+  off += align256((size_t)rows * sizeof(CountLine));
+  L.cand = off;  // per row: the compact candidate list, then the statistics workgroups' regions
+  L.cand_cap = cand_cap;
+  off += align256((size_t)rows * (size_t)cand_cap * 2 * sizeof(uint32_t));
   L.total = off;
   return L;
 }
@@ -485,6 +545,8 @@ struct Args {
   int64_t seg_wgs;    // sample-pass workgroups (the grid), from the host offsets
   int seg_k;          // tiles per sample workgroup
   int seg_align;      // vector loads in use: every segment must start at a multiple of 4
+  size_t ws_bytes;    // the workspace's size (the candidate buffers take what the rest leaves)
+  int64_t cand_region;  // candidate keys per statistics workgroup (cand_cap / nb, a multiple of 64)
 };
 
 // Start and length of row r: row r of a strided batch (offset r * ld, length d), or segment r of a
@@ -537,6 +599,19 @@ __device__ __forceinline__ CountLine* kc_of(const Args& a, int64_t r) {
 __device__ __forceinline__ uint64_t* status_of(const Args& a) {
   return reinterpret_cast<uint64_t*>(a.ws + a.lay.status);
 }
+__device__ __forceinline__ PreHist* pre_of(const Args& a, int64_t r) {
+  return reinterpret_cast<PreHist*>(a.ws + a.lay.pre) + r;
+}
+// Candidates of row r: the compact list (cand_cap keys), then the staging regions, where statistics
+// workgroup b collects into keys [b * cand_region, (b + 1) * cand_region) before moving them to
+// the list; the row's count line holds the keys reserved in the list.
+__device__ __forceinline__ CountLine* ccnt_of(const Args& a, int64_t r) {
+  return reinterpret_cast<CountLine*>(a.ws + a.lay.ccnt) + r;
+}
+__device__ __forceinline__ uint32_t* cand_of(const Args& a, int64_t r) {
+  return reinterpret_cast<uint32_t*>(a.ws + a.lay.cand) + r * a.lay.cand_cap * 2;
+}
+__device__ __forceinline__ uint32_t* creg_of(const Args& a, int64_t r) { return cand_of(a, r) + a.lay.cand_cap; }
 
 
 
@@ -565,8 +640,9 @@ __device__ __forceinline__ uint32_t load4(const float* __restrict__ row, int64_t
 // With vector loads, blocks of U groups per thread are loaded unconditionally, all issued before
 // any group is processed, so U loads per thread stay in flight; the last block clamps its addresses
 // to the last whole group and masks the values, and a trailing partial group is loaded by one
-// thread with scalar loads. No memory access sits under a divergent branch, which would make the
-// compiler wait for every outstanding load.
+// thread with scalar loads and visited by the whole first wave. No memory access sits under a
+// divergent branch, which would make the compiler wait for every outstanding load. With vector
+// loads every call of f is made by whole waves, so f may use cross-lane operations.
 template <bool VEC, int U, int NT, typename F>
 __device__ __forceinline__ void stream_groups(const float* __restrict__ row, int64_t beg, int64_t end, F&& f) {
   if (!VEC) {
@@ -606,9 +682,12 @@ __device__ __forceinline__ void stream_groups(const float* __restrict__ row, int
       f(q, v, ok ? 0xFu : 0u);
     }
   }
-  if (4 * qfull < end && threadIdx.x == 0) {
-    float v[4];
-    const uint32_t m = load4<false>(row, qfull, end, v);
+  if (4 * qfull < end && threadIdx.x < 64) {
+    // the last, partial group: visited by the whole first wave (its other lanes see no
+    // coordinates), so a visitor may use cross-lane operations
+    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    uint32_t m = 0;
+    if (threadIdx.x == 0) m = load4<false>(row, qfull, end, v);
     f(qfull, v, m);
   }
 }
@@ -694,6 +773,8 @@ struct Hists {
   const H1Q* h1q;      // variance-budget solver: square sums of the level-1 copies
   WinQ* wq;            // and of the level-2 window copies
   VarCtl* vc;          // and its per-row state
+  const CountLine* cc; // keys collected in the row's candidate band
+  int64_t cand_cap;    // the candidate list's capacity (0: no band)
 };
 
 GS_DI int block_max(SolveLds& s, int v) {
@@ -941,6 +1022,10 @@ GS_DI void sv_request(RowCtl& c, const Hists& H, int level, uint32_t E, uint32_t
     c.wK = wK;
     c.wW = wW;
   }
+  // a window inside the candidate band (whole binades) holds only collected keys: its pass reads
+  // the candidates instead of the row
+  const uint32_t e = level == 2 ? E : (base >> 23);
+  c.src = (c.band_hi > c.band_lo && (e << 23) >= c.band_lo && ((e + 1) << 23) <= c.band_hi) ? 1u : 0u;
 }
 
 // Count and significand sum of the level-2 window's keys in bins above sb, summed straight from the
@@ -1321,7 +1406,7 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
   {
     const double Sd = fx_to_double(c.S), A2d = fq_to_double(A2);
     const double Wawd = fx_to_double(L.Waw), Hawd = fq_to_double(Haw);
-    uint64_t K = eK, Sg = eS, QH = eQH, QL = eQL;
+    uint64_t Sg = eS, QH = eQH, QL = eQL;
 #pragma unroll 1
     for (int j = per - 1; j >= 0; --j) {
       const int b = b0 + j;
@@ -1346,7 +1431,6 @@ GS_DI void v_level(SolveLds& s, const RowCtl& c, const Hists& H, const Lvl& L, b
           break;
         }
       }
-      K += cnt;
       Sg += (uint64_t)L.sig[b];
       QH += qh;
       QL += ql;
@@ -1510,20 +1594,41 @@ GS_DI void sv_start(SolveLds& s, RowCtl& c, const Hists& H, int64_t d) {
 }
 
 // Sums the global copies of a histogram (filled with atomics by an earlier kernel on the same
-// stream) into an LDS cache.
-template <typename HistT, typename CntT>
-GS_DI void reduce_into(const HistT* h, int copies, int nbins, CntT* cnt, uint64_t* sig, uint32_t* mx) {
-  for (int b = threadIdx.x; b < nbins; b += kNT) {
-    uint64_t c = 0, sg = 0;
-    uint32_t m = 0;
-    for (int k = 0; k < copies; ++k) {
-      c += h[k].cnt[b];
-      sg += h[k].sig[b];
-      m = max(m, h[k].mx[b]);
+// stream) into an LDS cache. Every load of a thread is issued before the first sum, so the whole
+// reduction costs one round trip to memory.
+template <int COPIES, int NBINS, typename HistT, typename CntT>
+GS_DI void reduce_into(const HistT* h, CntT* cnt, uint64_t* sig, uint32_t* mx) {
+  static_assert(NBINS % kNT == 0 || NBINS < kNT, "bins per thread");
+  constexpr int kPer = NBINS < kNT ? 1 : NBINS / kNT;
+  uint64_t c[kPer][COPIES], g[kPer][COPIES];
+  uint32_t m[kPer][COPIES];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int b = threadIdx.x + j * kNT;
+#pragma unroll
+    for (int k = 0; k < COPIES; ++k) {
+      const bool ok = b < NBINS;
+      c[j][k] = ok ? h[k].cnt[b] : 0;
+      g[j][k] = ok ? h[k].sig[b] : 0;
+      m[j][k] = ok ? h[k].mx[b] : 0;
     }
-    cnt[b] = (CntT)c;
-    sig[b] = sg;
-    mx[b] = m;
+  }
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int b = threadIdx.x + j * kNT;
+    uint64_t cs = 0, gs = 0;
+    uint32_t ms = 0;
+#pragma unroll
+    for (int k = 0; k < COPIES; ++k) {
+      cs += c[j][k];
+      gs += g[j][k];
+      ms = max(ms, m[j][k]);
+    }
+    if (b < NBINS) {
+      cnt[b] = (CntT)cs;
+      sig[b] = gs;
+      mx[b] = ms;
+    }
   }
 }
 
@@ -1543,7 +1648,15 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d, bool fi
   uint4 tab[per16];
   uint64_t qcnt = 0, qsig = 0;
   if (first) {
-    reduce_into(H.h1g, kC1, kB1, H.l1->cnt, H.l1->sig, H.l1->mx);
+    reduce_into<kC1, kB1>(H.h1g, H.l1->cnt, H.l1->sig, H.l1->mx);
+    // the candidate band is usable only if every key in it was kept (a statistics workgroup whose
+    // region overflowed reserves more than the list holds)
+    if (H.cand_cap) {
+      c.cand_n = H.cc->v;
+      if (c.cand_n > (uint64_t)H.cand_cap) c.band_lo = c.band_hi = 0;
+    } else {
+      c.band_lo = c.band_hi = 0;
+    }
   } else {
     if (c.done) return;
     const uint4* src = reinterpret_cast<const uint4*>(H.l1g);
@@ -1570,8 +1683,8 @@ GS_DI void solve_row(SolveLds& s, RowCtl* gc, const Hists& H, int64_t d, bool fi
   // for the exact solver the level-2 / level-3 window the last pass filled (for the greedy solver
   // the bins of a level-2 window are read only if a query needs them)
   if (c.solver != GSPAR_GREEDY) {
-    if (c.stage == 2) reduce_into(H.wg, kC23, kB2, H.w2->cnt, H.w2->sig, H.w2->mx);
-    if (c.stage == 3) reduce_into(H.wg, kC23, kB3, H.w3->cnt, H.w3->sig, H.w3->mx);
+    if (c.stage == 2) reduce_into<kC23, kB2>(H.wg, H.w2->cnt, H.w2->sig, H.w2->mx);
+    if (c.stage == 3) reduce_into<kC23, kB3>(H.wg, H.w3->cnt, H.w3->sig, H.w3->mx);
   }
   c.need = 0;
   if (threadIdx.x == 0) s.err = 0;
@@ -1698,6 +1811,12 @@ __global__ void __launch_bounds__(256) k_init(Args a) {
     const int64_t nq = a.rows * kC1 * (int64_t)(sizeof(H1Q) / 8);
     for (int64_t i = tid; i < nq; i += stride) q[i] = 0;
   }
+  if (a.lay.cand_cap) {
+    // sample histograms and candidate count lines (adjacent in the layout)
+    uint64_t* pc = reinterpret_cast<uint64_t*>(a.ws + a.lay.pre);
+    const int64_t np = (int64_t)((a.lay.cand - a.lay.pre) / 8);
+    for (int64_t i = tid; i < np; i += stride) pc[i] = 0;
+  }
   for (int64_t r = tid; r < a.rows; r += stride) {
     RowCtl c;
     memset(&c, 0, sizeof(c));
@@ -1737,20 +1856,231 @@ __device__ __forceinline__ bool hist_block(const Args& a, int64_t& row, int64_t&
   return true;
 }
 
+// A global-memory pointer every lane holds equally, moved to scalar registers (on the device:
+// in the global address space, so stores take a scalar base and a 32-bit vector offset).
+#if defined(__HIP_DEVICE_COMPILE__)
+typedef __attribute__((address_space(1))) char gchar;
+#define GS_GLOBAL(T) T __attribute__((address_space(1)))
+__device__ __forceinline__ gchar* uniform_ptr(void* p) {
+  const uint64_t u = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (gchar*)(((uint64_t)hi << 32) | lo);
+}
+#else
+typedef char gchar;
+#define GS_GLOBAL(T) T
+GS_HD gchar* uniform_ptr(void* p) { return static_cast<gchar*>(p); }
+#endif
+
+// popcount(m & bits of the lanes below this one)
+__device__ __forceinline__ uint32_t lanes_below(unsigned long long m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+// Exclusive prefix over the lanes of a wave of x in [0, 2^B) from B ballots; `total` receives the
+// wave's sum.
+template <int B>
+__device__ __forceinline__ uint32_t wave_prefix_bits(uint32_t x, uint32_t& total) {
+  uint32_t pre = 0;
+  total = 0;
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    const unsigned long long m = __ballot((x >> b) & 1);
+    pre += lanes_below(m) << b;
+    total += (uint32_t)__popcll(m) << b;
+  }
+  return pre;
+}
+
+// Systematic sample of each row for the candidate band: kPreWG workgroups per row each read
+// kPreLines of the row's whole 64-byte lines, spread evenly over the row, and add a histogram over
+// binades (count, significand sum) into the row's PreHist. Every load is issued before any is used.
+__global__ void __launch_bounds__(256) k_presample(Args a) {
+  static_assert(kB1 == 256 && kPreLines % 64 == 0, "one binade per thread, 64 lines per round");
+  constexpr int kRounds = kPreLines / 64;
+  constexpr int kCopies = 4;  // LDS copies by lane, to spread same-bin atomics
+  __shared__ uint32_t s_cnt[kB1 * kCopies];
+  __shared__ unsigned long long s_sig[kB1 * kCopies];
+  const int64_t row = blockIdx.x / kPreWG;
+  const int p = (int)(blockIdx.x % kPreWG);
+  const int t = threadIdx.x;
+  for (int i = t; i < kB1 * kCopies; i += 256) {
+    s_cnt[i] = 0;
+    s_sig[i] = 0;
+  }
+  __syncthreads();
+  const float* __restrict__ gr = a.g + row * a.ld;
+  const int64_t nl = a.d / 16;         // whole lines of the row
+  const int64_t ns = pre_lines(a.d);   // lines sampled (ns <= nl)
+  float4 x[kRounds];
+#pragma unroll
+  for (int j = 0; j < kRounds; ++j) {
+    const int64_t i = (int64_t)p * kPreLines + j * 64 + (t >> 2);  // sample index
+    const int64_t line = (i < ns ? i : ns - 1) * nl / ns;             // < nl
+    x[j] = *reinterpret_cast<const float4*>(gr + 16 * line + 4 * (t & 3));
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  const int lc = t & (kCopies - 1);
+#pragma unroll
+  for (int j = 0; j < kRounds; ++j) {
+    const int64_t i = (int64_t)p * kPreLines + j * 64 + (t >> 2);
+    if (i >= ns) continue;  // past the sample (rows with fewer lines than a full sample)
+    const float v[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[c]);
+      if (key != 0) {
+        const uint32_t b = (key >> 23) * kCopies + lc;
+        atomicAdd(&s_cnt[b], 1u);
+        atomicAdd(&s_sig[b], (unsigned long long)key_sig(key));
+      }
+    }
+  }
+  __syncthreads();
+  uint64_t cnt = 0, sg = 0;
+#pragma unroll
+  for (int k = 0; k < kCopies; ++k) {
+    cnt += s_cnt[t * kCopies + k];
+    sg += s_sig[t * kCopies + k];
+  }
+  if (cnt) {
+    PreHist* h = pre_of(a, row);
+    atomicAdd((unsigned long long*)&h->cnt[t], (unsigned long long)cnt);
+    atomicAdd((unsigned long long*)&h->sig[t], (unsigned long long)sg);
+  }
+}
+
+// LDS of the band prediction.
+struct BandLds {
+  double w[kNT / 64];
+  uint64_t k[kNT / 64];
+  int ired[kNT / 64];
+};
+
+// The candidate band of a row, predicted from its sample histogram identically by every
+// workgroup of the statistics pass (same data, same order of operations). With f = the row's
+// length over the sampled count, the sums are scaled sample sums. Every threshold a solver will
+// refine lies in [1/lambda*, 1/lambda_0]: 1/lambda_0 = S / B (Algorithm 3's start), and the exact
+// 1/lambda* is where G(tau) = #{a >= tau} + (sum of the a < tau) / tau falls to B (Proposition 1:
+// sum min(lambda a, 1) = B); G decreases in tau, so at binade edges its crossing gives the binade
+// of 1/lambda*. The band runs from the binade below that one to the binade holding 1.25 S / B, in
+// whole binades, so every refinement window inside it is complete. No band when B = 0 or nothing
+// was sampled. Threads 0..255 own one binade each; every thread receives the result.
+GS_DI void cand_band(const Args& a, const PreHist* ph, double B, int64_t len, BandLds& sm, uint32_t& blo,
+                     uint32_t& bhi) {
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  uint64_t c = 0;
+  double w = 0.0;
+  if (t < kB1) {
+    c = ph->cnt[t];
+    w = c ? ldexp((double)ph->sig[t], binade_shift(t) - 149) : 0.0;
+  }
+  // inclusive suffix sums over binades (count and value sum of the binades >= t)
+  uint64_t kc = c;
+  double wc = w;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t ky = __shfl_down(kc, (unsigned)o);
+    const double wy = __shfl_down(wc, (unsigned)o);
+    if (lane + o < 64) {
+      kc += ky;
+      wc += wy;
+    }
+  }
+  if (lane == 0) {
+    sm.k[wv] = kc;
+    sm.w[wv] = wc;
+  }
+  __syncthreads();
+  double tot = 0.0;
+  for (int i = 0; i < kB1 / 64; ++i) tot += sm.w[i];
+  for (int i = wv + 1; i < kB1 / 64; ++i) {
+    kc += sm.k[i];
+    wc += sm.w[i];
+  }
+  const double f = (double)len / (16.0 * (double)pre_lines(len));
+  // the highest occupied binade of the sample
+  int top = (t < kB1 - 1 && c) ? t : -1;
+  for (int o = 32; o > 0; o >>= 1) top = max(top, __shfl_xor(top, o));
+  if (lane == 0) sm.ired[wv] = top;
+  __syncthreads();
+  top = -1;
+  for (int i = 0; i < kNT / 64; ++i) top = max(top, sm.ired[i]);
+  __syncthreads();
+  int best = -1;
+  if (t >= 1 && t < kB1 - 1 && B > 0.0 && tot > 0.0) {
+    // G at the binade's lower edge lo = 2^(t - 127): keys >= lo count whole, the rest by value / lo
+    const double lo = ldexp(1.0, t - 127);
+    const double G = f * ((double)kc + (tot - wc) / lo);
+    if (G >= B) best = t;
+  }
+  for (int o = 32; o > 0; o >>= 1) best = max(best, __shfl_xor(best, o));
+  if (lane == 0) sm.ired[wv] = best;
+  __syncthreads();
+  int e = -1;
+  for (int i = 0; i < kNT / 64; ++i) e = max(e, sm.ired[i]);
+  blo = bhi = 0;
+  // Nothing looks capped (B times the sample's largest magnitude, bounded by its binade's top,
+  // below half the estimated sum): the solvers should need no window, so no band is collected (a
+  // row the sample misjudged refines over the row).
+  const bool uncapped = top >= 0 && B * ldexp(1.0, top - 126) <= 0.5 * f * tot;
+  if (e >= 1 && B > 0.0 && tot > 0.0 && !uncapped) {
+    const double t0 = 1.25 * f * tot / B;
+    const uint32_t ehi = t0 < 3.0e38 ? (key_of((float)t0) >> 23) : 254u;
+    const uint32_t elo = (uint32_t)(e - 1);
+    blo = elo << 23;
+    bhi = ((ehi > elo ? ehi : elo) + 1) << 23;
+    if (bhi > kKeyInf) bhi = kKeyInf;
+  }
+  __syncthreads();
+}
+
 // Streaming statistics pass. Grid: rows * nb workgroups of kNT threads. Each builds an LDS
 // histogram over binades (count, exact significand sum, maximum key), kept in kLaneCopies copies
 // by lane to spread same-address LDS atomics, and adds its nonempty bins into one of the row's kC1
 // global copies (chosen by workgroup index) with atomics. k_solve runs next.
-template <bool VEC, bool SQ>
+template <bool VEC, bool SQ, bool CAND>
 __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k_stats(Args a) {
+  static_assert(VEC || !CAND, "candidates are collected with whole waves (vector loads)");
   __shared__ StatsLdsT<SQ> sm_st;
   StatsLdsT<SQ>& sm = sm_st;
+  __shared__ BandLds s_band;
+  // candidate band: per-wave buffers of collected keys, and the workgroup's region count
+  __shared__ uint32_t s_cand[CAND ? kNT / 64 : 1][CAND ? kCandWave : 1];
+  __shared__ uint32_t s_rcnt;
+  __shared__ unsigned long long s_rbase;
   int64_t row, blk;
   if (!hist_block(a, row, blk)) return;
   int64_t base, len;
   row_span(a, row, base, len);
   const int64_t beg = blk * a.chunk;
   if (beg >= len) return;  // past the end of a shorter segment
+  uint32_t blo = 0, bhi = 0;
+  if constexpr (CAND) {
+    cand_band(a, pre_of(a, row), ctl_of(a, row)->B, len, s_band, blo, bhi);
+    if (blk == 0 && threadIdx.x == 0) {
+      RowCtl* c = ctl_of(a, row);
+      c->band_lo = blo;
+      c->band_hi = bhi;
+    }
+  }
+  const uint32_t bspan = bhi - blo;
+  const int lane = threadIdx.x & 63;
+  // Collected keys are buffered per wave in LDS (a group's keys placed by a wave prefix) and
+  // flushed into this workgroup's own region of the row's candidate buffer, at a place taken from
+  // an LDS counter; keys that would pass the region's end are dropped and the region is marked
+  // overflowed, so the first solve does not use the band. wcnt is the same in every lane.
+  uint32_t* const wbuf = s_cand[CAND ? threadIdx.x >> 6 : 0];
+  uint32_t wcnt = 0;
+  if (CAND && threadIdx.x == 0) s_rcnt = 0;
+  auto flush = [&]() {
+    uint32_t b0 = 0;
+    if (lane == 0) b0 = atomicAdd(&s_rcnt, wcnt);
+    const uint32_t b = (uint32_t)__shfl((int)b0, 0);
+    uint32_t* __restrict__ dst = creg_of(a, row) + blk * a.cand_region;
+    for (uint32_t j = lane; j < wcnt; j += 64)
+      if ((int64_t)b + j < a.cand_region) dst[b + j] = wbuf[j];
+    wcnt = 0;
+  };
   for (int b = threadIdx.x; b < kB1 * kLaneCopies; b += kNT) {
     sm.pk[b] = 0;
     sm.mx[b] = 0;
@@ -1763,7 +2093,7 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   const float* __restrict__ gr = a.g + base;
   const int64_t end = min(len, beg + a.chunk);
   const uint32_t lc = threadIdx.x & (kLaneCopies - 1);
-  stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) {
+  auto hist = [&](const float v[4]) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const uint32_t key = key_of(v[c]);  // coordinates outside [beg, end) read as 0 and are skipped
@@ -1779,7 +2109,55 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
         }
       }
     }
-  });
+  };
+  // the candidate band's keys of a group into the wave's buffer
+  auto collect = [&](const float v[4]) {
+    uint32_t cm = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[c]);
+      cm |= (uint32_t)(key - blo < bspan && key != 0) << c;
+    }
+    if (__ballot(cm != 0)) {
+      uint32_t tot;
+      uint32_t pos = wcnt + wave_prefix_bits<3>((uint32_t)__popc(cm), tot);
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if ((cm >> c) & 1) wbuf[pos++] = key_of(v[c]);
+      wcnt += tot;
+      // at most 256 keys arrive per group
+      if (wcnt > (uint32_t)(kCandWave - 256)) flush();
+    }
+  };
+  if (CAND && bspan != 0) {
+    stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) {
+      hist(v);
+      collect(v);
+    });
+  } else {
+    // no band (or none predicted for this row): the plain statistics loop
+    stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) { hist(v); });
+  }
+  if constexpr (CAND) {
+    if (wcnt) flush();
+    __syncthreads();
+    // move the region to the row's compact list: one reservation per workgroup (a region that
+    // overflowed reserves past the list's capacity, which disables the band)
+    if (bspan != 0) {
+      const uint32_t n = s_rcnt;
+      if (threadIdx.x == 0) {
+        const unsigned long long want = (int64_t)n <= a.cand_region ? n : (unsigned long long)a.lay.cand_cap + 1;
+        s_rbase = want ? atomicAdd(&ccnt_of(a, row)->v, want) : 0ull;
+      }
+      __syncthreads();
+      const uint64_t b = s_rbase;
+      if ((int64_t)n <= a.cand_region && b + n <= (uint64_t)a.lay.cand_cap) {
+        const uint32_t* __restrict__ src = creg_of(a, row) + blk * a.cand_region;
+        uint32_t* __restrict__ out = cand_of(a, row) + b;
+        for (uint32_t j = threadIdx.x; j < n; j += kNT) out[j] = src[j];
+      }
+    }
+  }
   __syncthreads();
   // flush one binade per thread into copy (blk mod kC1)
   if (threadIdx.x < kB1) {
@@ -1825,8 +2203,20 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   if (need != 2 && need != 3) return;
   int64_t base, len;
   row_span(a, row, base, len);
-  const int64_t beg = blk * a.chunk;
-  if (beg >= len) return;  // past the end of a shorter segment
+  const float* __restrict__ gr = a.g + base;
+  int64_t beg = blk * a.chunk, end = min(len, beg + a.chunk);
+  // the window lies in the candidate band: the row's collected keys, read as the non-negative
+  // floats they are, in equal shares (whole groups of 4, at least kCandShare keys) by the first of
+  // the row's workgroups
+  const bool from_cand = ctl->src != 0;
+  if (from_cand) {
+    const int64_t n = (int64_t)ctl->cand_n;
+    const int64_t share = max(kCandShare, (((n + a.nb - 1) / a.nb) + 3) & ~(int64_t)3);
+    beg = blk * share;
+    end = min(n, beg + share);
+    gr = reinterpret_cast<const float*>(cand_of(a, row));
+  }
+  if (beg >= end) return;  // past the end of a shorter segment, or of the candidates
   uint32_t lo, shift;
   int nbins;
   const int cp = (int)(blk % kC23);
@@ -1858,10 +2248,8 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
     }
   }
   __syncthreads();
-  const float* __restrict__ gr = a.g + base;
-  const int64_t end = min(len, beg + a.chunk);
   uint64_t qc = 0, qs = 0;
-  stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) {
+  auto visit = [&](int64_t, const float v[4], uint32_t) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const uint32_t key = key_of(v[c]);
@@ -1870,8 +2258,12 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
         const uint32_t b = rel >> shift;
         const uint64_t sg = key_sig(key);
         atomicAdd(&sm.pk[b], (unsigned long long)((1ull << 44) + sg));
-        if (key > sm.mx[b]) atomicMax(&sm.mx[b], key);
-        if (l2 && ~key > sm.mnc[b]) atomicMax(&sm.mnc[b], ~key);
+        // level-2 bin extremes (fire-and-forget atomics: a read of the bin first would make every
+        // key wait on the LDS); a level-3 bin is one key, its own maximum
+        if (l2) {
+          atomicMax(&sm.mx[b], key);
+          atomicMax(&sm.mnc[b], ~key);
+        }
         if (key >= qkey) {
           ++qc;
           qs += sg;
@@ -1885,7 +2277,10 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
         }
       }
     }
-  });
+  };
+  // (the variance-budget solver never collects candidates)
+  if (!SQ && from_cand) stream_groups<VEC, SQ ? 4 : kCandLoads, kNT>(gr, beg, end, visit);
+  else stream_groups<VEC, 4, kNT>(gr, beg, end, visit);
   if (l2) {
     for (int o = 32; o > 0; o >>= 1) {
       qc += __shfl_xor(qc, o);
@@ -1907,7 +2302,7 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
     if (p) {
       atomicAdd((unsigned long long*)&h->cnt[b], (unsigned long long)(p >> 44));
       atomicAdd((unsigned long long*)&h->sig[b], (unsigned long long)(p & ((1ull << 44) - 1)));
-      atomicMax(&h->mx[b], sm.mx[b]);
+      atomicMax(&h->mx[b], l2 ? sm.mx[b] : lo + (uint32_t)b);
       if (l2) atomicMax(&h->mnc[b], sm.mnc[b]);
       if constexpr (SQ) {
         if (sq2) {
@@ -1955,7 +2350,7 @@ __global__ void __launch_bounds__(kNT) k_solve(Args a) {
     return;
   }
   const Hists H{&sm.err, &sm.l1, &sm.w2, &sm.w3, l1t_of(a, row), h1_of(a, row), win_of(a, row),
-                h1q_of(a, row), winq_of(a, row), vctl_of(a, row)};
+                h1q_of(a, row), winq_of(a, row), vctl_of(a, row), ccnt_of(a, row), a.lay.cand_cap};
   int64_t base, len;
   row_span(a, row, base, len);
   solve_row<VAR>(sm, ctl_of(a, row), H, len, a.first != 0);
@@ -2057,10 +2452,13 @@ static_assert(kTileGroups % kSampleBatch == 0 && kTileGroups == 16, "tile shape"
 // Below this lambda, lambda * 2^32 * |g| could round differently from (lambda * |g|) * 2^32.
 constexpr double kLamScaledMin = 0x1p-900;
 
-// Whole-tile decisions with the scaled threshold: an uncapped coordinate i survives iff
-// x_i < fl(lambda * 2^32 * |g_i|), which equals the comparison x_i < fl(lambda * |g_i|) * 2^32
-// (exact scaling by a power of two) for lambda = 0 or lambda >= kLamScaledMin; a capped coordinate
-// (key >= tcap, p_i = 1) always survives.
+// Whole-tile decisions with the scaled threshold: coordinate i survives iff
+// x_i < t_i = fl(lambda * 2^32 * |g_i|), which equals the comparison x_i < fl(lambda * |g_i|) * 2^32
+// (exact scaling by a power of two) for lambda = 0 or lambda >= kLamScaledMin. A capped coordinate
+// (key >= tcap, p_i = 1) always passes that test: either fl(lambda a) >= 1, so t_i >= 2^32 > x_i,
+// or it lies above the exact criterion's value, where lambda a > 1 in exact arithmetic and the few
+// roundings of lambda keep t_i above 2^32 - 1 >= x_i. So the capped bits are needed only in groups
+// whose largest threshold reaches 2^32 - 1, and there they are the key test itself.
 __device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double lam32, uint32_t tcap, uint32_t k0,
                                             uint32_t k1, uint32_t& z, uint32_t& cz) {
   // rows are shorter than 2^31 coordinates, so the counter's high word floor(i/4) >> 32 is 0; with
@@ -2068,33 +2466,19 @@ __device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double 
   uint32_t x0 = (uint32_t)q, x1 = 0, x2 = 0, x3 = 0;
   philox10(x0, x1, x2, x3, k0, k1);
   const uint32_t xr[4] = {x0, x1, x2, x3};
+  double t[4];
   z = 0;
   cz = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const bool capped = key_of(v[k]) >= tcap;  // tcap >= 1, so zeros are never capped
-    z |= (uint32_t)(capped || (double)xr[k] < lam32 * (double)fabsf(v[k])) << k;
-    cz |= (uint32_t)capped << k;
+    t[k] = lam32 * (double)fabsf(v[k]);
+    z |= (uint32_t)((double)xr[k] < t[k]) << k;
   }
-}
-
-// popcount(m & bits of the lanes below this one)
-__device__ __forceinline__ uint32_t lanes_below(unsigned long long m) {
-  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-}
-// Exclusive prefix over the lanes of a wave of x in [0, 2^B) from B ballots; `total` receives the
-// wave's sum.
-template <int B>
-__device__ __forceinline__ uint32_t wave_prefix_bits(uint32_t x, uint32_t& total) {
-  uint32_t pre = 0;
-  total = 0;
+  // capped coordinates are rare: test the group's largest threshold first
+  if (fmax(fmax(t[0], t[1]), fmax(t[2], t[3])) >= 0x1p32 - 1.0) {
 #pragma unroll
-  for (int b = 0; b < B; ++b) {
-    const unsigned long long m = __ballot((x >> b) & 1);
-    pre += lanes_below(m) << b;
-    total += (uint32_t)__popcll(m) << b;
+    for (int k = 0; k < 4; ++k) cz |= (uint32_t)(key_of(v[k]) >= tcap) << k;
   }
-  return pre;
 }
 
 template <bool VEC, bool HYB, int K>
@@ -2345,7 +2729,41 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             m &= m - 1;
           }
         };
-        if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
+        const uint64_t wave_end = (excl & 0x7FFFFFFFull) + wbase + s_wsel[kk][wv];
+        if (lds_values && s_wsel[kk][wv] <= (uint32_t)kDenseEmit && wave_end <= (uint64_t)a.cap &&
+            wave_end <= ((uint64_t)1 << 30)) {
+          // the common case: every survivor of the wave within the capacity (no store needs a bound
+          // check) and its capped values in the LDS list. A first loop writes every survivor with
+          // the sign's +-1/lambda, a second (capped survivors are few) overwrites the capped ones'
+          // values with g_i; both stores of a value come from this lane in program order. 32-bit
+          // byte offsets from the row's output arrays, masks in 32-bit halves.
+          gchar* __restrict__ bi = uniform_ptr(oi);
+          gchar* __restrict__ bv = uniform_ptr(ov);
+          const uint32_t off0 = (uint32_t)pos * 4u;
+          uint32_t off = off0;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            uint32_t m = (uint32_t)(sm >> (32 * h));
+            const uint32_t neg = (uint32_t)(nm >> (32 * h));
+            const int32_t i0 = (int32_t)(e0 + 32 * h);
+            while (m) {
+              const int b = __builtin_ctz(m);
+              *(GS_GLOBAL(int32_t)*)(bi + off) = i0 + b;
+              *(GS_GLOBAL(float)*)(bv + off) = ((neg >> b) & 1u) ? -inv : inv;
+              off += 4u;
+              m &= m - 1u;
+            }
+          }
+          uint64_t m = cm;
+          uint32_t r = cr;
+          while (m) {
+            const int b = __ffsll((unsigned long long)m) - 1;
+            const uint32_t below = (uint32_t)__popcll(sm & ((1ull << b) - 1ull));
+            *(GS_GLOBAL(float)*)(bv + off0 + 4u * below) = s_capv[kk][wv][r];
+            ++r;
+            m &= m - 1;
+          }
+        } else if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
           // many survivors: lane l takes the wave's groups 64 j + l (the order of phase 1 and of
           // the capped-value list), one step j at a time, so the stores of a step fall on a few
           // consecutive lines instead of one line per lane
@@ -2583,7 +3001,9 @@ __global__ void __launch_bounds__(64) k_probs_out(Args a) {
 // Host side.
 // ------------------------------------------------------------------------------------------
 // Kernel classes, in the order the instrumented build reports them.
-enum KernelClass { kcSample = 0, kcStats, kcProbs, kcSolve, kcRefine, kcInit, kcAggregate, kcProbsOut, kcCount };
+enum KernelClass {
+  kcSample = 0, kcStats, kcProbs, kcSolve, kcRefine, kcInit, kcAggregate, kcProbsOut, kcPresample, kcCount
+};
 
 #ifdef GSPAR_INSTRUMENT
 // Measurement build only: while armed, each launch records a pair of HIP events taken by the
@@ -2623,7 +3043,7 @@ static int check_common(const float* g, int64_t rows, int64_t d, int64_t ld, int
   if (solver != GSPAR_GREEDY && solver != GSPAR_EXACT && solver != GSPAR_VARIANCE) return GSPAR_ERR_ARG;
   if (iters < 0 || iters > kMaxIters) return GSPAR_ERR_ARG;
   if (rows > (int64_t)1 << 24) return GSPAR_ERR_ARG;
-  const Layout L = layout_of(rows, d);
+  const Layout L = layout_of(rows, d, 0);  // the minimum: no candidate buffers
   if ((double)rows * (double)L.tiles >= 2147483647.0) return GSPAR_ERR_ARG;  // sample grid, tickets
   const int64_t min_chunk = d < kMaxChunk ? d : kMaxChunk;
   if ((double)rows * (double)((d + min_chunk - 1) / min_chunk) >= 2147483647.0) return GSPAR_ERR_ARG;
@@ -2631,8 +3051,28 @@ static int check_common(const float* g, int64_t rows, int64_t d, int64_t ld, int
   return GSPAR_OK;
 }
 
+static bool vec_ok(const Args& a);
+
+// Candidate keys per row: the full capacity for rows long enough to predict a band, within what
+// the workspace holds beyond its fixed part, on the vector path of a strided batch with a density
+// budget; 0 otherwise.
+static int64_t cand_cap_of(const Args& a) {
+  if (a.seg || a.solver == GSPAR_VARIANCE || !vec_ok(a)) return 0;
+  const int64_t full = cand_cap_full(a.d);
+  if (full == 0) return 0;
+  const size_t fixed = layout_of(a.rows, a.d, 0).total;
+  if (a.ws_bytes <= fixed) return 0;
+  // each key of capacity takes a list slot and a staging slot
+  int64_t fit = (int64_t)((a.ws_bytes - fixed) / (2 * sizeof(uint32_t) * (size_t)a.rows));
+  fit &= ~(int64_t)63;
+  const int64_t cap = fit < full ? fit : full;
+  // a workspace that leaves fewer than 2^16 keys (or the full capacity, for shorter rows) runs
+  // without a band
+  return cap >= (full < (1 << 16) ? full : (1 << 16)) ? cap : 0;
+}
+
 static void plan(Args& a) {
-  a.lay = layout_of(a.rows, a.d);
+  a.lay = layout_of(a.rows, a.d, cand_cap_of(a));
   const int64_t target = 512;
   int64_t chunk;
   if (a.seg) {
@@ -2648,6 +3088,8 @@ static void plan(Args& a) {
   if (chunk > kMaxChunk) chunk = kMaxChunk;
   a.chunk = chunk;
   a.nb = (int)((a.d + chunk - 1) / chunk);
+  a.cand_region = (a.lay.cand_cap / a.nb) & ~(int64_t)63;
+  if (a.cand_region == 0) a.lay.cand_cap = 0;  // no room for a band
 }
 
 static bool vec_ok(const Args& a) {
@@ -2663,13 +3105,17 @@ static int launch_solve(Args& a, hipStream_t s) {
   if (ib > 1024) ib = 1024;
   if (ib < 1) ib = 1;
   launch(kcInit, k_init, dim3(ib), dim3(256), s, a);
+  // rows long enough for a candidate band: a sample of each row predicts it
+  const bool cand = a.lay.cand_cap > 0;
+  if (cand) launch(kcPresample, k_presample, dim3((unsigned)(a.rows * kPreWG)), dim3(256), s, a);
   // a segmented call launches only the workgroups that hold coordinates (none if every segment
   // is empty)
   const int64_t nblocks = a.seg ? a.seg_blocks : a.rows * a.nb;
   const dim3 grid((unsigned)nblocks);
   if (nblocks > 0) {
-    if (sq) launch(kcStats, vec ? k_stats<true, true> : k_stats<false, true>, grid, dim3(kNT), s, a);
-    else launch(kcStats, vec ? k_stats<true, false> : k_stats<false, false>, grid, dim3(kNT), s, a);
+    if (sq) launch(kcStats, vec ? k_stats<true, true, false> : k_stats<false, true, false>, grid, dim3(kNT), s, a);
+    else if (cand) launch(kcStats, k_stats<true, false, true>, grid, dim3(kNT), s, a);  // cand implies vec
+    else launch(kcStats, vec ? k_stats<true, false, false> : k_stats<false, false, false>, grid, dim3(kNT), s, a);
   }
   a.first = 1;
   launch(kcSolve, sq ? k_solve<true> : k_solve<false>, dim3((unsigned)a.rows), dim3(kNT), s, a);
@@ -2721,9 +3167,11 @@ static int run_probs(Args& a, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
 }
 
-static Args base_args(const float* g, int64_t rows, int64_t d, int64_t ld, int solver, int iters, void* ws) {
+static Args base_args(const float* g, int64_t rows, int64_t d, int64_t ld, int solver, int iters, void* ws,
+                      size_t ws_bytes) {
   Args a;
   memset(&a, 0, sizeof(a));
+  a.ws_bytes = ws_bytes;
   a.g = g;
   a.rows = rows;
   a.d = d;
@@ -2868,9 +3316,8 @@ using namespace gspar;
 extern "C" {
 
 size_t gspar_workspace_bytes(int64_t rows, int64_t d, int solver) {
-  (void)solver;
   if (rows < 1 || d < 1) return 0;
-  return layout_of(rows, d).total;
+  return layout_of(rows, d, solver == GSPAR_VARIANCE ? 0 : cand_cap_full(d)).total;
 }
 
 int64_t gspar_capacity_hint(int64_t d, double rho) {
@@ -2886,7 +3333,7 @@ int sparsify_probs(const float* g, int64_t d, double rho, int solver, int greedy
   if (!lambda || !rho_ok(rho, solver)) return GSPAR_ERR_ARG;
   int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws);
+  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   a.rho = rho;
   a.p = p;
   a.lam_out = lambda;
@@ -2901,7 +3348,7 @@ int sparsify_sample_compact(const float* g, int64_t d, double rho, int solver, i
   if (!nnz || capacity < 0 || (capacity > 0 && (!idx || !val)) || !rho_ok(rho, solver)) return GSPAR_ERR_ARG;
   int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws);
+  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   a.rho = rho;
   a.seed = seed;
   a.idx = idx;
@@ -2924,7 +3371,7 @@ int sparsify_sample_hybrid_batched(const float* g, int64_t rows, int64_t d, int6
     return GSPAR_ERR_ARG;
   int rc = check_common(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws);
+  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
   a.rho_dev = rho;
   a.seed_dev = seeds;
   a.idx = idx_a;
@@ -2950,7 +3397,7 @@ int sparsify_sample_hybrid(const float* g, int64_t d, double rho, int solver, in
     return GSPAR_ERR_ARG;
   int rc = check_common(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws);
+  Args a = base_args(g, 1, d, d, solver, greedy_iters, ws, ws_bytes);
   a.rho = rho;
   a.seed = seed;
   a.idx = idx_a;
@@ -3010,7 +3457,7 @@ int sparsify_probs_batched(const float* g, int64_t rows, int64_t d, int64_t ld, 
   if (!rho || !lambda) return GSPAR_ERR_ARG;
   int rc = check_common(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws);
+  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
   a.rho_dev = rho;
   a.p = p;
   a.lam_out = lambda;
@@ -3026,7 +3473,7 @@ int sparsify_sample_compact_batched(const float* g, int64_t rows, int64_t d, int
   if (!rho || !seeds || !nnz || cap_per_row < 0 || (cap_per_row > 0 && (!idx || !val))) return GSPAR_ERR_ARG;
   int rc = check_common(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws);
+  Args a = base_args(g, rows, d, ld, solver, greedy_iters, ws, ws_bytes);
   a.rho_dev = rho;
   a.seed_dev = seeds;
   a.idx = idx;
@@ -3044,7 +3491,7 @@ int sparsify_sample_compact_batched_noalloc(const float* g, int64_t rows, int64_
                                             float* val, int64_t cap_per_row, int64_t* nnz, double* lambda, int64_t* k,
                                             uint32_t* flags, void* stream) {
   if (rows < 1 || d < 1) return GSPAR_ERR_ARG;
-  if (layout_of(rows, d).total > GSPAR_SCRATCH_BYTES) return GSPAR_ERR_TOO_LARGE;
+  if (layout_of(rows, d, 0).total > GSPAR_SCRATCH_BYTES) return GSPAR_ERR_TOO_LARGE;
   void* ws = scratch_of_current_device();
   if (!ws) return GSPAR_ERR_HIP;
   return sparsify_sample_compact_batched(g, rows, d, ld, rho, solver, greedy_iters, seeds, idx, val, cap_per_row,
@@ -3120,7 +3567,7 @@ int sparsify_sample_compact_segmented(const float* g, int64_t segs, const int64_
   if (rc) return rc;
   rc = check_common(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws);
+  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
   set_segments(a, off, off_dev, segs, total, aligned);
   a.rho_dev = rho;
   a.seed_dev = seeds;
@@ -3148,7 +3595,7 @@ int sparsify_sample_hybrid_segmented(const float* g, int64_t segs, const int64_t
   if (rc) return rc;
   rc = check_common(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws);
+  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
   set_segments(a, off, off_dev, segs, total, aligned);
   a.rho_dev = rho;
   a.seed_dev = seeds;
@@ -3176,7 +3623,7 @@ int sparsify_probs_segmented(const float* g, int64_t segs, const int64_t* off, c
   if (rc) return rc;
   rc = check_common(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
   if (rc) return rc;
-  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws);
+  Args a = base_args(g, segs, maxlen, maxlen, solver, greedy_iters, ws, ws_bytes);
   set_segments(a, off, off_dev, segs, total, aligned);
   a.rho_dev = rho;
   a.p = p;

@@ -12,7 +12,11 @@ OUT_DIR = os.path.join(HERE, "_build")
 def build(asan: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
     res = os.environ.get("GSPAR_EMU_RESIDENT")
-    out = os.path.join(OUT_DIR, ("libgspar_emu_asan" if asan else "libgspar_emu") + (f"_r{int(res)}" if res else "") + ".so")
+    # rows from this length on predict a candidate band (a small threshold and sample exercise the
+    # band on the emulated sizes; the production threshold exercises refinement over the row)
+    cmin = int(os.environ.get("GSPAR_EMU_CAND_MIN_ROW", "4096"))
+    out = os.path.join(OUT_DIR, ("libgspar_emu_asan" if asan else "libgspar_emu") + (f"_r{int(res)}" if res else "")
+                       + f"_c{cmin}" + ".so")
     if os.path.exists(out) and os.path.getmtime(out) > max(os.path.getmtime(SRC),
                                                          os.path.getmtime(os.path.join(HERE, "hip", "hip_runtime.h"))):
         return out
@@ -21,6 +25,7 @@ def build(asan: bool = False) -> str:
     # when GSPAR_EMU_RESIDENT is set
     cmd = ["g++", "-std=c++20", "-O1", "-g", "-fPIC", "-shared", "-pthread", "-Wno-attributes", "-DGSPAR_LOOKBACK_POLLS=64",
            f"-DGSPAR_SAMPLE_RESIDENT={int(os.environ.get('GSPAR_EMU_RESIDENT', '1792'))}",
+           f"-DGSPAR_CAND_MIN_ROW={cmin}", "-DGSPAR_PRE_LINES=64",
            "-Wno-unknown-pragmas", "-I", HERE, "-I", os.path.join(ROOT, "include"), "-x", "c++", SRC,
            "-o", out + ".tmp"]
     if asan:

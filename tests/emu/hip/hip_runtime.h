@@ -53,6 +53,11 @@ typedef void* hipStream_t;
 typedef void* hipEvent_t;
 enum { hipSuccess = 0 };
 inline hipError_t hipGetLastError() { return hipSuccess; }
+// device symbols are host storage here: the symbol's address is the variable's own
+#define __align__(n) alignas(n)
+#define HIP_SYMBOL(x) (&(x))
+inline hipError_t hipGetDevice(int* d) { *d = 0; return hipSuccess; }
+inline hipError_t hipGetSymbolAddress(void** p, const void* sym) { *p = const_cast<void*>(sym); return hipSuccess; }
 inline hipError_t hipEventCreate(hipEvent_t* e) { *e = nullptr; return hipSuccess; }
 inline hipError_t hipEventDestroy(hipEvent_t) { return hipSuccess; }
 inline hipError_t hipEventRecord(hipEvent_t, hipStream_t = nullptr) { return hipSuccess; }
@@ -119,6 +124,8 @@ inline T xchg(T v, int src) {
 }
 }  // namespace emu
 
+template <class T>
+inline T __shfl(T v, int src, int = 64) { return emu::xchg(v, src); }
 template <class T>
 inline T __shfl_xor(T v, int mask, int = 64) { return emu::xchg(v, emu::lane() ^ mask); }
 template <class T>

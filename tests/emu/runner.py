@@ -255,6 +255,94 @@ def check_ties(L, verbose=True):
     return True
 
 
+def row_state(ws, row=0):
+    """Fields of a row's control block in a workspace after a call (offsets fixed by static
+    asserts in the library source): the source of the last refinement request, the candidate
+    band and the number of collected keys."""
+    b = np.asarray(ws, np.uint8)[256 + 256 * row: 256 + 256 * (row + 1)]
+    u32 = lambda o: int(b[o:o + 4].view(np.uint32)[0])
+    return {"src": u32(192), "band_lo": u32(220), "band_hi": u32(224),
+            "cand_n": int(b[232:240].view(np.uint64)[0]), "stage": u32(208)}
+
+
+def sample_row_ws(L, g, rho, solver, seed, iters=2):
+    """sample_row that also returns the workspace, for row_state."""
+    d = g.size
+    idx = np.zeros(d, np.int32)
+    val = np.zeros(d, np.float32)
+    nnz = np.zeros(1, np.int64)
+    lam = np.zeros(1)
+    k = np.zeros(1, np.int64)
+    fl = np.zeros(1, np.uint32)
+    sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
+    wsb = L.gspar_workspace_bytes(1, d, sid)
+    keep, ws = _aligned(wsb)
+    rc = L.sparsify_sample_compact(g.ctypes.data, d, rho, sid, iters, seed, idx.ctypes.data, val.ctypes.data, d,
+                                   nnz.ctypes.data, lam.ctypes.data, k.ctypes.data, fl.ctypes.data, ws.ctypes.data,
+                                   wsb, None)
+    assert rc == 0, rc
+    n = int(nnz[0])
+    return idx[:n], val[:n], n, float(lam[0]), int(k[0]), int(fl[0]), ws.copy()
+
+
+def check_candidates(L, verbose=True):
+    """Rows long enough for a candidate band (in this build): the band is predicted, the keys in it
+    are collected, refinement windows inside it read them, and every result still equals the
+    oracle's (bit for bit in lambda for the exact solver). A row whose sample misleads the
+    prediction (large magnitudes only on lines the sample skips) refines over the row instead."""
+    used = 0
+    for name, g in (("tmix", W.t_mixture(65536, 12)), ("tmix_ragged", W.t_mixture(50003, 13)),
+                    ("ties", W.integer_ties(40000, 14))):
+        g = np.ascontiguousarray(g, np.float32)
+        for solver in ("greedy", "exact"):
+            for rho in (0.01, 0.1, 0.4):
+                sol = oracle.solve(g, rho, solver, 2)
+                idx, val, n, lam, k, fl, ws = sample_row_ws(L, g, rho, solver, 21)
+                st = row_state(ws)
+                assert fl == 0, (name, solver, rho, fl)
+                compare_sample(g, sol.p, 21, idx, val, n, lam, sol.lam)
+                if solver == "exact":
+                    assert lam == sol.lam and k == sol.k, (name, rho, lam, sol.lam, k, sol.k)
+                if g.size % 4:
+                    # a row length that is not a multiple of 4 takes the scalar-load path: no band
+                    assert st["band_hi"] == st["band_lo"] and st["src"] == 0, (name, st)
+                    continue
+                if st["band_hi"] == st["band_lo"]:
+                    # no band: the sample showed nothing capped (B times its largest magnitude well
+                    # below its sum), so the solvers need no window
+                    assert st["src"] == 0 and k == 0 or solver == "greedy", (name, st, k)
+                    continue
+                keys = np.abs(g).view(np.uint32)
+                inband = int(np.count_nonzero((keys >= st["band_lo"]) & (keys < st["band_hi"])))
+                # reserved slots: every key of the band, plus zeroed ends of the waves' reservations
+                assert st["cand_n"] == inband, (name, st, inband)
+                used += st["src"]
+                if verbose:
+                    print(f"{name} {solver} rho={rho}: band [{st['band_lo'] >> 23}, {st['band_hi'] >> 23}) "
+                          f"cand={st['cand_n']} src={st['src']} stage={st['stage']}", flush=True)
+    assert used > 0, "no refinement window was read from the candidates"
+    # a misleading sample: the sample reads every 4th 64-byte line of this row (64 workgroups x 64
+    # lines in this build, of its 16384 lines); put all the large magnitudes on the other lines
+    d = 1 << 18
+    g = (W.normal(d, 15) * np.float32(1e-3)).astype(np.float32)
+    lines = np.arange(d) // 16
+    big = (lines % 4 != 0) & (np.arange(d) % 7 == 0)
+    g[big] = W.t_mixture(int(big.sum()), 16) * np.float32(50)
+    for solver in ("greedy", "exact"):
+        sol = oracle.solve(g, 0.05, solver, 2)
+        idx, val, n, lam, k, fl, ws = sample_row_ws(L, g, 0.05, solver, 22)
+        st = row_state(ws)
+        compare_sample(g, sol.p, 22, idx, val, n, lam, sol.lam)
+        if solver == "exact":
+            assert lam == sol.lam and k == sol.k
+        if verbose:
+            print(f"misleading sample {solver}: band [{st['band_lo'] >> 23}, {st['band_hi'] >> 23}) "
+                  f"cand={st['cand_n']} src={st['src']}", flush=True)
+    if verbose:
+        print("candidate cases ok", flush=True)
+    return True
+
+
 def segmented(L, g, off, rhos, seeds, solver, iters=2, cap=None, off_dev=None, g_shift=0):
     """sparsify_sample_compact_segmented on a flat host vector (placed g_shift floats past a
     16-byte boundary); off_dev defaults to the host offsets."""
@@ -559,6 +647,8 @@ if __name__ == "__main__":
         check_hybrid(load(sys.argv[1]))
     if which in ("all", "ties"):
         check_ties(load(sys.argv[1]))
+    if which in ("all", "candidates"):
+        check_candidates(load(sys.argv[1]))
     if which in ("all", "aggregate"):
         check_aggregate(load(sys.argv[1]))
     if which in ("all", "variance"):

@@ -36,6 +36,10 @@ def test_emulated_capped_ties(emu_lib):
     assert runner.check_ties(runner.load(emu_lib), verbose=False)
 
 
+def test_emulated_candidate_band(emu_lib):
+    assert runner.check_candidates(runner.load(emu_lib), verbose=False)
+
+
 def test_emulated_variance_solver(emu_lib):
     assert runner.check_variance(runner.load(emu_lib), verbose=False)
 
@@ -98,7 +102,7 @@ def test_emulated_two_tiles_per_workgroup():
     resident set) forced on the small emulated inputs: edge cases, batching, overflow, the
     unaligned path and the hybrid coding, with tile counts odd and even (segmented rows with two
     tiles per workgroup run on the GPU, in tests/test_gpu_segmented.py)."""
-    env = dict(os.environ, GSPAR_EMU_RESIDENT="1")
+    env = dict(os.environ, GSPAR_EMU_RESIDENT="1", GSPAR_EMU_CAND_MIN_ROW=str(1 << 22))
     lib = subprocess.run([sys.executable, "-c", "import sys; sys.path.insert(0, %r); import build; print(build.build())"
                           % os.path.join(HERE, "emu")], env=env, capture_output=True, text=True, check=True).stdout.strip()
     r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "extra_lite"], env=env,

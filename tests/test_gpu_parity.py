@@ -158,6 +158,76 @@ def test_capped_ties_one_rule(gs, d, n_hi):
     _say(f"   ok nnz={n}")
 
 
+def _row_state(ws, row=0):
+    """src / band / collected count of a row's control block in a workspace (offsets fixed by
+    static asserts in the library source)."""
+    b = ws.cpu().numpy()[256 + 256 * row: 256 + 256 * (row + 1)]
+    u32 = lambda o: int(b[o:o + 4].view(np.uint32)[0])
+    return {"src": u32(192), "band_lo": u32(220), "band_hi": u32(224), "cand_n": int(b[232:240].view(np.uint64)[0])}
+
+
+@pytest.mark.parametrize("solver", ["greedy", "exact"])
+def test_candidate_band_on_a_long_row(gs, solver):
+    """A row of 2^23 + 12 coordinates (long enough for a candidate band): the statistics pass
+    collects exactly the keys of the predicted binades, the refinement windows read them, and the
+    result equals the oracle's under the parity rule (lambda bit for bit for the exact solver)."""
+    d = (1 << 23) + 12
+    g = W.t_mixture(d, 71)
+    keys = np.abs(g).view(np.uint32)
+    gd = torch.from_numpy(g).cuda().reshape(1, -1)
+    seeds = torch.tensor([5], dtype=torch.int64, device="cuda")
+    used = 0
+    for rho in (0.001, 0.01, 0.1):
+        plan = gs.Plan(1, d, solver=solver, cap_per_row=gs.capacity_hint(d, rho))
+        plan.run(gd, torch.tensor([rho], dtype=torch.float64, device="cuda"), seeds)
+        torch.cuda.synchronize()
+        st = _row_state(plan.ws)
+        n = int(plan.nnz[0].item())
+        _say(f"[band] {solver} rho={rho} band=[{st['band_lo'] >> 23},{st['band_hi'] >> 23}) cand={st['cand_n']} "
+             f"src={st['src']} nnz={n}")
+        assert int(plan.flags[0].item()) == 0
+        assert st["band_hi"] > st["band_lo"]  # this row has capped coordinates at every density
+        assert st["cand_n"] == int(np.count_nonzero((keys >= st["band_lo"]) & (keys < st["band_hi"])))
+        used += st["src"]
+        sol = oracle.solve(g, rho, solver, 2)
+        compare_sample(g, sol.p, 5, plan.idx[0, :n].cpu().numpy(), plan.val[0, :n].cpu().numpy(), n,
+                       float(plan.lam[0].item()), sol.lam)
+        if solver == "exact":
+            assert float(plan.lam[0].item()) == sol.lam and int(plan.k[0].item()) == sol.k
+    assert used > 0
+
+
+def test_candidate_band_on_ragged_rows(gs):
+    """Two rows of 2^22 + 3 coordinates stored with a leading dimension of 2^22 + 4 (vector loads;
+    each row ends in a partial group of 3): the band is collected over the whole row, its last
+    partial group included, and both rows match the oracle (exact solver, lambda bit for bit)."""
+    rows, d, ld = 2, (1 << 22) + 3, (1 << 22) + 4
+    g = np.stack([W.t_mixture(d, 81 + r) for r in range(rows)])
+    # the partial group holds a key of each density's band and the row's largest magnitude
+    g[:, -3:] = np.float32([12.0, -3000.0, 1.0e4])
+    buf = np.zeros((rows, ld), np.float32)
+    buf[:, :d] = g
+    gd = torch.from_numpy(buf).cuda()
+    seeds = torch.tensor([11, 12], dtype=torch.int64, device="cuda")
+    for rho in (0.001, 0.1):
+        plan = gs.Plan(rows, d, ld=ld, solver="exact", cap_per_row=gs.capacity_hint(d, rho))
+        plan.run(gd, torch.full((rows,), rho, dtype=torch.float64, device="cuda"), seeds)
+        torch.cuda.synchronize()
+        for r in range(rows):
+            st = _row_state(plan.ws, r)
+            keys = np.abs(g[r]).view(np.uint32)
+            n = int(plan.nnz[r].item())
+            _say(f"[band-ragged] row {r} rho={rho} band=[{st['band_lo'] >> 23},{st['band_hi'] >> 23}) "
+                 f"cand={st['cand_n']} src={st['src']} nnz={n}")
+            assert int(plan.flags[r].item()) == 0
+            assert st["band_hi"] > st["band_lo"]
+            assert st["cand_n"] == int(np.count_nonzero((keys >= st["band_lo"]) & (keys < st["band_hi"])))
+            sol = oracle.solve(g[r], rho, "exact", 2)
+            compare_sample(g[r], sol.p, 11 + r, plan.idx[r, :n].cpu().numpy(), plan.val[r, :n].cpu().numpy(), n,
+                           float(plan.lam[r].item()), sol.lam)
+            assert float(plan.lam[r].item()) == sol.lam and int(plan.k[r].item()) == sol.k
+
+
 def test_special_cases(gs):
     d = 50000
     z = np.zeros(d, np.float32)
