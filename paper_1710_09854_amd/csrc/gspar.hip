@@ -1955,7 +1955,10 @@ struct BandLds {
   double w[kNT / 64];
   uint64_t k[kNT / 64];
   int ired[kNT / 64];
+  double ge;  // the sample's G at the lower edge of the binade of 1/lambda*
 };
+// G within this fraction of B at that edge: 1/lambda* may lie in the binade below.
+constexpr double kBandNear = 0.125;
 
 // The candidate band of a row, predicted from its sample histogram identically by every
 // workgroup of the statistics pass (same data, same order of operations). With f = the row's
@@ -1963,9 +1966,13 @@ struct BandLds {
 // refine lies in [1/lambda*, 1/lambda_0]: 1/lambda_0 = S / B (Algorithm 3's start), and the exact
 // 1/lambda* is where G(tau) = #{a >= tau} + (sum of the a < tau) / tau falls to B (Proposition 1:
 // sum min(lambda a, 1) = B); G decreases in tau, so at binade edges its crossing gives the binade
-// of 1/lambda*. The band runs from the binade below that one to the binade holding 1.25 S / B, in
-// whole binades, so every refinement window inside it is complete. No band when B = 0 or nothing
-// was sampled. Threads 0..255 own one binade each; every thread receives the result.
+// e* of 1/lambda*. The exact solver refines the binade of 1/lambda* or the next occupied one above
+// it, so its band is e* and e* + 1, and e* - 1 too when the sample's G at e*'s lower edge is
+// within kBandNear of B (the sample may have misplaced the crossing); the greedy solver's
+// thresholds run from 1/lambda_0 = S / B down towards 1/lambda*, so its band reaches up to the
+// binade of 1.25 S / B (slack for the sample's estimate of S). Whole binades, so every refinement
+// window inside the band is complete. No band when B = 0 or nothing was sampled. Threads 0..255
+// own one binade each; every thread receives the result.
 GS_DI void cand_band(const Args& a, const PreHist* ph, double B, int64_t len, BandLds& sm, uint32_t& blo,
                      uint32_t& bhi) {
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -2007,10 +2014,11 @@ GS_DI void cand_band(const Args& a, const PreHist* ph, double B, int64_t len, Ba
   for (int i = 0; i < kNT / 64; ++i) top = max(top, sm.ired[i]);
   __syncthreads();
   int best = -1;
+  double G = 0.0;
   if (t >= 1 && t < kB1 - 1 && B > 0.0 && tot > 0.0) {
     // G at the binade's lower edge lo = 2^(t - 127): keys >= lo count whole, the rest by value / lo
     const double lo = ldexp(1.0, t - 127);
-    const double G = f * ((double)kc + (tot - wc) / lo);
+    G = f * ((double)kc + (tot - wc) / lo);
     if (G >= B) best = t;
   }
   for (int o = 32; o > 0; o >>= 1) best = max(best, __shfl_xor(best, o));
@@ -2018,17 +2026,23 @@ GS_DI void cand_band(const Args& a, const PreHist* ph, double B, int64_t len, Ba
   __syncthreads();
   int e = -1;
   for (int i = 0; i < kNT / 64; ++i) e = max(e, sm.ired[i]);
+  if (t == e) sm.ge = G;
+  __syncthreads();
   blo = bhi = 0;
   // Nothing looks capped (B times the sample's largest magnitude, bounded by its binade's top,
   // below half the estimated sum): the solvers should need no window, so no band is collected (a
   // row the sample misjudged refines over the row).
   const bool uncapped = top >= 0 && B * ldexp(1.0, top - 126) <= 0.5 * f * tot;
   if (e >= 1 && B > 0.0 && tot > 0.0 && !uncapped) {
-    const double t0 = 1.25 * f * tot / B;
-    const uint32_t ehi = t0 < 3.0e38 ? (key_of((float)t0) >> 23) : 254u;
-    const uint32_t elo = (uint32_t)(e - 1);
+    const uint32_t elo = (uint32_t)e - (sm.ge < (1.0 + kBandNear) * B ? 1u : 0u);
+    uint32_t ehi = (uint32_t)e + 1;
+    if (a.solver == GSPAR_GREEDY) {
+      const double t0 = 1.25 * f * tot / B;
+      const uint32_t e0 = t0 < 3.0e38 ? (key_of((float)t0) >> 23) : 254u;
+      ehi = e0 > ehi ? e0 : ehi;
+    }
     blo = elo << 23;
-    bhi = ((ehi > elo ? ehi : elo) + 1) << 23;
+    bhi = (ehi + 1) << 23;
     if (bhi > kKeyInf) bhi = kKeyInf;
   }
   __syncthreads();

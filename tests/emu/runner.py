@@ -569,6 +569,53 @@ def check_aggregate(L, verbose=True):
     return True
 
 
+def check_asan_subset(L, verbose=True):
+    """A bounded selection for the AddressSanitizer build: every kernel family once, on shapes that
+    reach the ragged ends. A padded batch whose rows end in a partial group on the vector path
+    (long enough for a candidate band in this build), the scalar path, the variance budget,
+    segments on both paths with the hybrid coding, and aggregation of the batch's lists."""
+    rows, d = 2, 12003
+    g2 = np.stack([W.t_mixture(d, 310 + r) for r in range(rows)])
+    for solver, ld, rhos in (("greedy", d + 1, [0.1, 0.01]), ("exact", d + 1, [0.01, 0.1]), ("exact", d + 2, [0.05, 0.2])):
+        seeds = [3 + r for r in range(rows)]
+        idx, val, nnz, lam, k, fl = batched(L, g2, rhos, seeds, solver, ld=ld)
+        assert not fl.any(), fl
+        for r in range(rows):
+            sol = oracle.solve(g2[r], rhos[r], solver, 2)
+            n = int(nnz[r])
+            compare_sample(g2[r], sol.p, seeds[r], idx[r, :n], val[r, :n], n, lam[r], sol.lam)
+            if solver == "exact":
+                assert lam[r] == sol.lam and k[r] == sol.k
+        v = aggregate(L, idx, val, nnz, d)
+        assert np.array_equal(v, oracle.aggregate(_lists(idx, val, nnz), d), equal_nan=True)
+    g = np.ascontiguousarray(W.t_mixture(9001, 2), np.float32)
+    sol = oracle.solve_variance(g, 0.05)
+    idx, val, n, lam, k, fl = sample_row(L, g, 0.05, "variance", 31)
+    assert fl == 0 and lam == sol.lam and k == sol.k
+    compare_sample(g, sol.p, 31, idx, val, n, lam, sol.lam)
+    for lengths in ([3000, 0, 3, 16384 + 8, 1], [4096, 16388, 12, 0, 8]):
+        g, off = layered(lengths, 620 + len(lengths))
+        segs = len(lengths)
+        rhos = [(0.01, 0.1, 0.5, 0.3, 1.0)[i % 5] for i in range(segs)]
+        seeds = [7100 + i for i in range(segs)]
+        idx, val, nnz, lam, k, fl = segmented(L, g, off, rhos, seeds, "exact")
+        ref = oracle.sparsify_segments(g, off, rhos, seeds, "exact")
+        for s_ in range(segs):
+            seg = g[off[s_]:off[s_ + 1]]
+            n = int(nnz[s_])
+            if seg.size == 0 or not np.any(seg):
+                assert n == 0 and fl[s_] & 4
+                continue
+            sol = ref[s_][0]
+            compare_sample(seg, sol.p, seeds[s_], idx[s_, :n], val[s_, :n], n, lam[s_], sol.lam)
+            assert lam[s_] == sol.lam and k[s_] == sol.k
+        ia, va, na, cb, nb, inv, q, lam3, fl3 = hybrid_segmented(L, g, off, rhos, seeds, "exact")
+        assert np.array_equal(lam3, lam, equal_nan=True) and np.all(na + nb == nnz)
+    if verbose:
+        print("asan subset ok", flush=True)
+    return True
+
+
 def run_extra(path, verbose=True, lite=False):
     """Edge cases, batching, overflow and the unaligned path; `lite` (for reruns of the same cases
     under other launch conditions) keeps one greedy step count and skips the single-row repeats."""
@@ -655,5 +702,7 @@ if __name__ == "__main__":
         check_variance(load(sys.argv[1]))
     if which in ("all", "segmented"):
         check_segmented(load(sys.argv[1]))
+    if which == "asan_subset":
+        check_asan_subset(load(sys.argv[1]))
     if which in ("all", "main"):
         print("checked", run_all(sys.argv[1]))

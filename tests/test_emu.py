@@ -76,6 +76,18 @@ def test_emulated_full_sweep(emu_lib):
     assert runner.run_all(emu_lib, verbose=False) == 64
 
 
+def test_emulated_asan_subset():
+    """Kernel indexing under AddressSanitizer in the default suite (about a minute): a padded batch
+    ending in partial groups with a candidate band, the scalar path, the variance budget, segments
+    on both paths with the hybrid coding, and aggregation (the full sweep under ASan is below)."""
+    lib = emu_build.build(asan=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0", LD_PRELOAD=emu_build.asan_runtime())
+    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "asan_subset"], env=env,
+                       capture_output=True, text=True, timeout=1200)
+    assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-2000:]
+    assert "asan subset ok" in r.stdout, r.stdout[-2000:]
+
+
 @pytest.mark.skipif(os.environ.get("GSPAR_EMU_ASAN") != "1", reason="ASan sweep: set GSPAR_EMU_ASAN=1")
 def test_emulated_under_asan():
     lib = emu_build.build(asan=True)
