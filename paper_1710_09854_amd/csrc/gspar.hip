@@ -964,17 +964,32 @@ GS_DI void l1_exact(const Hists& H, double B, const Fx& S, SolveLds& s, int& b1,
   if (t < kB1 && t > b1 && H.l1->cnt[t]) occupied = t;
   b2 = block_min(s, occupied);
 }
+// Inside a window each thread walks its bins from the top. A double-precision screen decides the
+// criterion at every bin whose margin exceeds 2^-46 S: T = S - W is approximated by
+// fl(S) - (fl(W above the window) + fl(window sum above)), within 2^-50 S of fl(T), and the
+// left-hand side is computed exactly as the criterion computes it, so the screen and the exact
+// evaluation agree wherever the screen decides; the exact criterion decides the rest (the bins
+// next to the threshold).
 GS_DI void lvl_exact(const Lvl& L, const Walk& w, double B, const Fx& S, SolveLds& s, int& b1, int& b2) {
   int best = -1;
   uint64_t K = w.exK, Sg = w.exS;
+  const double Sd = fx_to_double(S), Wawd = fx_to_double(L.Waw);
+  const double tol = 0x1p-46 * Sd + 0x1p-1000;
+#pragma unroll 1
   for (int j = L.per - 1; j >= 0 && best < 0; --j) {
     const int b = threadIdx.x * L.per + j;
     if (b >= L.nbins) continue;
     const uint64_t c = (uint64_t)L.cnt[b];
     if (!c) continue;
-    uint64_t Kt;
-    const Fx W = lvl_total(L, K, Sg, Kt);
-    if (criterion(B, S, Kt, W, L.mx[b])) best = b;
+    const double lhs = (B - (double)(L.Kaw + K)) * key_value(L.mx[b]);
+    const double Td = Sd - (Wawd + ldexp((double)Sg, L.shift - 149));
+    int pass = lhs <= Td - tol ? 1 : (lhs > Td + tol ? 0 : -1);
+    if (pass < 0) {
+      uint64_t Kt;
+      const Fx W = lvl_total(L, K, Sg, Kt);
+      pass = criterion(B, S, Kt, W, L.mx[b]) ? 1 : 0;
+    }
+    if (pass) best = b;
     K += c;
     Sg += (uint64_t)L.sig[b];
   }
@@ -2077,7 +2092,9 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
       c->band_hi = bhi;
     }
   }
-  const uint32_t bspan = bhi - blo;
+  // zero keys are never candidates (no window counts them): the band starts at key 1 at least
+  const uint32_t blo1 = blo ? blo : 1u;
+  const uint32_t bspan = bhi > blo1 ? bhi - blo1 : 0u;
   const int lane = threadIdx.x & 63;
   // Collected keys are buffered per wave in LDS (a group's keys placed by a wave prefix) and
   // flushed into this workgroup's own region of the row's candidate buffer, at a place taken from
@@ -2108,30 +2125,35 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   const int64_t end = min(len, beg + a.chunk);
   const uint32_t lc = threadIdx.x & (kLaneCopies - 1);
   auto hist = [&](const float v[4]) {
+    // the group's additions first (atomics without return), then its four bin maxima read
+    // together: one LDS round trip per group. The bin maximum only grows, so a read that already
+    // covers the key skips the atomic. Zero keys (also the coordinates outside [beg, end), read as
+    // 0) add nothing, and their bin-0 reads are not acted on.
+    uint32_t key[4], f[4], cur[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const uint32_t key = key_of(v[c]);  // coordinates outside [beg, end) read as 0 and are skipped
-      if (key != 0) {
-        const uint32_t f = (key >> 23) * kLaneCopies + lc;
-        atomicAdd(&sm.pk[f], (unsigned long long)((1ull << 44) + key_sig(key)));
-        // the bin maximum only grows, so a plain read that already covers key skips the atomic
-        if (key > sm.mx[f]) atomicMax(&sm.mx[f], key);
+      key[c] = key_of(v[c]);
+      f[c] = (key[c] >> 23) * kLaneCopies + lc;
+      if (key[c] != 0) {
+        atomicAdd(&sm.pk[f[c]], (unsigned long long)((1ull << 44) + key_sig(key[c])));
         if constexpr (SQ) {
-          const uint64_t m = key_sig(key), m2 = m * m;
-          atomicAdd(&sm.qh[f], (unsigned long long)(m2 >> 24));
-          atomicAdd(&sm.ql[f], (unsigned long long)(m2 & 0xFFFFFFu));
+          const uint64_t m = key_sig(key[c]), m2 = m * m;
+          atomicAdd(&sm.qh[f[c]], (unsigned long long)(m2 >> 24));
+          atomicAdd(&sm.ql[f[c]], (unsigned long long)(m2 & 0xFFFFFFu));
         }
       }
     }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) cur[c] = sm.mx[f[c]];
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (key[c] > cur[c]) atomicMax(&sm.mx[f[c]], key[c]);
   };
   // the candidate band's keys of a group into the wave's buffer
   auto collect = [&](const float v[4]) {
     uint32_t cm = 0;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const uint32_t key = key_of(v[c]);
-      cm |= (uint32_t)(key - blo < bspan && key != 0) << c;
-    }
+    for (int c = 0; c < 4; ++c) cm |= (uint32_t)(key_of(v[c]) - blo1 < bspan) << c;
     if (__ballot(cm != 0)) {
       uint32_t tot;
       uint32_t pos = wcnt + wave_prefix_bits<3>((uint32_t)__popc(cm), tot);
@@ -2495,6 +2517,16 @@ __device__ __forceinline__ void decide_fast(int64_t q, const float v[4], double 
   }
 }
 
+// A group's code byte: the selection bits z (bits 0-3) and the signs of its four values (bits 4-7).
+// v_perm_b32's sign-replicating selectors (9: bit 31 of the low word of the pair, 11: of the high
+// word) turn each sign into a 0x00 / 0xFF byte, one bit of each byte is kept, and v_sad_u8 adds
+// the four bytes to z.
+__device__ __forceinline__ uint32_t group_code(const float v[4], uint32_t z) {
+  const uint32_t s01 = __builtin_amdgcn_perm(__float_as_uint(v[1]), __float_as_uint(v[0]), 0x0C0C0B09u);
+  const uint32_t s23 = __builtin_amdgcn_perm(__float_as_uint(v[3]), __float_as_uint(v[2]), 0x0B090C0Cu);
+  return __builtin_amdgcn_sad_u8((s01 | s23) & 0x80402010u, 0u, z);
+}
+
 template <bool VEC, bool HYB, int K>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   __shared__ float s_capv[K][kTileThreads / 64][kCapList];
@@ -2556,10 +2588,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     uint32_t ncl = 0;  // capped survivors of this wave so far (the LDS list keeps the first kCapList)
     auto record = [&](int j, const float v[4], uint32_t z, uint32_t cz) {
       cz &= z;
-      uint32_t neg = 0;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) neg |= (__float_as_uint(v[k]) >> 31) << k;
-      s_code[kk][tg0 + 64 * j] = (uint8_t)(z | (neg << 4));
+      s_code[kk][tg0 + 64 * j] = (uint8_t)group_code(v, z);
       s_capb[kk][tg0 + 64 * j] = (uint8_t)cz;
       nsel += (uint32_t)__popc(z);
       if (__ballot(cz != 0)) {

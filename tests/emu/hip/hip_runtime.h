@@ -157,6 +157,32 @@ inline unsigned __builtin_amdgcn_mbcnt_hi(unsigned m, unsigned acc) {
   const int l = emu::lane();
   return acc + (unsigned)__builtin_popcount(l < 32 ? 0u : (m & (l == 63 ? 0x7fffffffu : ((1u << (l - 32)) - 1u))));
 }
+// v_perm_b32: byte i of the result is chosen by byte i of sel from the eight bytes of {s0, s1}
+// (s1 the low word): 0-7 a byte, 8-11 the sign bit of byte 1, 3, 5 or 7 replicated, 12 zero,
+// 13 and above 0xFF.
+inline unsigned __builtin_amdgcn_perm(unsigned s0, unsigned s1, unsigned sel) {
+  const unsigned long long in = ((unsigned long long)s0 << 32) | s1;
+  unsigned r = 0;
+  for (int i = 0; i < 4; ++i) {
+    const unsigned s = (sel >> (8 * i)) & 0xFF;
+    unsigned b;
+    if (s >= 13) b = 0xFF;
+    else if (s == 12) b = 0x00;
+    else if (s >= 8) b = ((in >> (16 * (s - 8) + 15)) & 1) ? 0xFF : 0x00;
+    else b = (unsigned)(in >> (8 * s)) & 0xFF;
+    r |= b << (8 * i);
+  }
+  return r;
+}
+// v_sad_u8: the sum over the four bytes of |a_i - b_i|, plus c.
+inline unsigned __builtin_amdgcn_sad_u8(unsigned a, unsigned b, unsigned c) {
+  unsigned r = c;
+  for (int i = 0; i < 4; ++i) {
+    const int x = (int)((a >> (8 * i)) & 0xFF), y = (int)((b >> (8 * i)) & 0xFF);
+    r += (unsigned)(x > y ? x - y : y - x);
+  }
+  return r;
+}
 struct uint4 {
   unsigned x, y, z, w;
 };
