@@ -453,9 +453,10 @@ GS_HD int64_t pre_lines(int64_t len) {
 // kCandLoads float4 per thread at a time.
 constexpr int64_t kCandShare = 1 << 14;
 constexpr int kCandLoads = 8;
-// keys a wave buffers in LDS (flushed above kCandWave - 256); sized so that the statistics
-// workgroup stays within a quarter of the LDS (four resident per compute unit)
-constexpr int kCandWave = 496;
+// keys a lane buffers in LDS before its wave flushes (an odd stride keeps the lanes on different
+// banks); sized so that the statistics workgroup stays within a quarter of the LDS (four resident
+// per compute unit)
+constexpr int kCandLane = 7;
 // Candidate capacity per row a full workspace provides.
 GS_HD int64_t cand_cap_full(int64_t d) {
   if (d < kCandMinRow) return 0;
@@ -2074,7 +2075,7 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   StatsLdsT<SQ>& sm = sm_st;
   __shared__ BandLds s_band;
   // candidate band: per-wave buffers of collected keys, and the workgroup's region count
-  __shared__ uint32_t s_cand[CAND ? kNT / 64 : 1][CAND ? kCandWave : 1];
+  __shared__ uint32_t s_cand[CAND ? kNT / 64 : 1][CAND ? 64 * kCandLane : 1];
   __shared__ uint32_t s_rcnt;
   __shared__ unsigned long long s_rbase;
   int64_t row, blk;
@@ -2096,21 +2097,24 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   const uint32_t blo1 = blo ? blo : 1u;
   const uint32_t bspan = bhi > blo1 ? bhi - blo1 : 0u;
   const int lane = threadIdx.x & 63;
-  // Collected keys are buffered per wave in LDS (a group's keys placed by a wave prefix) and
-  // flushed into this workgroup's own region of the row's candidate buffer, at a place taken from
-  // an LDS counter; keys that would pass the region's end are dropped and the region is marked
-  // overflowed, so the first solve does not use the band. wcnt is the same in every lane.
-  uint32_t* const wbuf = s_cand[CAND ? threadIdx.x >> 6 : 0];
-  uint32_t wcnt = 0;
+  // Collected keys are buffered per lane in LDS (kCandLane slots, no cross-lane work per group).
+  // When some lane could not take a whole group's keys the wave flushes every lane's buffer into
+  // this workgroup's own region of the row's candidate buffer, at a place taken from an LDS
+  // counter, lanes in order by a wave prefix; keys that would pass the region's end are dropped and
+  // the region is marked overflowed, so the first solve does not use the band.
+  uint32_t* const lbuf = &s_cand[CAND ? threadIdx.x >> 6 : 0][CAND ? lane * kCandLane : 0];
+  uint32_t lcnt = 0;
   if (CAND && threadIdx.x == 0) s_rcnt = 0;
   auto flush = [&]() {
+    uint32_t wtot;
+    const uint32_t pre = wave_prefix_bits<3>(lcnt, wtot);
     uint32_t b0 = 0;
-    if (lane == 0) b0 = atomicAdd(&s_rcnt, wcnt);
-    const uint32_t b = (uint32_t)__shfl((int)b0, 0);
+    if (lane == 0) b0 = atomicAdd(&s_rcnt, wtot);
+    const uint32_t b = (uint32_t)__shfl((int)b0, 0) + pre;
     uint32_t* __restrict__ dst = creg_of(a, row) + blk * a.cand_region;
-    for (uint32_t j = lane; j < wcnt; j += 64)
-      if ((int64_t)b + j < a.cand_region) dst[b + j] = wbuf[j];
-    wcnt = 0;
+    for (uint32_t j = 0; j < lcnt; ++j)
+      if ((int64_t)b + j < a.cand_region) dst[b + j] = lbuf[j];
+    lcnt = 0;
   };
   for (int b = threadIdx.x; b < kB1 * kLaneCopies; b += kNT) {
     sm.pk[b] = 0;
@@ -2149,20 +2153,13 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
     for (int c = 0; c < 4; ++c)
       if (key[c] > cur[c]) atomicMax(&sm.mx[f[c]], key[c]);
   };
-  // the candidate band's keys of a group into the wave's buffer
+  // the candidate band's keys of a group into the lane's buffer (room for four made first)
   auto collect = [&](const float v[4]) {
-    uint32_t cm = 0;
+    if (__ballot(lcnt > (uint32_t)(kCandLane - 4))) flush();
 #pragma unroll
-    for (int c = 0; c < 4; ++c) cm |= (uint32_t)(key_of(v[c]) - blo1 < bspan) << c;
-    if (__ballot(cm != 0)) {
-      uint32_t tot;
-      uint32_t pos = wcnt + wave_prefix_bits<3>((uint32_t)__popc(cm), tot);
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if ((cm >> c) & 1) wbuf[pos++] = key_of(v[c]);
-      wcnt += tot;
-      // at most 256 keys arrive per group
-      if (wcnt > (uint32_t)(kCandWave - 256)) flush();
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t key = key_of(v[c]);
+      if (key - blo1 < bspan) lbuf[lcnt++] = key;
     }
   };
   if (CAND && bspan != 0) {
@@ -2175,7 +2172,7 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
     stream_groups<VEC, 4, kNT>(gr, beg, end, [&](int64_t, const float v[4], uint32_t) { hist(v); });
   }
   if constexpr (CAND) {
-    if (wcnt) flush();
+    if (__ballot(lcnt != 0)) flush();
     __syncthreads();
     // move the region to the row's compact list: one reservation per workgroup (a region that
     // overflowed reserves past the list's capacity, which disables the band)
@@ -2481,7 +2478,11 @@ __device__ __forceinline__ uint32_t wave_prefix_small(uint32_t n, int lane, uint
 // the wave's lanes places it, and it writes only its own set bits. Phase 2 reads no global memory
 // (a load would wait for every store issued before it), except for capped survivors beyond the
 // LDS list's capacity (a separate instantiation).
-constexpr int kCapList = 256;    // capped survivor values kept per wave
+// Capped survivors' values are kept in LDS by the phase-1 lane that decided them, kLaneCap per
+// lane and tile (rows padded to kLaneStride floats so that lanes fall on different banks); a wave
+// with a lane past that reads its capped values from global memory in phase 2.
+constexpr int kLaneCap = 8;
+constexpr int kLaneStride = kLaneCap + 1;
 constexpr int kSampleBatch = 8;  // float4 loads in flight per lane in the sampling pass
 constexpr int kDenseEmit = 1024;  // survivors of a wave's quarter tile (of 4096) above which emission goes by groups
 static_assert(kTileGroups % kSampleBatch == 0 && kTileGroups == 16, "tile shape");
@@ -2529,9 +2530,10 @@ __device__ __forceinline__ uint32_t group_code(const float v[4], uint32_t z) {
 
 template <bool VEC, bool HYB, int K>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
-  __shared__ float s_capv[K][kTileThreads / 64][kCapList];
+  __shared__ float s_capl[K][kTileThreads / 64][64 * kLaneStride];
   __shared__ alignas(16) uint8_t s_code[K][kTileElems / 4];  // per group: selection | sign << 4
-  __shared__ alignas(16) uint8_t s_capb[K][kTileElems / 4];  // per group: capped-survivor bits
+  // per group: capped-survivor bits | the deciding lane's capped count before the group << 4
+  __shared__ alignas(16) uint8_t s_capb[K][kTileElems / 4];
   __shared__ uint32_t s_wsel[K][kTileThreads / 64];
   __shared__ uint32_t s_wcap[K][kTileThreads / 64];
   __shared__ uint32_t s_wcl[K][kTileThreads / 64];
@@ -2576,6 +2578,10 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   // group j of this lane in a tile is tile group wv * (kWaveElems / 4) + 64 j + lane
   const int tg0 = wv * (kWaveElems / 4) + lane;
   uint64_t agg[K];  // per tile: (capped survivors << 31) | survivors
+  // capped-survivor bytes start at zero, so phase 1 writes only the groups that have some
+#pragma unroll
+  for (int kk = 0; kk < K; ++kk) *reinterpret_cast<uint4*>(&s_capb[kk][16 * tid]) = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
 
 #pragma unroll
   for (int kk = 0; kk < K; ++kk) {
@@ -2584,25 +2590,22 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     // phase 1 of tile part0 + kk
     const int64_t part = part0 + kk;
     const int64_t q0 = part * (kTileElems / 4) + tg0;
-    uint32_t nsel = 0, ncap = 0;
-    uint32_t ncl = 0;  // capped survivors of this wave so far (the LDS list keeps the first kCapList)
+    uint32_t nsel = 0;
+    uint32_t run = 0;  // this lane's capped survivors in the tile so far
+    float* const capl = &s_capl[kk][wv][lane * kLaneStride];
+    // cz lies inside z: a capped coordinate always passes its selection test
     auto record = [&](int j, const float v[4], uint32_t z, uint32_t cz) {
-      cz &= z;
       s_code[kk][tg0 + 64 * j] = (uint8_t)group_code(v, z);
-      s_capb[kk][tg0 + 64 * j] = (uint8_t)cz;
       nsel += (uint32_t)__popc(z);
-      if (__ballot(cz != 0)) {
-        ncap += (uint32_t)__popc(cz);
-        uint32_t tot;
-        uint32_t p = ncl + wave_prefix_bits<3>((uint32_t)__popc(cz), tot);
+      if (cz) {
+        s_capb[kk][tg0 + 64 * j] = (uint8_t)(cz | (min(run, 15u) << 4));
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           if ((cz >> k) & 1) {
-            if (p < (uint32_t)kCapList) s_capv[kk][wv][p] = v[k];
-            ++p;
+            if (run < (uint32_t)kLaneCap) capl[run] = v[k];
+            ++run;
           }
         }
-        ncl += tot;
       }
     };
     if (VEC && fast && (part + 1) * (int64_t)kTileElems <= c.d) {
@@ -2633,14 +2636,17 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         record(j, v, z, cz);
       }
     }
+    const bool lane_over = run > (uint32_t)kLaneCap;
+    uint32_t ncap = run;
     for (int o = 32; o > 0; o >>= 1) {
       nsel += __shfl_xor(nsel, o);
       ncap += __shfl_xor(ncap, o);
     }
+    const bool wave_over = __ballot(lane_over) != 0;
     if (lane == 0) {
       s_wsel[kk][wv] = nsel;
       s_wcap[kk][wv] = ncap;
-      s_wcl[kk][wv] = ncl;
+      s_wcl[kk][wv] = wave_over ? 1u : 0u;
     }
     __syncthreads();
     uint32_t tsel = 0, tcp = 0;
@@ -2728,7 +2734,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     }
     const int64_t e0 = part * (int64_t)kTileElems + 64 * tid;
     uint64_t sm = 0, nm = 0, cm = 0;  // selected, negative, capped-and-selected coordinates
-    uint32_t cr = 0;                  // rank of this thread's first capped survivor in its wave's list
+    uint32_t cr = 0;                  // hybrid: rank of this thread's first capped survivor in its wave
+    uint32_t cwd[4] = {0u, 0u, 0u, 0u};  // this thread's 16 capped-survivor bytes
     if (s_wsel[kk][wv]) {
       const uint4 cw = *reinterpret_cast<const uint4*>(&s_code[kk][16 * tid]);
       const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
@@ -2740,29 +2747,41 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
       }
       if (s_wcap[kk][wv]) {
         const uint4 bw = *reinterpret_cast<const uint4*>(&s_capb[kk][16 * tid]);
-        const uint32_t cwd[4] = {bw.x, bw.y, bw.z, bw.w};
+        cwd[0] = bw.x;
+        cwd[1] = bw.y;
+        cwd[2] = bw.z;
+        cwd[3] = bw.w;
 #pragma unroll
         for (int b = 0; b < 16; ++b) cm |= (uint64_t)((cwd[b >> 2] >> (8 * (b & 3))) & 0xF) << (4 * b);
-        uint32_t ctot;
-        cr = wave_prefix_bits<7>((uint32_t)__popcll(cm), ctot);
+        if constexpr (HYB) {
+          uint32_t ctot;
+          cr = wave_prefix_bits<7>((uint32_t)__popcll(cm), ctot);
+        }
       }
-      const bool lds_values = s_wcl[kk][wv] <= (uint32_t)kCapList;
+      const bool lds_values = s_wcl[kk][wv] == 0;
+      // the value of capped survivor b (0..63) of this thread's coordinates: its group 16 tid + b/4
+      // was decided by phase-1 lane (16 tid + b/4) mod 64, whose list holds it after the lane's
+      // earlier capped survivors (the byte's high nibble) and the group's lower ones
+      auto capval = [&](int b) -> float {
+        const int gi = b >> 2;
+        const uint32_t cb = (cwd[gi >> 2] >> (8 * (gi & 3))) & 0xFFu;
+        const uint32_t slot = (cb >> 4) + (uint32_t)__popc(cb & ((1u << (b & 3)) - 1u));
+        return s_capl[kk][wv][((16 * tid + gi) & 63) * kLaneStride + slot];
+      };
       if constexpr (!HYB) {
         uint32_t wtot;
         uint64_t pos = (excl & 0x7FFFFFFFull) + wbase + wave_prefix_bits<7>((uint32_t)__popcll(sm), wtot);
         int32_t* __restrict__ oi = a.idx + row * a.cap;
         float* __restrict__ ov = a.val + row * a.cap;
         auto emit = [&](auto from_lds) {
-          uint32_t r = cr;
           uint64_t m = sm;
           while (m) {
             const int b = __ffsll((unsigned long long)m) - 1;
             const uint64_t bit = 1ull << b;
             float val = (nm & bit) ? -inv : inv;
             if (cm & bit) {
-              if constexpr (decltype(from_lds)::value) val = s_capv[kk][wv][r];
+              if constexpr (decltype(from_lds)::value) val = capval(b);
               else val = c.row[e0 + b];
-              ++r;
             }
             if ((int64_t)pos < a.cap) {
               oi[pos] = (int32_t)(e0 + b);
@@ -2798,12 +2817,10 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             }
           }
           uint64_t m = cm;
-          uint32_t r = cr;
           while (m) {
             const int b = __ffsll((unsigned long long)m) - 1;
             const uint32_t below = (uint32_t)__popcll(sm & ((1ull << b) - 1ull));
-            *(GS_GLOBAL(float)*)(bv + off0 + 4u * below) = s_capv[kk][wv][r];
-            ++r;
+            *(GS_GLOBAL(float)*)(bv + off0 + 4u * below) = capval(b);
             m &= m - 1;
           }
         } else if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
@@ -2811,26 +2828,23 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
           // the capped-value list), one step j at a time, so the stores of a step fall on a few
           // consecutive lines instead of one line per lane
           const uint64_t base0 = (excl & 0x7FFFFFFFull) + wbase;
-          uint32_t carry = 0, ccarry = 0;
+          uint32_t carry = 0;
           for (int j = 0; j < kTileGroups; ++j) {
-            const int q = wv * (kWaveElems / 4) + 64 * j + lane;  // tile group
+            const int q = wv * (kWaveElems / 4) + 64 * j + lane;  // tile group (decided by this lane)
             const uint32_t code = s_code[kk][q];
             const uint32_t sel = code & 0xFu, neg = code >> 4;
-            const uint32_t cap = (uint32_t)s_capb[kk][q] & sel;
-            uint32_t stot, ctot;
+            const uint32_t cb = s_capb[kk][q], cap = cb & sel;
+            uint32_t stot;
             const uint32_t sp = wave_prefix_bits<3>((uint32_t)__popc(sel), stot);
-            const uint32_t cp = wave_prefix_bits<3>((uint32_t)__popc(cap), ctot);
             uint64_t p = base0 + carry + sp;
-            uint32_t r = ccarry + cp;
             const int64_t eq = part * (int64_t)kTileElems + 4 * (int64_t)q;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
               if ((sel >> k) & 1) {
                 float val = ((neg >> k) & 1) ? -inv : inv;
-                if ((cap >> k) & 1) {
-                  val = lds_values ? s_capv[kk][wv][r] : c.row[eq + k];
-                  ++r;
-                }
+                if ((cap >> k) & 1)
+                  val = lds_values ? s_capl[kk][wv][lane * kLaneStride + (cb >> 4) + __popc(cap & ((1u << k) - 1u))]
+                                   : c.row[eq + k];
                 if ((int64_t)p < a.cap) {
                   oi[p] = (int32_t)(eq + k);
                   ov[p] = val;
@@ -2839,7 +2853,6 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
               }
             }
             carry += stot;
-            ccarry += ctot;
           }
         } else if (lds_values) {
           emit(std::true_type{});
@@ -2859,14 +2872,12 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         float* __restrict__ va = a.val + row * a.cap;
         int32_t* __restrict__ ob = a.code_b + row * a.cap_b;
         auto emit_a = [&](auto from_lds) {
-          uint32_t r = cr;
           uint64_t m = cm;
           while (m) {
             const int b = __ffsll((unsigned long long)m) - 1;
             float val;
-            if constexpr (decltype(from_lds)::value) val = s_capv[kk][wv][r];
+            if constexpr (decltype(from_lds)::value) val = capval(b);
             else val = c.row[e0 + b];
-            ++r;
             if ((int64_t)pa < a.cap) {
               oa[pa] = (int32_t)(e0 + b);
               va[pa] = val;
@@ -2883,17 +2894,17 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             const int q = wv * (kWaveElems / 4) + 64 * j + lane;  // tile group
             const uint32_t code = s_code[kk][q];
             const uint32_t sel = code & 0xFu, neg = code >> 4;
-            const uint32_t cap = (uint32_t)s_capb[kk][q] & sel, oth = sel & ~cap;
+            const uint32_t cb = s_capb[kk][q], cap = cb & sel, oth = sel & ~cap;
             uint32_t atot, btot2;
             uint64_t qa = pa0 + wave_prefix_bits<3>((uint32_t)__popc(cap), atot);
             uint64_t qb = pb0 + wave_prefix_bits<3>((uint32_t)__popc(oth), btot2);
-            uint32_t r = (uint32_t)(qa - excl_cap - wbase_cap);  // rank in the wave's capped list
             const int64_t eq = part * (int64_t)kTileElems + 4 * (int64_t)q;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
               if ((cap >> k) & 1) {
-                const float val = lds_values ? s_capv[kk][wv][r] : c.row[eq + k];
-                ++r;
+                const float val =
+                    lds_values ? s_capl[kk][wv][lane * kLaneStride + (cb >> 4) + __popc(cap & ((1u << k) - 1u))]
+                               : c.row[eq + k];
                 if ((int64_t)qa < a.cap) {
                   oa[qa] = (int32_t)(eq + k);
                   va[qa] = val;

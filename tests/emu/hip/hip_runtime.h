@@ -186,6 +186,7 @@ inline unsigned __builtin_amdgcn_sad_u8(unsigned a, unsigned b, unsigned c) {
 struct uint4 {
   unsigned x, y, z, w;
 };
+inline uint4 make_uint4(unsigned x, unsigned y, unsigned z, unsigned w) { return uint4{x, y, z, w}; }
 inline int __popc(unsigned v) { return __builtin_popcount(v); }
 inline int __popcll(unsigned long long v) { return __builtin_popcountll(v); }
 inline void __builtin_amdgcn_s_sleep(int) { std::this_thread::yield(); }
