@@ -448,10 +448,11 @@ GS_HD int64_t pre_lines(int64_t len) {
   const int64_t nl = len / 16, ns = (int64_t)kPreWG * kPreLines;
   return nl < ns ? nl : ns;
 }
-// Refinement over candidates: at least kCandShare keys per workgroup (each workgroup adds its whole
-// window into the global copies, so fewer, fuller workgroups cost fewer global atomics), read
-// kCandLoads float4 per thread at a time.
+// Refinement over candidates: at least kCandShare keys per workgroup and at most kCandGroups
+// workgroups per row (each workgroup adds its whole window into the global copies, so fewer,
+// fuller workgroups cost fewer global atomics), read kCandLoads float4 per thread at a time.
 constexpr int64_t kCandShare = 1 << 14;
+constexpr int64_t kCandGroups = 128;
 constexpr int kCandLoads = 8;
 // keys a lane buffers in LDS before its wave flushes (an odd stride keeps the lanes on different
 // banks); sized so that the statistics workgroup stays within a quarter of the LDS (four resident
@@ -2239,12 +2240,13 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   const float* __restrict__ gr = a.g + base;
   int64_t beg = blk * a.chunk, end = min(len, beg + a.chunk);
   // the window lies in the candidate band: the row's collected keys, read as the non-negative
-  // floats they are, in equal shares (whole groups of 4, at least kCandShare keys) by the first of
-  // the row's workgroups
+  // floats they are, in equal shares (whole groups of 4, at least kCandShare keys, at most
+  // kCandGroups shares) by the first of the row's workgroups
   const bool from_cand = ctl->src != 0;
   if (from_cand) {
     const int64_t n = (int64_t)ctl->cand_n;
-    const int64_t share = max(kCandShare, (((n + a.nb - 1) / a.nb) + 3) & ~(int64_t)3);
+    const int64_t groups = min((int64_t)a.nb, kCandGroups);
+    const int64_t share = max(kCandShare, (((n + groups - 1) / groups) + 3) & ~(int64_t)3);
     beg = blk * share;
     end = min(n, beg + share);
     gr = reinterpret_cast<const float*>(cand_of(a, row));
