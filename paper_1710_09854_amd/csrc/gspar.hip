@@ -1972,7 +1972,8 @@ struct BandLds {
   double w[kNT / 64];
   uint64_t k[kNT / 64];
   int ired[kNT / 64];
-  double ge;  // the sample's G at the lower edge of the binade of 1/lambda*
+  double ge;   // the sample's G at the lower edge of the binade of 1/lambda*
+  double ge1;  // and at the lower edge of the next binade up
 };
 // G within this fraction of B at that edge: 1/lambda* may lie in the binade below.
 constexpr double kBandNear = 0.125;
@@ -1983,8 +1984,9 @@ constexpr double kBandNear = 0.125;
 // refine lies in [1/lambda*, 1/lambda_0]: 1/lambda_0 = S / B (Algorithm 3's start), and the exact
 // 1/lambda* is where G(tau) = #{a >= tau} + (sum of the a < tau) / tau falls to B (Proposition 1:
 // sum min(lambda a, 1) = B); G decreases in tau, so at binade edges its crossing gives the binade
-// e* of 1/lambda*. The exact solver refines the binade of 1/lambda* or the next occupied one above
-// it, so its band is e* and e* + 1, and e* - 1 too when the sample's G at e*'s lower edge is
+// e* of 1/lambda*. The exact solver refines the binade of 1/lambda*, or the next occupied one
+// above it when no key of that binade lies above 1/lambda* (only when the crossing is at its top),
+// so its band is e*, with e* - 1 or e* + 1 too when the sample's G at e*'s lower or upper edge is
 // within kBandNear of B (the sample may have misplaced the crossing); the greedy solver's
 // thresholds run from 1/lambda_0 = S / B down towards 1/lambda*, so its band reaches up to the
 // binade of 1.25 S / B (slack for the sample's estimate of S). Whole binades, so every refinement
@@ -2044,6 +2046,7 @@ GS_DI void cand_band(const Args& a, const PreHist* ph, double B, int64_t len, Ba
   int e = -1;
   for (int i = 0; i < kNT / 64; ++i) e = max(e, sm.ired[i]);
   if (t == e) sm.ge = G;
+  if (t == e + 1) sm.ge1 = G;
   __syncthreads();
   blo = bhi = 0;
   // Nothing looks capped (B times the sample's largest magnitude, bounded by its binade's top,
@@ -2052,7 +2055,7 @@ GS_DI void cand_band(const Args& a, const PreHist* ph, double B, int64_t len, Ba
   const bool uncapped = top >= 0 && B * ldexp(1.0, top - 126) <= 0.5 * f * tot;
   if (e >= 1 && B > 0.0 && tot > 0.0 && !uncapped) {
     const uint32_t elo = (uint32_t)e - (sm.ge < (1.0 + kBandNear) * B ? 1u : 0u);
-    uint32_t ehi = (uint32_t)e + 1;
+    uint32_t ehi = (uint32_t)e + (sm.ge1 >= (1.0 - kBandNear) * B ? 1u : 0u);
     if (a.solver == GSPAR_GREEDY) {
       const double t0 = 1.25 * f * tot / B;
       const uint32_t e0 = t0 < 3.0e38 ? (key_of((float)t0) >> 23) : 254u;
@@ -2154,8 +2157,11 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
     for (int c = 0; c < 4; ++c)
       if (key[c] > cur[c]) atomicMax(&sm.mx[f[c]], key[c]);
   };
-  // the candidate band's keys of a group into the lane's buffer (room for four made first)
+  // the candidate band's keys of a group into the lane's buffer (room for four made first); a wave
+  // whose groups all lie below the band (most of them) skips the group
   auto collect = [&](const float v[4]) {
+    const uint32_t kmax = max(max(key_of(v[0]), key_of(v[1])), max(key_of(v[2]), key_of(v[3])));
+    if (!__ballot(kmax >= blo1)) return;
     if (__ballot(lcnt > (uint32_t)(kCandLane - 4))) flush();
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
