@@ -72,7 +72,61 @@ def parse():
     ap.add_argument("--cells", action="store_true",
                     help="one JSON line per (workload, solver, rho) cell instead of the step line: median call "
                          "time warm and after evicting the caches, algorithmic HBM fraction, oracle rate")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="one JSON line instead of the step line: the bandwidth a plain read kernel and a plain "
+                         "copy kernel reach on 1 GiB (the default workload's gradient size)")
     return ap.parse_args()
+
+
+def stream_probe():
+    """Achievable stream bandwidth on this part: the measurement build's plain read kernel over a
+    1 GiB buffer (4 B per element read once) and its copy kernel over 512 MiB (read + written), each
+    the median of 20 timings with events on the stream: warm (ten runs back to back per timing) and
+    right after a 512 MiB write that evicts the last-level cache (one run)."""
+    import numpy as np
+    import torch
+
+    import paper_1710_09854_amd as gs
+
+    dev = torch.device("cuda:0")
+    n = 1 << 28
+    src = torch.rand(n, dtype=torch.float32, device=dev)
+    sink = torch.zeros(1, dtype=torch.float64, device=dev)
+    half = n // 2
+    dst = torch.empty(half, dtype=torch.float32, device=dev)
+    scratch = torch.empty(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+
+    def timed(fn, evict):
+        # warm: ten runs back to back, so the host's launch time is hidden behind the kernels;
+        # cold: one run queued right behind the eviction (which keeps the device busy meanwhile)
+        reps = 1 if evict else 10
+        if evict:
+            scratch.fill_(0.5)
+        else:
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e-3 / reps
+
+    read = lambda: gs.probe_stream(src, sink=sink)
+    copy = lambda: gs.probe_stream(src[:half], dst=dst)
+    for _ in range(3):
+        read()
+        copy()
+    torch.cuda.synchronize()
+    out = {"probe": "stream", "read_bytes": 4 * n, "copy_bytes": 8 * half}
+    for name, fn, nbytes in (("read", read, 4 * n), ("copy", copy, 8 * half)):
+        for evict in (False, True):
+            t = float(np.median([timed(fn, evict) for _ in range(20)]))
+            key = name + ("_cold" if evict else "_warm")
+            out[key + "_us"] = t * 1e6
+            out[key + "_GBps"] = nbytes / t / 1e9
+            out[key + "_frac_of_8TBps"] = nbytes / t / 1e9 / HBM_PEAK_GBS
+    print(json.dumps(out), flush=True)
 
 
 def src_hash() -> str:
@@ -407,6 +461,9 @@ def main():
         sys.exit(2)
     if args.cells:
         cells(args)
+        return
+    if args.stream_probe:
+        stream_probe()
         return
     if args.workload == "all":
         print("--workload all needs --cells", file=sys.stderr)

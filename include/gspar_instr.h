@@ -49,6 +49,13 @@ uint32_t gspar_check_cap_key(double lam);
 /* Philox4x32-10 of counter ctr[4] under key[2]. */
 void gspar_check_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out);
 
+/* Stream probe on `stream` (not timed here; the caller brackets it with events): with dst NULL,
+ * reads the n floats of src (device, 16-byte aligned, n a multiple of 4) and adds their sum to
+ * *sink (device double); otherwise copies them to dst (device, 16-byte aligned, not overlapping
+ * src). A plain kernel that reads (or reads and writes) each byte once, to compare the path's
+ * bandwidth with. Returns GSPAR_ERR_ARG for bad pointers or sizes. */
+int gspar_probe_stream(const float* src, float* dst, int64_t n, double* sink, void* stream);
+
 #pragma GCC visibility pop
 
 #ifdef __cplusplus

@@ -128,8 +128,24 @@ def instr_lib():
         L.gspar_prof_read.restype = i32
         L.gspar_prof_disarm.argtypes = []
         L.gspar_prof_disarm.restype = i32
+        vp, i64 = ctypes.c_void_p, ctypes.c_int64
+        L.gspar_probe_stream.argtypes = [vp, vp, i64, vp, vp]
+        L.gspar_probe_stream.restype = i32
         _instr = L
     return _instr
+
+
+def probe_stream(src, dst=None, sink=None, stream=None):
+    """The measurement build's stream probe on the current stream: reads src (fp32, contiguous,
+    on the device) and adds its sum into sink (a one-element float64 device tensor), or copies it
+    into dst. For bandwidth comparisons only."""
+    import torch
+
+    L = instr_lib()
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    rc = L.gspar_probe_stream(src.data_ptr(), dst.data_ptr() if dst is not None else None, src.numel(),
+                              sink.data_ptr() if sink is not None else None, s)
+    _check(rc, "gspar_probe_stream")
 
 
 def _solver_id(solver) -> int:

@@ -3375,6 +3375,38 @@ static void* scratch_of_current_device() {
 
 using namespace gspar;
 
+#ifdef GSPAR_INSTRUMENT
+// ------------------------------------------------------------------------------------------
+// Stream probes (measurement build only): the bandwidth a plain kernel reaches on the same
+// buffers, to set the path's figures against. Laid out like the statistics pass of one row:
+// kProbeGroups workgroups of kNT threads, each streaming one contiguous chunk through the same
+// loop (stream_groups, four float4 loads in flight per thread); the read probe adds the values (so
+// no load is dead) into one double per wave, the copy probe writes them to dst.
+// ------------------------------------------------------------------------------------------
+namespace gspar {
+constexpr int kProbeGroups = 512;
+__global__ void __launch_bounds__(kNT) k_probe_read(const float* __restrict__ src, int64_t n, double* sink) {
+  const int64_t chunk = ((n + kProbeGroups - 1) / kProbeGroups + 3) & ~(int64_t)3;
+  const int64_t beg = (int64_t)blockIdx.x * chunk, end = min(n, beg + chunk);
+  float acc = 0.0f;
+  if (beg < end)
+    stream_groups<true, 4, kNT>(src, beg, end, [&](int64_t, const float v[4], uint32_t) {
+      acc += (v[0] + v[1]) + (v[2] + v[3]);
+    });
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if ((threadIdx.x & 63) == 0) atomicAdd(sink, (double)acc);
+}
+__global__ void __launch_bounds__(kNT) k_probe_copy(const float* __restrict__ src, float* __restrict__ dst, int64_t n) {
+  const int64_t chunk = ((n + kProbeGroups - 1) / kProbeGroups + 3) & ~(int64_t)3;
+  const int64_t beg = (int64_t)blockIdx.x * chunk, end = min(n, beg + chunk);
+  if (beg < end)
+    stream_groups<true, 4, kNT>(src, beg, end, [&](int64_t q, const float v[4], uint32_t m) {
+      if (m == 0xFu) *reinterpret_cast<float4*>(dst + 4 * q) = make_float4(v[0], v[1], v[2], v[3]);
+    });
+}
+}  // namespace gspar
+#endif  // GSPAR_INSTRUMENT
+
 extern "C" {
 
 size_t gspar_workspace_bytes(int64_t rows, int64_t d, int solver) {
@@ -3789,6 +3821,17 @@ double gspar_check_exact_sum(const float* x, int64_t n) {
 }
 
 uint32_t gspar_check_cap_key(double lam) { return cap_key(lam); }
+
+int gspar_probe_stream(const float* src, float* dst, int64_t n, double* sink, void* stream) {
+  if (!src || n < 0 || n % 4 != 0 || (uintptr_t)src % 16 || (dst && (uintptr_t)dst % 16) || (!dst && !sink))
+    return GSPAR_ERR_ARG;
+  if (n == 0) return GSPAR_OK;
+  hipStream_t s = (hipStream_t)stream;
+  const dim3 grid(kProbeGroups), block(kNT);
+  if (dst) hipLaunchKernelGGL(k_probe_copy, grid, block, 0, s, src, dst, n);
+  else hipLaunchKernelGGL(k_probe_read, grid, block, 0, s, src, n, sink);
+  return hipGetLastError() == hipSuccess ? GSPAR_OK : GSPAR_ERR_HIP;
+}
 
 void gspar_check_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
   uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
