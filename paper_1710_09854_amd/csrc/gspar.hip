@@ -431,10 +431,13 @@ constexpr int64_t kMinChunk = 8192;  // fewest coordinates per histogram workgro
 
 // Candidate band: rows of at least kCandMinRow coordinates predict, from a sample of the row, the
 // binades holding every threshold the solvers will refine, and the statistics pass copies the keys
-// inside them to a per-row buffer, so refinement passes read those keys instead of the row.
-// (a build may lower the row-length threshold to exercise the band on small inputs)
+// inside them to a per-row buffer, so refinement passes read those keys instead of the row. The
+// sample costs a launch (about 5 us) and the collection a few per cent of the statistics pass, a
+// loss on rows whose passes over the row take about as long or that need no window at all, so
+// only rows of 2^25 coordinates and more take the band (a build may lower the threshold to
+// exercise the band on small inputs).
 #ifndef GSPAR_CAND_MIN_ROW
-#define GSPAR_CAND_MIN_ROW (1 << 22)
+#define GSPAR_CAND_MIN_ROW (1 << 25)
 #endif
 constexpr int64_t kCandMinRow = GSPAR_CAND_MIN_ROW;
 static_assert(kCandMinRow >= 1024, "a row must hold at least 64 whole lines to be sampled");

@@ -168,10 +168,10 @@ def _row_state(ws, row=0):
 
 @pytest.mark.parametrize("solver", ["greedy", "exact"])
 def test_candidate_band_on_a_long_row(gs, solver):
-    """A row of 2^23 + 12 coordinates (long enough for a candidate band): the statistics pass
+    """A row of 2^25 + 12 coordinates (long enough for a candidate band): the statistics pass
     collects exactly the keys of the predicted binades, the refinement windows read them, and the
     result equals the oracle's under the parity rule (lambda bit for bit for the exact solver)."""
-    d = (1 << 23) + 12
+    d = (1 << 25) + 12
     g = W.t_mixture(d, 71)
     keys = np.abs(g).view(np.uint32)
     gd = torch.from_numpy(g).cuda().reshape(1, -1)
@@ -198,10 +198,10 @@ def test_candidate_band_on_a_long_row(gs, solver):
 
 
 def test_candidate_band_on_ragged_rows(gs):
-    """Two rows of 2^22 + 3 coordinates stored with a leading dimension of 2^22 + 4 (vector loads;
+    """Two rows of 2^25 + 3 coordinates stored with a leading dimension of 2^25 + 4 (vector loads;
     each row ends in a partial group of 3): the band is collected over the whole row, its last
     partial group included, and both rows match the oracle (exact solver, lambda bit for bit)."""
-    rows, d, ld = 2, (1 << 22) + 3, (1 << 22) + 4
+    rows, d, ld = 2, (1 << 25) + 3, (1 << 25) + 4
     g = np.stack([W.t_mixture(d, 81 + r) for r in range(rows)])
     # the partial group holds a key of each density's band and the row's largest magnitude
     g[:, -3:] = np.float32([12.0, -3000.0, 1.0e4])
