@@ -53,7 +53,7 @@ constexpr uint32_t kKeyInf = 0x7F800000u;   // bit pattern of +inf: keys >= this
 constexpr uint32_t kNone = 0xFFFFFFFFu;
 constexpr int kNT = 512;                    // threads of the histogram / solver workgroups
 constexpr int kLaneCopies = 8;              // LDS copies of the statistics histogram (by lane)
-constexpr int kC1 = 8;                      // global copies of the level-1 histogram per row
+constexpr int kC1 = 4;                      // global copies of the level-1 histogram per row
 constexpr int kC23 = 2;                     // global copies of the level-2 / level-3 histograms
 constexpr int kB1 = 256;                    // level 1: one bin per binade (key >> 23)
 constexpr int kB2 = 4096;                   // level 2: one binade, 2^11 keys per bin
