@@ -2610,12 +2610,12 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
       nsel += (uint32_t)__popc(z);
       if (cz) {
         s_capb[kk][tg0 + 64 * j] = (uint8_t)(cz | (min(run, 15u) << 4));
+        // every value goes to the next free slot (the row's pad slot once the row is full), and
+        // only a capped one takes it, so no lane branches per coordinate
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          if ((cz >> k) & 1) {
-            if (run < (uint32_t)kLaneCap) capl[run] = v[k];
-            ++run;
-          }
+          capl[min(run, (uint32_t)kLaneCap)] = v[k];
+          run += (cz >> k) & 1u;
         }
       }
     };
