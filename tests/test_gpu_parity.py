@@ -228,6 +228,40 @@ def test_candidate_band_on_ragged_rows(gs):
             assert float(plan.lam[r].item()) == sol.lam and int(plan.k[r].item()) == sol.k
 
 
+def test_candidate_band_with_smaller_workspaces(gs):
+    """The same long row with the full workspace (band used), a workspace with room for 2^16
+    candidates only (the band overflows and is dropped) and the fixed part alone (no band): the
+    three calls return identical results, equal to the oracle's."""
+    d = (1 << 25) + 12
+    g = W.t_mixture(d, 73)
+    gd = torch.from_numpy(g).cuda().reshape(1, -1)
+    seeds = torch.tensor([9], dtype=torch.int64, device="cuda")
+    rho = 0.1
+    fixed = gs.workspace_bytes(1, d, "variance")  # the layout without candidate buffers
+    full = gs.workspace_bytes(1, d, "exact")
+    outs = []
+    for name, size in (("full", full), ("2^16 candidates", fixed + 8 * (1 << 16) + 4096), ("fixed part", fixed)):
+        plan = gs.Plan(1, d, solver="exact", cap_per_row=gs.capacity_hint(d, rho))
+        assert size <= plan.ws.numel()
+        plan.ws = plan.ws[:size]
+        plan.run(gd, torch.tensor([rho], dtype=torch.float64, device="cuda"), seeds)
+        torch.cuda.synchronize()
+        st = _row_state(plan.ws)
+        n = int(plan.nnz[0].item())
+        _say(f"[band-ws] {name}: {size} bytes band=[{st['band_lo'] >> 23},{st['band_hi'] >> 23}) cand={st['cand_n']} "
+             f"src={st['src']} nnz={n}")
+        assert int(plan.flags[0].item()) == 0
+        outs.append((plan.idx[0, :n].cpu().numpy(), plan.val[0, :n].cpu().numpy(), float(plan.lam[0].item()),
+                     int(plan.k[0].item()), st["src"]))
+    assert outs[0][4] == 1 and outs[1][4] == 0 and outs[2][4] == 0
+    for o in outs[1:]:
+        assert np.array_equal(o[0], outs[0][0]) and np.array_equal(o[1], outs[0][1]) and o[2:4] == outs[0][2:4]
+    sol = oracle.solve(g, rho, "exact", 2)
+    idx, val, lam, k, _ = outs[0]
+    compare_sample(g, sol.p, 9, idx, val, idx.size, lam, sol.lam)
+    assert lam == sol.lam and k == sol.k
+
+
 def test_special_cases(gs):
     d = 50000
     z = np.zeros(d, np.float32)
