@@ -2481,14 +2481,15 @@ __device__ __forceinline__ uint32_t wave_prefix_small(uint32_t n, int lane, uint
 
 // Phase 1: each lane decides kTileGroups groups of its wave's quarter (coalesced loads, one
 // Philox block per group) and writes one byte per group to LDS: selection bits (low nibble) and
-// sign bits (high nibble); capped survivors (emitted unscaled) append their value, in index
-// order, to a small per-wave LDS list and set their bit in a second byte array. The wave totals
-// give the tile aggregate, published at once; wave 0 then looks back for the tile's prefix.
+// sign bits (high nibble); capped survivors (emitted unscaled) append their value to the deciding
+// lane's own LDS row, and a second byte array holds per group their bits and the lane's running
+// count of them. The wave totals give the tile aggregate, published at once; wave 0 then looks back
+// for the tile's prefix.
 // Phase 2: thread t owns the tile's groups [16t, 16t + 16), i.e. 64 consecutive coordinates
 // inside its own wave's quarter, so its survivors are contiguous in the output: one prefix over
 // the wave's lanes places it, and it writes only its own set bits. Phase 2 reads no global memory
-// (a load would wait for every store issued before it), except for capped survivors beyond the
-// LDS list's capacity (a separate instantiation).
+// (a load would wait for every store issued before it), except in a wave where some lane kept
+// more capped values than its LDS row holds (a separate instantiation).
 // Capped survivors' values are kept in LDS by the phase-1 lane that decided them, kLaneCap per
 // lane and tile (rows padded to kLaneStride floats so that lanes fall on different banks); a wave
 // with a lane past that reads its capped values from global memory in phase 2.
@@ -2806,7 +2807,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         if (lds_values && s_wsel[kk][wv] <= (uint32_t)kDenseEmit && wave_end <= (uint64_t)a.cap &&
             wave_end <= ((uint64_t)1 << 30)) {
           // the common case: every survivor of the wave within the capacity (no store needs a bound
-          // check) and its capped values in the LDS list. A first loop writes every survivor with
+          // check) and its capped values in the lanes' LDS rows. A first loop writes every survivor with
           // the sign's +-1/lambda, a second (capped survivors are few) overwrites the capped ones'
           // values with g_i; both stores of a value come from this lane in program order. 32-bit
           // byte offsets from the row's output arrays, masks in 32-bit halves.
@@ -2836,7 +2837,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
           }
         } else if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
           // many survivors: lane l takes the wave's groups 64 j + l (the order of phase 1 and of
-          // the capped-value list), one step j at a time, so the stores of a step fall on a few
+          // this lane's capped-value row), one step j at a time, so the stores of a step fall on a few
           // consecutive lines instead of one line per lane
           const uint64_t base0 = (excl & 0x7FFFFFFFull) + wbase;
           uint32_t carry = 0;
