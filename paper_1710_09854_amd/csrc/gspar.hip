@@ -2470,15 +2470,6 @@ __device__ uint64_t wave_tile_aggregate(const TileCtx& c, int64_t part, int lane
   return (nc << 31) | n;
 }
 
-// Exclusive prefix over the lanes of a wave of n in [0, 7], from three ballots; `total` receives
-// the wave's sum.
-__device__ __forceinline__ uint32_t wave_prefix_small(uint32_t n, int lane, uint32_t& total) {
-  const unsigned long long b0 = __ballot(n & 1), b1 = __ballot(n & 2), b2 = __ballot(n & 4);
-  const unsigned long long lt = (1ull << lane) - 1;
-  total = (uint32_t)(__popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2));
-  return (uint32_t)(__popcll(b0 & lt) + 2 * __popcll(b1 & lt) + 4 * __popcll(b2 & lt));
-}
-
 // Phase 1: each lane decides kTileGroups groups of its wave's quarter (coalesced loads, one
 // Philox block per group) and writes one byte per group to LDS: selection bits (low nibble) and
 // sign bits (high nibble); capped survivors (emitted unscaled) append their value to the deciding
@@ -2487,7 +2478,9 @@ __device__ __forceinline__ uint32_t wave_prefix_small(uint32_t n, int lane, uint
 // for the tile's prefix.
 // Phase 2: thread t owns the tile's groups [16t, 16t + 16), i.e. 64 consecutive coordinates
 // inside its own wave's quarter, so its survivors are contiguous in the output: one prefix over
-// the wave's lanes places it, and it writes only its own set bits. Phase 2 reads no global memory
+// the wave's lanes places it, and it writes only its own set bits (for up to kStageEmit survivors
+// per wave through an LDS staging area that the wave then stores with consecutive lanes on
+// consecutive slots). Phase 2 reads no global memory
 // (a load would wait for every store issued before it), except in a wave where some lane kept
 // more capped values than its LDS row holds (a separate instantiation).
 // Capped survivors' values are kept in LDS by the phase-1 lane that decided them, kLaneCap per
@@ -2497,7 +2490,12 @@ constexpr int kLaneCap = 8;
 constexpr int kLaneStride = kLaneCap + 1;
 constexpr int kSampleBatch = 8;  // float4 loads in flight per lane in the sampling pass
 constexpr int kDenseEmit = 1024;  // survivors of a wave's quarter tile (of 4096) above which emission goes by groups
+// Survivors of a wave's quarter tile up to which emission is staged in LDS: 4-byte entries in the
+// quarter's 2 KB of code and capped-survivor bytes, free once every lane has read its own.
+constexpr int kStageEmit = 512;
 static_assert(kTileGroups % kSampleBatch == 0 && kTileGroups == 16, "tile shape");
+static_assert(2 * kStageEmit <= kWaveElems / 4 && kTileElems <= 65536 && 64 * kLaneStride <= 1024,
+              "a staged entry: 16-bit tile coordinate, 10-bit capped-value place, within the quarter's bytes");
 // Below this lambda, lambda * 2^32 * |g| could round differently from (lambda * |g|) * 2^32.
 constexpr double kLamScaledMin = 0x1p-900;
 
@@ -2804,9 +2802,60 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
           }
         };
         const uint64_t wave_end = (excl & 0x7FFFFFFFull) + wbase + s_wsel[kk][wv];
-        if (lds_values && s_wsel[kk][wv] <= (uint32_t)kDenseEmit && wave_end <= (uint64_t)a.cap &&
+        if (lds_values && s_wsel[kk][wv] <= (uint32_t)kStageEmit && wave_end <= (uint64_t)a.cap &&
             wave_end <= ((uint64_t)1 << 30)) {
-          // the common case: every survivor of the wave within the capacity (no store needs a bound
+          // the common case, staged: every survivor of the wave within the capacity and its capped
+          // values in the lanes' LDS rows. Each lane writes its survivors' entries (tile coordinate,
+          // 16 bits; value code: sign in bit 15, or bit 14 and the capped value's place in the LDS
+          // rows) at its prefix in the wave's quarter of the code and capped-survivor bytes, which
+          // every lane of the wave has read by now (LDS operations of a wave complete in order);
+          // then lane l writes entries l, l + 64, ... so that each store covers consecutive
+          // addresses, instead of one address per lane far apart.
+          uint16_t* const si = reinterpret_cast<uint16_t*>(&s_code[kk][wv * (kWaveElems / 4)]);
+          uint16_t* const sc = reinterpret_cast<uint16_t*>(&s_capb[kk][wv * (kWaveElems / 4)]);
+          const uint64_t wpos = (excl & 0x7FFFFFFFull) + wbase;  // the wave's first output slot
+          const uint32_t lpre = (uint32_t)(pos - wpos);
+          __builtin_amdgcn_wave_barrier();
+          uint32_t j = lpre;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            uint32_t m = (uint32_t)(sm >> (32 * h));
+            const uint32_t neg = (uint32_t)(nm >> (32 * h));
+            const uint32_t c0 = (uint32_t)(64 * tid + 32 * h);
+            while (m) {
+              const int b = __builtin_ctz(m);
+              si[j] = (uint16_t)(c0 + b);
+              sc[j] = (uint16_t)(((neg >> b) & 1u) << 15);
+              ++j;
+              m &= m - 1u;
+            }
+          }
+          uint64_t mc = cm;
+          while (mc) {
+            const int b = __ffsll((unsigned long long)mc) - 1;
+            const uint32_t below = (uint32_t)__popcll(sm & ((1ull << b) - 1ull));
+            const int gi = b >> 2;
+            const uint32_t cb = (cwd[gi >> 2] >> (8 * (gi & 3))) & 0xFFu;
+            const uint32_t slot = (cb >> 4) + (uint32_t)__popc(cb & ((1u << (b & 3)) - 1u));
+            sc[lpre + below] = (uint16_t)(0x4000u | (uint32_t)(((16 * tid + gi) & 63) * kLaneStride + slot));
+            mc &= mc - 1;
+          }
+          __builtin_amdgcn_wave_barrier();
+          const uint32_t wn = s_wsel[kk][wv];
+          const float* const capw = &s_capl[kk][wv][0];
+          gchar* __restrict__ bi = uniform_ptr(oi) + 4u * (uint32_t)wpos;
+          gchar* __restrict__ bv = uniform_ptr(ov) + 4u * (uint32_t)wpos;
+          const int32_t t0c = (int32_t)(part * (int64_t)kTileElems);
+          for (uint32_t i = (uint32_t)lane; i < wn; i += 64u) {
+            const uint32_t x = si[i], cc = sc[i];
+            const float cv = capw[cc & 0x3FFu];
+            const float val = (cc & 0x4000u) ? cv : ((cc & 0x8000u) ? -inv : inv);
+            *(GS_GLOBAL(int32_t)*)(bi + 4u * i) = t0c + (int32_t)x;
+            *(GS_GLOBAL(float)*)(bv + 4u * i) = val;
+          }
+        } else if (lds_values && s_wsel[kk][wv] <= (uint32_t)kDenseEmit && wave_end <= (uint64_t)a.cap &&
+                   wave_end <= ((uint64_t)1 << 30)) {
+          // the same between kStageEmit and kDenseEmit survivors, unstaged: every survivor of the wave within the capacity (no store needs a bound
           // check) and its capped values in the lanes' LDS rows. A first loop writes every survivor with
           // the sign's +-1/lambda, a second (capped survivors are few) overwrites the capped ones'
           // values with g_i; both stores of a value come from this lane in program order. 32-bit

@@ -74,6 +74,26 @@ def test_row_parity(gs, name, solver, rho):
     _say(f"   ok nnz={n} oracle={rep['nnz_oracle']} excused={rep['excused']} lam={lam:.12g}")
 
 
+def test_emission_paths(gs):
+    """Rows whose waves emit through each of the sampling pass's paths: staged in LDS (up to 512
+    survivors in a wave's 4096 coordinates), written directly lane by lane (up to 1024), written
+    group by group (more), and a row that mixes them (a loud half and a quiet half, with a tile and
+    a wave's quarter across the boundary)."""
+    loud = W.normal(100000, 41)
+    quiet = W.normal(100003, 42) * np.float32(0.01)
+    cases = [("staged", W.t_mixture(200003, 40), 0.1), ("direct", W.normal(200003, 43), 0.2),
+             ("groups", W.normal(200003, 44), 0.4), ("mixed", np.concatenate([loud, quiet]), 0.1)]
+    for label, g, rho in cases:
+        for solver in ("exact", "greedy"):
+            seed = 77
+            _say(f"[emission] {label} d={g.size} solver={solver} rho={rho} seed={seed}")
+            sol = oracle.solve(g, rho, solver, 2)
+            idx, val, n, lam, k, fl = _run_row(gs, g, rho, solver, seed, cap=g.size)
+            assert fl == 0, fl
+            rep = compare_sample(g, sol.p, seed, idx, val, n, lam, sol.lam)
+            _say(f"   ok nnz={n} oracle={rep['nnz_oracle']} excused={rep['excused']}")
+
+
 @pytest.mark.parametrize("iters", [0, 1, 3, 8])
 def test_greedy_iterations(gs, iters):
     g = W.t_mixture(150000, 11)

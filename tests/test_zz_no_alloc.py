@@ -1,7 +1,7 @@
 """The no-allocation entry point, sparsify_sample_compact_batched_noalloc, through the C ABI: its
 scratch is the library's fixed device array instead of a caller workspace. Its outputs must equal
-those of sparsify_sample_compact_batched bit for bit (the same kernels), on two calls in a row
-with the second one smaller (the array keeps the first call's contents), and a call that needs
+those of sparsify_sample_compact_batched bit for bit (the same kernels), on calls in a row, each
+smaller than the one before (the array keeps the earlier calls' contents), and a call that needs
 more scratch than the array holds is rejected before anything is enqueued."""
 import sys
 
@@ -54,9 +54,11 @@ def _noalloc(gs, g, rhos, seeds, solver, cap):
 
 @pytest.mark.parametrize("solver", ["greedy", "exact"])
 def test_noalloc_matches_the_workspace_entry_point(gs, solver):
-    """Two calls in a row, the second on fewer and shorter rows, each against the workspace entry
-    point (bit for bit) and, for its first row, against the oracle under the parity rule."""
-    for rows, d, seed in ((8, 300007, 10), (3, 70001, 40)):
+    """Three calls in a row, each smaller than the one before, the first a single row of
+    2^25 + 8 coordinates (long enough for a candidate band, kept in the array too), each against
+    the workspace entry point (bit for bit) and, for its first row, against the oracle under the
+    parity rule."""
+    for rows, d, seed in ((1, (1 << 25) + 8, 70), (8, 300007, 10), (3, 70001, 40)):
         gh = _batch(rows, d, seed)
         g = torch.from_numpy(gh).cuda()
         rhos = [(0.01, 0.1, 0.3)[r % 3] for r in range(rows)]
