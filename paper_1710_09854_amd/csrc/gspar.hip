@@ -2538,6 +2538,16 @@ __device__ __forceinline__ uint32_t group_code(const float v[4], uint32_t z) {
   return __builtin_amdgcn_sad_u8((s01 | s23) & 0x80402010u, 0u, z);
 }
 
+// The nibbles of the eight bytes of (w0, w1), byte 0 of w0 first: lo holds their low nibbles and hi
+// their high nibbles, byte k's at bits [4k, 4k + 4). v_perm_b32 gathers the even and the odd bytes
+// (selectors 0-7 pick a byte of the pair, w1 above w0), and one bit-field insert interleaves each.
+__device__ __forceinline__ void byte_nibbles(uint32_t w0, uint32_t w1, uint32_t& lo, uint32_t& hi) {
+  const uint32_t ev = __builtin_amdgcn_perm(w1, w0, 0x06040200u);  // bytes 6, 4, 2, 0
+  const uint32_t od = __builtin_amdgcn_perm(w1, w0, 0x07050301u);  // bytes 7, 5, 3, 1
+  lo = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
+  hi = ((ev >> 4) & 0x0F0F0F0Fu) | (od & 0xF0F0F0F0u);
+}
+
 template <bool VEC, bool HYB, int K>
 __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
   __shared__ float s_capl[K][kTileThreads / 64][64 * kLaneStride];
@@ -2748,21 +2758,21 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
     uint32_t cwd[4] = {0u, 0u, 0u, 0u};  // this thread's 16 capped-survivor bytes
     if (s_wsel[kk][wv]) {
       const uint4 cw = *reinterpret_cast<const uint4*>(&s_code[kk][16 * tid]);
-      const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
-#pragma unroll
-      for (int b = 0; b < 16; ++b) {
-        const uint64_t byte = (words[b >> 2] >> (8 * (b & 3))) & 0xFF;
-        sm |= (byte & 0xF) << (4 * b);
-        nm |= (byte >> 4) << (4 * b);
-      }
+      uint32_t s0, s1, n0, n1;
+      byte_nibbles(cw.x, cw.y, s0, n0);
+      byte_nibbles(cw.z, cw.w, s1, n1);
+      sm = ((uint64_t)s1 << 32) | s0;
+      nm = ((uint64_t)n1 << 32) | n0;
       if (s_wcap[kk][wv]) {
         const uint4 bw = *reinterpret_cast<const uint4*>(&s_capb[kk][16 * tid]);
         cwd[0] = bw.x;
         cwd[1] = bw.y;
         cwd[2] = bw.z;
         cwd[3] = bw.w;
-#pragma unroll
-        for (int b = 0; b < 16; ++b) cm |= (uint64_t)((cwd[b >> 2] >> (8 * (b & 3))) & 0xF) << (4 * b);
+        uint32_t c0, c1, u0, u1;
+        byte_nibbles(bw.x, bw.y, c0, u0);
+        byte_nibbles(bw.z, bw.w, c1, u1);
+        cm = ((uint64_t)c1 << 32) | c0;
         if constexpr (HYB) {
           uint32_t ctot;
           cr = wave_prefix_bits<7>((uint32_t)__popcll(cm), ctot);
