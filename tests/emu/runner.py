@@ -265,8 +265,9 @@ def row_state(ws, row=0):
             "cand_n": int(b[232:240].view(np.uint64)[0]), "stage": u32(208)}
 
 
-def sample_row_ws(L, g, rho, solver, seed, iters=2):
-    """sample_row that also returns the workspace, for row_state."""
+def sample_row_ws(L, g, rho, solver, seed, iters=2, ws_bytes=None):
+    """sample_row that also returns the workspace, for row_state (a workspace of ws_bytes bytes
+    when given, else the size the library asks for)."""
     d = g.size
     idx = np.zeros(d, np.int32)
     val = np.zeros(d, np.float32)
@@ -275,7 +276,7 @@ def sample_row_ws(L, g, rho, solver, seed, iters=2):
     k = np.zeros(1, np.int64)
     fl = np.zeros(1, np.uint32)
     sid = {"greedy": 0, "exact": 1, "variance": 2}[solver]
-    wsb = L.gspar_workspace_bytes(1, d, sid)
+    wsb = L.gspar_workspace_bytes(1, d, sid) if ws_bytes is None else ws_bytes
     keep, ws = _aligned(wsb)
     rc = L.sparsify_sample_compact(g.ctypes.data, d, rho, sid, iters, seed, idx.ctypes.data, val.ctypes.data, d,
                                    nnz.ctypes.data, lam.ctypes.data, k.ctypes.data, fl.ctypes.data, ws.ctypes.data,
@@ -340,6 +341,38 @@ def check_candidates(L, verbose=True):
                   f"cand={st['cand_n']} src={st['src']}", flush=True)
     if verbose:
         print("candidate cases ok", flush=True)
+    return True
+
+
+def check_band_region_overflow(L, verbose=True):
+    """A band row whose first statistics workgroup holds more band keys than its staging region:
+    2^17 coordinates, a workspace with room for 2^16 candidates (16 regions of 4096 for chunks of
+    8192), the first chunk's magnitudes uniform in [8, 16) and the rest 1e-3 N(0, 1), rho putting
+    1/lambda near 12. The band is predicted and collected, the overflowing region makes the first
+    solve drop it, the solver refines over the row, and the result equals the oracle's (lambda bit
+    for bit for the exact solver)."""
+    d = 1 << 17
+    rng = np.random.default_rng(92)
+    g = (rng.standard_normal(d) * 1e-3).astype(np.float32)
+    big = rng.uniform(8.0, 16.0, 8192) * np.where(rng.random(8192) < 0.5, -1.0, 1.0)
+    g[:8192] = big.astype(np.float32)
+    rho = 0.0574
+    fixed = L.gspar_workspace_bytes(1, d, 2)  # the layout without candidate buffers
+    for solver in ("greedy", "exact"):
+        sol = oracle.solve(g, rho, solver, 2)
+        assert sol.k > 0 and 8.0 <= 1.0 / sol.lam < 16.0, (sol.k, sol.lam)
+        idx, val, n, lam, k, fl, ws = sample_row_ws(L, g, rho, solver, 23, ws_bytes=fixed + 8 * (1 << 16) + 4096)
+        st = row_state(ws)
+        if verbose:
+            print(f"region overflow {solver}: band [{st['band_lo'] >> 23}, {st['band_hi'] >> 23}) "
+                  f"cand={st['cand_n']} src={st['src']}", flush=True)
+        assert fl == 0, fl
+        # collected (the count exceeds the list's capacity: the overflowing region reserved past
+        # it), then dropped by the first solve, and no window read the candidates
+        assert st["cand_n"] > (1 << 16) and st["band_lo"] == st["band_hi"] == 0 and st["src"] == 0, st
+        compare_sample(g, sol.p, 23, idx, val, n, lam, sol.lam)
+        if solver == "exact":
+            assert lam == sol.lam and k == sol.k, (lam, sol.lam, k, sol.k)
     return True
 
 

@@ -40,6 +40,10 @@ def test_emulated_candidate_band(emu_lib):
     assert runner.check_candidates(runner.load(emu_lib), verbose=False)
 
 
+def test_emulated_band_region_overflow(emu_lib):
+    assert runner.check_band_region_overflow(runner.load(emu_lib), verbose=False)
+
+
 def test_emulated_variance_solver(emu_lib):
     assert runner.check_variance(runner.load(emu_lib), verbose=False)
 

@@ -248,6 +248,40 @@ def test_candidate_band_on_ragged_rows(gs):
             assert float(plan.lam[r].item()) == sol.lam and int(plan.k[r].item()) == sol.k
 
 
+@pytest.mark.parametrize("solver", ["greedy", "exact"])
+def test_candidate_band_region_overflow(gs, solver):
+    """A row of 2^25 coordinates whose first statistics workgroup's chunk (65,536 coordinates) lies
+    wholly in the predicted band (magnitudes uniform in [8, 16), the rest of the row 1e-3 N(0, 1),
+    rho putting 1/lambda near 12): that workgroup has more band keys than its staging region holds,
+    so the band is dropped and the solver refines over the row; the result still equals the
+    oracle's (lambda bit for bit for the exact solver)."""
+    d = 1 << 25
+    rng = np.random.default_rng(91)
+    g = (rng.standard_normal(d) * 1e-3).astype(np.float32)
+    big = rng.uniform(8.0, 16.0, 1 << 16) * np.where(rng.random(1 << 16) < 0.5, -1.0, 1.0)
+    g[: 1 << 16] = big.astype(np.float32)
+    rho = 0.00186
+    gd = torch.from_numpy(g).cuda().reshape(1, -1)
+    seeds = torch.tensor([13], dtype=torch.int64, device="cuda")
+    plan = gs.Plan(1, d, solver=solver, cap_per_row=gs.capacity_hint(d, rho))
+    plan.run(gd, torch.tensor([rho], dtype=torch.float64, device="cuda"), seeds)
+    torch.cuda.synchronize()
+    st = _row_state(plan.ws)
+    n = int(plan.nnz[0].item())
+    _say(f"[band-region] {solver} band=[{st['band_lo'] >> 23},{st['band_hi'] >> 23}) cand={st['cand_n']} "
+         f"src={st['src']} nnz={n} k={int(plan.k[0].item())}")
+    assert int(plan.flags[0].item()) == 0
+    # collected (the count exceeds the list's capacity, d / 16 keys: the overflowing region
+    # reserved past it), then dropped by the first solve, and no window read the candidates
+    assert st["cand_n"] > d // 16 and st["band_lo"] == st["band_hi"] == 0 and st["src"] == 0
+    sol = oracle.solve(g, rho, solver, 2)
+    assert sol.k > 0
+    compare_sample(g, sol.p, 13, plan.idx[0, :n].cpu().numpy(), plan.val[0, :n].cpu().numpy(), n,
+                   float(plan.lam[0].item()), sol.lam)
+    if solver == "exact":
+        assert float(plan.lam[0].item()) == sol.lam and int(plan.k[0].item()) == sol.k
+
+
 def test_candidate_band_with_smaller_workspaces(gs):
     """The same long row with the full workspace (band used), a workspace with room for 2^16
     candidates only (the band overflows and is dropped) and the fixed part alone (no band): the
