@@ -2480,9 +2480,9 @@ __device__ uint64_t wave_tile_aggregate(const TileCtx& c, int64_t part, int lane
 // inside its own wave's quarter, so its survivors are contiguous in the output: one prefix over
 // the wave's lanes places it, and it writes only its own set bits (for up to kStageEmit survivors
 // per wave through an LDS staging area that the wave then stores with consecutive lanes on
-// consecutive slots). Phase 2 reads no global memory
-// (a load would wait for every store issued before it), except in a wave where some lane kept
-// more capped values than its LDS row holds (a separate instantiation).
+// consecutive slots). Phase 2 reads no global memory (a load would wait for every store issued
+// before it), except in a wave where some lane kept more capped values than its LDS row holds (a
+// separate instantiation).
 // Capped survivors' values are kept in LDS by the phase-1 lane that decided them, kLaneCap per
 // lane and tile (rows padded to kLaneStride floats so that lanes fall on different banks); a wave
 // with a lane past that reads its capped values from global memory in phase 2.
@@ -2865,11 +2865,11 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
           }
         } else if (lds_values && s_wsel[kk][wv] <= (uint32_t)kDenseEmit && wave_end <= (uint64_t)a.cap &&
                    wave_end <= ((uint64_t)1 << 30)) {
-          // the same between kStageEmit and kDenseEmit survivors, unstaged: every survivor of the wave within the capacity (no store needs a bound
-          // check) and its capped values in the lanes' LDS rows. A first loop writes every survivor with
-          // the sign's +-1/lambda, a second (capped survivors are few) overwrites the capped ones'
-          // values with g_i; both stores of a value come from this lane in program order. 32-bit
-          // byte offsets from the row's output arrays, masks in 32-bit halves.
+          // the same between kStageEmit and kDenseEmit survivors, unstaged (no store needs a bound
+          // check): a first loop writes every survivor with the sign's +-1/lambda, a second
+          // (capped survivors are few) overwrites the capped ones' values with g_i; both stores of
+          // a value come from this lane in program order. 32-bit byte offsets from the row's
+          // output arrays, masks in 32-bit halves.
           gchar* __restrict__ bi = uniform_ptr(oi);
           gchar* __restrict__ bv = uniform_ptr(ov);
           const uint32_t off0 = (uint32_t)pos * 4u;
@@ -2896,8 +2896,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
           }
         } else if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
           // many survivors: lane l takes the wave's groups 64 j + l (the order of phase 1 and of
-          // this lane's capped-value row), one step j at a time, so the stores of a step fall on a few
-          // consecutive lines instead of one line per lane
+          // this lane's capped-value row), one step j at a time, so the stores of a step fall on a
+          // few consecutive lines instead of one line per lane
           const uint64_t base0 = (excl & 0x7FFFFFFFull) + wbase;
           uint32_t carry = 0;
           for (int j = 0; j < kTileGroups; ++j) {
