@@ -344,6 +344,31 @@ def check_candidates(L, verbose=True):
     return True
 
 
+def check_lane_rows(L, verbose=True):
+    """Capped coordinates that one decide-phase lane takes beyond its LDS row (workloads.strided_large):
+    those waves read their capped values from g while emitting, lane by lane (rho 0.002, 0.01) or
+    group by group (rho 0.5), in the compaction and the hybrid coding; every capped coordinate
+    survives with value g_i and the rest follows the oracle."""
+    g = W.strided_large(65536 + 123, 7)
+    big = np.flatnonzero(np.abs(g) >= 100.0)
+    for rho in (0.002, 0.01, 0.5):
+        for solver in ("exact", "greedy"):
+            sol = oracle.solve(g, rho, solver, 2)
+            idx, val, n, lam, k, fl = sample_row(L, g, rho, solver, 17)
+            assert fl == 0, fl
+            compare_sample(g, sol.p, 17, idx, val, n, lam, sol.lam)
+            assert np.all(np.isin(big, idx)) and np.array_equal(val[np.isin(idx, big)], g[big])
+            ia, va, na, cb, nb, inv, q, lam3, fl3 = hybrid_batched(L, g[None, :], [rho], [17], solver)
+            A_, B_ = int(na[0]), int(nb[0])
+            assert not fl3.any() and A_ + B_ == n
+            bi = cb[0, :B_] & 0x7FFFFFFF
+            assert np.all(np.isin(big, ia[0, :A_])) and np.array_equal(va[0, :A_], g[ia[0, :A_]])
+            assert np.array_equal(np.sort(np.concatenate([ia[0, :A_], bi])), idx)
+            if verbose:
+                print(f"lane rows {solver} rho={rho}: nnz={n} capped={k}", flush=True)
+    return True
+
+
 def check_band_region_overflow(L, verbose=True):
     """A band row whose first statistics workgroup holds more band keys than its staging region:
     2^17 coordinates, a workspace with room for 2^16 candidates (16 regions of 4096 for chunks of

@@ -40,6 +40,10 @@ def test_emulated_candidate_band(emu_lib):
     assert runner.check_candidates(runner.load(emu_lib), verbose=False)
 
 
+def test_emulated_capped_values_past_the_lane_rows(emu_lib):
+    assert runner.check_lane_rows(runner.load(emu_lib), verbose=False)
+
+
 def test_emulated_band_region_overflow(emu_lib):
     assert runner.check_band_region_overflow(runner.load(emu_lib), verbose=False)
 

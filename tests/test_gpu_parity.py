@@ -142,6 +142,36 @@ def _tied_boundary(d, n_hi, seed):
     return g
 
 
+def test_capped_values_past_the_lane_rows(gs):
+    """A row whose 76 capped coordinates sit in two strided patterns that one lane of the sampling
+    pass's decide phase takes (64 and 12 coordinates, against LDS rows of 8): those waves read their
+    capped values from g while emitting, at densities whose waves emit lane by lane (rho 0.002 and
+    0.01) or group by group (rho 0.5), in the compaction and in the hybrid coding. Every capped
+    coordinate survives with value g_i, and the rest follows the oracle under the parity rule."""
+    g = W.strided_large(65536 + 123, 7)
+    d = g.size
+    big = np.flatnonzero(np.abs(g) >= 100.0)
+    gd = torch.from_numpy(g).cuda()
+    for rho in (0.002, 0.01, 0.5):
+        for solver in ("exact", "greedy"):
+            _say(f"[lane-rows] d={d} solver={solver} rho={rho}")
+            sol = oracle.solve(g, rho, solver, 2)
+            assert np.all(sol.p[big] == 1.0)
+            idx, val, n, lam, k, fl = _run_row(gs, g, rho, solver, 17, cap=d)
+            assert fl == 0, fl
+            compare_sample(g, sol.p, 17, idx, val, n, lam, sol.lam)
+            assert np.all(np.isin(big, idx)) and np.array_equal(val[np.isin(idx, big)], g[big])
+            h = gs.sparsify_sample_hybrid(gd, rho, seed=17, solver=solver, cap_a=d, cap_b=d)
+            torch.cuda.synchronize()
+            A, B = int(h.n_a.item()), int(h.n_b.item())
+            assert int(h.flags.item()) == 0 and A + B == n
+            ia = h.idx_a[:A].cpu().numpy()
+            bi = h.code_b[:B].cpu().numpy() & 0x7FFFFFFF
+            assert np.all(np.isin(big, ia)) and np.array_equal(h.val_a[:A].cpu().numpy(), g[ia])
+            assert np.all(np.diff(ia) > 0) and np.all(np.diff(bi) > 0)
+            assert np.array_equal(np.sort(np.concatenate([ia, bi])), idx)
+
+
 @pytest.mark.parametrize("d,n_hi", [(40000, 3000), (1000003, 77777), ((1 << 25) + 5, 1 << 20)])
 def test_capped_ties_one_rule(gs, d, n_hi):
     """Every pass takes the same capped set {p_i = 1}: compaction (whole tiles and the partial last

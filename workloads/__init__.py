@@ -174,6 +174,18 @@ def integer_ties(d: int, seed: int, levels: int = 6) -> np.ndarray:
     return (rng.integers(0, levels, d) * rng.choice([-1.0, 1.0], size=d)).astype(np.float32)
 
 
+def strided_large(d: int, seed: int) -> np.ndarray:
+    """1e-3 N(0, 1) with 76 large magnitudes (about 100, random signs) in two strided patterns of
+    the first 16,384 coordinates: 4-coordinate runs at 256 j for j < 16, and at 4096 + 256 j + 20
+    for j < 3. (Runs 256 apart fall to one lane of the sampling pass's decide phase, so at most
+    densities that lane keeps more capped survivors than its LDS row holds.) d >= 16384."""
+    rng = np.random.default_rng(seed)
+    g = (rng.standard_normal(d) * 1e-3).astype(np.float32)
+    pos = [256 * j + c for j in range(16) for c in range(4)] + [4096 + 256 * j + 20 + c for j in range(3) for c in range(4)]
+    g[pos] = ((100.0 + rng.uniform(0.0, 8.0, len(pos))) * rng.choice([-1.0, 1.0], size=len(pos))).astype(np.float32)
+    return g
+
+
 def wide_range(d: int, seed: int) -> np.ndarray:
     """Magnitudes spread over many binades, including subnormals."""
     rng = np.random.default_rng(seed)
