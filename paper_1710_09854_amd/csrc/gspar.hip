@@ -355,6 +355,7 @@ struct alignas(256) RowCtl {
   uint32_t band_lo;  // candidate band [band_lo, band_hi) of keys (whole binades) the statistics pass
   uint32_t band_hi;  // collected, written by its first workgroup (equal bounds: no band)
   uint64_t cand_n;   // candidates collected (first solve; above the capacity: incomplete, unused)
+  uint32_t qonly;    // greedy, last rescale step: the level-2 pass only counts the keys >= qkey
 };
 static_assert(sizeof(RowCtl) == 256, "RowCtl layout");
 // offsets read by the tests to see which source a refinement pass used
@@ -1028,10 +1029,22 @@ GS_DI void sv_finalize(RowCtl& c, double lam, uint32_t tcap) {
 // the stores before the pass).
 GS_DI void sv_request(RowCtl& c, const Hists& H, int level, uint32_t E, uint32_t base, uint32_t qkey, uint64_t wK,
                       const Fx& wW) {
-  uint4 z;
-  z.x = z.y = z.z = z.w = 0u;
-  uint4* w = reinterpret_cast<uint4*>(H.wg);
-  for (int i = threadIdx.x; i < (int)(kC23 * sizeof(WinHist) / 16); i += kNT) w[i] = z;
+  // The greedy solver's query of its last rescale step is answered by the direct count alone (no
+  // later query reads a bin of this window), so that pass builds no bins and only the direct
+  // count's fields are cleared.
+  const bool qonly = level == 2 && c.solver == GSPAR_GREEDY && c.iter + 1 >= c.T;
+  if (qonly) {
+    if (threadIdx.x < kC23) {
+      H.wg[threadIdx.x].qcnt = 0;
+      H.wg[threadIdx.x].qsig = 0;
+    }
+  } else {
+    uint4 z;
+    z.x = z.y = z.z = z.w = 0u;
+    uint4* w = reinterpret_cast<uint4*>(H.wg);
+    for (int i = threadIdx.x; i < (int)(kC23 * sizeof(WinHist) / 16); i += kNT) w[i] = z;
+  }
+  c.qonly = qonly ? 1u : 0u;
   c.need = level;
   if (level == 2) {
     c.l2exp = E;
@@ -2279,10 +2292,12 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   // window when set; kNone matches no key)
   const bool l2 = need == 2;
   const uint32_t qkey = l2 ? ctl->qkey : kNone;
+  // the greedy solver's last query needs the direct count only: no bins are built or flushed
+  const bool bins = !(l2 && ctl->qonly);
   // the variance-budget solver's level-2 windows also sum squared significands (level 3 has one
   // key per bin, whose square follows from the count)
-  const bool sq2 = SQ && l2;
-  for (int b = threadIdx.x; b < nbins; b += kNT) {
+  const bool sq2 = SQ && l2 && bins;
+  for (int b = threadIdx.x; bins && b < nbins; b += kNT) {
     sm.pk[b] = 0;
     sm.mx[b] = 0;
     sm.mnc[b] = 0;
@@ -2301,12 +2316,14 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
       if (key != 0 && rel < span) {
         const uint32_t b = rel >> shift;
         const uint64_t sg = key_sig(key);
-        atomicAdd(&sm.pk[b], (unsigned long long)((1ull << 44) + sg));
-        // level-2 bin extremes (fire-and-forget atomics: a read of the bin first would make every
-        // key wait on the LDS); a level-3 bin is one key, its own maximum
-        if (l2) {
-          atomicMax(&sm.mx[b], key);
-          atomicMax(&sm.mnc[b], ~key);
+        if (bins) {
+          atomicAdd(&sm.pk[b], (unsigned long long)((1ull << 44) + sg));
+          // level-2 bin extremes (fire-and-forget atomics: a read of the bin first would make
+          // every key wait on the LDS); a level-3 bin is one key, its own maximum
+          if (l2) {
+            atomicMax(&sm.mx[b], key);
+            atomicMax(&sm.mnc[b], ~key);
+          }
         }
         if (key >= qkey) {
           ++qc;
@@ -2339,7 +2356,7 @@ __global__ void __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4))) k
   // flush: workgroups start at different blocks of kNT bins, so they do not queue on the same
   // addresses at the same time
   static_assert(kB2 % kNT == 0 && kB3 % kNT == 0, "whole blocks of bins");
-  const int nblk = nbins / kNT;
+  const int nblk = bins ? nbins / kNT : 0;
   for (int i = 0; i < nblk; ++i) {
     const int b = ((i + (int)blk) % nblk) * kNT + threadIdx.x;
     const uint64_t p = sm.pk[b];
