@@ -382,6 +382,26 @@ def test_capacity_overflow(gs):
     compare_sample(g, sol.p, 9, idx, val, n, lam, sol.lam, cap=cap)
 
 
+def test_capacity_boundaries(gs):
+    """Output capacities at and around the survivor count n: exactly n (no overflow, the same
+    output as with room to spare), n - 1 and a cut inside a wave's run of survivors (overflow
+    flagged, n still reported, the first cap entries identical)."""
+    g = W.t_mixture(300007, 52)
+    gd = torch.from_numpy(g).cuda()
+    for rho, solver in ((0.1, "exact"), (0.01, "greedy")):
+        ref = gs.sparsify_sample_compact(gd, rho, seed=19, solver=solver, capacity=g.size)
+        torch.cuda.synchronize()
+        n = int(ref.nnz.item())
+        for cap in (n, n - 1, n // 2 + 37):
+            _say(f"[capacity] {solver} rho={rho} n={n} cap={cap}")
+            out = gs.sparsify_sample_compact(gd, rho, seed=19, solver=solver, capacity=cap)
+            torch.cuda.synchronize()
+            fl = int(out.flags.item())
+            assert int(out.nnz.item()) == n and float(out.lam.item()) == float(ref.lam.item())
+            assert bool(fl & gs.FLAG_OVERFLOW) == (cap < n)
+            assert torch.equal(out.idx[:cap], ref.idx[:cap]) and torch.equal(out.val[:cap], ref.val[:cap])
+
+
 def test_unaligned_scalar_path(gs):
     g = W.t_mixture(100001, 61)
     big = torch.from_numpy(np.concatenate([np.zeros(1, np.float32), g])).cuda()
