@@ -346,12 +346,13 @@ def check_candidates(L, verbose=True):
 
 def check_lane_rows(L, verbose=True):
     """Capped coordinates that one decide-phase lane takes beyond its LDS row (workloads.strided_large):
-    those waves read their capped values from g while emitting, lane by lane (rho 0.002, 0.01) or
+    those waves read their capped values from g while emitting, lane by lane (rho 0.01, 0.05) or
     group by group (rho 0.5), in the compaction and the hybrid coding; every capped coordinate
-    survives with value g_i and the rest follows the oracle."""
-    g = W.strided_large(65536 + 123, 7)
+    survives with value g_i and the rest follows the oracle. (One tile and a ragged tail: the
+    patterns lie in the first tile.)"""
+    g = W.strided_large(16384 + 123, 7)
     big = np.flatnonzero(np.abs(g) >= 100.0)
-    for rho in (0.002, 0.01, 0.5):
+    for rho in (0.01, 0.05, 0.5):
         for solver in ("exact", "greedy"):
             sol = oracle.solve(g, rho, solver, 2)
             idx, val, n, lam, k, fl = sample_row(L, g, rho, solver, 17)
