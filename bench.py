@@ -456,8 +456,8 @@ def main():
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], wl_name)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); multi-GPU runs are not part of "
-              "this build", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the sparsifier runs each "
+              "worker's rows on its own GPU and has no multi-GPU step to time", file=sys.stderr)
         sys.exit(2)
     if args.cells:
         cells(args)

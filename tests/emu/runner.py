@@ -287,7 +287,7 @@ def sample_row_ws(L, g, rho, solver, seed, iters=2, ws_bytes=None):
 
 
 def check_candidates(L, verbose=True):
-    """Rows long enough for a candidate band (in this build): the band is predicted, the keys in it
+    """Rows long enough for a candidate band (in the emulation build): the band is predicted, the keys in it
     are collected, refinement windows inside it read them, and every result still equals the
     oracle's (bit for bit in lambda for the exact solver). A row whose sample misleads the
     prediction (large magnitudes only on lines the sample skips) refines over the row instead."""
@@ -323,7 +323,7 @@ def check_candidates(L, verbose=True):
                           f"cand={st['cand_n']} src={st['src']} stage={st['stage']}", flush=True)
     assert used > 0, "no refinement window was read from the candidates"
     # a misleading sample: the sample reads every 4th 64-byte line of this row (64 workgroups x 64
-    # lines in this build, of its 16384 lines); put all the large magnitudes on the other lines
+    # lines in the emulation build, of its 16384 lines); put all the large magnitudes on the other lines
     d = 1 << 18
     g = (W.normal(d, 15) * np.float32(1e-3)).astype(np.float32)
     lines = np.arange(d) // 16
@@ -631,7 +631,7 @@ def check_aggregate(L, verbose=True):
 def check_asan_subset(L, verbose=True):
     """A bounded selection for the AddressSanitizer build: every kernel family once, on shapes that
     reach the ragged ends. A padded batch whose rows end in a partial group on the vector path
-    (long enough for a candidate band in this build), the scalar path, the variance budget,
+    (long enough for a candidate band in the emulation build), the scalar path, the variance budget,
     segments on both paths with the hybrid coding, and aggregation of the batch's lists."""
     rows, d = 2, 12003
     g2 = np.stack([W.t_mixture(d, 310 + r) for r in range(rows)])
