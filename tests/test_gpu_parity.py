@@ -94,6 +94,45 @@ def test_emission_paths(gs):
             _say(f"   ok nnz={n} oracle={rep['nnz_oracle']} excused={rep['excused']}")
 
 
+def _random_case(rng):
+    """A seeded draw of a row: length (1 to ~300 K, log-uniform, often ragged), distribution,
+    scale, density and solver."""
+    d = int(np.exp(rng.uniform(0.0, np.log(300000.0))))
+    seed = int(rng.integers(1 << 30))
+    kind = int(rng.integers(6))
+    if kind == 0:
+        g = W.normal(d, seed)
+    elif kind == 1:
+        g = W.t_mixture(d, seed)
+    elif kind == 2:
+        g = W.integer_ties(d, seed)
+    elif kind == 3:
+        g = W.wide_range(d, seed)
+    elif kind == 4:
+        g = W.two_level(d, max(1, d // 50), 30.0, 1.0, seed)
+    else:
+        g = W.approx_sparse(d, max(1, d // 20), 0.05, seed) if d >= 20 else W.normal(d, seed)
+    g = (g * np.float32(10.0 ** rng.uniform(-6, 4))).astype(np.float32)
+    rho = float(10.0 ** rng.uniform(-3.5, 0.0))
+    solver = ("greedy", "exact")[int(rng.integers(2))]
+    return g, rho, solver, seed % 100000
+
+
+def test_random_rows(gs):
+    """Two hundred seeded random rows (length, distribution, scale over ten decades, density,
+    solver) against the oracle under the parity rule, lambda bit for bit for the exact solver."""
+    rng = np.random.default_rng(2024)
+    for case in range(200):
+        g, rho, solver, seed = _random_case(rng)
+        _say(f"[random] case={case} d={g.size} rho={rho:.5g} solver={solver} seed={seed}")
+        sol = oracle.solve(g, rho, solver, 2)
+        idx, val, n, lam, k, fl = _run_row(gs, g, rho, solver, seed, cap=g.size)
+        assert fl == (0 if g.any() else gs.FLAG_ALLZERO), (case, fl)  # an all-zero row is reported
+        compare_sample(g, sol.p, seed, idx, val, n, lam, sol.lam)
+        if solver == "exact":
+            assert lam == sol.lam and k == sol.k, (case, lam, sol.lam, k, sol.k)
+
+
 @pytest.mark.parametrize("iters", [0, 1, 3, 8])
 def test_greedy_iterations(gs, iters):
     g = W.t_mixture(150000, 11)
@@ -443,6 +482,37 @@ def test_batched_equals_rows_and_oracle(gs):
             assert int(one.nnz.item()) == n
             assert torch.equal(one.idx[:n], out.idx[r, :n]) and torch.equal(one.val[:n], out.val[r, :n])
             assert float(one.lam.item()) == float(out.lam[r].item())
+
+
+def test_random_batches(gs):
+    """Thirty seeded random batches: 1 to 24 rows of one random length (1 to ~100 K), stored with a
+    random padding of the leading dimension (so both the vector and the scalar load paths occur),
+    a random density per row and one solver per batch; every row against the oracle under the
+    parity rule (lambda bit for bit for the exact solver)."""
+    rng = np.random.default_rng(4048)
+    for case in range(30):
+        rows = int(rng.integers(1, 25))
+        d = int(np.exp(rng.uniform(0.0, np.log(100000.0))))
+        ld = d + int(rng.integers(0, 9))
+        solver = ("greedy", "exact")[int(rng.integers(2))]
+        g = np.stack([W.t_mixture(d, 5000 + 31 * case + r) * np.float32(10.0 ** rng.uniform(-4, 2))
+                      for r in range(rows)]).astype(np.float32)
+        rhos = [float(10.0 ** rng.uniform(-3.0, 0.0)) for _ in range(rows)]
+        seeds = [int(rng.integers(1 << 62)) for _ in range(rows)]
+        buf = np.zeros((rows, ld), np.float32)
+        buf[:, :d] = g
+        gd = torch.from_numpy(buf).cuda()[:, :d]
+        _say(f"[random-batch] case={case} rows={rows} d={d} ld={ld} solver={solver}")
+        out = gs.sparsify_sample_compact_batched(gd, rhos, seeds, solver=solver, iters=2, cap_per_row=d)
+        torch.cuda.synchronize()
+        assert not out.flags.cpu().numpy().any(), out.flags
+        for r in range(rows):
+            n = int(out.nnz[r].item())
+            sol = oracle.solve(g[r], rhos[r], solver, 2)
+            compare_sample(g[r], sol.p, seeds[r], out.idx[r, :n].cpu().numpy(), out.val[r, :n].cpu().numpy(), n,
+                           float(out.lam[r].item()), sol.lam)
+            if solver == "exact":
+                assert float(out.lam[r].item()) == sol.lam and int(out.k[r].item()) == sol.k
 
 
 def test_deterministic_reruns(gs):
