@@ -484,6 +484,37 @@ def test_batched_equals_rows_and_oracle(gs):
             assert float(one.lam.item()) == float(out.lam[r].item())
 
 
+def test_random_rows_hybrid_and_probs(gs):
+    """Sixty seeded random rows through the hybrid coding and the probabilities entry point: Q_A
+    holds the capped survivors with their values, Q_B the others in ascending order, together the
+    compaction's indices; p equals the oracle's to 1e-6 with the same lambda and capped count."""
+    rng = np.random.default_rng(7070)
+    for case in range(60):
+        g, rho, solver, seed = _random_case(rng)
+        if not g.any():
+            continue
+        d = g.size
+        _say(f"[random-hyb] case={case} d={d} rho={rho:.5g} solver={solver} seed={seed}")
+        gd = torch.from_numpy(g).cuda()
+        out = gs.sparsify_sample_compact(gd, rho, seed=seed, solver=solver, capacity=d)
+        h = gs.sparsify_sample_hybrid(gd, rho, seed=seed, solver=solver, cap_a=d, cap_b=d)
+        pr = gs.sparsify_probs(gd, rho, solver=solver)
+        torch.cuda.synchronize()
+        n = int(out.nnz.item())
+        idx = out.idx[:n].cpu().numpy()
+        A, B = int(h.n_a.item()), int(h.n_b.item())
+        assert int(h.flags.item()) == 0 and A + B == n and A == int(out.k.item())  # every capped one survives
+        ia = h.idx_a[:A].cpu().numpy()
+        bi = h.code_b[:B].cpu().numpy() & 0x7FFFFFFF
+        assert np.array_equal(h.val_a[:A].cpu().numpy(), g[ia])
+        assert np.all(np.diff(ia) > 0) and np.all(np.diff(bi) > 0)
+        assert np.array_equal(np.sort(np.concatenate([ia, bi])), idx)
+        sol = oracle.solve(g, rho, solver, 2)
+        compare_probs(pr.p.cpu().numpy(), sol.p)
+        if solver == "exact":
+            assert float(pr.lam.item()) == sol.lam and int(pr.k.item()) == sol.k
+
+
 def test_random_batches(gs):
     """Thirty seeded random batches: 1 to 24 rows of one random length (1 to ~100 K), stored with a
     random padding of the leading dimension (so both the vector and the scalar load paths occur),
