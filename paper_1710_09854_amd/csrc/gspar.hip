@@ -1217,28 +1217,31 @@ GS_DI void sv_exact(SolveLds& s, RowCtl& c, const Hists& H) {
     if (b1 >= 0) lvl_bin_info(L, w, b1, s, c1);
     if (b2 != INT_MAX) lvl_bin_info(L, w, b2, s, c2);
   }
-  if (b1 < 0) {
-    // no value in this window passes: the answer is the candidate found one level up
-    if (c.fbValid) {
-      sv_exact_finish(c, c.fbK, c.fbW, c.fbTcap);
-    } else {
-      c.flags |= kFlagInternal;
-      sv_finalize(c, NAN, kKeyInf);
-    }
-    return;
-  }
-  const uint32_t cand_tcap = c1.mx + 1;
+  // refine b2 when it holds two or more values, of which a smaller one may pass; also when no
+  // bin's maximum passes at this level (b1 < 0): the lowest occupied bin may still hold a passing
+  // value below its maximum (when the answer lies in the row's lowest binade, or in a window's
+  // lowest bin), and the candidate from a level up, if any, stays the fallback
   if (b2 != INT_MAX && level < 3 && c2.cnt >= 2) {
-    c.fbValid = 1;
-    c.fbK = c1.Kab;
-    c.fbW = c1.Wab;
-    c.fbTcap = cand_tcap;
+    if (b1 >= 0) {
+      c.fbValid = 1;
+      c.fbK = c1.Kab;
+      c.fbW = c1.Wab;
+      c.fbTcap = c1.mx + 1;
+    }
     c.stage = level + 1;
     if (level == 1) sv_request(c, H, 2, (uint32_t)b2, 0, kNone, 0, fx_zero());
     else sv_request(c, H, 3, 0, (E << 23) | ((uint32_t)b2 << 11), kNone, c2.Kab, c2.Wab);
     return;
   }
-  sv_exact_finish(c, c1.Kab, c1.Wab, cand_tcap);
+  if (b1 >= 0) {
+    sv_exact_finish(c, c1.Kab, c1.Wab, c1.mx + 1);
+  } else if (c.fbValid) {
+    // no value in this window passes: the answer is the candidate found one level up
+    sv_exact_finish(c, c.fbK, c.fbW, c.fbTcap);
+  } else {
+    c.flags |= kFlagInternal;
+    sv_finalize(c, NAN, kKeyInf);
+  }
 }
 
 // ------------------------------------------------------------------------------------------

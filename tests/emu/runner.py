@@ -344,6 +344,25 @@ def check_candidates(L, verbose=True):
     return True
 
 
+def check_lowest_binade(L, verbose=True):
+    """Exact solver with 1/lambda inside the row's lowest occupied binade (workloads.lowest_binade):
+    no binade's maximum passes the criterion, and the solver refines that binade instead of giving
+    up; lambda and k bit for bit, the sample under the parity rule, the probabilities too."""
+    for d, rho in ((500, 0.96), (5003, 0.97)):
+        g = W.lowest_binade(d, 3)
+        sol = oracle.solve_exact(g, rho)
+        assert 1.0e-3 <= 1.0 / sol.lam < 1.9e-3
+        idx, val, n, lam, k, fl = sample_row(L, g, rho, "exact", 29)
+        assert fl == 0 and lam == sol.lam and k == sol.k, (d, fl, lam, sol.lam, k, sol.k)
+        compare_sample(g, sol.p, 29, idx, val, n, lam, sol.lam)
+        p, lam2, k2, fl2 = probs_row(L, g, rho, "exact")
+        assert fl2 == 0 and lam2 == sol.lam and k2 == sol.k
+        compare_probs(p, sol.p)
+        if verbose:
+            print(f"lowest binade d={d} rho={rho}: k={k} lambda={lam!r}", flush=True)
+    return True
+
+
 def check_lane_rows(L, verbose=True):
     """Capped coordinates that one decide-phase lane takes beyond its LDS row (workloads.strided_large):
     those waves read their capped values from g while emitting, lane by lane (rho 0.01, 0.05) or

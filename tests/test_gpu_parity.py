@@ -484,6 +484,28 @@ def test_batched_equals_rows_and_oracle(gs):
             assert float(one.lam.item()) == float(out.lam[r].item())
 
 
+@pytest.mark.parametrize("d,rho", [(500, 0.96), (5003, 0.97), ((1 << 25) + 7, 0.97)])
+def test_answer_inside_the_lowest_binade(gs, d, rho):
+    """Exact solver, 1/lambda inside the row's lowest occupied binade: no binade's maximum passes
+    Algorithm 2's criterion, so the solver refines that binade (and its lowest sub-bin) instead of
+    giving up; lambda and k equal the oracle's bit for bit, and the probabilities entry point and
+    the hybrid coding agree."""
+    g = W.lowest_binade(d, 3)
+    _say(f"[lowest-binade] d={d} rho={rho}")
+    sol = oracle.solve_exact(g, rho)
+    assert 1.0e-3 <= 1.0 / sol.lam < 1.9e-3
+    idx, val, n, lam, k, fl = _run_row(gs, g, rho, "exact", 29, cap=d)
+    assert fl == 0, fl
+    assert lam == sol.lam and k == sol.k, (lam, sol.lam, k, sol.k)
+    compare_sample(g, sol.p, 29, idx, val, n, lam, sol.lam)
+    gd = torch.from_numpy(g).cuda()
+    pr = gs.sparsify_probs(gd, rho, solver="exact")
+    torch.cuda.synchronize()
+    assert int(pr.flags.item()) == 0 and float(pr.lam.item()) == sol.lam and int(pr.k.item()) == sol.k
+    if d <= 1 << 20:
+        compare_probs(pr.p.cpu().numpy(), sol.p)
+
+
 def test_random_rows_hybrid_and_probs(gs):
     """Sixty seeded random rows through the hybrid coding and the probabilities entry point: Q_A
     holds the capped survivors with their values, Q_B the others in ascending order, together the

@@ -104,6 +104,24 @@ def test_layouts(gs, layout, solver):
     _check(g, off, rhos, seeds, solver, out, solver == "exact")
 
 
+def test_random_layouts(gs):
+    """Twenty seeded random layer layouts: 1 to 40 segments with lengths from 0 to ~200 K
+    (log-uniform, some empty, offsets of any alignment), a random density per segment and one
+    solver per call; every segment against the oracle run on it alone."""
+    rng = np.random.default_rng(515)
+    for case in range(20):
+        segs = int(rng.integers(1, 41))
+        lengths = [0 if rng.random() < 0.08 else int(np.exp(rng.uniform(0.0, np.log(200000.0)))) for _ in range(segs)]
+        g, off = _layered(lengths, 7000 + case)
+        rhos = [float(10.0 ** rng.uniform(-3.0, 0.0)) for _ in range(segs)]
+        seeds = [int(rng.integers(1 << 62)) for _ in range(segs)]
+        solver = ("greedy", "exact")[int(rng.integers(2))]
+        _say(f"[random-layout] case={case} segments={segs} total={int(off[-1])} solver={solver}")
+        out = gs.sparsify_sample_compact_segmented(torch.from_numpy(g).cuda(), gs.Segments(off), rhos, seeds, solver)
+        torch.cuda.synchronize()
+        _check(g, off, rhos, seeds, solver, out, solver == "exact")
+
+
 @pytest.mark.parametrize("layout", ["aligned_mixed", "unaligned_tiny", "two_tiles_per_workgroup"])
 def test_hybrid_segmented(gs, layout):
     """Per-layer hybrid coding: the compaction's survivors split by the capped set, row by row,

@@ -186,6 +186,19 @@ def strided_large(d: int, seed: int) -> np.ndarray:
     return g
 
 
+def lowest_binade(d: int, seed: int) -> np.ndarray:
+    """Four fifths of the magnitudes uniform in [0.5, 4), one fifth uniform in [1.0e-3, 1.9e-3)
+    (one binade, the row's lowest), random signs and order. At densities near 1 the capped set
+    reaches into the small magnitudes, so 1/lambda lies inside the row's lowest binade."""
+    rng = np.random.default_rng(seed)
+    nt = d // 5
+    g = np.empty(d, np.float32)
+    g[: d - nt] = rng.uniform(0.5, 4.0, d - nt)
+    g[d - nt:] = rng.uniform(1.0e-3, 1.9e-3, nt)
+    g *= rng.choice([-1.0, 1.0], size=d).astype(np.float32)
+    return g[rng.permutation(d)].astype(np.float32)
+
+
 def wide_range(d: int, seed: int) -> np.ndarray:
     """Magnitudes spread over many binades, including subnormals."""
     rng = np.random.default_rng(seed)
