@@ -238,6 +238,7 @@ def _kkt_check(g, rho, sol, tol=1e-12):
     (lambda: W.integer_ties(5000, 4), 0.3),
     (lambda: W.wide_range(8000, 5), 0.05),
     (lambda: W.approx_sparse(3000, 40, 0.05, 6), 0.02),
+    (lambda: W.lowest_binade(5003, 3), 0.97),  # 1/lambda inside the row's lowest binade
 ])
 def test_exact_density_kkt(maker, rho):
     g = maker()
