@@ -195,6 +195,27 @@ def test_probs_segmented(gs, layout):
             assert pr.lam[s].item() == sol.lam and int(pr.k[s].item()) == sol.k
 
 
+def test_random_layouts_probs(gs):
+    """Twenty seeded random layer layouts through the probabilities entry point (exact solver):
+    every segment's p against the oracle to 1e-6, lambda and k bit for bit."""
+    rng = np.random.default_rng(616)
+    for case in range(20):
+        segs = int(rng.integers(1, 41))
+        lengths = [0 if rng.random() < 0.08 else int(np.exp(rng.uniform(0.0, np.log(200000.0)))) for _ in range(segs)]
+        g, off = _layered(lengths, 8000 + case)
+        rhos = [float(10.0 ** rng.uniform(-3.0, 0.0)) for _ in range(segs)]
+        _say(f"[random-layout-probs] case={case} segments={segs} total={int(off[-1])}")
+        pr = gs.sparsify_probs_segmented(torch.from_numpy(g).cuda(), gs.Segments(off), rhos, "exact")
+        torch.cuda.synchronize()
+        p = pr.p.cpu().numpy()
+        for s_ in range(segs):
+            seg = g[off[s_]:off[s_ + 1]]
+            if seg.size and np.any(seg):
+                sol = oracle.solve_exact(seg, rhos[s_])
+                compare_probs(p[off[s_]:off[s_ + 1]], sol.p)
+                assert pr.lam[s_].item() == sol.lam and int(pr.k[s_].item()) == sol.k, (case, s_)
+
+
 def test_device_offsets_that_disagree_are_flagged(gs):
     """Device offsets that break the host's bounds (a start that is not a multiple of 4 on the
     vector path, an end past the host's last offset) change the launch shape: every segment is

@@ -61,6 +61,34 @@ def test_variance_vectors(gs, name, eps):
     compare_probs(pr.p.cpu().numpy(), sol.p)
 
 
+def test_variance_random_rows(gs):
+    """One hundred seeded random rows for the variance budget (length 1 to ~300 K log-uniform,
+    distribution, scale over ten decades, eps from 1e-3 to 1e2): lambda and k bit for bit, the
+    sample under the parity rule, the probabilities to 1e-6."""
+    rng = np.random.default_rng(9191)
+    makers = (W.normal, W.t_mixture, W.integer_ties, W.wide_range, W.lowest_binade)
+    for case in range(100):
+        d = int(np.exp(rng.uniform(0.0, np.log(300000.0))))
+        seed = int(rng.integers(1 << 30))
+        g = makers[int(rng.integers(len(makers)))](d, seed)
+        g = (g * np.float32(10.0 ** rng.uniform(-6, 4))).astype(np.float32)
+        if not g.any():
+            continue
+        eps = float(10.0 ** rng.uniform(-3.0, 2.0))
+        _say(f"[variance-random] case={case} d={d} eps={eps:.5g}")
+        sol = oracle.solve_variance(g, eps)
+        gd = torch.from_numpy(g).cuda()
+        out = gs.sparsify_sample_compact(gd, eps, seed % 100000, "variance", capacity=d)
+        n = int(out.nnz[0].item())
+        assert int(out.flags[0].item()) == 0, (case, int(out.flags[0].item()))
+        assert out.lam[0].item() == sol.lam and int(out.k[0].item()) == sol.k, (case, out.lam[0].item(), sol.lam)
+        compare_sample(g, sol.p, seed % 100000, out.idx[:n].cpu().numpy(), out.val[:n].cpu().numpy(), n,
+                       out.lam[0].item(), sol.lam)
+        pr = gs.sparsify_probs(gd, eps, "variance")
+        assert pr.lam[0].item() == sol.lam
+        compare_probs(pr.p.cpu().numpy(), sol.p)
+
+
 def test_variance_batched_laplace_rows(gs):
     """The 16 x 2^20 Laplace batch, one eps per row, through the batched entry point."""
     w = W.c2()
