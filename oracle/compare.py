@@ -68,9 +68,15 @@ def compare_sample(g, p, seed, idx, val, nnz, lam_gpu, lam_oracle, band=1e-6, va
     vg = val_cmp[ig].astype(np.float64)
     vo = np.asarray(ov, np.float64)[io]
     if common.size:
-        rel = np.abs(vg - vo) / np.maximum(np.abs(vo), 1e-300)
-        rep["max_val_rel"] = float(rel.max())
-        assert rel.max() <= val_rtol, f"value mismatch {rel.max()} at {common[np.argmax(rel)]}"
+        # an amplified value sign(g_i)/lambda beyond fp32's range rounds to an infinity of that sign
+        # on both sides (lambda below about 2.9e-39): equal infinities agree, any other infinity
+        # does not
+        inf = np.isinf(vo) | np.isinf(vg)
+        assert np.array_equal(vg[inf], vo[inf]), f"infinite value mismatch at {common[inf][vg[inf] != vo[inf]][:5]}"
+        fin = ~inf
+        rel = np.abs(vg[fin] - vo[fin]) / np.maximum(np.abs(vo[fin]), 1e-300)
+        rep["max_val_rel"] = float(rel.max(initial=0.0))
+        assert rel.max(initial=0.0) <= val_rtol, f"value mismatch {rel.max()} at {common[fin][np.argmax(rel)]}"
     return rep
 
 

@@ -363,6 +363,37 @@ def check_lowest_binade(L, verbose=True):
     return True
 
 
+def check_full_range(L, verbose=True):
+    """Rows whose magnitudes span all of fp32's binades (workloads.full_range), both solvers, and a
+    row of magnitudes in [2^120, 2^127.9) at rho = 0.01, whose 1/lambda lies beyond fp32's range: its
+    amplified values are +-inf on both sides, as is the hybrid coding's shared 1/lambda."""
+    rng = np.random.default_rng(12)
+    for case in range(12):
+        d = int(np.exp(rng.uniform(0.0, np.log(20000.0))))
+        g = W.full_range(d, 100 + case)
+        rho = float(10.0 ** rng.uniform(-3.0, 0.0))
+        for solver in ("exact", "greedy"):
+            sol = oracle.solve(g, rho, solver, 2)
+            idx, val, n, lam, k, fl = sample_row(L, g, rho, solver, 31 + case)
+            assert fl == 0, (case, solver, fl)
+            compare_sample(g, sol.p, 31 + case, idx, val, n, lam, sol.lam)
+            if solver == "exact":
+                assert lam == sol.lam and k == sol.k, (case, lam, sol.lam, k, sol.k)
+    r2 = np.random.default_rng(9)
+    g = (r2.choice([-1.0, 1.0], 3001) * np.exp2(r2.uniform(120.0, 127.9, 3001))).astype(np.float32)
+    for solver in ("exact", "greedy"):
+        sol = oracle.solve(g, 0.01, solver, 2)
+        assert sol.lam < 2.0 ** -128
+        idx, val, n, lam, k, fl = sample_row(L, g, 0.01, solver, 5)
+        assert fl == 0 and np.isinf(val[:n]).any()
+        compare_sample(g, sol.p, 5, idx, val, n, lam, sol.lam)
+        ia, va, na, cb, nb, inv, q, lam2, fl2 = hybrid_batched(L, g[None, :], [0.01], [5], solver)
+        assert fl2[0] == 0 and lam2[0] == lam and inv[0] == np.inf and int(na[0] + nb[0]) == n
+    if verbose:
+        print("full-range rows ok", flush=True)
+    return True
+
+
 def check_lane_rows(L, verbose=True):
     """Capped coordinates that one decide-phase lane takes beyond its LDS row (workloads.strided_large):
     those waves read their capped values from g while emitting, lane by lane (rho 0.01, 0.05) or

@@ -133,6 +133,40 @@ def test_random_rows(gs):
             assert lam == sol.lam and k == sol.k, (case, lam, sol.lam, k, sol.k)
 
 
+def test_full_range_rows(gs):
+    """Forty seeded rows whose magnitudes span all of fp32's binades (subnormals to near the
+    largest finite value), random length, density and solver, against the oracle; then a row of
+    magnitudes in [2^120, 2^127.9) at rho = 0.01, whose 1/lambda lies beyond fp32's range, so the
+    amplified values are +-inf on both sides and the hybrid coding's shared 1/lambda is +inf."""
+    rng = np.random.default_rng(77)
+    for case in range(40):
+        d = int(np.exp(rng.uniform(0.0, np.log(300000.0))))
+        g = W.full_range(d, 500 + case)
+        rho = float(10.0 ** rng.uniform(-3.5, 0.0))
+        solver = ("greedy", "exact")[case % 2]
+        _say(f"[full-range] case={case} d={d} rho={rho:.5g} solver={solver}")
+        sol = oracle.solve(g, rho, solver, 2)
+        idx, val, n, lam, k, fl = _run_row(gs, g, rho, solver, case, cap=d)
+        assert fl == 0, (case, fl)
+        compare_sample(g, sol.p, case, idx, val, n, lam, sol.lam)
+        if solver == "exact":
+            assert lam == sol.lam and k == sol.k, (case, lam, sol.lam, k, sol.k)
+    r2 = np.random.default_rng(9)
+    d = 100003
+    g = (r2.choice([-1.0, 1.0], d) * np.exp2(r2.uniform(120.0, 127.9, d))).astype(np.float32)
+    for solver in ("exact", "greedy"):
+        _say(f"[full-range] overflow row solver={solver}")
+        sol = oracle.solve(g, 0.01, solver, 2)
+        assert sol.lam < 2.0 ** -128
+        idx, val, n, lam, k, fl = _run_row(gs, g, 0.01, solver, 5, cap=d)
+        assert fl == 0 and np.isinf(val[:n]).any()
+        compare_sample(g, sol.p, 5, idx, val, n, lam, sol.lam)
+        h = gs.sparsify_sample_hybrid(torch.from_numpy(g).cuda(), 0.01, seed=5, solver=solver, cap_a=d, cap_b=d)
+        torch.cuda.synchronize()
+        assert int(h.flags.item()) == 0 and float(h.inv_lam.item()) == float("inf")
+        assert int(h.n_a.item()) + int(h.n_b.item()) == n
+
+
 @pytest.mark.parametrize("iters", [0, 1, 3, 8])
 def test_greedy_iterations(gs, iters):
     g = W.t_mixture(150000, 11)

@@ -206,6 +206,14 @@ def wide_range(d: int, seed: int) -> np.ndarray:
     return (rng.choice([-1.0, 1.0], size=d) * np.exp2(e)).astype(np.float32)
 
 
+def full_range(d: int, seed: int) -> np.ndarray:
+    """Magnitudes log-uniform over all of fp32's binades, subnormals to just below the largest
+    finite value, with random signs."""
+    rng = np.random.default_rng(seed)
+    e = rng.uniform(-149.0, 127.99, d)
+    return np.minimum(np.exp2(e), 3.4e38).astype(np.float32) * rng.choice([-1.0, 1.0], size=d).astype(np.float32)
+
+
 def sparse_lists(workers: int, d: int, cap: int, seed: int, empty=(), over=()):
     """Per-worker strictly ascending index lists with fp32 values, as [workers, cap] arrays and an
     int64 length per worker: mixed lengths, every third list clustered into a short index range,
