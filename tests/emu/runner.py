@@ -811,6 +811,12 @@ if __name__ == "__main__":
         check_variance(load(sys.argv[1]))
     if which in ("all", "segmented"):
         check_segmented(load(sys.argv[1]))
+    if which in ("all", "edges"):
+        L = load(sys.argv[1])
+        check_lowest_binade(L)
+        check_full_range(L)
+        check_lane_rows(L)
+        check_band_region_overflow(L)
     if which == "asan_subset":
         check_asan_subset(load(sys.argv[1]))
     if which in ("all", "main"):

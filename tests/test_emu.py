@@ -1,10 +1,11 @@
 """CPU runs of the HIP kernels through the host emulation in tests/emu (no GPU needed).
 
 The unchanged library source is compiled with g++ against a small HIP-runtime emulation in which
-workgroup threads are host threads. These tests check kernel indexing, the solver's control flow
-(every thread of a workgroup must pass the same barriers) and the whole pipeline against the
-oracle, on small inputs. GSPAR_EMU_FULL=1 runs the full sweep, GSPAR_EMU_ASAN=1 reruns it under
-AddressSanitizer in a subprocess."""
+the threads of a workgroup are fibers switched at barriers, shuffles, ballots and sleeps. These
+tests check kernel indexing, the solver's control flow (every thread of a workgroup must pass the
+same barriers; a barrier that can never release is reported) and the whole pipeline against the
+oracle, on small inputs: each check once in the default schedule, the whole sweep again under
+AddressSanitizer, and again with the fibers scheduled at random."""
 import os
 import subprocess
 import sys
@@ -87,15 +88,14 @@ def test_emulated_parity_subset(emu_lib):
                     assert lam == sol.lam and k == sol.k
 
 
-@pytest.mark.skipif(os.environ.get("GSPAR_EMU_FULL") != "1", reason="full emulated sweep: set GSPAR_EMU_FULL=1")
 def test_emulated_full_sweep(emu_lib):
     assert runner.run_all(emu_lib, verbose=False) == 64
 
 
 def test_emulated_asan_subset():
-    """Kernel indexing under AddressSanitizer in the default suite (about a minute): a padded batch
-    ending in partial groups with a candidate band, the scalar path, the variance budget, segments
-    on both paths with the hybrid coding, and aggregation (the full sweep under ASan is below)."""
+    """Kernel indexing under AddressSanitizer: a padded batch ending in partial groups with a
+    candidate band, the scalar path, the variance budget, segments on both paths with the hybrid
+    coding, and aggregation (the whole sweep under ASan is below)."""
     lib = emu_build.build(asan=True)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0", LD_PRELOAD=emu_build.asan_runtime())
     r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "asan_subset"], env=env,
@@ -104,13 +104,27 @@ def test_emulated_asan_subset():
     assert "asan subset ok" in r.stdout, r.stdout[-2000:]
 
 
-@pytest.mark.skipif(os.environ.get("GSPAR_EMU_ASAN") != "1", reason="ASan sweep: set GSPAR_EMU_ASAN=1")
 def test_emulated_under_asan():
+    """Every emulated check (edge cases, batching, overflow, the unaligned path, hybrid coding,
+    ties, the candidate band and its overflows, aggregation, the variance budget, segments and the
+    parity sweep) under AddressSanitizer."""
     lib = emu_build.build(asan=True)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0", LD_PRELOAD=emu_build.asan_runtime())
     r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), lib, "all"], env=env,
-                       capture_output=True, text=True, timeout=3600)
+                       capture_output=True, text=True, timeout=1200)
     assert r.returncode == 0 and "AddressSanitizer" not in r.stderr, r.stderr[-2000:]
+    assert "checked 64" in r.stdout, r.stdout[-2000:]
+
+
+def test_emulated_random_schedule(emu_lib):
+    """Every emulated check again with the fibers of each workgroup scheduled at random, so that
+    lanes run in another order after each barrier: a read of shared state that no barrier
+    separates from another lane's write sees the wrong value in some workgroup."""
+    env = dict(os.environ, EMU_SHUFFLE="1")
+    r = subprocess.run([sys.executable, os.path.join(HERE, "emu", "runner.py"), emu_lib, "all"], env=env,
+                       capture_output=True, text=True, timeout=1200)
+    assert r.returncode == 0, (r.stdout[-2000:], r.stderr[-2000:])
+    assert "checked 64" in r.stdout, r.stdout[-2000:]
 
 
 def test_emulated_lookback_fallback():
