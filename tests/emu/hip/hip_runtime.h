@@ -9,7 +9,7 @@
 // point; a barrier releases when every fiber of its group that has not returned has arrived, and
 // the fiber that completes it runs on first, so the others observe its later writes only after
 // their own next switch. EMU_SHUFFLE=1 picks the next fiber at random instead of round robin
-// (with a seed per workgroup), which changes which lanes run first after each barrier and exposes
+// (seeded per launch and workgroup, and by EMU_SHUFFLE_SEED), which changes which lanes run first after each barrier and exposes
 // reads of shared state that no barrier separates from another lane's write. __shared__ variables
 // become static storage, shared by the fibers of the running workgroup. Because workgroups never
 // overlap, inter-workgroup waits (the look-back) always find their predecessors finished.
@@ -106,6 +106,9 @@ struct LaneTrace {
 };
 inline LaneTrace g_trace[1024];
 inline bool g_shuffle = getenv("EMU_SHUFFLE") && atoi(getenv("EMU_SHUFFLE")) != 0;
+// EMU_SHUFFLE_SEED varies the random schedules between runs
+inline unsigned g_shuffle_seed = getenv("EMU_SHUFFLE_SEED") ? (unsigned)atoi(getenv("EMU_SHUFFLE_SEED")) : 0u;
+inline unsigned long g_launches = 0;
 inline std::minstd_rand g_rng;
 
 // scheduler state of the running launch (launches come from one host thread at a time)
@@ -410,6 +413,7 @@ void launch(K kernel, dim3 grid, dim3 block, A... args) {
   const unsigned nb = grid.x * grid.y * grid.z;
   const unsigned nt = block.x;
   ensure_fibers(nt);
+  ++g_launches;
   Block blk;
   // EMU_STALL_SECONDS: a launch still running after that long reports each lane's last block
   // barrier and exits (a lane that loops without reaching a barrier)
@@ -448,7 +452,7 @@ void launch(K kernel, dim3 grid, dim3 block, A... args) {
     tl_bdim.x = block.x;
     tl_gdim.x = grid.x;
     tl_gdim.y = grid.y;
-    g_rng.seed(1234567u + b);
+    g_rng.seed(1234567u + b + 7919u * (unsigned)g_launches + 104729u * g_shuffle_seed);
     for (unsigned t = 0; t < nt; ++t) {
       Fiber& f = g_fibers[t];
       f.tid = t;

@@ -394,6 +394,96 @@ def check_full_range(L, verbose=True):
     return True
 
 
+def _draw(rng, d):
+    """A seeded random vector of length d: one of seven distributions, scaled over ten decades
+    (the full-range one spans all of fp32's binades as it is)."""
+    seed = int(rng.integers(1 << 30))
+    kind = int(rng.integers(7))
+    if kind == 0:
+        g = W.normal(d, seed)
+    elif kind == 1:
+        g = W.t_mixture(d, seed)
+    elif kind == 2:
+        g = W.integer_ties(d, seed)
+    elif kind == 3:
+        g = W.wide_range(d, seed)
+    elif kind == 4:
+        g = W.two_level(d, max(1, d // 50), 30.0, 1.0, seed)
+    elif kind == 5:
+        return W.full_range(d, seed)
+    else:
+        g = W.approx_sparse(d, max(1, d // 20), 0.05, seed) if d >= 20 else W.normal(d, seed)
+    return (g * np.float32(10.0 ** rng.uniform(-6, 4))).astype(np.float32)
+
+
+def _random_row(rng, dmax):
+    """A seeded random row: log-uniform length up to dmax, random distribution, density and solver."""
+    d = int(np.exp(rng.uniform(0.0, np.log(dmax))))
+    g = _draw(rng, d)
+    return g, float(10.0 ** rng.uniform(-3.5, 0.0)), ("greedy", "exact")[int(rng.integers(2))], int(rng.integers(100000))
+
+
+def check_random(L, verbose=True, cases=40, seed=4242):
+    """Seeded random rows (up to 60 K coordinates) for the density solvers and the variance budget,
+    padded batches of one random length and segmented layouts with random lengths (empty segments
+    among them), each against the oracle; lambda and k bit for bit for the exact solvers."""
+    rng = np.random.default_rng(seed)
+    for case in range(cases):
+        g, rho, solver, seed = _random_row(rng, 60000.0)
+        sol = oracle.solve(g, rho, solver, 2)
+        idx, val, n, lam, k, fl = sample_row(L, g, rho, solver, seed)
+        assert fl == (0 if g.any() else 4), (case, fl)
+        compare_sample(g, sol.p, seed, idx, val, n, lam, sol.lam)
+        if solver == "exact":
+            assert lam == sol.lam and k == sol.k, (case, lam, sol.lam, k, sol.k)
+    for case in range(cases // 4):
+        g = _draw(rng, int(np.exp(rng.uniform(0.0, np.log(60000.0)))))
+        eps = float(10.0 ** rng.uniform(-3.0, 1.0))
+        sol = oracle.solve_variance(g, eps)
+        idx, val, n, lam, k, fl = sample_row(L, g, eps, "variance", 50 + case)
+        assert fl == (0 if g.any() else 4), (case, fl)
+        compare_sample(g, sol.p, 50 + case, idx, val, n, lam, sol.lam)
+        assert lam == sol.lam and k == sol.k, (case, eps, lam, sol.lam, k, sol.k)
+    for case in range(cases // 4):
+        rows = int(rng.integers(1, 6))
+        d = int(np.exp(rng.uniform(0.0, np.log(30000.0))))
+        solver = ("greedy", "exact")[case % 2]
+        g2 = np.stack([_draw(rng, d) for _ in range(rows)])
+        rhos = [float(10.0 ** rng.uniform(-3.0, 0.0)) for _ in range(rows)]
+        seeds = [int(rng.integers(1 << 40)) for _ in range(rows)]
+        idx, val, nnz, lam, k, fl = batched(L, g2, rhos, seeds, solver, ld=d + int(rng.integers(0, 9)))
+        for r in range(rows):
+            sol = oracle.solve(g2[r], rhos[r], solver, 2)
+            n = int(nnz[r])
+            assert fl[r] == (0 if g2[r].any() else 4), (case, r, fl[r])
+            compare_sample(g2[r], sol.p, seeds[r], idx[r, :n], val[r, :n], n, lam[r], sol.lam)
+            if solver == "exact":
+                assert lam[r] == sol.lam and k[r] == sol.k
+    for case in range(cases // 4):
+        segs = int(rng.integers(1, 9))
+        lengths = [int(np.exp(rng.uniform(0.0, np.log(20000.0)))) if rng.random() > 0.15 else 0 for _ in range(segs)]
+        g, off = layered(lengths, 1300 + case)
+        rhos = [float(10.0 ** rng.uniform(-3.0, 0.0)) for _ in range(segs)]
+        seeds = [int(rng.integers(1 << 30)) for _ in range(segs)]
+        solver = ("exact", "greedy")[case % 2]
+        idx, val, nnz, lam, k, fl = segmented(L, g, off, rhos, seeds, solver, g_shift=int(rng.integers(0, 4)))
+        ref = oracle.sparsify_segments(g, off, rhos, seeds, solver)
+        for s_ in range(segs):
+            seg = g[off[s_]:off[s_ + 1]]
+            n = int(nnz[s_])
+            if seg.size == 0 or not np.any(seg):
+                assert n == 0 and fl[s_] & 4
+                continue
+            sol = ref[s_][0]
+            assert fl[s_] == 0
+            compare_sample(seg, sol.p, seeds[s_], idx[s_, :n], val[s_, :n], n, lam[s_], sol.lam)
+            if solver == "exact":
+                assert lam[s_] == sol.lam and k[s_] == sol.k
+    if verbose:
+        print("random cases ok", flush=True)
+    return True
+
+
 def check_lane_rows(L, verbose=True):
     """Capped coordinates that one decide-phase lane takes beyond its LDS row (workloads.strided_large):
     those waves read their capped values from g while emitting, lane by lane (rho 0.01, 0.05) or
@@ -817,6 +907,8 @@ if __name__ == "__main__":
         check_full_range(L)
         check_lane_rows(L)
         check_band_region_overflow(L)
+    if which in ("all", "random"):
+        check_random(load(sys.argv[1]))
     if which == "asan_subset":
         check_asan_subset(load(sys.argv[1]))
     if which in ("all", "main"):

@@ -49,6 +49,10 @@ def test_emulated_full_range_rows(emu_lib):
     assert runner.check_full_range(runner.load(emu_lib), verbose=False)
 
 
+def test_emulated_random_rows_batches_segments(emu_lib):
+    assert runner.check_random(runner.load(emu_lib), verbose=False)
+
+
 def test_emulated_capped_values_past_the_lane_rows(emu_lib):
     assert runner.check_lane_rows(runner.load(emu_lib), verbose=False)
 
