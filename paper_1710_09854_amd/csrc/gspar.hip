@@ -649,6 +649,27 @@ __device__ __forceinline__ uint32_t load4(const float* __restrict__ row, int64_t
 // thread with scalar loads and visited by the whole first wave. No memory access sits under a
 // divergent branch, which would make the compiler wait for every outstanding load. With vector
 // loads every call of f is made by whole waves, so f may use cross-lane operations.
+// Streaming accesses: g is read once per pass and the compacted lists are written once, so those
+// loads and stores (and those of the probabilities) carry the non-temporal hint and do not
+// displace what the caches keep (the level-1 copies, windows and status words). On 2^28 coordinates this takes the statistics pass
+// from about 213 to 192 microseconds per call.
+#if defined(__HIP_DEVICE_COMPILE__)
+typedef float gs_f4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 load_stream(const float* p) {
+  const gs_f4v v = __builtin_nontemporal_load(reinterpret_cast<const gs_f4v*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void store_stream(float* p, float4 x) {
+  const gs_f4v v = {x.x, x.y, x.z, x.w};
+  __builtin_nontemporal_store(v, reinterpret_cast<gs_f4v*>(p));
+}
+#define GS_STORE_STREAM(ptr, v) __builtin_nontemporal_store((v), (ptr))
+#else
+GS_HD float4 load_stream(const float* p) { return *reinterpret_cast<const float4*>(p); }
+GS_HD void store_stream(float* p, float4 x) { *reinterpret_cast<float4*>(p) = x; }
+#define GS_STORE_STREAM(ptr, v) (*(ptr) = (v))
+#endif
+
 template <bool VEC, int U, int NT, typename F>
 __device__ __forceinline__ void stream_groups(const float* __restrict__ row, int64_t beg, int64_t end, F&& f) {
   if (!VEC) {
@@ -664,7 +685,7 @@ __device__ __forceinline__ void stream_groups(const float* __restrict__ row, int
   for (; qb + (int64_t)U * NT <= qfull; qb += (int64_t)U * NT) {
     float4 x[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) x[u] = *reinterpret_cast<const float4*>(row + 4 * (qb + threadIdx.x + u * NT));
+    for (int u = 0; u < U; ++u) x[u] = load_stream(row + 4 * (qb + threadIdx.x + u * NT));
     __builtin_amdgcn_sched_barrier(0);  // keep every load of the block ahead of the first use
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -2655,7 +2676,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
         float4 x[kSampleBatch];
 #pragma unroll
         for (int u = 0; u < kSampleBatch; ++u)
-          x[u] = *reinterpret_cast<const float4*>(c.row + 4 * (q0 + 64 * (jb + u)));
+          x[u] = load_stream(c.row + 4 * (q0 + 64 * (jb + u)));
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < kSampleBatch; ++u) {
@@ -2824,8 +2845,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
               else val = c.row[e0 + b];
             }
             if ((int64_t)pos < a.cap) {
-              oi[pos] = (int32_t)(e0 + b);
-              ov[pos] = val;
+              GS_STORE_STREAM(&oi[pos], (int32_t)(e0 + b));
+              GS_STORE_STREAM(&ov[pos], val);
             }
             ++pos;
             m &= m - 1;
@@ -2880,8 +2901,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             const uint32_t x = si[i], cc = sc[i];
             const float cv = capw[cc & 0x3FFu];
             const float val = (cc & 0x4000u) ? cv : ((cc & 0x8000u) ? -inv : inv);
-            *(GS_GLOBAL(int32_t)*)(bi + 4u * i) = t0c + (int32_t)x;
-            *(GS_GLOBAL(float)*)(bv + 4u * i) = val;
+            GS_STORE_STREAM((GS_GLOBAL(int32_t)*)(bi + 4u * i), t0c + (int32_t)x);
+            GS_STORE_STREAM((GS_GLOBAL(float)*)(bv + 4u * i), val);
           }
         } else if (lds_values && s_wsel[kk][wv] <= (uint32_t)kDenseEmit && wave_end <= (uint64_t)a.cap &&
                    wave_end <= ((uint64_t)1 << 30)) {
@@ -2901,8 +2922,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             const int32_t i0 = (int32_t)(e0 + 32 * h);
             while (m) {
               const int b = __builtin_ctz(m);
-              *(GS_GLOBAL(int32_t)*)(bi + off) = i0 + b;
-              *(GS_GLOBAL(float)*)(bv + off) = ((neg >> b) & 1u) ? -inv : inv;
+              GS_STORE_STREAM((GS_GLOBAL(int32_t)*)(bi + off), i0 + b);
+              GS_STORE_STREAM((GS_GLOBAL(float)*)(bv + off), ((neg >> b) & 1u) ? -inv : inv);
               off += 4u;
               m &= m - 1u;
             }
@@ -2911,7 +2932,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
           while (m) {
             const int b = __ffsll((unsigned long long)m) - 1;
             const uint32_t below = (uint32_t)__popcll(sm & ((1ull << b) - 1ull));
-            *(GS_GLOBAL(float)*)(bv + off0 + 4u * below) = capval(b);
+            GS_STORE_STREAM((GS_GLOBAL(float)*)(bv + off0 + 4u * below), capval(b));
             m &= m - 1;
           }
         } else if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
@@ -2937,8 +2958,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
                   val = lds_values ? s_capl[kk][wv][lane * kLaneStride + (cb >> 4) + __popc(cap & ((1u << k) - 1u))]
                                    : c.row[eq + k];
                 if ((int64_t)p < a.cap) {
-                  oi[p] = (int32_t)(eq + k);
-                  ov[p] = val;
+                  GS_STORE_STREAM(&oi[p], (int32_t)(eq + k));
+                  GS_STORE_STREAM(&ov[p], val);
                 }
                 ++p;
               }
@@ -3110,7 +3131,7 @@ __global__ void __launch_bounds__(256) k_probs(Args a) {
     }
     if (pr) {
       if (VEC && m == 0xF) {
-        *reinterpret_cast<float4*>(pr + 4 * q) = make_float4(o[0], o[1], o[2], o[3]);
+        store_stream(pr + 4 * q, make_float4(o[0], o[1], o[2], o[3]));
       } else {
         for (int c = 0; c < 4; ++c)
           if ((m >> c) & 1) pr[4 * q + c] = o[c];
