@@ -641,18 +641,13 @@ __device__ __forceinline__ uint32_t load4(const float* __restrict__ row, int64_t
   return m;
 }
 
-// Visits the coordinates [beg, end) of one row (beg a multiple of 4) with the NT threads of a
-// workgroup, calling f(q, v, m) for each float4 group q (m: bit c set when coordinate 4q+c exists).
-// With vector loads, blocks of U groups per thread are loaded unconditionally, all issued before
-// any group is processed, so U loads per thread stay in flight; the last block clamps its addresses
-// to the last whole group and masks the values, and a trailing partial group is loaded by one
-// thread with scalar loads and visited by the whole first wave. No memory access sits under a
-// divergent branch, which would make the compiler wait for every outstanding load. With vector
-// loads every call of f is made by whole waves, so f may use cross-lane operations.
-// Streaming accesses: g is read once per pass and the compacted lists are written once, so those
-// loads and stores (and those of the probabilities) carry the non-temporal hint and do not
-// displace what the caches keep (the level-1 copies, windows and status words). On 2^28 coordinates this takes the statistics pass
-// from about 213 to 192 microseconds per call.
+// Streaming accesses: g is read once per pass and the outputs are written once, so those loads,
+// the probabilities' stores and the compaction's staged stores (whole runs of consecutive words)
+// carry the non-temporal hint and do not displace what the caches keep (the level-1 copies,
+// windows and status words). Stores that lanes make one word at a time to scattered places (the
+// other emission paths, the hybrid coding's lists, the candidate band) keep the default policy:
+// there the hint made the hybrid coding's sampling pass a third slower at rho = 0.1. On 2^28
+// coordinates the hint takes the statistics pass from about 213 to 192 microseconds per call.
 #if defined(__HIP_DEVICE_COMPILE__)
 typedef float gs_f4v __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float4 load_stream(const float* p) {
@@ -670,6 +665,14 @@ GS_HD void store_stream(float* p, float4 x) { *reinterpret_cast<float4*>(p) = x;
 #define GS_STORE_STREAM(ptr, v) (*(ptr) = (v))
 #endif
 
+// Visits the coordinates [beg, end) of one row (beg a multiple of 4) with the NT threads of a
+// workgroup, calling f(q, v, m) for each float4 group q (m: bit c set when coordinate 4q+c exists).
+// With vector loads, blocks of U groups per thread are loaded unconditionally, all issued before
+// any group is processed, so U loads per thread stay in flight; the last block clamps its addresses
+// to the last whole group and masks the values, and a trailing partial group is loaded by one
+// thread with scalar loads and visited by the whole first wave. No memory access sits under a
+// divergent branch, which would make the compiler wait for every outstanding load. With vector
+// loads every call of f is made by whole waves, so f may use cross-lane operations.
 template <bool VEC, int U, int NT, typename F>
 __device__ __forceinline__ void stream_groups(const float* __restrict__ row, int64_t beg, int64_t end, F&& f) {
   if (!VEC) {
@@ -2845,8 +2848,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
               else val = c.row[e0 + b];
             }
             if ((int64_t)pos < a.cap) {
-              GS_STORE_STREAM(&oi[pos], (int32_t)(e0 + b));
-              GS_STORE_STREAM(&ov[pos], val);
+              oi[pos] = (int32_t)(e0 + b);
+              ov[pos] = val;
             }
             ++pos;
             m &= m - 1;
@@ -2922,8 +2925,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
             const int32_t i0 = (int32_t)(e0 + 32 * h);
             while (m) {
               const int b = __builtin_ctz(m);
-              GS_STORE_STREAM((GS_GLOBAL(int32_t)*)(bi + off), i0 + b);
-              GS_STORE_STREAM((GS_GLOBAL(float)*)(bv + off), ((neg >> b) & 1u) ? -inv : inv);
+              *(GS_GLOBAL(int32_t)*)(bi + off) = i0 + b;
+              *(GS_GLOBAL(float)*)(bv + off) = ((neg >> b) & 1u) ? -inv : inv;
               off += 4u;
               m &= m - 1u;
             }
@@ -2932,7 +2935,7 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
           while (m) {
             const int b = __ffsll((unsigned long long)m) - 1;
             const uint32_t below = (uint32_t)__popcll(sm & ((1ull << b) - 1ull));
-            GS_STORE_STREAM((GS_GLOBAL(float)*)(bv + off0 + 4u * below), capval(b));
+            *(GS_GLOBAL(float)*)(bv + off0 + 4u * below) = capval(b);
             m &= m - 1;
           }
         } else if (s_wsel[kk][wv] > (uint32_t)kDenseEmit) {
@@ -2958,8 +2961,8 @@ __global__ void __launch_bounds__(kTileThreads) k_sample(Args a) {
                   val = lds_values ? s_capl[kk][wv][lane * kLaneStride + (cb >> 4) + __popc(cap & ((1u << k) - 1u))]
                                    : c.row[eq + k];
                 if ((int64_t)p < a.cap) {
-                  GS_STORE_STREAM(&oi[p], (int32_t)(eq + k));
-                  GS_STORE_STREAM(&ov[p], val);
+                  oi[p] = (int32_t)(eq + k);
+                  ov[p] = val;
                 }
                 ++p;
               }
