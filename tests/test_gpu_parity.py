@@ -98,6 +98,15 @@ def _random_case(rng):
     """A seeded draw of a row: length (1 to ~300 K, log-uniform, often ragged), distribution,
     scale, density and solver."""
     d = int(np.exp(rng.uniform(0.0, np.log(300000.0))))
+    g, seed = _random_vector(rng, d)
+    rho = float(10.0 ** rng.uniform(-3.5, 0.0))
+    solver = ("greedy", "exact")[int(rng.integers(2))]
+    return g, rho, solver, seed % 100000
+
+
+def _random_vector(rng, d):
+    """A seeded vector of length d: one of six distributions, scaled over ten decades; and the seed
+    it was drawn with."""
     seed = int(rng.integers(1 << 30))
     kind = int(rng.integers(6))
     if kind == 0:
@@ -112,10 +121,7 @@ def _random_case(rng):
         g = W.two_level(d, max(1, d // 50), 30.0, 1.0, seed)
     else:
         g = W.approx_sparse(d, max(1, d // 20), 0.05, seed) if d >= 20 else W.normal(d, seed)
-    g = (g * np.float32(10.0 ** rng.uniform(-6, 4))).astype(np.float32)
-    rho = float(10.0 ** rng.uniform(-3.5, 0.0))
-    solver = ("greedy", "exact")[int(rng.integers(2))]
-    return g, rho, solver, seed % 100000
+    return (g * np.float32(10.0 ** rng.uniform(-6, 4))).astype(np.float32), seed
 
 
 def test_random_rows(gs):
@@ -129,6 +135,25 @@ def test_random_rows(gs):
         idx, val, n, lam, k, fl = _run_row(gs, g, rho, solver, seed, cap=g.size)
         assert fl == (0 if g.any() else gs.FLAG_ALLZERO), (case, fl)  # an all-zero row is reported
         compare_sample(g, sol.p, seed, idx, val, n, lam, sol.lam)
+        if solver == "exact":
+            assert lam == sol.lam and k == sol.k, (case, lam, sol.lam, k, sol.k)
+
+
+def test_random_long_rows(gs):
+    """Eight seeded rows of 2^22 to 2^26 coordinates (log-uniform, ragged; from 2^25 on the
+    statistics pass collects a candidate band) with random distribution, scale and density, both
+    solvers, against the oracle; lambda and k bit for bit for the exact solver."""
+    rng = np.random.default_rng(9090)
+    for case in range(8):
+        d = int(2.0 ** rng.uniform(22.0, 26.0))
+        g, seed = _random_vector(rng, d)
+        rho = float(10.0 ** rng.uniform(-3.5, -0.5))
+        solver = ("greedy", "exact")[case % 2]
+        _say(f"[random-long] case={case} d={d} rho={rho:.5g} solver={solver} seed={seed}")
+        sol = oracle.solve(g, rho, solver, 2)
+        idx, val, n, lam, k, fl = _run_row(gs, g, rho, solver, seed % 100000)
+        assert fl == 0, (case, fl)
+        compare_sample(g, sol.p, seed % 100000, idx, val, n, lam, sol.lam)
         if solver == "exact":
             assert lam == sol.lam and k == sol.k, (case, lam, sol.lam, k, sol.k)
 
